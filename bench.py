@@ -1,0 +1,247 @@
+"""Benchmark of the shifted-window attention hot path on one MI355X.
+
+One step = one pass of the whole path over one synthetic batch:
+  route Q, K, V (NHWC -> window-major)      terra_window_route x3
+  attention forward (O, LSE)                terra_winattn_fwd
+  route dOut                                terra_window_route
+  attention backward (dQ, dK, dV, dTable)   terra_winattn_bwd
+  inverse route O, dQ, dK, dV               terra_window_unroute x4
+Inputs are resident in HBM before timing starts.  W warm-up steps, then K
+timed steps between device synchronisations; every launch is bracketed by
+HIP events on the stream it runs on.
+
+The printed JSON line's `value` is the attention forward+backward
+algorithmic TFLOP/s of the whole step (flops 12 n^2 hd per window and head,
+divided by the full step time including the routes); per-phase figures,
+the roofline of the dominant phase and the oracle CPU baseline ride along.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config NAME]
+"""
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import terra_synth as ts  # noqa: E402
+
+METRIC = "Swin window-attn fwd+bwd TFLOP/s (% MFMA peak); routing GB/s (% HBM)"
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3       # MI355X fp32 matrix
+PEAK_HBM_GBPS = 8000.0        # MI355X HBM3E
+DEFAULT_CONFIG = "c4_bf16_128x1080_w8x16"
+
+
+def window_sizes(cfg):
+    mh, mw = -(-cfg.H // cfg.wh), -(-cfg.W // cfg.ww)
+    rows = [min(cfg.wh, cfg.H - i * cfg.wh) for i in range(mh)]
+    cols = [min(cfg.ww, cfg.W - j * cfg.ww) for j in range(mw)]
+    return [r * c for r in rows for c in cols]
+
+
+def algorithmic(cfg):
+    """Flops and compulsory HBM bytes per launch of each phase."""
+    e = 4 if cfg.dtype == "f32" else 2
+    ns = np.asarray(window_sizes(cfg), np.float64)
+    n2 = float((ns ** 2).sum()) * cfg.B * cfg.heads
+    tok = cfg.B * cfg.H * cfg.W
+    t = tok * cfg.C * e                        # one tensor
+    lse = tok * cfg.heads * 4
+    tab = (2 * cfg.wh - 1) * (2 * cfg.ww - 1) * cfg.heads * 4
+    return {
+        "fwd_flops": 4.0 * n2 * cfg.head_dim,
+        "bwd_flops": 8.0 * n2 * cfg.head_dim,
+        "route_bytes": 2.0 * t,                                  # read + write one tensor
+        "fwd_bytes": 4.0 * t + lse + tab,                        # Q,K,V in; O, LSE out
+        "bwd_bytes": 8.0 * t + lse + 2 * tab,                    # Q,K,V,O,dO,LSE in; dQ,dK,dV,dT out
+    }
+
+
+def cpu_baseline(cfg, seconds_target=15.0):
+    """Time the fp64 oracle (as it stands) on a bounded sample of windows."""
+    import threadpoolctl
+    from oracle import Geometry, route, attn_fwd_windows, attn_bwd_windows
+    from oracle.geometry import window_slots
+
+    g = Geometry(**cfg.geom_kwargs())
+    inp = ts.make_inputs(cfg)
+    slots = window_slots(g)
+    rng = np.random.default_rng(1)
+    t0 = time.perf_counter()
+    q, k, v, do = (route(inp[n], g) for n in ("q", "k", "v", "dout"))
+    t_route = (time.perf_counter() - t0) / 4.0
+    # grow the sample until it costs about seconds_target
+    nsel = 8
+    sample_time, sample_flops, used = 0.0, 0.0, 0
+    with threadpoolctl.threadpool_limits() as _:
+        info = threadpoolctl.threadpool_info()
+    threads = max([i.get("num_threads", 1) for i in info] + [1])
+    while True:
+        sel = sorted(int(x) for x in rng.choice(len(slots), size=min(nsel, len(slots)), replace=False))
+        t0 = time.perf_counter()
+        attn_fwd_windows(q, k, v, inp["table"], g, sel)
+        attn_bwd_windows(q, k, v, do, inp["table"], g, sel)
+        dt = time.perf_counter() - t0
+        n2 = sum(float(slots[w][2]) ** 2 for w in sel) * cfg.B * cfg.heads
+        sample_time, sample_flops, used = dt, 12.0 * n2 * cfg.head_dim, len(sel)
+        if dt >= seconds_target / 3 or nsel >= len(slots):
+            break
+        nsel = min(len(slots), int(nsel * max(2.0, seconds_target / 3 / max(dt, 1e-3))))
+    e = 4 if cfg.dtype == "f32" else 2
+    route_gbps = 2.0 * cfg.B * cfg.H * cfg.W * cfg.C * e / t_route / 1e9
+    return {
+        "value": sample_flops / sample_time / 1e12,
+        "unit": "TFLOP/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": "fp64 oracle fwd+bwd on %d of %d windows x %d heads (%.1f s); route of 4 full "
+                  "tensors %.1f GB/s; host %s, %d logical CPUs" % (
+                      used, len(slots), cfg.heads, sample_time, route_gbps,
+                      platform.processor() or platform.machine(), os.cpu_count()),
+        "route_GBps": route_gbps,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default=DEFAULT_CONFIG, choices=ts.ORDER)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the path has no multi-GPU leg in this build "
+              "(see DESIGN.md for how it would shard); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2608_15211_amd as P
+
+    cfg = ts.CONFIGS[args.config]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    tdt = torch.float32 if cfg.dtype == "f32" else torch.bfloat16
+    print("bench: generating %s inputs" % cfg.name, file=sys.stderr, flush=True)
+    inp = ts.make_inputs(cfg)
+    x = {n: torch.from_numpy(inp[n]).to(dev).to(tdt) for n in ("q", "k", "v", "dout")}
+    table = torch.from_numpy(inp["table"]).to(dev)
+    del inp
+    shape_w = (cfg.B, cfg.H * cfg.W, cfg.C)
+    w = {n: torch.empty(shape_w, dtype=tdt, device=dev) for n in ("q", "k", "v", "dout")}
+    o = torch.empty(shape_w, dtype=tdt, device=dev)
+    lse = torch.empty((cfg.B, cfg.heads, cfg.H * cfg.W), dtype=torch.float32, device=dev)
+    grads = (torch.empty(shape_w, dtype=tdt, device=dev), torch.empty(shape_w, dtype=tdt, device=dev),
+             torch.empty(shape_w, dtype=tdt, device=dev), torch.empty_like(table))
+    back = {n: torch.empty((cfg.B, cfg.H, cfg.W, cfg.C), dtype=tdt, device=dev)
+            for n in ("o", "dq", "dk", "dv")}
+    ws = torch.empty(max(1, P.terra_winattn_bwd_workspace_bytes(cfg, tdt)), dtype=torch.uint8, device=dev)
+
+    phases = ["route", "fwd", "bwd", "unroute"]
+
+    def step(ev):
+        def rec(name, fn):
+            if ev is not None:
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record()
+                fn()
+                b.record()
+                ev[name].append((a, b))
+            else:
+                fn()
+        for n in ("q", "k", "v"):
+            rec("route", lambda n=n: P.terra_window_route(x[n], cfg, out=w[n]))
+        rec("fwd", lambda: P.terra_winattn_fwd(w["q"], w["k"], w["v"], table, cfg, out=o, lse=lse))
+        rec("route", lambda: P.terra_window_route(x["dout"], cfg, out=w["dout"]))
+        rec("bwd", lambda: P.terra_winattn_bwd(w["q"], w["k"], w["v"], o, w["dout"], lse, table, cfg,
+                                               out=grads, workspace=ws))
+        for n, t in (("o", o), ("dq", grads[0]), ("dk", grads[1]), ("dv", grads[2])):
+            rec("unroute", lambda n=n, t=t: P.terra_window_unroute(t, cfg, out=back[n]))
+
+    print("bench: warm-up %d steps" % args.warmup, file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        step(None)
+    torch.cuda.synchronize()
+    ev = {p: [] for p in phases}
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(args.steps):
+        step(ev)
+    stop.record()
+    torch.cuda.synchronize()
+    print("bench: timed %d steps" % args.steps, file=sys.stderr, flush=True)
+    total_ms = start.elapsed_time(stop)
+    ms_step = total_ms / args.steps
+    per_launch = {p: float(np.mean([a.elapsed_time(b) for a, b in ev[p]])) for p in phases}
+    per_step = {p: float(np.sum([a.elapsed_time(b) for a, b in ev[p]])) / args.steps for p in phases}
+
+    alg = algorithmic(cfg)
+    attn_flops = alg["fwd_flops"] + alg["bwd_flops"]
+    peak = PEAK_F32_TFLOPS if cfg.dtype == "f32" else PEAK_BF16_TFLOPS
+    value = attn_flops / (ms_step * 1e-3) / 1e12
+    attn_ms = per_step["fwd"] + per_step["bwd"]
+    attn_tflops = attn_flops / (attn_ms * 1e-3) / 1e12
+    ai = attn_flops / (alg["fwd_bytes"] + alg["bwd_bytes"])
+    attainable = min(peak, ai * PEAK_HBM_GBPS / 1e3)
+    route_gbps = alg["route_bytes"] / (per_launch["route"] * 1e-3) / 1e9
+    unroute_gbps = alg["route_bytes"] / (per_launch["unroute"] * 1e-3) / 1e9
+
+    # dominant phase (by time per step) -> roofline object
+    unit_bytes = {"route": alg["route_bytes"], "unroute": alg["route_bytes"],
+                  "fwd": alg["fwd_bytes"], "bwd": alg["bwd_bytes"]}
+    dom = max(phases, key=lambda p: per_step[p])
+    achieved = unit_bytes[dom] / (per_launch[dom] * 1e-3) / 1e9
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS,
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": None,
+                "kernel": {"route": "terra_window_route", "unroute": "terra_window_unroute",
+                           "fwd": "terra_winattn_fwd", "bwd": "terra_winattn_bwd"}[dom],
+                "algorithmic_bytes_per_launch": unit_bytes[dom],
+                "avg_launch_ms": round(per_launch[dom], 4)}
+
+    line = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "B": cfg.B, "grid": [cfg.H, cfg.W], "C": cfg.C,
+                   "heads": cfg.heads, "head_dim": cfg.head_dim, "window": [cfg.wh, cfg.ww],
+                   "shift": [cfg.sh, cfg.sw], "parallelism": "single-gpu"},
+        "roofline": roofline,
+        "attn": {"fwd_ms": round(per_step["fwd"], 4), "bwd_ms": round(per_step["bwd"], 4),
+                 "tflops_kernels_only": round(attn_tflops, 2),
+                 "frac_mfma_peak": round(attn_tflops / peak, 4),
+                 "attainable_tflops": round(attainable, 1),
+                 "frac_attainable": round(attn_tflops / attainable, 4),
+                 "fwd_hbm_GBps": round(alg["fwd_bytes"] / (per_launch["fwd"] * 1e-3) / 1e9, 1),
+                 "bwd_hbm_GBps": round(alg["bwd_bytes"] / (per_launch["bwd"] * 1e-3) / 1e9, 1)},
+        "routing": {"route_ms": round(per_launch["route"], 4), "route_GBps": round(route_gbps, 1),
+                    "route_frac_hbm": round(route_gbps / PEAK_HBM_GBPS, 4),
+                    "unroute_ms": round(per_launch["unroute"], 4),
+                    "unroute_GBps": round(unroute_gbps, 1),
+                    "unroute_frac_hbm": round(unroute_gbps / PEAK_HBM_GBPS, 4)},
+    }
+    if not args.no_cpu_baseline:
+        print("bench: timing the oracle on a sample", file=sys.stderr, flush=True)
+        cb = cpu_baseline(cfg)
+        line["cpu_baseline"] = {k: cb[k] for k in ("value", "unit", "cores", "kind", "sample")}
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,150 @@
+/*
+ * terra_swin.h - C ABI of the MI355X (gfx950) shifted-window attention path.
+ *
+ * The library implements the per-GPU hot path inside the Swin blocks of the
+ * paper's hierarchical Earth-forecasting model: the token route between the
+ * spatially contiguous layout and the window-major layout (Sec. IV-D), and
+ * shifted-window multi-head self-attention with relative-position bias,
+ * forward and backward (W-MSA / SW-MSA of the Swin blocks, Sec. IV-A).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Geometry.  The Transformer-stage token grid is H x W (Sec. IV-D, Eq. (2)),
+ *   B images, C = heads * head_dim channels (Table I: d, N_h), attention
+ *   window wh x ww (Table I: w, generalised to a rectangle) and window shift
+ *   (sh, sw) with 0 <= sh < wh <= H, 0 <= sw < ww <= W.
+ * Shift.  The grid is rolled so that content moves toward the top-left: the
+ *   rolled coordinate of original token (u, v) is ((u - sh) mod H,
+ *   (v - sw) mod W).  Windows partition the rolled grid (Eq. (2)); when wh
+ *   does not divide H (ww does not divide W) the last window row (column) is
+ *   partial - there is no padding.
+ * Mask.  mask_flags bit 0 (TERRA_MASK_LAT) labels the sh rows that wrapped
+ *   across the latitude edge, bit 1 (TERRA_MASK_LON) the sw wrapped columns;
+ *   tokens attend only to tokens of their own window with equal labels.
+ *   Longitude is normally periodic (bit 1 clear).
+ * Layouts.  NHWC tensors are B x H x W x C, contiguous.  Window-major tensors
+ *   are B x (H*W) x C: per image, windows in row-major order (Sec. V-A,
+ *   Eq. (4) flattening), tokens row-major over each window's actual extent,
+ *   channel c = h * head_dim + e.  LSE is B x heads x (H*W) float32 in
+ *   window-major token order.  Bias tables are float32
+ *   [2wh-1][2ww-1][heads]; the bias of query q and key k is
+ *   T[a_q - a_k + wh - 1][c_q - c_k + ww - 1][h], (a, c) = in-window offset.
+ * Element types.  TERRA_F32 (float) or TERRA_BF16 (bfloat16 storage, float32
+ *   accumulation, results rounded to nearest even).  Bias tables, LSE and the
+ *   bias-table gradient are always float32.
+ * Memory.  Every tensor pointer is a DEVICE pointer allocated by the caller;
+ *   the library allocates nothing and keeps no device state.  Geometry
+ *   structs and host arrays stay owned by the caller.  Tensors of one call
+ *   must not overlap unless stated.
+ * Streams.  `stream` is a hipStream_t (NULL = the default stream).  Calls
+ *   only enqueue work on it and never synchronise.
+ * Errors.  Every int-returning call returns a terra_status.  Argument checks
+ *   run on the host before any device work, so an error status means nothing
+ *   was enqueued (except TERRA_ERR_HIP, reported by the HIP runtime after a
+ *   launch).  terra_last_error() gives a message for the calling thread.
+ */
+#ifndef TERRA_SWIN_H
+#define TERRA_SWIN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct terra_geom {
+  int32_t B, H, W, C;        /* images, grid rows/cols, channels          */
+  int32_t heads, head_dim;   /* C == heads * head_dim                     */
+  int32_t wh, ww;            /* window extent                             */
+  int32_t sh, sw;            /* window shift                              */
+  int32_t mask_flags;        /* TERRA_MASK_LAT | TERRA_MASK_LON           */
+} terra_geom;
+
+enum terra_dtype { TERRA_F32 = 0, TERRA_BF16 = 1 };
+
+enum terra_status {
+  TERRA_OK = 0,
+  TERRA_ERR_INVALID = 1,      /* geometry rule broken, null pointer, bad dtype value */
+  TERRA_ERR_UNSUPPORTED = 2,  /* valid but outside what the kernels handle          */
+  TERRA_ERR_WORKSPACE = 3,    /* workspace missing or smaller than required         */
+  TERRA_ERR_HIP = 4           /* the HIP runtime reported an error                  */
+};
+
+#define TERRA_MASK_LAT 1
+#define TERRA_MASK_LON 2
+
+/* Library version, major*10000 + minor*100 + patch. */
+int terra_version(void);
+
+/* Checks the geometry rules above (host only, no device call).  Returns
+ * TERRA_OK, TERRA_ERR_INVALID, or TERRA_ERR_UNSUPPORTED when the attention
+ * kernels cannot take it (head_dim not 32 or 64, more than 8192 bias bins
+ * per head, more than 2^31 elements per tensor).  Routing accepts any
+ * geometry that is valid. */
+int terra_validate_geometry(const terra_geom* g);
+
+/* Window grid size Mh = ceil(H/wh), Mw = ceil(W/ww) (Eq. (2), with ragged
+ * edges).  Host pointers. */
+int terra_window_count(const terra_geom* g, int32_t* Mh, int32_t* Mw);
+
+/* Window-major layout of ONE image (Sec. IV-D / Sec. V-A): for window
+ * w = i*Mw + j, offsets[w] is its first token slot and counts[w] its token
+ * count rows_i * cols_j; offsets[Mh*Mw] = H*W.  Host arrays of Mh*Mw+1 and
+ * Mh*Mw int32 entries owned by the caller.  Image b's slots start at b*H*W. */
+int terra_window_layout(const terra_geom* g, int32_t* offsets, int32_t* counts);
+
+/* Token route, NHWC -> window-major (Sec. IV-D: the route gathers every
+ * token into its window-major slot after the window shift).  Bit copy of
+ * B*H*W*C elements of `dtype`; x_nhwc and y_win must not overlap. */
+int terra_window_route(const terra_geom* g, int dtype, const void* x_nhwc,
+                       void* y_win, void* stream);
+
+/* Inverse token route, window-major -> NHWC: the exact inverse scatter of
+ * terra_window_route, and also its adjoint (the backward of the route is the
+ * inverse route, Sec. IV-D). */
+int terra_window_unroute(const terra_geom* g, int dtype, const void* y_win,
+                         void* x_nhwc, void* stream);
+
+/* Shifted-window attention forward (Sec. IV-A, W-MSA / SW-MSA).  For every
+ * image, window and head: S = Q K^T / sqrt(head_dim) + bias, masked pairs
+ * excluded, P = softmax(S), O = P V, LSE = ln sum exp S (natural log).
+ * q, k, v, o: window-major, `dtype`; bias_table: float32 table;
+ * lse: float32 B x heads x (H*W).  o and lse are overwritten. */
+int terra_winattn_fwd(const terra_geom* g, int dtype, const void* q,
+                      const void* k, const void* v, const float* bias_table,
+                      void* o, float* lse, void* stream);
+
+/* Bytes of device workspace terra_winattn_bwd needs for this geometry
+ * (0 on invalid input). */
+size_t terra_winattn_bwd_workspace_bytes(const terra_geom* g, int dtype);
+
+/* Shifted-window attention backward.  Inputs are the forward's inputs, its
+ * outputs o and lse, and the upstream gradient dout (window-major).
+ * Outputs dq, dk, dv (window-major, `dtype`) and dbias_table (float32,
+ * table shape, summed over images, windows and allowed pairs) are
+ * OVERWRITTEN.  dS = P * (dP - D) where D_q = sum_k P[q,k] dP[q,k] is
+ * recomputed inside each window in float32 (it equals <dO_q, O_q> for the
+ * unrounded O; `o` is accepted for symmetry with the forward and is not
+ * read, because a bf16-rounded O would bias the bias-table gradient).  The
+ * bias-table gradient is reduced in a fixed order, so results are
+ * bit-reproducible.
+ * workspace: device buffer of at least terra_winattn_bwd_workspace_bytes. */
+int terra_winattn_bwd(const terra_geom* g, int dtype, const void* q,
+                      const void* k, const void* v, const void* o,
+                      const void* dout, const float* lse,
+                      const float* bias_table, void* dq, void* dk, void* dv,
+                      float* dbias_table, void* workspace,
+                      size_t workspace_bytes, void* stream);
+
+/* Static string naming a status code. */
+const char* terra_status_string(int status);
+
+/* Message of the last failed call on the calling thread ("" if none). */
+const char* terra_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TERRA_SWIN_H */

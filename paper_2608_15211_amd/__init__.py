@@ -1,0 +1,219 @@
+"""Python binding of libterra_swin.so, the gfx950 shifted-window attention
+library (C ABI in include/terra_swin.h).
+
+Argument marshalling only: every step of the path runs in the HIP kernels of
+the library.  Tensors are torch tensors used as device memory; the current
+torch stream is passed as the HIP stream.  If the library has not been built
+the functions raise; there is no fallback.
+
+Entry points (same names as the C ABI):
+    terra_validate_geometry, terra_window_count, terra_window_layout,
+    terra_window_route, terra_window_unroute, terra_winattn_fwd,
+    terra_winattn_bwd_workspace_bytes, terra_winattn_bwd
+"""
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libterra_swin.so")
+
+TERRA_F32 = 0
+TERRA_BF16 = 1
+TERRA_MASK_LAT = 1
+TERRA_MASK_LON = 2
+STATUS = {0: "TERRA_OK", 1: "TERRA_ERR_INVALID", 2: "TERRA_ERR_UNSUPPORTED",
+          3: "TERRA_ERR_WORKSPACE", 4: "TERRA_ERR_HIP"}
+
+
+class TerraError(RuntimeError):
+    def __init__(self, status, message):
+        super().__init__("%s: %s" % (STATUS.get(status, status), message))
+        self.status = status
+
+
+class terra_geom(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in
+                ("B", "H", "W", "C", "heads", "head_dim", "wh", "ww", "sh", "sw", "mask_flags")]
+
+    @classmethod
+    def make(cls, B, H, W, C, heads, head_dim, wh, ww, sh, sw, mask_flags=TERRA_MASK_LAT):
+        return cls(B, H, W, C, heads, head_dim, wh, ww, sh, sw, mask_flags)
+
+    def as_dict(self):
+        return {n: getattr(self, n) for n, _ in self._fields_}
+
+
+_lib = None
+
+
+def lib():
+    """The loaded shared library; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError("libterra_swin.so is not built (%s); run __graft_entry__.build() "
+                           "or python paper_2608_15211_amd/build.py" % LIB_PATH)
+    L = ctypes.CDLL(LIB_PATH)
+    G = ctypes.POINTER(terra_geom)
+    vp, i32, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
+    L.terra_version.restype = i32
+    L.terra_validate_geometry.argtypes = [G]
+    L.terra_window_count.argtypes = [G, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32)]
+    L.terra_window_layout.argtypes = [G, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32)]
+    L.terra_window_route.argtypes = [G, i32, vp, vp, vp]
+    L.terra_window_unroute.argtypes = [G, i32, vp, vp, vp]
+    L.terra_winattn_fwd.argtypes = [G, i32, vp, vp, vp, vp, vp, vp, vp]
+    L.terra_winattn_bwd_workspace_bytes.argtypes = [G, i32]
+    L.terra_winattn_bwd_workspace_bytes.restype = sz
+    L.terra_winattn_bwd.argtypes = [G, i32] + [vp] * 12 + [sz, vp]
+    L.terra_status_string.argtypes = [i32]
+    L.terra_status_string.restype = ctypes.c_char_p
+    L.terra_last_error.restype = ctypes.c_char_p
+    for name in ("terra_validate_geometry", "terra_window_count", "terra_window_layout",
+                 "terra_window_route", "terra_window_unroute", "terra_winattn_fwd",
+                 "terra_winattn_bwd"):
+        getattr(L, name).restype = i32
+    _lib = L
+    return L
+
+
+def _check(status):
+    if status != 0:
+        raise TerraError(status, lib().terra_last_error().decode())
+
+
+def _geom(g):
+    if isinstance(g, terra_geom):
+        return g
+    if isinstance(g, dict):
+        return terra_geom.make(**g)
+    return terra_geom.make(**g.geom_kwargs())
+
+
+# ---------------------------------------------------------------- host-only
+def terra_validate_geometry(g):
+    """Raises TerraError if the geometry is invalid or unsupported."""
+    _check(lib().terra_validate_geometry(ctypes.byref(_geom(g))))
+
+
+def terra_window_count(g):
+    mh, mw = ctypes.c_int32(), ctypes.c_int32()
+    _check(lib().terra_window_count(ctypes.byref(_geom(g)), ctypes.byref(mh), ctypes.byref(mw)))
+    return mh.value, mw.value
+
+
+def terra_window_layout(g):
+    """(offsets[Mh*Mw+1], counts[Mh*Mw]) of one image, as Python lists."""
+    mh, mw = terra_window_count(g)
+    off = (ctypes.c_int32 * (mh * mw + 1))()
+    cnt = (ctypes.c_int32 * (mh * mw))()
+    _check(lib().terra_window_layout(ctypes.byref(_geom(g)), off, cnt))
+    return list(off), list(cnt)
+
+
+def terra_winattn_bwd_workspace_bytes(g, dtype):
+    return int(lib().terra_winattn_bwd_workspace_bytes(ctypes.byref(_geom(g)), _dtype_code(dtype)))
+
+
+# ---------------------------------------------------------------- device calls
+def _dtype_code(dtype):
+    if isinstance(dtype, int):
+        return dtype
+    import torch
+    if dtype in (torch.float32, "f32"):
+        return TERRA_F32
+    if dtype in (torch.bfloat16, "bf16"):
+        return TERRA_BF16
+    raise TypeError("unsupported dtype %r" % (dtype,))
+
+
+def _stream():
+    import torch
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _dev(t, name, dtype=None, numel=None):
+    if not t.is_cuda:
+        raise ValueError("%s must be a device tensor" % name)
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError("%s has dtype %s, expected %s" % (name, t.dtype, dtype))
+    if numel is not None and t.numel() != numel:
+        raise ValueError("%s has %d elements, expected %d" % (name, t.numel(), numel))
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _sizes(gg):
+    return gg.B * gg.H * gg.W * gg.C, gg.B * gg.heads * gg.H * gg.W, \
+        (2 * gg.wh - 1) * (2 * gg.ww - 1) * gg.heads
+
+
+def terra_window_route(x_nhwc, g, out=None):
+    """NHWC (B,H,W,C) -> window-major (B,H*W,C), same dtype."""
+    import torch
+    gg = _geom(g)
+    n, _, _ = _sizes(gg)
+    if out is None:
+        out = torch.empty((gg.B, gg.H * gg.W, gg.C), dtype=x_nhwc.dtype, device=x_nhwc.device)
+    _check(lib().terra_window_route(ctypes.byref(gg), _dtype_code(x_nhwc.dtype),
+                                    _dev(x_nhwc, "x", None, n), _dev(out, "out", x_nhwc.dtype, n),
+                                    _stream()))
+    return out
+
+
+def terra_window_unroute(y_win, g, out=None):
+    """window-major (B,H*W,C) -> NHWC (B,H,W,C), same dtype."""
+    import torch
+    gg = _geom(g)
+    n, _, _ = _sizes(gg)
+    if out is None:
+        out = torch.empty((gg.B, gg.H, gg.W, gg.C), dtype=y_win.dtype, device=y_win.device)
+    _check(lib().terra_window_unroute(ctypes.byref(gg), _dtype_code(y_win.dtype),
+                                      _dev(y_win, "y", None, n), _dev(out, "out", y_win.dtype, n),
+                                      _stream()))
+    return out
+
+
+def terra_winattn_fwd(q, k, v, table, g, out=None, lse=None):
+    """Window-major q, k, v (B,H*W,C) and float32 bias table
+    (2wh-1,2ww-1,heads) -> (O (B,H*W,C), LSE float32 (B,heads,H*W))."""
+    import torch
+    gg = _geom(g)
+    n, nl, nt = _sizes(gg)
+    dt = q.dtype
+    if out is None:
+        out = torch.empty((gg.B, gg.H * gg.W, gg.C), dtype=dt, device=q.device)
+    if lse is None:
+        lse = torch.empty((gg.B, gg.heads, gg.H * gg.W), dtype=torch.float32, device=q.device)
+    _check(lib().terra_winattn_fwd(
+        ctypes.byref(gg), _dtype_code(dt), _dev(q, "q", dt, n), _dev(k, "k", dt, n),
+        _dev(v, "v", dt, n), _dev(table, "table", torch.float32, nt), _dev(out, "o", dt, n),
+        _dev(lse, "lse", torch.float32, nl), _stream()))
+    return out, lse
+
+
+def terra_winattn_bwd(q, k, v, o, dout, lse, table, g, out=None, workspace=None):
+    """Returns (dQ, dK, dV, dTable).  `out` may hold preallocated
+    (dq, dk, dv, dtable); `workspace` a uint8 device tensor."""
+    import torch
+    gg = _geom(g)
+    n, nl, nt = _sizes(gg)
+    dt = q.dtype
+    code = _dtype_code(dt)
+    if out is None:
+        out = (torch.empty_like(q), torch.empty_like(q), torch.empty_like(q),
+               torch.empty(table.shape, dtype=torch.float32, device=q.device))
+    dq, dk, dv, dtab = out
+    need = terra_winattn_bwd_workspace_bytes(gg, code)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
+    _check(lib().terra_winattn_bwd(
+        ctypes.byref(gg), code, _dev(q, "q", dt, n), _dev(k, "k", dt, n), _dev(v, "v", dt, n),
+        _dev(o, "o", dt, n), _dev(dout, "dout", dt, n), _dev(lse, "lse", torch.float32, nl),
+        _dev(table, "table", torch.float32, nt), _dev(dq, "dq", dt, n), _dev(dk, "dk", dt, n),
+        _dev(dv, "dv", dt, n), _dev(dtab, "dtable", torch.float32, nt),
+        _dev(workspace, "workspace"), ctypes.c_size_t(workspace.numel()), _stream()))
+    return dq, dk, dv, dtab

@@ -1,0 +1,234 @@
+// abi.hip - C ABI of the shifted-window attention library (declared in
+// include/terra_swin.h): host-side argument checks, geometry set-up and
+// dispatch to the gfx950 kernels.  No allocation, no synchronisation.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string>
+
+#include "terra_common.h"
+#include "../../include/terra_swin.h"
+
+namespace terra {
+hipError_t launch_route(const Geo& g, int row_bytes, const void* src, void* dst, bool forward,
+                        hipStream_t stream);
+hipError_t launch_attn_fwd(const Geo& g, bool bf16, const void* q, const void* k, const void* v,
+                           const float* table, void* o, float* lse, hipStream_t st);
+hipError_t launch_attn_bwd(const Geo& g, bool bf16, const void* q, const void* k, const void* v,
+                           const void* o, const void* dout, const float* lse, const float* table,
+                           void* dq, void* dk, void* dv, float* dtab, void* ws, hipStream_t st);
+size_t bwd_workspace(const Geo& g);
+size_t attn_max_lds(const Geo& g, bool bf16);
+}  // namespace terra
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int status, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int status, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return status;
+}
+
+int ok() {
+  g_last_error.clear();
+  return TERRA_OK;
+}
+
+int hip_status(hipError_t e, const char* what) {
+  if (e != hipSuccess) return fail(TERRA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+  return ok();
+}
+
+constexpr int64_t kMaxElems = (int64_t)1 << 31;   // per tensor, attention kernels
+constexpr int kMaxBins = 8192;                    // bias bins per head
+constexpr size_t kMaxLds = 64 * 1024;             // dynamic LDS per workgroup
+
+// Geometry rules shared by every entry point.
+int check_geom(const terra_geom* g) {
+  if (!g) return fail(TERRA_ERR_INVALID, "geometry pointer is NULL");
+  if (g->B < 1 || g->H < 1 || g->W < 1 || g->C < 1 || g->heads < 1 || g->head_dim < 1)
+    return fail(TERRA_ERR_INVALID, "B, H, W, C, heads and head_dim must be >= 1");
+  if ((int64_t)g->heads * g->head_dim != g->C)
+    return fail(TERRA_ERR_INVALID, "C (%d) != heads (%d) * head_dim (%d)", g->C, g->heads,
+                g->head_dim);
+  if (g->wh < 1 || g->wh > g->H || g->ww < 1 || g->ww > g->W)
+    return fail(TERRA_ERR_INVALID, "window %dx%d must satisfy 1 <= wh <= H (%d), 1 <= ww <= W (%d)",
+                g->wh, g->ww, g->H, g->W);
+  if (g->sh < 0 || g->sh >= g->wh || g->sw < 0 || g->sw >= g->ww)
+    return fail(TERRA_ERR_INVALID, "shift (%d,%d) must satisfy 0 <= sh < wh, 0 <= sw < ww", g->sh,
+                g->sw);
+  if (g->mask_flags < 0 || g->mask_flags > 3)
+    return fail(TERRA_ERR_INVALID, "mask_flags %d has bits other than 0 and 1", g->mask_flags);
+  if ((int64_t)g->B * g->H * g->W >= ((int64_t)1 << 31))
+    return fail(TERRA_ERR_UNSUPPORTED, "B*H*W must be below 2^31 tokens");
+  return ok();
+}
+
+int check_dtype(int dtype) {
+  if (dtype != TERRA_F32 && dtype != TERRA_BF16)
+    return fail(TERRA_ERR_INVALID, "dtype %d is neither TERRA_F32 nor TERRA_BF16", dtype);
+  return ok();
+}
+
+terra::Geo make_geo(const terra_geom* g) {
+  terra::Geo G;
+  G.B = g->B; G.H = g->H; G.W = g->W; G.C = g->C; G.heads = g->heads; G.hd = g->head_dim;
+  G.wh = g->wh; G.ww = g->ww; G.sh = g->sh; G.sw = g->sw; G.flags = g->mask_flags;
+  G.Mh = (g->H + g->wh - 1) / g->wh;
+  G.Mw = (g->W + g->ww - 1) / g->ww;
+  G.nwin = G.Mh * G.Mw;
+  G.HW = g->H * g->W;
+  G.bstride = 2 * g->ww - 1;
+  G.nbins = (2 * g->wh - 1) * G.bstride;
+  return G;
+}
+
+// Attention-specific limits.
+int check_attn(const terra_geom* g, int dtype) {
+  int s = check_geom(g);
+  if (s) return s;
+  if ((s = check_dtype(dtype))) return s;
+  if (g->head_dim != 32 && g->head_dim != 64)
+    return fail(TERRA_ERR_UNSUPPORTED, "head_dim %d: the attention kernels take 32 or 64",
+                g->head_dim);
+  if ((int64_t)g->B * g->H * g->W * g->C >= kMaxElems)
+    return fail(TERRA_ERR_UNSUPPORTED, "tensors above 2^31 elements are not supported");
+  terra::Geo G = make_geo(g);
+  if (G.nbins > kMaxBins)
+    return fail(TERRA_ERR_UNSUPPORTED, "(2wh-1)(2ww-1) = %d bias bins exceeds %d", G.nbins,
+                kMaxBins);
+  if (terra::attn_max_lds(G, dtype == TERRA_BF16) > kMaxLds)
+    return fail(TERRA_ERR_UNSUPPORTED, "window needs more LDS than one workgroup has");
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+int terra_version(void) { return 100; }
+
+int terra_validate_geometry(const terra_geom* g) {
+  int s = check_geom(g);
+  if (s) return s;
+  if (g->head_dim != 32 && g->head_dim != 64)
+    return fail(TERRA_ERR_UNSUPPORTED, "head_dim %d: the attention kernels take 32 or 64",
+                g->head_dim);
+  terra::Geo G = make_geo(g);
+  if (G.nbins > kMaxBins)
+    return fail(TERRA_ERR_UNSUPPORTED, "(2wh-1)(2ww-1) = %d bias bins exceeds %d", G.nbins,
+                kMaxBins);
+  if ((int64_t)g->B * g->H * g->W * g->C >= kMaxElems)
+    return fail(TERRA_ERR_UNSUPPORTED, "tensors above 2^31 elements are not supported");
+  return ok();
+}
+
+int terra_window_count(const terra_geom* g, int32_t* Mh, int32_t* Mw) {
+  int s = check_geom(g);
+  if (s) return s;
+  if (!Mh || !Mw) return fail(TERRA_ERR_INVALID, "output pointer is NULL");
+  terra::Geo G = make_geo(g);
+  *Mh = G.Mh;
+  *Mw = G.Mw;
+  return ok();
+}
+
+int terra_window_layout(const terra_geom* g, int32_t* offsets, int32_t* counts) {
+  int s = check_geom(g);
+  if (s) return s;
+  if (!offsets || !counts) return fail(TERRA_ERR_INVALID, "output pointer is NULL");
+  terra::Geo G = make_geo(g);
+  for (int i = 0; i < G.Mh; ++i)
+    for (int j = 0; j < G.Mw; ++j) {
+      const int w = i * G.Mw + j;
+      offsets[w] = terra::win_offset(G, i, j);
+      counts[w] = terra::win_rows(G, i) * terra::win_cols(G, j);
+    }
+  offsets[G.nwin] = G.HW;
+  return ok();
+}
+
+static int route_common(const terra_geom* g, int dtype, const void* src, void* dst, bool forward,
+                        void* stream) {
+  int s = check_geom(g);
+  if (s) return s;
+  if ((s = check_dtype(dtype))) return s;
+  if (!src || !dst) return fail(TERRA_ERR_INVALID, "tensor pointer is NULL");
+  if (src == dst) return fail(TERRA_ERR_INVALID, "route source and destination must differ");
+  const int esize = dtype == TERRA_BF16 ? 2 : 4;
+  const int64_t row_bytes = (int64_t)g->C * esize;
+  // The per-window chunk index must stay below 2^22 (worst case 2-byte chunks).
+  if ((int64_t)g->wh * g->ww * (row_bytes / 2) >= ((int64_t)1 << 22))
+    return fail(TERRA_ERR_UNSUPPORTED, "window of %d tokens x %lld bytes is too large to route",
+                g->wh * g->ww, (long long)row_bytes);
+  terra::Geo G = make_geo(g);
+  return hip_status(terra::launch_route(G, (int)row_bytes, src, dst, forward, (hipStream_t)stream),
+                    forward ? "terra_window_route launch" : "terra_window_unroute launch");
+}
+
+int terra_window_route(const terra_geom* g, int dtype, const void* x_nhwc, void* y_win,
+                       void* stream) {
+  return route_common(g, dtype, x_nhwc, y_win, true, stream);
+}
+
+int terra_window_unroute(const terra_geom* g, int dtype, const void* y_win, void* x_nhwc,
+                         void* stream) {
+  return route_common(g, dtype, y_win, x_nhwc, false, stream);
+}
+
+int terra_winattn_fwd(const terra_geom* g, int dtype, const void* q, const void* k, const void* v,
+                      const float* bias_table, void* o, float* lse, void* stream) {
+  int s = check_attn(g, dtype);
+  if (s) return s;
+  if (!q || !k || !v || !bias_table || !o || !lse)
+    return fail(TERRA_ERR_INVALID, "tensor pointer is NULL");
+  terra::Geo G = make_geo(g);
+  return hip_status(terra::launch_attn_fwd(G, dtype == TERRA_BF16, q, k, v, bias_table, o, lse,
+                                           (hipStream_t)stream),
+                    "terra_winattn_fwd launch");
+}
+
+size_t terra_winattn_bwd_workspace_bytes(const terra_geom* g, int dtype) {
+  if (check_attn(g, dtype)) return 0;
+  return terra::bwd_workspace(make_geo(g));
+}
+
+int terra_winattn_bwd(const terra_geom* g, int dtype, const void* q, const void* k, const void* v,
+                      const void* o, const void* dout, const float* lse, const float* bias_table,
+                      void* dq, void* dk, void* dv, float* dbias_table, void* workspace,
+                      size_t workspace_bytes, void* stream) {
+  int s = check_attn(g, dtype);
+  if (s) return s;
+  if (!q || !k || !v || !o || !dout || !lse || !bias_table || !dq || !dk || !dv || !dbias_table)
+    return fail(TERRA_ERR_INVALID, "tensor pointer is NULL");
+  terra::Geo G = make_geo(g);
+  const size_t need = terra::bwd_workspace(G);
+  if (!workspace || workspace_bytes < need)
+    return fail(TERRA_ERR_WORKSPACE, "workspace of %zu bytes given, %zu needed",
+                workspace ? workspace_bytes : (size_t)0, need);
+  return hip_status(terra::launch_attn_bwd(G, dtype == TERRA_BF16, q, k, v, o, dout, lse,
+                                           bias_table, dq, dk, dv, dbias_table, workspace,
+                                           (hipStream_t)stream),
+                    "terra_winattn_bwd launch");
+}
+
+const char* terra_status_string(int status) {
+  switch (status) {
+    case TERRA_OK: return "ok";
+    case TERRA_ERR_INVALID: return "invalid argument";
+    case TERRA_ERR_UNSUPPORTED: return "unsupported";
+    case TERRA_ERR_WORKSPACE: return "workspace too small";
+    case TERRA_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+const char* terra_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,132 @@
+// route.hip - token route between the NHWC layout and the window-major
+// layout, and its inverse (Sec. IV-D: the route gathers each token into its
+// window-major slot after the window shift; the inverse route scatters it
+// back and is the route's backward).
+//
+// Pure HBM streaming: every token row (C elements) moves once in each
+// direction.  A workgroup copies a contiguous part of one window; inside a
+// window, the tokens of one window row come from a contiguous run of the
+// source row (two runs where the run crosses the longitude edge), so loads
+// and stores are wide (16 B per lane) and coalesced.
+#include "terra_common.h"
+
+namespace terra {
+
+template <int VEC> struct VecT;
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+template <> struct VecT<16> { typedef u32x4_t type; };
+template <> struct VecT<8> { typedef u32x2_t type; };
+template <> struct VecT<4> { typedef uint32_t type; };
+template <> struct VecT<2> { typedef uint16_t type; };
+
+struct RouteArgs {
+  Geo g;
+  int cpr;          // VEC-sized chunks per token row
+  float rcp_cpr;
+  int split;        // workgroups per window
+};
+
+constexpr int kRouteThreads = 256;
+constexpr int kRouteUnroll = 4;
+
+// FORWARD=true: NHWC -> window-major.  FORWARD=false: window-major -> NHWC.
+template <int VEC, bool FORWARD>
+__global__ __launch_bounds__(kRouteThreads) void route_kernel(
+    const typename VecT<VEC>::type* __restrict__ src,
+    typename VecT<VEC>::type* __restrict__ dst, RouteArgs A) {
+  typedef typename VecT<VEC>::type V;
+  const Geo& g = A.g;
+  const int wid = blockIdx.x / A.split;
+  const int part = blockIdx.x - wid * A.split;
+  const int b = wid / g.nwin;
+  const int w = wid - b * g.nwin;
+  const int i = w / g.Mw;
+  const int j = w - i * g.Mw;
+  const int rows = win_rows(g, i);
+  const int cols = win_cols(g, j);
+  const int off = win_offset(g, i, j);
+  const float rcp_cols = 1.0f / (float)cols;
+  const int nchunk = rows * cols * A.cpr;
+  const int step = kRouteThreads * kRouteUnroll;
+  const int per = ((nchunk + A.split - 1) / A.split + step - 1) / step * step;
+  const int start = part * per;
+  const int end = min(nchunk, start + per);
+  const int64_t img_base = (int64_t)b * g.HW;
+
+  for (int k0 = start + threadIdx.x; k0 < end; k0 += step) {
+    V val[kRouteUnroll];
+    int64_t nhwc[kRouteUnroll], win[kRouteUnroll];
+#pragma unroll
+    for (int u = 0; u < kRouteUnroll; ++u) {
+      const int k = k0 + u * kRouteThreads;
+      const int t = fast_div(k, A.cpr, A.rcp_cpr);      // token within window
+      const int ch = k - t * A.cpr;
+      const int a = fast_div(t, cols, rcp_cols);          // in-window row
+      const int c = t - a * cols;                         // in-window column
+      int r = i * g.wh + a + g.sh;                        // original row
+      if (r >= g.H) r -= g.H;
+      int s = j * g.ww + c + g.sw;                        // original column
+      if (s >= g.W) s -= g.W;
+      nhwc[u] = ((img_base + (int64_t)r * g.W + s) * A.cpr) + ch;
+      win[u] = ((img_base + off + t) * (int64_t)A.cpr) + ch;
+      if (k < end) {
+        val[u] = FORWARD ? __builtin_nontemporal_load(src + nhwc[u])
+                         : __builtin_nontemporal_load(src + win[u]);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kRouteUnroll; ++u) {
+      const int k = k0 + u * kRouteThreads;
+      if (k < end) {
+        if (FORWARD) __builtin_nontemporal_store(val[u], dst + win[u]);
+        else __builtin_nontemporal_store(val[u], dst + nhwc[u]);
+      }
+    }
+  }
+}
+
+template <int VEC>
+static hipError_t launch_route_vec(const RouteArgs& A, const void* src, void* dst,
+                                   bool forward, hipStream_t stream) {
+  typedef typename VecT<VEC>::type V;
+  const int grid = A.g.B * A.g.nwin * A.split;
+  if (forward)
+    hipLaunchKernelGGL((route_kernel<VEC, true>), dim3(grid), dim3(kRouteThreads), 0, stream,
+                       (const V*)src, (V*)dst, A);
+  else
+    hipLaunchKernelGGL((route_kernel<VEC, false>), dim3(grid), dim3(kRouteThreads), 0, stream,
+                       (const V*)src, (V*)dst, A);
+  return hipGetLastError();
+}
+
+// Host entry used by the C ABI.  row_bytes = C * element size.
+hipError_t launch_route(const Geo& g, int row_bytes, const void* src, void* dst,
+                        bool forward, hipStream_t stream) {
+  RouteArgs A;
+  A.g = g;
+  int vec = 2;
+  if (row_bytes % 16 == 0 && ((uintptr_t)src % 16 == 0) && ((uintptr_t)dst % 16 == 0)) vec = 16;
+  else if (row_bytes % 8 == 0 && ((uintptr_t)src % 8 == 0) && ((uintptr_t)dst % 8 == 0)) vec = 8;
+  else if (row_bytes % 4 == 0 && ((uintptr_t)src % 4 == 0) && ((uintptr_t)dst % 4 == 0)) vec = 4;
+  A.cpr = row_bytes / vec;
+  A.rcp_cpr = 1.0f / (float)A.cpr;
+  // Enough workgroups to keep every CU streaming: aim for ~4096 in total,
+  // each with at least one full unrolled sweep of work.
+  const int64_t chunks_per_win = (int64_t)g.wh * g.ww * A.cpr;
+  const int64_t nwin_total = (int64_t)g.B * g.nwin;
+  int split = (int)((4096 + nwin_total - 1) / nwin_total);
+  const int64_t max_split = (chunks_per_win + kRouteThreads * kRouteUnroll - 1) /
+                            (kRouteThreads * kRouteUnroll);
+  if (split > max_split) split = (int)max_split;
+  if (split < 1) split = 1;
+  A.split = split;
+  switch (vec) {
+    case 16: return launch_route_vec<16>(A, src, dst, forward, stream);
+    case 8: return launch_route_vec<8>(A, src, dst, forward, stream);
+    case 4: return launch_route_vec<4>(A, src, dst, forward, stream);
+    default: return launch_route_vec<2>(A, src, dst, forward, stream);
+  }
+}
+
+}  // namespace terra

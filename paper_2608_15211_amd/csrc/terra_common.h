@@ -1,0 +1,108 @@
+// terra_common.h - device-side helpers shared by the gfx950 kernels.
+//
+// Window geometry in closed form (Sec. IV-D, Eq. (2) generalised to a
+// wh x ww window, ragged last row/column, row-major window order of
+// Sec. V-A), the packed kernel argument block, and thin wrappers around the
+// CDNA4 matrix-core instructions used by the attention kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace terra {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned short u16x4 __attribute__((ext_vector_type(4)));
+typedef unsigned short u16x8 __attribute__((ext_vector_type(8)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+// Everything a kernel needs to know about the grid, passed by value.
+struct Geo {
+  int B, H, W, C, heads, hd;
+  int wh, ww, sh, sw, flags;
+  int Mh, Mw, nwin;   // window grid; nwin = Mh * Mw per image
+  int HW;
+  int nbins;          // (2wh-1)(2ww-1)
+  int bstride;        // 2ww-1
+};
+
+// Extent of window row i / column j (partial at the far edge).
+__device__ __host__ inline int win_rows(const Geo& g, int i) {
+  int r = g.H - i * g.wh;
+  return r < g.wh ? r : g.wh;
+}
+__device__ __host__ inline int win_cols(const Geo& g, int j) {
+  int c = g.W - j * g.ww;
+  return c < g.ww ? c : g.ww;
+}
+// First window-major slot of window (i, j) within its image: all window rows
+// above i are full (wh rows each), and the windows to the left in row i hold
+// rows_i * ww tokens each.
+__device__ __host__ inline int win_offset(const Geo& g, int i, int j) {
+  return i * g.wh * g.W + win_rows(g, i) * j * g.ww;
+}
+// Wrap labels of rolled row r / rolled column s (bit 0 latitude, bit 1 longitude).
+__device__ __host__ inline int row_label(const Geo& g, int r) {
+  return ((g.flags & 1) && g.sh > 0 && r >= g.H - g.sh) ? 1 : 0;
+}
+__device__ __host__ inline int col_label(const Geo& g, int s) {
+  return ((g.flags & 2) && g.sw > 0 && s >= g.W - g.sw) ? 2 : 0;
+}
+
+// n / d for 0 <= n < 2^22, 1 <= d < 2^16, via a float reciprocal and one
+// correction step each way.
+__device__ inline int fast_div(int n, int d, float rcp) {
+  int q = (int)((float)n * rcp);
+  int r = n - q * d;
+  if (r < 0) { q -= 1; }
+  else if (r >= d) { q += 1; }
+  return q;
+}
+
+// ---------------------------------------------------------------------------
+// Matrix-core tiles.  One MFMA "operand" is 8 consecutive contraction-dim
+// elements per lane: lane l supplies row/column (l % 32) and contraction
+// slots 8*(l/32) .. 8*(l/32)+7 of a 16-deep chunk.  The 32x32 float result
+// D[m][n] sits in lane n + 32*((m/4)%2), register (m%4) + 4*(m/8).
+// ---------------------------------------------------------------------------
+template <typename T> struct Operand;
+template <> struct Operand<__bf16> { typedef bf16x8 type; };
+template <> struct Operand<float> { typedef f32x8 type; };
+
+__device__ inline void mma16(f32x16& acc, const bf16x8& a, const bf16x8& b) {
+  acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc, 0, 0, 0);
+}
+// fp32: eight 32x32x2 steps; step i contracts slot i of both lane halves, so
+// the slot numbering matches the bf16 instruction exactly.
+__device__ inline void mma16(f32x16& acc, const f32x8& a, const f32x8& b) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i], b[i], acc, 0, 0, 0);
+}
+
+// Result-register index -> row m within the 32x32 tile, for lane half h.
+__device__ __host__ constexpr int acc_row(int r, int h) { return 8 * (r / 4) + 4 * h + (r % 4); }
+
+template <typename T> __device__ inline T from_float(float x);
+template <> __device__ inline float from_float<float>(float x) { return x; }
+template <> __device__ inline __bf16 from_float<__bf16>(float x) { return (__bf16)x; }
+
+template <typename T> __device__ inline float to_float(T x);
+template <> __device__ inline float to_float<float>(float x) { return x; }
+template <> __device__ inline float to_float<__bf16>(__bf16 x) { return (float)x; }
+
+// Pack result registers r0..r0+7 (as float) into an operand.
+template <typename T>
+__device__ inline typename Operand<T>::type pack8(const f32x16& acc, int r0) {
+  typename Operand<T>::type o;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) o[i] = from_float<T>(acc[r0 + i]);
+  return o;
+}
+
+}  // namespace terra

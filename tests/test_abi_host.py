@@ -1,0 +1,117 @@
+"""Host-side checks of the C-ABI library (no GPU needed).
+
+The library must load, export every function declared in include/*.h, and
+reject bad arguments with the documented status codes before any device
+work.  Window counts and layouts from the library are compared with closed
+forms and with the oracle's enumeration.
+"""
+
+import ctypes
+import glob
+import os
+import re
+
+import pytest
+
+import terra_synth as ts
+from oracle import Geometry
+from oracle.geometry import window_slots
+
+P = pytest.importorskip("paper_2608_15211_amd")
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _have_lib():
+    return os.path.exists(P.LIB_PATH)
+
+
+pytestmark = pytest.mark.skipif(not _have_lib(), reason="libterra_swin.so not built")
+
+
+def _declared_functions():
+    names = set()
+    for h in glob.glob(os.path.join(ROOT, "include", "*.h")):
+        text = open(h).read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        for m in re.finditer(r"\b(terra_[a-z0-9_]+)\s*\(", text):
+            names.add(m.group(1))
+    return sorted(names)
+
+
+def test_library_exports_every_declared_function():
+    names = _declared_functions()
+    assert len(names) >= 11
+    L = ctypes.CDLL(P.LIB_PATH)
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_version():
+    assert P.lib().terra_version() >= 100
+
+
+@pytest.mark.parametrize("name", ts.ORDER)
+def test_configs_validate(name):
+    P.terra_validate_geometry(ts.CONFIGS[name])
+
+
+BAD = [
+    (dict(C=63), 1),                          # C != heads * head_dim
+    (dict(wh=17), 1),                         # window taller than the grid
+    (dict(ww=0), 1),
+    (dict(sh=8), 1),                          # shift not below window
+    (dict(sw=-1), 1),
+    (dict(mask_flags=4), 1),
+    (dict(B=0), 1),
+    (dict(heads=1, head_dim=64, C=64, wh=16, ww=32), 0),
+    (dict(heads=4, head_dim=16, C=64), 2),    # head_dim outside {32, 64}
+]
+
+
+@pytest.mark.parametrize("change,status", BAD)
+def test_bad_geometry_is_rejected(change, status):
+    base = dict(B=1, H=16, W=32, C=64, heads=2, head_dim=32, wh=8, ww=8, sh=4, sw=4, mask_flags=1)
+    base.update(change)
+    g = P.terra_geom.make(**base)
+    if status == 0:
+        P.terra_validate_geometry(g)
+        return
+    with pytest.raises(P.TerraError) as e:
+        P.terra_validate_geometry(g)
+    assert e.value.status == status
+    assert P.lib().terra_last_error().decode() != ""
+
+
+def test_device_calls_reject_bad_arguments_before_launch():
+    L = P.lib()
+    g = P.terra_geom.make(1, 16, 32, 64, 2, 32, 8, 8, 4, 4, 1)
+    fake = ctypes.c_void_p(0x1000)
+    null = ctypes.c_void_p(0)
+    s = ctypes.c_void_p(0)
+    assert L.terra_window_route(ctypes.byref(g), 7, fake, fake, s) == 1       # bad dtype
+    assert L.terra_window_route(ctypes.byref(g), 1, null, fake, s) == 1       # NULL
+    assert L.terra_window_route(ctypes.byref(g), 1, fake, fake, s) == 1       # in place
+    assert L.terra_winattn_fwd(ctypes.byref(g), 1, fake, fake, null, fake, fake, fake, s) == 1
+    assert L.terra_winattn_fwd(None, 1, fake, fake, fake, fake, fake, fake, s) == 1
+    need = L.terra_winattn_bwd_workspace_bytes(ctypes.byref(g), 1)
+    assert need > 0
+    args = [fake] * 11
+    assert L.terra_winattn_bwd(ctypes.byref(g), 1, *args, fake, ctypes.c_size_t(need - 4), s) == 3
+    assert L.terra_winattn_bwd(ctypes.byref(g), 1, *args, null, ctypes.c_size_t(need), s) == 3
+    g2 = P.terra_geom.make(1, 16, 32, 48, 3, 16, 8, 8, 4, 4, 1)
+    assert L.terra_winattn_fwd(ctypes.byref(g2), 1, *([fake] * 6), s) == 2
+    assert L.terra_winattn_bwd_workspace_bytes(ctypes.byref(g2), 1) == 0
+    for code in range(5):
+        assert L.terra_status_string(code)
+
+
+@pytest.mark.parametrize("name", ts.ORDER)
+def test_window_layout_matches_oracle_enumeration(name):
+    cfg = ts.CONFIGS[name]
+    mh, mw = P.terra_window_count(cfg)
+    assert mh == -(-cfg.H // cfg.wh) and mw == -(-cfg.W // cfg.ww)
+    off, cnt = P.terra_window_layout(cfg)
+    slots = window_slots(Geometry(**cfg.geom_kwargs()))
+    assert [s for _, s, _ in slots] == off[:-1]
+    assert [n for _, _, n in slots] == cnt
+    assert off[-1] == cfg.H * cfg.W

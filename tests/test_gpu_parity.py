@@ -1,0 +1,227 @@
+"""GPU parity: the HIP path through the C ABI against the fp64 oracle.
+
+Routing must match bit for bit.  Attention must match within max abs 1e-5
+(fp32) or max abs 2e-2 and relative L2 5e-3 (bf16, fp32 accumulation), on O,
+LSE, dQ, dK, dV and the bias-table gradient.  Small configurations are
+compared everywhere; the two full-size ones on sampled windows (first, last,
+latitude-seam, partial-column and random windows) plus the whole bias-table
+gradient from stored oracle values.
+"""
+
+import os
+import sys
+
+import numpy as np
+import pytest
+
+import terra_synth as ts
+from oracle import Geometry, route as o_route, unroute as o_unroute
+from oracle import attn_fwd, attn_bwd, attn_fwd_windows, attn_bwd_windows
+from oracle.geometry import window_slots
+
+torch = pytest.importorskip("torch")
+P = pytest.importorskip("paper_2608_15211_amd")
+
+pytestmark = pytest.mark.gpu
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+SMALL = ["c1_f32_16x32_w8", "c2_bf16_128x256_w8", "c3_bf16_85x180_w12"]
+LARGE = ["c4_bf16_128x1080_w8x16", "c5_bf16_256x540_w24"]
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    P.lib()
+    yield
+    torch.cuda.synchronize()
+
+
+def _tdtype(cfg):
+    return torch.float32 if cfg.dtype == "f32" else torch.bfloat16
+
+
+def _dev(x, cfg):
+    return torch.from_numpy(np.ascontiguousarray(x)).to("cuda").to(_tdtype(cfg))
+
+
+def _host(t):
+    return t.float().cpu().numpy().astype(np.float64)
+
+
+def _bits(t):
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).cpu().numpy()
+    return t.view(torch.int32).cpu().numpy()
+
+
+def _assert_close(name, got, ref, cfg):
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    err = np.abs(got - ref).max()
+    if cfg.dtype == "f32":
+        assert err <= 1e-5, "%s max abs err %.3g > 1e-5" % (name, err)
+    else:
+        assert err <= 2e-2, "%s max abs err %.3g > 2e-2" % (name, err)
+        ref_norm = np.linalg.norm(ref)
+        if ref_norm > 1e-6:   # a relative error of an all-zero reference is meaningless
+            rel = np.linalg.norm(got - ref) / ref_norm
+            assert rel <= 5e-3, "%s rel L2 err %.3g > 5e-3" % (name, rel)
+
+
+# ------------------------------------------------------------------ routing
+@pytest.mark.parametrize("name", ts.ORDER)
+def test_route_bit_exact(name):
+    cfg = ts.CONFIGS[name]
+    g = Geometry(**cfg.geom_kwargs())
+    _say("route %s" % name)
+    width = 4 if cfg.dtype == "f32" else 2
+    pat = ts.token_pattern(cfg, width)
+    tdt = _tdtype(cfg)
+    idt = torch.int32 if width == 4 else torch.int16
+    x = torch.from_numpy(pat.view(np.int32 if width == 4 else np.int16)).to("cuda").view(tdt)
+    y = P.terra_window_route(x, cfg)
+    torch.cuda.synchronize()
+    expect = o_route(pat, g)
+    assert np.array_equal(y.view(idt).cpu().numpy().view(pat.dtype), expect)
+    back = P.terra_window_unroute(y, cfg)
+    torch.cuda.synchronize()
+    assert np.array_equal(back.view(idt).cpu().numpy().view(pat.dtype), pat)
+
+
+def test_route_f32_and_bf16_on_one_geometry():
+    # The same geometry routed as 4-byte and as 2-byte elements.
+    cfg32 = ts.small_config("r32", "f32", 2, 13, 10, 1, 32, 6, 4, 3, 1, 3)
+    cfg16 = ts.small_config("r16", "bf16", 2, 13, 10, 1, 32, 6, 4, 3, 1, 3)
+    for cfg, width in ((cfg32, 4), (cfg16, 2)):
+        g = Geometry(**cfg.geom_kwargs())
+        pat = ts.token_pattern(cfg, width)
+        idt = torch.int32 if width == 4 else torch.int16
+        x = torch.from_numpy(pat.view(np.int32 if width == 4 else np.int16)).to("cuda").view(_tdtype(cfg))
+        y = P.terra_window_route(x, cfg)
+        assert np.array_equal(y.view(idt).cpu().numpy().view(pat.dtype), o_route(pat, g))
+
+
+# ------------------------------------------------------------------ attention, small configs
+def _run_gpu(cfg, inp):
+    q, k, v, do = (P.terra_window_route(_dev(inp[n], cfg), cfg) for n in ("q", "k", "v", "dout"))
+    table = torch.from_numpy(inp["table"]).to("cuda")
+    o, lse = P.terra_winattn_fwd(q, k, v, table, cfg)
+    dq, dk, dv, dt = P.terra_winattn_bwd(q, k, v, o, do, lse, table, cfg)
+    torch.cuda.synchronize()
+    return dict(o=o, lse=lse, dq=dq, dk=dk, dv=dv, dt=dt)
+
+
+@pytest.mark.parametrize("name", SMALL)
+def test_attention_small_configs(name):
+    cfg = ts.CONFIGS[name]
+    g = Geometry(**cfg.geom_kwargs())
+    _say("attention %s" % name)
+    inp = ts.make_inputs(cfg)
+    got = _run_gpu(cfg, inp)
+    q, k, v, do = (o_route(inp[n], g) for n in ("q", "k", "v", "dout"))
+    o, lse = attn_fwd(q, k, v, inp["table"], g)
+    dq, dk, dv, dt = attn_bwd(q, k, v, do, inp["table"], g)
+    _assert_close("O", _host(got["o"]), o, cfg)
+    _assert_close("LSE", _host(got["lse"]), lse, cfg)
+    _assert_close("dQ", _host(got["dq"]), dq, cfg)
+    _assert_close("dK", _host(got["dk"]), dk, cfg)
+    _assert_close("dV", _host(got["dv"]), dv, cfg)
+    _assert_close("dT", _host(got["dt"]), dt, cfg)
+
+
+EDGE = [
+    # one window = the whole grid, no shift, fp32 and bf16
+    ("one_window_f32", ts.small_config("e1", "f32", 1, 8, 16, 2, 32, 8, 16, 0, 0)),
+    ("one_window_bf16", ts.small_config("e2", "bf16", 1, 8, 16, 2, 64, 8, 16, 0, 0)),
+    # 1-token-wide ragged edges in both directions and both wraps masked
+    ("ragged_both", ts.small_config("e3", "bf16", 2, 9, 17, 3, 32, 4, 4, 2, 3, 3)),
+    # windows larger than one 128-query chunk, ragged, hd 64
+    ("big_window", ts.small_config("e4", "bf16", 1, 30, 20, 2, 64, 15, 12, 7, 5, 1)),
+    ("big_window_f32", ts.small_config("e5", "f32", 1, 30, 20, 2, 64, 15, 12, 7, 5, 1)),
+    # no mask at all, 1x1 windows
+    ("unit_windows", ts.small_config("e6", "bf16", 1, 4, 6, 1, 32, 1, 1, 0, 0, 0)),
+    # periodic longitude only shift
+    ("lon_shift", ts.small_config("e7", "f32", 1, 8, 24, 1, 32, 8, 8, 0, 5, 1)),
+]
+
+
+@pytest.mark.parametrize("label,cfg", EDGE, ids=[e[0] for e in EDGE])
+def test_attention_edge_cases(label, cfg):
+    g = Geometry(**cfg.geom_kwargs())
+    _say("edge %s" % label)
+    inp = ts.make_inputs(cfg, seed=3)
+    got = _run_gpu(cfg, inp)
+    q, k, v, do = (o_route(inp[n], g) for n in ("q", "k", "v", "dout"))
+    o, lse = attn_fwd(q, k, v, inp["table"], g)
+    dq, dk, dv, dt = attn_bwd(q, k, v, do, inp["table"], g)
+    for nm, a, b in (("O", got["o"], o), ("LSE", got["lse"], lse), ("dQ", got["dq"], dq),
+                     ("dK", got["dk"], dk), ("dV", got["dv"], dv), ("dT", got["dt"], dt)):
+        _assert_close(nm, _host(a), b, cfg)
+
+
+def test_large_logits_stay_finite():
+    # Q scaled by 4 -> logits of several units; exercises the running max.
+    cfg = ts.CONFIGS["c2_bf16_128x256_w8"]
+    g = Geometry(**cfg.geom_kwargs())
+    inp = ts.make_inputs(cfg, seed=5, q_scale=4.0)
+    got = _run_gpu(cfg, inp)
+    sel = [0, 31, 480, 511]
+    q, k, v, do = (o_route(inp[n], g) for n in ("q", "k", "v", "dout"))
+    ref = attn_fwd_windows(q, k, v, inp["table"], g, sel)
+    slots = {w: (s, n) for w, s, n in window_slots(g)}
+    for w in sel:
+        s, n = slots[w]
+        _assert_close("O", _host(got["o"][:, s:s + n]), ref[w][0], cfg)
+        _assert_close("LSE", _host(got["lse"][:, :, s:s + n]), ref[w][1], cfg)
+
+
+def test_bias_gradient_is_bit_reproducible():
+    cfg = ts.CONFIGS["c3_bf16_85x180_w12"]
+    inp = ts.make_inputs(cfg)
+    a = _run_gpu(cfg, inp)["dt"].cpu().numpy()
+    b = _run_gpu(cfg, inp)["dt"].cpu().numpy()
+    assert np.array_equal(a.view(np.int32), b.view(np.int32))
+
+
+# ------------------------------------------------------------------ full-size configs
+def _sample_windows(cfg, g, seed=0):
+    mh, mw = -(-cfg.H // cfg.wh), -(-cfg.W // cfg.ww)
+    last = mh * mw - 1
+    pick = {0, mw - 1, (mh - 1) * mw, last, (mh - 2) * mw + 3, mw + mw - 1}
+    rng = np.random.default_rng(seed)
+    pick.update(int(x) for x in rng.integers(0, last + 1, 4))
+    return sorted(pick)
+
+
+@pytest.mark.parametrize("name", LARGE)
+def test_attention_full_size_sampled(name):
+    cfg = ts.CONFIGS[name]
+    g = Geometry(**cfg.geom_kwargs())
+    _say("full-size attention %s" % name)
+    inp = ts.make_inputs(cfg)
+    got = _run_gpu(cfg, inp)
+    sel = _sample_windows(cfg, g)
+    q, k, v, do = (o_route(inp[n], g) for n in ("q", "k", "v", "dout"))
+    fw = attn_fwd_windows(q, k, v, inp["table"], g, sel)
+    bw = attn_bwd_windows(q, k, v, do, inp["table"], g, sel)
+    slots = {w: (s, n) for w, s, n in window_slots(g)}
+    for w in sel:
+        s, n = slots[w]
+        _assert_close("O[w%d]" % w, _host(got["o"][:, s:s + n]), fw[w][0], cfg)
+        _assert_close("LSE[w%d]" % w, _host(got["lse"][:, :, s:s + n]), fw[w][1], cfg)
+        _assert_close("dQ[w%d]" % w, _host(got["dq"][:, s:s + n]), bw[w][0], cfg)
+        _assert_close("dK[w%d]" % w, _host(got["dk"][:, s:s + n]), bw[w][1], cfg)
+        _assert_close("dV[w%d]" % w, _host(got["dv"][:, s:s + n]), bw[w][2], cfg)
+    # whole bias-table gradient against the stored oracle result
+    gold = np.load(os.path.join(GOLDEN, "dtable_%s.npy" % name))
+    _assert_close("dT", _host(got["dt"]), gold, cfg)
+    # every head's bias gradient sums to zero (each row of dS sums to zero)
+    sums = _host(got["dt"]).sum(axis=(0, 1))
+    assert np.abs(sums).max() < 1e-2
