@@ -16,7 +16,7 @@ hipError_t launch_attn_fwd(const Geo& g, bool bf16, const void* q, const void* k
 hipError_t launch_attn_bwd(const Geo& g, bool bf16, const void* q, const void* k, const void* v,
                            const void* o, const void* dout, const float* lse, const float* table,
                            void* dq, void* dk, void* dv, float* dtab, void* ws, hipStream_t st);
-size_t bwd_workspace(const Geo& g);
+size_t bwd_workspace(const Geo& g, bool bf16);
 size_t attn_max_lds(const Geo& g, bool bf16);
 }  // namespace terra
 
@@ -47,7 +47,7 @@ int hip_status(hipError_t e, const char* what) {
 
 constexpr int64_t kMaxElems = (int64_t)1 << 31;   // per tensor, attention kernels
 constexpr int kMaxBins = 8192;                    // bias bins per head
-constexpr size_t kMaxLds = 64 * 1024;             // dynamic LDS per workgroup
+constexpr size_t kMaxLds = 160 * 1024;            // LDS per workgroup on gfx950
 
 // Geometry rules shared by every entry point.
 int check_geom(const terra_geom* g) {
@@ -196,7 +196,7 @@ int terra_winattn_fwd(const terra_geom* g, int dtype, const void* q, const void*
 
 size_t terra_winattn_bwd_workspace_bytes(const terra_geom* g, int dtype) {
   if (check_attn(g, dtype)) return 0;
-  return terra::bwd_workspace(make_geo(g));
+  return terra::bwd_workspace(make_geo(g), dtype == TERRA_BF16);
 }
 
 int terra_winattn_bwd(const terra_geom* g, int dtype, const void* q, const void* k, const void* v,
@@ -208,7 +208,7 @@ int terra_winattn_bwd(const terra_geom* g, int dtype, const void* q, const void*
   if (!q || !k || !v || !o || !dout || !lse || !bias_table || !dq || !dk || !dv || !dbias_table)
     return fail(TERRA_ERR_INVALID, "tensor pointer is NULL");
   terra::Geo G = make_geo(g);
-  const size_t need = terra::bwd_workspace(G);
+  const size_t need = terra::bwd_workspace(G, dtype == TERRA_BF16);
   if (!workspace || workspace_bytes < need)
     return fail(TERRA_ERR_WORKSPACE, "workspace of %zu bytes given, %zu needed",
                 workspace ? workspace_bytes : (size_t)0, need);

@@ -30,6 +30,18 @@
 
 namespace terra {
 
+// Window-resident path (attn_win.hip) for windows of at most 128 tokens.
+bool win_fwd_ok(const Geo& g, bool bf16_);
+bool win_bwd_ok(const Geo& g, bool bf16_);
+int win_bwd_nslice(const Geo& g);
+size_t win_fwd_lds(const Geo& g);
+size_t win_bwd_lds(const Geo& g);
+hipError_t launch_win_fwd(const Geo& g, const void* q, const void* k, const void* v,
+                          const float* table, void* o, float* lse, hipStream_t st);
+hipError_t launch_win_bwd(const Geo& g, const void* q, const void* k, const void* v,
+                          const void* dout, const float* lse, const float* table, void* dq,
+                          void* dk, void* dv, float* partial, int nslice, hipStream_t st);
+
 constexpr int kThreads = 256;   // 4 waves
 constexpr int kWaveQ = 32;      // queries (or keys) per wave
 constexpr int kChunk = 128;     // queries (or keys) per workgroup
@@ -573,7 +585,8 @@ static hipError_t fwd_impl(const Geo& g, const void* q, const void* k, const voi
   return hipGetLastError();
 }
 
-size_t bwd_workspace(const Geo& g) {
+size_t bwd_workspace(const Geo& g, bool bf16) {
+  if (win_bwd_ok(g, bf16)) return (size_t)g.heads * win_bwd_nslice(g) * g.nbins * sizeof(float);
   const size_t dbytes = (size_t)g.B * g.heads * g.HW * sizeof(float);
   const size_t pbytes = (size_t)g.heads * bwd_nslice(g) * g.nbins * sizeof(float);
   return ((dbytes + 255) / 256) * 256 + pbytes;
@@ -613,13 +626,24 @@ static hipError_t bwd_impl(const Geo& g, const void* q, const void* k, const voi
 }
 
 size_t attn_max_lds(const Geo& g, bool bf16) {
-  if (bf16)
-    return g.hd == 32 ? dkdv_lds<__bf16, 32>(g) : dkdv_lds<__bf16, 64>(g);
-  return g.hd == 32 ? dkdv_lds<float, 32>(g) : dkdv_lds<float, 64>(g);
+  size_t m;
+  if (bf16) {
+    m = g.hd == 32 ? dkdv_lds<__bf16, 32>(g) : dkdv_lds<__bf16, 64>(g);
+    const size_t d = g.hd == 32 ? dq_lds<__bf16, 32>(g) : dq_lds<__bf16, 64>(g);
+    m = m > d ? m : d;
+  } else {
+    m = g.hd == 32 ? dkdv_lds<float, 32>(g) : dkdv_lds<float, 64>(g);
+    const size_t d = g.hd == 32 ? dq_lds<float, 32>(g) : dq_lds<float, 64>(g);
+    m = m > d ? m : d;
+  }
+  if (win_fwd_ok(g, bf16) && win_fwd_lds(g) > m) m = win_fwd_lds(g);
+  if (win_bwd_ok(g, bf16) && win_bwd_lds(g) > m) m = win_bwd_lds(g);
+  return m;
 }
 
 hipError_t launch_attn_fwd(const Geo& g, bool bf16, const void* q, const void* k, const void* v,
                            const float* table, void* o, float* lse, hipStream_t st) {
+  if (win_fwd_ok(g, bf16)) return launch_win_fwd(g, q, k, v, table, o, lse, st);
   if (bf16)
     return g.hd == 32 ? fwd_impl<__bf16, 32>(g, q, k, v, table, o, lse, st)
                       : fwd_impl<__bf16, 64>(g, q, k, v, table, o, lse, st);
@@ -630,6 +654,16 @@ hipError_t launch_attn_fwd(const Geo& g, bool bf16, const void* q, const void* k
 hipError_t launch_attn_bwd(const Geo& g, bool bf16, const void* q, const void* k, const void* v,
                            const void* o, const void* dout, const float* lse, const float* table,
                            void* dq, void* dk, void* dv, float* dtab, void* ws, hipStream_t st) {
+  if (win_bwd_ok(g, bf16)) {
+    const int nslice = win_bwd_nslice(g);
+    float* partial = reinterpret_cast<float*>(ws);
+    hipError_t e = launch_win_bwd(g, q, k, v, dout, lse, table, dq, dk, dv, partial, nslice, st);
+    if (e != hipSuccess) return e;
+    const int nred = g.nbins * g.heads;
+    hipLaunchKernelGGL(dtab_reduce_kernel, dim3((nred + kThreads - 1) / kThreads), dim3(kThreads), 0,
+                       st, partial, dtab, g, nslice);
+    return hipGetLastError();
+  }
   if (bf16)
     return g.hd == 32
                ? bwd_impl<__bf16, 32>(g, q, k, v, o, dout, lse, table, dq, dk, dv, dtab, ws, st)
