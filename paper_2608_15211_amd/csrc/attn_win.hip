@@ -130,6 +130,37 @@ __device__ inline bf16x8 pack_bf16(const f32x16& acc, int r0) {
   return o;
 }
 
+// True when some pair of the window must be excluded: a wrap label inside
+// the window or padding slots in its last 32-token block.
+__device__ inline bool window_needs_mask(const Geo& g, int wi, int wj, int n) {
+  const bool lat = (g.flags & 1) && g.sh > 0 && (wi * g.wh + win_rows(g, wi)) > g.H - g.sh;
+  const bool lon = (g.flags & 2) && g.sw > 0 && (wj * g.ww + win_cols(g, wj)) > g.W - g.sw;
+  return lat || lon || (n & 31) != 0;
+}
+
+// Accumulator initialiser of key block KB: the bias of each (query, key)
+// pair, pre-multiplied by sqrt(hd) so that one multiply by log2(e)/sqrt(hd)
+// after the QK^T product yields the log2-domain score; -inf for excluded
+// pairs (tab[nbins .. nbins+3] holds -inf).  qrev is the lane's reversed
+// bin offset, qlab its label.
+template <bool QUAD, bool MASK>
+__device__ inline f32x16 bias_init(const int* kinfo, const float* tab, int kb, int half, int qrev,
+                                   int qlab, int nbins) {
+  f32x16 c;
+#pragma unroll
+  for (int g4 = 0; g4 < 4; ++g4) {
+    int inf = kinfo[32 * kb + 8 * g4 + 4 * half];
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+      if (!QUAD && x > 0) inf = kinfo[32 * kb + 8 * g4 + 4 * half + x];
+      int rb = qrev + (inf & 0xFFFFFF);
+      if (MASK && (inf >> 24) != qlab) rb = nbins - (QUAD ? x : 0);
+      c[4 * g4 + x] = tab[rb + (QUAD ? x : 0)];
+    }
+  }
+  return c;
+}
+
 // Map a linear block index to a work index so that consecutive work items
 // run on the same XCD (blocks are dealt to the 8 XCDs round-robin).
 __device__ inline int xcd_work(int bid, int nblocks) {
@@ -166,10 +197,12 @@ __global__ __launch_bounds__(kWinThreads) void fwd_win_kernel(
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int half = lane >> 5, col = lane & 31;
 
-  // bias table of head h, log2 domain, stored in reverse bin order so that
-  // consecutive keys of a window row read consecutive addresses
-  for (int x = threadIdx.x; x < g.nbins; x += kWinThreads)
-    tab[g.nbins - 1 - x] = table[x * g.heads + h] * kLog2e;
+  // bias table of head h times sqrt(hd), stored in reverse bin order so that
+  // consecutive keys of a window row read consecutive addresses; four -inf
+  // entries after it serve excluded pairs
+  const float bscale = sqrtf((float)HD);
+  for (int x = threadIdx.x; x < g.nbins + 4; x += kWinThreads)
+    tab[x] = x < g.nbins ? table[(g.nbins - 1 - x) * g.heads + h] * bscale : -INFINITY;
   if (threadIdx.x < kWinMax) kinfo[threadIdx.x] = win_token_info(g, wi, wj, cols, threadIdx.x, n);
   stage_rows<HD>(k, tok0, n, g.C, hoff, ks);
   // V^T through LDS: stage V rows into the vts area's tail is not possible
@@ -207,31 +240,28 @@ __global__ __launch_bounds__(kWinThreads) void fwd_win_kernel(
     qop[c] = qvalid ? *reinterpret_cast<const bf16x8*>(q + (tok0 + qi) * g.C + hoff + 16 * c + 8 * half)
                     : zero8();
 
+  // raw scores with the bias folded into the accumulator: s = QK^T + bias*sqrt(hd)
   f32x16 s[4];
-  float m = -1e30f;
+  const bool mask = window_needs_mask(g, wi, wj, n);
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb) {
     if (kb < nkb) {
-      s[kb] = f32x16{};
+      s[kb] = mask ? bias_init<QUAD, true>(kinfo, tab, kb, half, qrev, qlab, g.nbins)
+                   : bias_init<QUAD, false>(kinfo, tab, kb, half, qrev, qlab, g.nbins);
 #pragma unroll
       for (int c = 0; c < HD / 16; ++c)
         mma16(s[kb], *reinterpret_cast<const bf16x8*>(ks + (32 * kb + col) * (HD + 8) + 16 * c + 8 * half),
               qop[c]);
-#pragma unroll
-      for (int g4 = 0; g4 < 4; ++g4) {
-        int inf = kinfo[32 * kb + 8 * g4 + 4 * half];
-#pragma unroll
-        for (int x = 0; x < 4; ++x) {
-          if (!QUAD && x > 0) inf = kinfo[32 * kb + 8 * g4 + 4 * half + x];
-          const int rb = qrev + (inf & 0xFFFFFF) + (QUAD ? x : 0);
-          const float val = ((inf >> 24) == qlab) ? s[kb][4 * g4 + x] * scale_log2 + tab[rb] : -INFINITY;
-          s[kb][4 * g4 + x] = val;
-          m = fmaxf(m, val);
-        }
-      }
     }
   }
-  m = fmaxf(m, __shfl_xor(m, 32));
+  float mr = -INFINITY;
+#pragma unroll
+  for (int kb = 0; kb < 4; ++kb)
+    if (kb < nkb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mr = fmaxf(mr, s[kb][r]);
+  mr = fmaxf(mr, __shfl_xor(mr, 32));
+  const float m = mr * scale_log2;            // row max, log2 domain
   float l = 0.0f;
   f32x16 oacc[HD / 32];
 #pragma unroll
@@ -241,7 +271,7 @@ __global__ __launch_bounds__(kWinThreads) void fwd_win_kernel(
     if (kb < nkb) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float p = __builtin_amdgcn_exp2f(s[kb][r] - m);
+        const float p = __builtin_amdgcn_exp2f(s[kb][r] * scale_log2 - m);
         s[kb][r] = p;
         l += p;
       }
@@ -262,6 +292,155 @@ __global__ __launch_bounds__(kWinThreads) void fwd_win_kernel(
 #pragma unroll
     for (int g4 = 0; g4 < 4; ++g4) store4_bf16(orow + 32 * eb + 8 * g4 + 4 * half, oacc[eb], g4, inv);
   if (half == 0) lse[(img0 * g.heads) + (int64_t)h * g.HW + (tok0 - img0) + qi] = (m + __log2f(l)) * kLn2;
+}
+
+// ---------------------------------------------------------------------------
+// Forward for head_dim 32 and an even head count: one workgroup of 8 waves
+// per (image, window, head pair).  Global memory is touched only in
+// row-contiguous 128-byte segments (8 lanes per token row): Q, K and V are
+// staged through LDS (V transposed by the staging stores) and O goes back
+// through LDS.  Wave w handles head 2*hp + (w >> 2) and queries
+// [32*(w&3), 32*(w&3)+32).
+// ---------------------------------------------------------------------------
+constexpr int kPairThreads = 512;
+
+template <bool QUAD>
+__global__ __launch_bounds__(kPairThreads) void fwd_win_pair_kernel(
+    const bf16* __restrict__ q, const bf16* __restrict__ k, const bf16* __restrict__ v,
+    const float* __restrict__ table, bf16* __restrict__ o, float* __restrict__ lse, Geo g,
+    float scale_log2) {
+  constexpr int HD = 32;
+  constexpr int KS = HD + 8, VS = kWinMax + 8;
+  extern __shared__ __align__(16) char smem[];
+  bf16* ks = reinterpret_cast<bf16*>(smem);                        // [2][128][KS] K rows
+  bf16* qs = ks + 2 * kWinMax * KS;                                // [2][128][KS] Q rows, then O
+  bf16* vts = qs + 2 * kWinMax * KS;                               // [2][HD][VS]  V^T
+  int* kinfo = reinterpret_cast<int*>(vts + 2 * HD * VS);          // [128]
+  float* tab = reinterpret_cast<float*>(kinfo + kWinMax);          // [2][nbins+4]
+
+  const int hpairs = g.heads >> 1;
+  int work = xcd_work(blockIdx.x, gridDim.x);
+  const int hp = work % hpairs; work /= hpairs;
+  const int w = work % g.nwin;
+  const int b = work / g.nwin;
+  const int wi = w / g.Mw, wj = w - (w / g.Mw) * g.Mw;
+  const int cols = win_cols(g, wj);
+  const int n = win_rows(g, wi) * cols;
+  const int nkb = (n + 31) >> 5;
+  const int64_t img0 = (int64_t)b * g.HW;
+  const int64_t tok0 = img0 + win_offset(g, wi, wj);
+  const int64_t cbase = (int64_t)2 * hp * HD;          // first channel of the pair
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int half = lane >> 5, col = lane & 31;
+  const int hs = wave >> 2, qb = wave & 3;
+  const int h = 2 * hp + hs;
+  const int qi = 32 * qb + col;
+  const bool qvalid = qi < n;
+
+  // ---- row-contiguous loads: thread -> (row, 16-byte chunk of the pair) ----
+  uint4 kr[2], qr[2], vr[2];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int idx = threadIdx.x + u * kPairThreads;
+    const int row = idx >> 3, ch = idx & 7;
+    kr[u] = qr[u] = vr[u] = make_uint4(0, 0, 0, 0);
+    if (row < n) {
+      const int64_t off = (tok0 + row) * g.C + cbase + ch * 8;
+      kr[u] = *reinterpret_cast<const uint4*>(k + off);
+      qr[u] = *reinterpret_cast<const uint4*>(q + off);
+      vr[u] = *reinterpret_cast<const uint4*>(v + off);
+    }
+  }
+  const float bscale = sqrtf((float)HD);
+  for (int x = threadIdx.x; x < 2 * (g.nbins + 4); x += kPairThreads) {
+    const int t = x / (g.nbins + 4), y = x - t * (g.nbins + 4);
+    tab[x] = y < g.nbins ? table[(g.nbins - 1 - y) * g.heads + 2 * hp + t] * bscale : -INFINITY;
+  }
+  if (threadIdx.x < kWinMax) kinfo[threadIdx.x] = win_token_info(g, wi, wj, cols, threadIdx.x, n);
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int idx = threadIdx.x + u * kPairThreads;
+    const int row = idx >> 3, ch = idx & 7;
+    const int t = ch >> 2, e0 = (ch & 3) * 8;
+    *reinterpret_cast<uint4*>(ks + (t * kWinMax + row) * KS + e0) = kr[u];
+    *reinterpret_cast<uint4*>(qs + (t * kWinMax + row) * KS + e0) = qr[u];
+    const bf16* ve = reinterpret_cast<const bf16*>(&vr[u]);
+#pragma unroll
+    for (int x = 0; x < 8; ++x) vts[(t * HD + e0 + x) * VS + row] = ve[x];
+  }
+  __syncthreads();
+
+  const bool active = qb < nkb;
+  const bf16* ksh = ks + hs * kWinMax * KS;
+  const bf16* vth = vts + hs * HD * VS;
+  const float* tabh = tab + hs * (g.nbins + 4);
+  f32x16 oacc = f32x16{};
+  float m = 0.0f, l = 1.0f;
+  if (active) {
+    bf16x8 qop[2];
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+      qop[c] = *reinterpret_cast<const bf16x8*>(qs + (hs * kWinMax + qi) * KS + 16 * c + 8 * half);
+    const int qinf = kinfo[qvalid ? qi : 0];
+    const int qlab = qinf >> 24;
+    const int qrev = g.nbins - 1 - ((qinf & 0xFFFFFF) + (g.wh - 1) * g.bstride + (g.ww - 1));
+    const bool mask = window_needs_mask(g, wi, wj, n);
+    f32x16 s[4];
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      if (kb < nkb) {
+        s[kb] = mask ? bias_init<QUAD, true>(kinfo, tabh, kb, half, qrev, qlab, g.nbins)
+                     : bias_init<QUAD, false>(kinfo, tabh, kb, half, qrev, qlab, g.nbins);
+#pragma unroll
+        for (int c = 0; c < 2; ++c)
+          mma16(s[kb], *reinterpret_cast<const bf16x8*>(ksh + (32 * kb + col) * KS + 16 * c + 8 * half), qop[c]);
+      }
+    }
+    float mr = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+      if (kb < nkb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mr = fmaxf(mr, s[kb][r]);
+    mr = fmaxf(mr, __shfl_xor(mr, 32));
+    m = mr * scale_log2;
+    l = 0.0f;
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      if (kb < nkb) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float p = __builtin_amdgcn_exp2f(s[kb][r] * scale_log2 - m);
+          s[kb][r] = p;
+          l += p;
+        }
+#pragma unroll
+        for (int c = 0; c < 2; ++c)
+          mma16(oacc, lds_perm_op(vth + col * VS + 32 * kb + 16 * c, half), pack_bf16(s[kb], 8 * c));
+      }
+    }
+    l += __shfl_xor(l, 32);
+  }
+  __syncthreads();   // every wave has read its Q rows; qs now takes O
+  if (active) {
+    const float inv = 1.0f / l;
+#pragma unroll
+    for (int g4 = 0; g4 < 4; ++g4)
+      store4_bf16(qs + (hs * kWinMax + qi) * KS + 8 * g4 + 4 * half, oacc, g4, inv);
+    if (qvalid && half == 0)
+      lse[(img0 * g.heads) + (int64_t)h * g.HW + (tok0 - img0) + qi] = (m + __log2f(l)) * kLn2;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int idx = threadIdx.x + u * kPairThreads;
+    const int row = idx >> 3, ch = idx & 7;
+    if (row < n) {
+      const int t = ch >> 2, e0 = (ch & 3) * 8;
+      *reinterpret_cast<uint4*>(o + (tok0 + row) * g.C + cbase + ch * 8) =
+          *reinterpret_cast<const uint4*>(qs + (t * kWinMax + row) * KS + e0);
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -315,22 +494,26 @@ __device__ inline void bwd_key_block(const BwdStep& st, const f32x16& p, f32x16&
   // (P or dS)^T of this block has lane = key; times dO or Q (lane = channel)
   const f32x16 tp = mfma_transpose(pb0, pb1, lds_ident(st.ident, 2), lds_ident(st.ident, 3));
   const f32x16 td = mfma_transpose(db0, db1, lds_ident(st.ident, 2), lds_ident(st.ident, 3));
-  f32x16 pv = f32x16{}, pk = f32x16{};
+  // partials: lane = channel, registers = keys 32KB + acc_row(r, half); the
+  // running sums from earlier steps enter as the accumulator input
+  f32x16 pv, pk;
+#pragma unroll
+  for (int g4 = 0; g4 < 4; ++g4) {
+    const int off = st.col * RS + 32 * KB + 8 * g4 + 4 * st.half;
+    const f32x4 a = T > 0 ? *reinterpret_cast<const f32x4*>(st.redv + off) : f32x4{0.f, 0.f, 0.f, 0.f};
+    const f32x4 b = T > 0 ? *reinterpret_cast<const f32x4*>(st.redk + off) : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int x = 0; x < 4; ++x) { pv[4 * g4 + x] = a[x]; pk[4 * g4 + x] = b[x]; }
+  }
   mma16(pv, pack_bf16(tp, 0), st.de[0]);
   mma16(pv, pack_bf16(tp, 8), st.de[1]);
   mma16(pk, pack_bf16(td, 0), st.qe[0]);
   mma16(pk, pack_bf16(td, 8), st.qe[1]);
-  // partials: lane = channel, registers = keys 32KB + acc_row(r, half)
 #pragma unroll
   for (int g4 = 0; g4 < 4; ++g4) {
     const int off = st.col * RS + 32 * KB + 8 * g4 + 4 * st.half;
-    f32x4* dv4 = reinterpret_cast<f32x4*>(st.redv + off);
-    f32x4* dk4 = reinterpret_cast<f32x4*>(st.redk + off);
-    f32x4 a = {pv[4 * g4], pv[4 * g4 + 1], pv[4 * g4 + 2], pv[4 * g4 + 3]};
-    f32x4 b = {pk[4 * g4], pk[4 * g4 + 1], pk[4 * g4 + 2], pk[4 * g4 + 3]};
-    if (T > 0) { a += *dv4; b += *dk4; }
-    *dv4 = a;
-    *dk4 = b;
+    *reinterpret_cast<f32x4*>(st.redv + off) = f32x4{pv[4 * g4], pv[4 * g4 + 1], pv[4 * g4 + 2], pv[4 * g4 + 3]};
+    *reinterpret_cast<f32x4*>(st.redk + off) = f32x4{pk[4 * g4], pk[4 * g4 + 1], pk[4 * g4 + 2], pk[4 * g4 + 3]};
   }
 }
 
@@ -367,7 +550,7 @@ __global__ __launch_bounds__(kWinThreads) void bwd_win_kernel(
   float* redk = redv + HD * RS;                                 // [HD][RS]
   int* kinfo = reinterpret_cast<int*>(redk + HD * RS);          // [128]
   float* tab = reinterpret_cast<float*>(kinfo + kWinMax);       // [nbins], reversed
-  float* dtb = tab + g.nbins;                                   // [4][nbins], reversed
+  float* dtb = tab + g.nbins + 4;                               // [4][nbins], reversed
 
   const int work = xcd_work(blockIdx.x, gridDim.x);
   const int slice = work / g.heads;
@@ -379,10 +562,12 @@ __global__ __launch_bounds__(kWinThreads) void bwd_win_kernel(
   float* mybins = dtb + wave * g.nbins;
 
   for (int x = threadIdx.x; x < g.nbins; x += kWinThreads) {
-    tab[g.nbins - 1 - x] = table[x * g.heads + h] * kLog2e;
 #pragma unroll
     for (int w4 = 0; w4 < 4; ++w4) dtb[w4 * g.nbins + x] = 0.0f;
   }
+  // bias table times sqrt(hd), reversed bin order, then four -inf entries
+  for (int x = threadIdx.x; x < g.nbins + 4; x += kWinThreads)
+    tab[x] = x < g.nbins ? table[(g.nbins - 1 - x) * g.heads + h] * sqrtf((float)HD) : -INFINITY;
   if (wave == 0) {
     ident[0 * 64 + lane] = ident_op<false>(0);
     ident[1 * 64 + lane] = ident_op<false>(1);
@@ -422,6 +607,46 @@ __global__ __launch_bounds__(kWinThreads) void bwd_win_kernel(
   const int total = g.B * g.nwin;
   const int wbeg = slice * per_slice;
   const int wend = min(total, wbeg + per_slice);
+
+  // Global loads of the next window are issued before the current window is
+  // computed, so their latency overlaps the work: K and V rows for LDS
+  // staging (2 x 16 B of each per thread), Q and dO of the lane's query and
+  // its log-sum-exp.
+  uint4 kpre[2], vpre[2];
+  bf16x8 qpre[2], dpre[2];
+  float lpre = 0.0f;
+  auto prefetch = [&](int wl) {
+    const int b = wl / g.nwin;
+    const int w = wl - b * g.nwin;
+    const int wi = w / g.Mw, wj = w - (w / g.Mw) * g.Mw;
+    const int n = win_rows(g, wi) * win_cols(g, wj);
+    const int64_t img0 = (int64_t)b * g.HW;
+    const int64_t tok0 = img0 + win_offset(g, wi, wj);
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int idx = threadIdx.x + u * kWinThreads;
+      const int row = idx >> 2, ch = idx & 3;
+      kpre[u] = make_uint4(0, 0, 0, 0);
+      vpre[u] = make_uint4(0, 0, 0, 0);
+      if (row < n) {
+        kpre[u] = *reinterpret_cast<const uint4*>(k + (tok0 + row) * g.C + hoff + ch * 8);
+        vpre[u] = *reinterpret_cast<const uint4*>(v + (tok0 + row) * g.C + hoff + ch * 8);
+      }
+    }
+    const int qi = 32 * wave + col;
+    const bool qvalid = qi < n;
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      qpre[c] = qvalid ? *reinterpret_cast<const bf16x8*>(q + (tok0 + qi) * g.C + hoff + 16 * c + 8 * half)
+                       : zero8();
+      dpre[c] = qvalid ? *reinterpret_cast<const bf16x8*>(dout + (tok0 + qi) * g.C + hoff + 16 * c + 8 * half)
+                       : zero8();
+    }
+    // (+inf for padding queries makes every P of theirs exactly 0)
+    lpre = qvalid ? lse[img0 * g.heads + (int64_t)h * g.HW + (tok0 - img0) + qi] * kLog2e : INFINITY;
+  };
+  if (wbeg < wend) prefetch(wbeg);
+
   for (int wl = wbeg; wl < wend; ++wl) {
     const int b = wl / g.nwin;
     const int w = wl - b * g.nwin;
@@ -436,9 +661,23 @@ __global__ __launch_bounds__(kWinThreads) void bwd_win_kernel(
     }
 
     __syncthreads();   // the previous window is done with LDS
-    stage_rows<HD>(k, tok0, n, g.C, hoff, ks);
-    stage_rows<HD>(v, tok0, n, g.C, hoff, vs);
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int idx = threadIdx.x + u * kWinThreads;
+      const int row = idx >> 2, ch = idx & 3;
+      *reinterpret_cast<uint4*>(ks + row * (HD + 8) + ch * 8) = kpre[u];
+      *reinterpret_cast<uint4*>(vs + row * (HD + 8) + ch * 8) = vpre[u];
+    }
     if (threadIdx.x < kWinMax) kinfo[threadIdx.x] = win_token_info(g, wi, wj, cols, threadIdx.x, n);
+    BwdStep st;
+    bf16x8 qop[2];
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      qop[c] = qpre[c];
+      st.dop[c] = dpre[c];
+    }
+    const float lse2 = lpre;
+    if (wl + 1 < wend) prefetch(wl + 1);
     __syncthreads();
     {
       // K^T: wave w transposes keys [32w, 32w+32) on the matrix cores
@@ -457,43 +696,27 @@ __global__ __launch_bounds__(kWinThreads) void bwd_win_kernel(
     const int qinf = qvalid ? win_token_info(g, wi, wj, cols, qi, n) : 0;
     const int qlab = qinf >> 24;
     const int qrev = g.nbins - 1 - ((qinf & 0xFFFFFF) + (g.wh - 1) * g.bstride + (g.ww - 1));
-    const int64_t lidx = img0 * g.heads + (int64_t)h * g.HW + (tok0 - img0) + (qvalid ? qi : 0);
-    const float lse2 = qvalid ? lse[lidx] * kLog2e : 0.0f;
-    BwdStep st;
-    bf16x8 qop[2];
-#pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      qop[c] = qvalid ? *reinterpret_cast<const bf16x8*>(q + (tok0 + qi) * g.C + hoff + 16 * c + 8 * half)
-                      : zero8();
-      st.dop[c] = qvalid ? *reinterpret_cast<const bf16x8*>(dout + (tok0 + qi) * g.C + hoff + 16 * c + 8 * half)
-                         : zero8();
-    }
 
-    // scores (transposed: lane = query, registers = keys), P, and D = sum P dP
+    // scores (transposed: lane = query, registers = keys) with the bias in
+    // the accumulator, P, and D = sum P dP
+    const bool mask = window_needs_mask(g, wi, wj, n);
     f32x16 p[4];
     float dsum = 0.0f;
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
       f32x16 dp = f32x16{};
-      p[kb] = f32x16{};
+      p[kb] = mask ? bias_init<QUAD, true>(kinfo, tab, kb, half, qrev, qlab, g.nbins)
+                   : bias_init<QUAD, false>(kinfo, tab, kb, half, qrev, qlab, g.nbins);
 #pragma unroll
       for (int c = 0; c < 2; ++c) {
         mma16(p[kb], *reinterpret_cast<const bf16x8*>(ks + (32 * kb + col) * (HD + 8) + 16 * c + 8 * half), qop[c]);
         mma16(dp, *reinterpret_cast<const bf16x8*>(vs + (32 * kb + col) * (HD + 8) + 16 * c + 8 * half), st.dop[c]);
       }
 #pragma unroll
-      for (int g4 = 0; g4 < 4; ++g4) {
-        int inf = kinfo[32 * kb + 8 * g4 + 4 * half];
-#pragma unroll
-        for (int x = 0; x < 4; ++x) {
-          if (!QUAD && x > 0) inf = kinfo[32 * kb + 8 * g4 + 4 * half + x];
-          const int rb = qrev + (inf & 0xFFFFFF) + (QUAD ? x : 0);
-          float pv = 0.0f;
-          if (((inf >> 24) == qlab) && qvalid)
-            pv = __builtin_amdgcn_exp2f(p[kb][4 * g4 + x] * scale_log2 + tab[rb] - lse2);
-          p[kb][4 * g4 + x] = pv;
-          dsum += pv * dp[4 * g4 + x];
-        }
+      for (int r = 0; r < 16; ++r) {
+        const float pv = __builtin_amdgcn_exp2f(p[kb][r] * scale_log2 - lse2);
+        p[kb][r] = pv;
+        dsum += pv * dp[r];
       }
     }
     st.D = dsum + __shfl_xor(dsum, 32);
@@ -579,12 +802,19 @@ int win_bwd_nslice(const Geo& g) {
   return (total + per - 1) / per;
 }
 
+size_t win_fwd_pair_lds(const Geo& g);
 size_t win_fwd_lds(const Geo& g) {
-  return sizeof(bf16) * (kWinMax * (g.hd + 8) + g.hd * (kWinMax + 8)) + 4 * kWinMax + 4 * g.nbins;
+  const size_t one = sizeof(bf16) * (kWinMax * (g.hd + 8) + g.hd * (kWinMax + 8)) + 4 * kWinMax +
+                     4 * (g.nbins + 4);
+  if (g.hd == 32 && g.heads % 2 == 0) {
+    const size_t pair = win_fwd_pair_lds(g);
+    return pair > one ? pair : one;
+  }
+  return one;
 }
 size_t win_bwd_lds(const Geo& g) {
   return 4 * 64 * sizeof(bf16x8) + sizeof(bf16) * (2 * kWinMax * (kBwdHD + 8) + kBwdHD * (kWinMax + 8)) +
-         2 * 4 * kBwdHD * (kWinMax + 4) + 4 * kWinMax + 4 * 5 * g.nbins;
+         2 * 4 * kBwdHD * (kWinMax + 4) + 4 * kWinMax + 4 * (5 * g.nbins + 4);
 }
 
 // Four consecutive result registers are four consecutive keys of one window
@@ -603,9 +833,27 @@ static void fwd_win_go(const Geo& g, const void* q, const void* k, const void* v
                      (const bf16*)q, (const bf16*)k, (const bf16*)v, table, (bf16*)o, lse, g, sl2);
 }
 
+size_t win_fwd_pair_lds(const Geo& g) {
+  return sizeof(bf16) * 2 * (2 * kWinMax * (32 + 8) + 32 * (kWinMax + 8)) + 4 * kWinMax +
+         4 * 2 * (g.nbins + 4);
+}
+
 hipError_t launch_win_fwd(const Geo& g, const void* q, const void* k, const void* v,
                           const float* table, void* o, float* lse, hipStream_t st) {
   const bool quad = quad_layout(g);
+  if (g.hd == 32 && g.heads % 2 == 0) {
+    const int grid = g.B * g.nwin * (g.heads / 2);
+    const float sl2 = kLog2e / sqrtf((float)g.hd);
+    if (quad)
+      hipLaunchKernelGGL((fwd_win_pair_kernel<true>), dim3(grid), dim3(kPairThreads),
+                         win_fwd_pair_lds(g), st, (const bf16*)q, (const bf16*)k, (const bf16*)v,
+                         table, (bf16*)o, lse, g, sl2);
+    else
+      hipLaunchKernelGGL((fwd_win_pair_kernel<false>), dim3(grid), dim3(kPairThreads),
+                         win_fwd_pair_lds(g), st, (const bf16*)q, (const bf16*)k, (const bf16*)v,
+                         table, (bf16*)o, lse, g, sl2);
+    return hipGetLastError();
+  }
   if (g.hd == 32) {
     if (quad) fwd_win_go<32, true>(g, q, k, v, table, o, lse, st);
     else fwd_win_go<32, false>(g, q, k, v, table, o, lse, st);
