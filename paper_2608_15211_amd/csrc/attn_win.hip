@@ -450,147 +450,206 @@ __global__ __launch_bounds__(kPairThreads) void fwd_win_pair_kernel(
 // ---------------------------------------------------------------------------
 constexpr int kBwdHD = 32;
 
-// Identity operands kept in LDS (re-read at each use so that they do not
-// occupy registers across the window loop): [natural c0, c1, permuted c0, c1][lane].
-__device__ inline bf16x8 lds_ident(const bf16x8* id, int which) {
-  return id[which * 64 + (threadIdx.x & 63)];
-}
-
-// Everything one wave needs for the per-key-block steps of one window.
-struct BwdStep {
-  const bf16* vs;       // V rows in LDS
-  const bf16* kts;      // K^T in LDS
-  const bf16x8* ident;
+// Per-wave state of the backward for one window.
+struct BwdWave {
+  const bf16* ks;       // K rows of the wave's head in LDS [128][HD+8]
+  const bf16* vs;       // V rows [128][HD+8]
+  const bf16* kts;      // K^T [HD][128+8]
+  const bf16x8* ident;  // 0/1 transpose operands [4][64]: (PERM, chunk)
+  const int* kinfo;     // key words of the window
+  const float* tab;     // bias table times sqrt(hd), reversed, then -inf
   float* redv;          // dV partial sums [HD][RS]
   float* redk;          // dK partial sums [HD][RS]
-  bf16x8 dop[2];        // dO of the wave's queries (row operand)
-  bf16x8 de[2], qe[2];  // dO and Q with lane = channel (column operand)
-  float D;
-  int col, half;
+  bf16x8 qop[2], dop[2];  // Q and dO of the wave's 32 queries (row operands)
+  bf16x8 de[2], qe[2];    // dO and Q with lane = channel (column operands)
+  float D, lse2, scale_log2;
+  int qrev, qlab, nbins, col, half;
 };
 
-// Key block KB of the wave: dP (recomputed), dS, the bias accumulators,
-// the dQ contribution, and the dV / dK partials added into LDS.  T is the
-// rotation step (0 stores, later steps add).
-template <int KB, int T>
-__device__ inline void bwd_key_block(const BwdStep& st, const f32x16& p, f32x16& dtacc,
-                                     f32x16& dqacc) {
+// Transpose operand `which` = 2*PERM + chunk, read from LDS so that the
+// compiler does not keep all four resident in registers.
+__device__ inline bf16x8 lds_ident(const bf16x8* ident, int which) {
+  return ident[which * 64 + (threadIdx.x & 63)];
+}
+
+// P of key block KB for the wave's queries (lane = query, registers = keys):
+// bias in the accumulator, S = K Q^T on the matrix cores, exp2 against the
+// saved log-sum-exp (+inf for padding queries, so their P is 0).
+template <int KB, bool QUAD, bool MASK>
+__device__ __forceinline__ f32x16 bwd_p(const BwdWave& st) {
   constexpr int HD = kBwdHD;
-  constexpr int RS = kWinMax + 4;
-  f32x16 ds = f32x16{};
+  f32x16 p = bias_init<QUAD, MASK>(st.kinfo, st.tab, KB, st.half, st.qrev, st.qlab, st.nbins);
 #pragma unroll
   for (int c = 0; c < 2; ++c)
-    mma16(ds, *reinterpret_cast<const bf16x8*>(st.vs + (32 * KB + st.col) * (HD + 8) + 16 * c + 8 * st.half),
-          st.dop[c]);
+    mma16(p, *reinterpret_cast<const bf16x8*>(st.ks + (32 * KB + st.col) * (HD + 8) + 16 * c + 8 * st.half),
+          st.qop[c]);
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    ds[r] = p[r] * (ds[r] - st.D);
-    dtacc[r] += ds[r];
+  for (int r = 0; r < 16; ++r) p[r] = __builtin_amdgcn_exp2f(p[r] * st.scale_log2 - st.lse2);
+  return p;
+}
+
+template <int KB>
+__device__ __forceinline__ f32x16 bwd_dp(const BwdWave& st) {
+  constexpr int HD = kBwdHD;
+  f32x16 dp = f32x16{};
+#pragma unroll
+  for (int c = 0; c < 2; ++c)
+    mma16(dp, *reinterpret_cast<const bf16x8*>(st.vs + (32 * KB + st.col) * (HD + 8) + 16 * c + 8 * st.half),
+          st.dop[c]);
+  return dp;
+}
+
+// One rotation step: key block KB.  P and dP are recomputed (so that P does
+// not occupy 64 registers across the steps), dS = P (dP - D) goes into the
+// bias accumulators and into dQ += dS K (K^T from LDS); P^T and dS^T (by
+// matrix-core transpose) times dO and Q give the block's dV and dK partials,
+// which are added to the running sums in LDS through the accumulator input.
+// Step T = 0 starts the sums.
+template <int KB, int T, bool QUAD, bool MASK>
+__device__ __forceinline__ void bwd_step(const BwdWave& st, f32x16& dtacc, f32x16& dqacc) {
+  constexpr int RS = kWinMax + 4;
+  bf16x8 pb0, pb1, db0, db1;
+  {
+    const f32x16 p = bwd_p<KB, QUAD, MASK>(st);
+    f32x16 ds = bwd_dp<KB>(st);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      ds[r] = p[r] * (ds[r] - st.D);
+      dtacc[r] += ds[r];
+    }
+    pb0 = pack_bf16(p, 0); pb1 = pack_bf16(p, 8);
+    db0 = pack_bf16(ds, 0); db1 = pack_bf16(ds, 8);
   }
-  const bf16x8 pb0 = pack_bf16(p, 0), pb1 = pack_bf16(p, 8);
-  const bf16x8 db0 = pack_bf16(ds, 0), db1 = pack_bf16(ds, 8);
   mma16(dqacc, lds_perm_op(st.kts + st.col * (kWinMax + 8) + 32 * KB, st.half), db0);
   mma16(dqacc, lds_perm_op(st.kts + st.col * (kWinMax + 8) + 32 * KB + 16, st.half), db1);
-  // (P or dS)^T of this block has lane = key; times dO or Q (lane = channel)
-  const f32x16 tp = mfma_transpose(pb0, pb1, lds_ident(st.ident, 2), lds_ident(st.ident, 3));
-  const f32x16 td = mfma_transpose(db0, db1, lds_ident(st.ident, 2), lds_ident(st.ident, 3));
-  // partials: lane = channel, registers = keys 32KB + acc_row(r, half); the
-  // running sums from earlier steps enter as the accumulator input
-  f32x16 pv, pk;
+  __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-  for (int g4 = 0; g4 < 4; ++g4) {
-    const int off = st.col * RS + 32 * KB + 8 * g4 + 4 * st.half;
-    const f32x4 a = T > 0 ? *reinterpret_cast<const f32x4*>(st.redv + off) : f32x4{0.f, 0.f, 0.f, 0.f};
-    const f32x4 b = T > 0 ? *reinterpret_cast<const f32x4*>(st.redk + off) : f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int which = 0; which < 2; ++which) {
+    const bf16x8 ip0 = lds_ident(st.ident, 2), ip1 = lds_ident(st.ident, 3);
+    const f32x16 tr = which == 0 ? mfma_transpose(pb0, pb1, ip0, ip1) : mfma_transpose(db0, db1, ip0, ip1);
+    float* red = which == 0 ? st.redv : st.redk;
+    f32x16 part;
 #pragma unroll
-    for (int x = 0; x < 4; ++x) { pv[4 * g4 + x] = a[x]; pk[4 * g4 + x] = b[x]; }
-  }
-  mma16(pv, pack_bf16(tp, 0), st.de[0]);
-  mma16(pv, pack_bf16(tp, 8), st.de[1]);
-  mma16(pk, pack_bf16(td, 0), st.qe[0]);
-  mma16(pk, pack_bf16(td, 8), st.qe[1]);
+    for (int g4 = 0; g4 < 4; ++g4) {
+      const f32x4 a = T > 0 ? *reinterpret_cast<const f32x4*>(red + st.col * RS + 32 * KB + 8 * g4 + 4 * st.half)
+                            : f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int g4 = 0; g4 < 4; ++g4) {
-    const int off = st.col * RS + 32 * KB + 8 * g4 + 4 * st.half;
-    *reinterpret_cast<f32x4*>(st.redv + off) = f32x4{pv[4 * g4], pv[4 * g4 + 1], pv[4 * g4 + 2], pv[4 * g4 + 3]};
-    *reinterpret_cast<f32x4*>(st.redk + off) = f32x4{pk[4 * g4], pk[4 * g4 + 1], pk[4 * g4 + 2], pk[4 * g4 + 3]};
+      for (int x = 0; x < 4; ++x) part[4 * g4 + x] = a[x];
+    }
+    mma16(part, pack_bf16(tr, 0), which == 0 ? st.de[0] : st.qe[0]);
+    mma16(part, pack_bf16(tr, 8), which == 0 ? st.de[1] : st.qe[1]);
+#pragma unroll
+    for (int g4 = 0; g4 < 4; ++g4)
+      *reinterpret_cast<f32x4*>(red + st.col * RS + 32 * KB + 8 * g4 + 4 * st.half) =
+          f32x4{part[4 * g4], part[4 * g4 + 1], part[4 * g4 + 2], part[4 * g4 + 3]};
+    __builtin_amdgcn_sched_barrier(0);
   }
 }
 
-// The four steps of wave W: key blocks W, W+1, W+2, W+3 (mod 4), so that at
-// every step each block is touched by exactly one wave; a barrier ends each
-// step.  The order of additions into every block is therefore fixed.
-template <int W>
-__device__ inline void bwd_rotation(const BwdStep& st, const f32x16 (&p)[4], f32x16 (&dtacc)[4],
-                                    f32x16& dqacc) {
-  bwd_key_block<(W + 0) & 3, 0>(st, p[(W + 0) & 3], dtacc[(W + 0) & 3], dqacc);
+// The four steps of the wave with query block W: key blocks W, W+1, W+2,
+// W+3 (mod 4), so that at every step each block of the head is touched by
+// exactly one wave; a barrier ends each step, so the order of additions
+// into every block is fixed.
+template <int W, bool QUAD, bool MASK>
+__device__ __forceinline__ void bwd_rotation(const BwdWave& st, f32x16 (&dtacc)[4], f32x16& dqacc) {
+  bwd_step<(W + 0) & 3, 0, QUAD, MASK>(st, dtacc[(W + 0) & 3], dqacc);
   __syncthreads();
-  bwd_key_block<(W + 1) & 3, 1>(st, p[(W + 1) & 3], dtacc[(W + 1) & 3], dqacc);
+  bwd_step<(W + 1) & 3, 1, QUAD, MASK>(st, dtacc[(W + 1) & 3], dqacc);
   __syncthreads();
-  bwd_key_block<(W + 2) & 3, 2>(st, p[(W + 2) & 3], dtacc[(W + 2) & 3], dqacc);
+  bwd_step<(W + 2) & 3, 2, QUAD, MASK>(st, dtacc[(W + 2) & 3], dqacc);
   __syncthreads();
-  bwd_key_block<(W + 3) & 3, 3>(st, p[(W + 3) & 3], dtacc[(W + 3) & 3], dqacc);
+  bwd_step<(W + 3) & 3, 3, QUAD, MASK>(st, dtacc[(W + 3) & 3], dqacc);
   __syncthreads();
 }
 
-template <bool QUAD>
-__global__ __launch_bounds__(kWinThreads) void bwd_win_kernel(
+template <bool QUAD, bool MASK>
+__device__ __forceinline__ void bwd_window_body(BwdWave& st, int qw, f32x16 (&dtacc)[4], f32x16& dqacc) {
+  // pass 1: D = sum_k P dP over the window
+  float dsum = 0.0f;
+#define TERRA_DSUM(KB)                                                          \
+  {                                                                             \
+    const f32x16 pk = bwd_p<KB, QUAD, MASK>(st);                                \
+    const f32x16 dk = bwd_dp<KB>(st);                                           \
+    _Pragma("unroll") for (int r = 0; r < 16; ++r) dsum += pk[r] * dk[r];       \
+    __builtin_amdgcn_sched_barrier(0);                                          \
+  }
+  TERRA_DSUM(0)
+  TERRA_DSUM(1)
+  TERRA_DSUM(2)
+  TERRA_DSUM(3)
+#undef TERRA_DSUM
+  st.D = dsum + __shfl_xor(dsum, 32);
+  __syncthreads();   // K^T of every key block is in LDS
+  switch (qw) {
+    case 0: bwd_rotation<0, QUAD, MASK>(st, dtacc, dqacc); break;
+    case 1: bwd_rotation<1, QUAD, MASK>(st, dtacc, dqacc); break;
+    case 2: bwd_rotation<2, QUAD, MASK>(st, dtacc, dqacc); break;
+    default: bwd_rotation<3, QUAD, MASK>(st, dtacc, dqacc); break;
+  }
+}
+
+// Backward, head_dim 32.  One workgroup of 4*NH waves per (NH heads, run of
+// consecutive windows); wave w works on head NH*hg + (w >> 2) and queries
+// [32*(w&3), 32*(w&3)+32).  K and V are staged in LDS with row-contiguous
+// loads (NH*64-byte segments per token row); dQ, dK and dV leave the same
+// way.  The bias-gradient sums of every register run over windows of equal
+// width and are flushed to per-wave LDS bins when the width changes (a
+// register holds the same query/key slot pair, hence the same bin, in every
+// such window).
+template <bool QUAD, int NH>
+__global__ __launch_bounds__(kWinThreads * NH) void bwd_win_kernel(
     const bf16* __restrict__ q, const bf16* __restrict__ k, const bf16* __restrict__ v,
     const bf16* __restrict__ dout, const float* __restrict__ lse, const float* __restrict__ table,
     bf16* __restrict__ dq, bf16* __restrict__ dk, bf16* __restrict__ dv,
     float* __restrict__ partial, Geo g, int nslice, int per_slice, float scale_log2, float scale) {
   constexpr int HD = kBwdHD;
-  constexpr int RS = kWinMax + 4;                               // red row stride (floats)
+  constexpr int KS = HD + 8;
+  constexpr int RS = kWinMax + 4;
+  constexpr int NT = kWinThreads * NH;
+  constexpr int CPR = 4 * NH;                                   // 16-byte chunks per row segment
   extern __shared__ __align__(16) char smem[];
   bf16x8* ident = reinterpret_cast<bf16x8*>(smem);              // [4][64]
-  bf16* ks = reinterpret_cast<bf16*>(ident + 4 * 64);           // K   [128][HD+8]
-  bf16* vs = ks + kWinMax * (HD + 8);                           // V   [128][HD+8]
-  bf16* kts = vs + kWinMax * (HD + 8);                          // K^T [HD][128+8]
-  float* redv = reinterpret_cast<float*>(kts + HD * (kWinMax + 8));  // [HD][RS]
-  float* redk = redv + HD * RS;                                 // [HD][RS]
-  int* kinfo = reinterpret_cast<int*>(redk + HD * RS);          // [128]
-  float* tab = reinterpret_cast<float*>(kinfo + kWinMax);       // [nbins], reversed
-  float* dtb = tab + g.nbins + 4;                               // [4][nbins], reversed
+  // per head: K rows, V rows, K^T, dV sums, dK sums
+  bf16* ks = reinterpret_cast<bf16*>(ident + 4 * 64);           // [NH][128][KS]
+  bf16* vs = ks + NH * kWinMax * KS;                            // [NH][128][KS]
+  bf16* kts = vs + NH * kWinMax * KS;                           // [NH][HD][128+8]
+  float* redv = reinterpret_cast<float*>(kts + NH * HD * (kWinMax + 8));   // [NH][HD][RS]
+  float* redk = redv + NH * HD * RS;                            // [NH][HD][RS]
+  int* kinfo = reinterpret_cast<int*>(redk + NH * HD * RS);     // [128]
+  float* tab = reinterpret_cast<float*>(kinfo + kWinMax);       // [NH][nbins+4]
+  float* dtb = tab + NH * (g.nbins + 4);                        // [4*NH][nbins], reversed
 
+  const int ngroups = g.heads / NH;
   const int work = xcd_work(blockIdx.x, gridDim.x);
-  const int slice = work / g.heads;
-  const int h = work - slice * g.heads;
-  const int hoff = h * HD;
+  const int slice = work / ngroups;
+  const int hg = work - slice * ngroups;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int hs = wave >> 2, qw = wave & 3;
+  const int h = NH * hg + hs;
+  const int64_t cbase = (int64_t)NH * hg * HD;
+  const int hoff = h * HD;
   const int half = lane >> 5, col = lane & 31;
   float* mybins = dtb + wave * g.nbins;
 
-  for (int x = threadIdx.x; x < g.nbins; x += kWinThreads) {
-#pragma unroll
-    for (int w4 = 0; w4 < 4; ++w4) dtb[w4 * g.nbins + x] = 0.0f;
-  }
-  // bias table times sqrt(hd), reversed bin order, then four -inf entries
-  for (int x = threadIdx.x; x < g.nbins + 4; x += kWinThreads)
-    tab[x] = x < g.nbins ? table[(g.nbins - 1 - x) * g.heads + h] * sqrtf((float)HD) : -INFINITY;
-  if (wave == 0) {
-    ident[0 * 64 + lane] = ident_op<false>(0);
-    ident[1 * 64 + lane] = ident_op<false>(1);
-    ident[2 * 64 + lane] = ident_op<true>(0);
-    ident[3 * 64 + lane] = ident_op<true>(1);
+  for (int x = threadIdx.x; x < 4 * NH * g.nbins; x += NT) dtb[x] = 0.0f;
+  if (wave < 4) ident[threadIdx.x] = (wave >> 1) ? ident_op<true>(wave & 1) : ident_op<false>(wave & 1);
+  for (int x = threadIdx.x; x < NH * (g.nbins + 4); x += NT) {
+    const int t = x / (g.nbins + 4), y = x - t * (g.nbins + 4);
+    tab[x] = y < g.nbins ? table[(g.nbins - 1 - y) * g.heads + NH * hg + t] * sqrtf((float)HD) : -INFINITY;
   }
 
-  // Bias-gradient accumulators, one per result register.  A register holds
-  // the same (query slot, key slot) pair in every window, and the pair's
-  // bin depends only on the window width, so dS is summed here over a run
-  // of windows of equal width and flushed to the per-wave LDS bins (in the
-  // same fixed order every time) when the width changes.
   f32x16 dtacc[4];
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb) dtacc[kb] = f32x16{};
   int acc_cols = 0;
-  // (hh is made opaque so that the per-register key slots below are not
-  // hoisted out of the window loop into 64 live registers)
+  // (hh is made opaque so that the per-register slots are not hoisted out of
+  // the window loop into live registers)
 #define TERRA_FLUSH_DT(cw)                                                              \
   {                                                                                     \
     const float rcw = 1.0f / (float)(cw);                                               \
-    const int qs = 32 * wave + col;                                                     \
-    const int aq = (int)(((float)qs + 0.5f) * rcw), cq = qs - aq * (cw);                \
+    const int qs_ = 32 * qw + col;                                                      \
+    const int aq = (int)(((float)qs_ + 0.5f) * rcw), cq = qs_ - aq * (cw);              \
     int hh = half;                                                                      \
     asm volatile("" : "+v"(hh));                                                        \
     _Pragma("unroll") for (int kb = 0; kb < 4; ++kb)                                    \
@@ -607,46 +666,6 @@ __global__ __launch_bounds__(kWinThreads) void bwd_win_kernel(
   const int total = g.B * g.nwin;
   const int wbeg = slice * per_slice;
   const int wend = min(total, wbeg + per_slice);
-
-  // Global loads of the next window are issued before the current window is
-  // computed, so their latency overlaps the work: K and V rows for LDS
-  // staging (2 x 16 B of each per thread), Q and dO of the lane's query and
-  // its log-sum-exp.
-  uint4 kpre[2], vpre[2];
-  bf16x8 qpre[2], dpre[2];
-  float lpre = 0.0f;
-  auto prefetch = [&](int wl) {
-    const int b = wl / g.nwin;
-    const int w = wl - b * g.nwin;
-    const int wi = w / g.Mw, wj = w - (w / g.Mw) * g.Mw;
-    const int n = win_rows(g, wi) * win_cols(g, wj);
-    const int64_t img0 = (int64_t)b * g.HW;
-    const int64_t tok0 = img0 + win_offset(g, wi, wj);
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int idx = threadIdx.x + u * kWinThreads;
-      const int row = idx >> 2, ch = idx & 3;
-      kpre[u] = make_uint4(0, 0, 0, 0);
-      vpre[u] = make_uint4(0, 0, 0, 0);
-      if (row < n) {
-        kpre[u] = *reinterpret_cast<const uint4*>(k + (tok0 + row) * g.C + hoff + ch * 8);
-        vpre[u] = *reinterpret_cast<const uint4*>(v + (tok0 + row) * g.C + hoff + ch * 8);
-      }
-    }
-    const int qi = 32 * wave + col;
-    const bool qvalid = qi < n;
-#pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      qpre[c] = qvalid ? *reinterpret_cast<const bf16x8*>(q + (tok0 + qi) * g.C + hoff + 16 * c + 8 * half)
-                       : zero8();
-      dpre[c] = qvalid ? *reinterpret_cast<const bf16x8*>(dout + (tok0 + qi) * g.C + hoff + 16 * c + 8 * half)
-                       : zero8();
-    }
-    // (+inf for padding queries makes every P of theirs exactly 0)
-    lpre = qvalid ? lse[img0 * g.heads + (int64_t)h * g.HW + (tok0 - img0) + qi] * kLog2e : INFINITY;
-  };
-  if (wbeg < wend) prefetch(wbeg);
-
   for (int wl = wbeg; wl < wend; ++wl) {
     const int b = wl / g.nwin;
     const int w = wl - b * g.nwin;
@@ -659,130 +678,117 @@ __global__ __launch_bounds__(kWinThreads) void bwd_win_kernel(
       if (acc_cols > 0) TERRA_FLUSH_DT(acc_cols);
       acc_cols = cols;
     }
+    const int qi = 32 * qw + col;
+    const bool qvalid = qi < n;
+    // global loads: K, V rows (row-contiguous), the wave's Q and dO rows, LSE
+    uint4 kr[2], vr[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int idx = threadIdx.x + u * NT;
+      const int row = idx / CPR, ch = idx - (idx / CPR) * CPR;
+      kr[u] = vr[u] = make_uint4(0, 0, 0, 0);
+      if (row < n) {
+        const int64_t off = (tok0 + row) * g.C + cbase + ch * 8;
+        kr[u] = *reinterpret_cast<const uint4*>(k + off);
+        vr[u] = *reinterpret_cast<const uint4*>(v + off);
+      }
+    }
+    BwdWave st;
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      st.qop[c] = qvalid ? *reinterpret_cast<const bf16x8*>(q + (tok0 + qi) * g.C + hoff + 16 * c + 8 * half)
+                         : zero8();
+      st.dop[c] = qvalid ? *reinterpret_cast<const bf16x8*>(dout + (tok0 + qi) * g.C + hoff + 16 * c + 8 * half)
+                         : zero8();
+    }
+    st.lse2 = qvalid ? lse[img0 * g.heads + (int64_t)h * g.HW + (tok0 - img0) + qi] * kLog2e : INFINITY;
 
     __syncthreads();   // the previous window is done with LDS
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
-      const int idx = threadIdx.x + u * kWinThreads;
-      const int row = idx >> 2, ch = idx & 3;
-      *reinterpret_cast<uint4*>(ks + row * (HD + 8) + ch * 8) = kpre[u];
-      *reinterpret_cast<uint4*>(vs + row * (HD + 8) + ch * 8) = vpre[u];
+      const int idx = threadIdx.x + u * NT;
+      const int row = idx / CPR, ch = idx - (idx / CPR) * CPR;
+      const int t = ch >> 2, c0 = (ch & 3) * 8;
+      *reinterpret_cast<uint4*>(ks + (t * kWinMax + row) * KS + c0) = kr[u];
+      *reinterpret_cast<uint4*>(vs + (t * kWinMax + row) * KS + c0) = vr[u];
     }
     if (threadIdx.x < kWinMax) kinfo[threadIdx.x] = win_token_info(g, wi, wj, cols, threadIdx.x, n);
-    BwdStep st;
-    bf16x8 qop[2];
-#pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      qop[c] = qpre[c];
-      st.dop[c] = dpre[c];
-    }
-    const float lse2 = lpre;
-    if (wl + 1 < wend) prefetch(wl + 1);
     __syncthreads();
+
+    st.ks = ks + hs * kWinMax * KS;
+    st.vs = vs + hs * kWinMax * KS;
+    st.kts = kts + hs * HD * (kWinMax + 8);
+    st.ident = ident;
+    st.kinfo = kinfo;
+    st.tab = tab + hs * (g.nbins + 4);
+    st.redv = redv + hs * HD * RS;
+    st.redk = redk + hs * HD * RS;
+    st.scale_log2 = scale_log2;
+    st.nbins = g.nbins;
+    st.col = col;
+    st.half = half;
     {
-      // K^T: wave w transposes keys [32w, 32w+32) on the matrix cores
-      const bf16* r = ks + (32 * wave + col) * (HD + 8) + 8 * half;
+      // K^T: wave (hs, qw) transposes keys [32qw, 32qw+32) of its head
+      const bf16* r = st.ks + (32 * qw + col) * KS + 8 * half;
       const f32x16 t = mfma_transpose(*reinterpret_cast<const bf16x8*>(r),
                                       *reinterpret_cast<const bf16x8*>(r + 16),
                                       lds_ident(ident, 0), lds_ident(ident, 1));
 #pragma unroll
       for (int g4 = 0; g4 < 4; ++g4)
-        store4_bf16(kts + col * (kWinMax + 8) + 32 * wave + 8 * g4 + 4 * half, t, g4, 1.0f);
+        store4_bf16(kts + (hs * HD + col) * (kWinMax + 8) + 32 * qw + 8 * g4 + 4 * half, t, g4, 1.0f);
     }
-
-    // ---- the wave's 32 queries (32*wave + col) ----
-    const int qi = 32 * wave + col;
-    const bool qvalid = qi < n;
     const int qinf = qvalid ? win_token_info(g, wi, wj, cols, qi, n) : 0;
-    const int qlab = qinf >> 24;
-    const int qrev = g.nbins - 1 - ((qinf & 0xFFFFFF) + (g.wh - 1) * g.bstride + (g.ww - 1));
-
-    // scores (transposed: lane = query, registers = keys) with the bias in
-    // the accumulator, P, and D = sum P dP
-    const bool mask = window_needs_mask(g, wi, wj, n);
-    f32x16 p[4];
-    float dsum = 0.0f;
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      f32x16 dp = f32x16{};
-      p[kb] = mask ? bias_init<QUAD, true>(kinfo, tab, kb, half, qrev, qlab, g.nbins)
-                   : bias_init<QUAD, false>(kinfo, tab, kb, half, qrev, qlab, g.nbins);
-#pragma unroll
-      for (int c = 0; c < 2; ++c) {
-        mma16(p[kb], *reinterpret_cast<const bf16x8*>(ks + (32 * kb + col) * (HD + 8) + 16 * c + 8 * half), qop[c]);
-        mma16(dp, *reinterpret_cast<const bf16x8*>(vs + (32 * kb + col) * (HD + 8) + 16 * c + 8 * half), st.dop[c]);
-      }
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float pv = __builtin_amdgcn_exp2f(p[kb][r] * scale_log2 - lse2);
-        p[kb][r] = pv;
-        dsum += pv * dp[r];
-      }
-    }
-    st.D = dsum + __shfl_xor(dsum, 32);
-    // dP is recomputed per key block on the matrix cores rather than kept in
-    // 64 registers (the fence stops the compiler from reusing the first one).
-    asm volatile("" ::: "memory");
+    st.qlab = qinf >> 24;
+    st.qrev = g.nbins - 1 - ((qinf & 0xFFFFFF) + (g.wh - 1) * g.bstride + (g.ww - 1));
     {
-      const f32x16 te = mfma_transpose(st.dop[0], st.dop[1], lds_ident(ident, 0), lds_ident(ident, 1));
+      const bf16x8 in0 = lds_ident(ident, 0), in1 = lds_ident(ident, 1);
+      const f32x16 te = mfma_transpose(st.dop[0], st.dop[1], in0, in1);
       st.de[0] = pack_bf16(te, 0);
       st.de[1] = pack_bf16(te, 8);
-      const f32x16 tq = mfma_transpose(qop[0], qop[1], lds_ident(ident, 0), lds_ident(ident, 1));
+      const f32x16 tq = mfma_transpose(st.qop[0], st.qop[1], in0, in1);
       st.qe[0] = pack_bf16(tq, 0);
       st.qe[1] = pack_bf16(tq, 8);
     }
-    st.vs = vs;
-    st.kts = kts;
-    st.ident = ident;
-    st.redv = redv;
-    st.redk = redk;
-    st.col = col;
-    st.half = half;
-    __syncthreads();   // K^T complete
     f32x16 dqacc = f32x16{};
-    switch (wave) {
-      case 0: bwd_rotation<0>(st, p, dtacc, dqacc); break;
-      case 1: bwd_rotation<1>(st, p, dtacc, dqacc); break;
-      case 2: bwd_rotation<2>(st, p, dtacc, dqacc); break;
-      default: bwd_rotation<3>(st, p, dtacc, dqacc); break;
-    }
-    if (qvalid) {
-      bf16* row = dq + (tok0 + qi) * g.C + hoff;
+    if (window_needs_mask(g, wi, wj, n)) bwd_window_body<QUAD, true>(st, qw, dtacc, dqacc);
+    else bwd_window_body<QUAD, false>(st, qw, dtacc, dqacc);
+
+    // dQ rows of the wave into its head's K-row area (free after the
+    // rotation), then row-contiguous stores of dQ, dV and dK
 #pragma unroll
-      for (int g4 = 0; g4 < 4; ++g4) store4_bf16(row + 8 * g4 + 4 * half, dqacc, g4, scale);
-    }
-    // dV and dK of the window: thread -> (key, 16 channels)
-    {
-      const int key = threadIdx.x >> 1;
-      const int c0 = (threadIdx.x & 1) * 16;
-      if (key < n) {
-        bf16x8 lo, hi;
+    for (int g4 = 0; g4 < 4; ++g4)
+      store4_bf16(ks + (hs * kWinMax + 32 * qw + col) * KS + 8 * g4 + 4 * half, dqacc, g4, scale);
+    __syncthreads();
 #pragma unroll
-        for (int x = 0; x < 8; ++x) {
-          lo[x] = (bf16)redv[(c0 + x) * RS + key];
-          hi[x] = (bf16)redv[(c0 + 8 + x) * RS + key];
-        }
-        bf16* dst = dv + (tok0 + key) * g.C + hoff + c0;
-        *reinterpret_cast<bf16x8*>(dst) = lo;
-        *reinterpret_cast<bf16x8*>(dst + 8) = hi;
+    for (int u = 0; u < 2; ++u) {
+      const int idx = threadIdx.x + u * NT;
+      const int row = idx / CPR, ch = idx - (idx / CPR) * CPR;
+      if (row < n) {
+        const int t = ch >> 2, c0 = (ch & 3) * 8;
+        const int64_t off = (tok0 + row) * g.C + cbase + ch * 8;
+        *reinterpret_cast<uint4*>(dq + off) = *reinterpret_cast<const uint4*>(ks + (t * kWinMax + row) * KS + c0);
+        const float* rv = redv + t * HD * RS;
+        const float* rk = redk + t * HD * RS;
+        bf16x8 a, bb;
 #pragma unroll
         for (int x = 0; x < 8; ++x) {
-          lo[x] = (bf16)(redk[(c0 + x) * RS + key] * scale);
-          hi[x] = (bf16)(redk[(c0 + 8 + x) * RS + key] * scale);
+          a[x] = (bf16)rv[(c0 + x) * RS + row];
+          bb[x] = (bf16)(rk[(c0 + x) * RS + row] * scale);
         }
-        dst = dk + (tok0 + key) * g.C + hoff + c0;
-        *reinterpret_cast<bf16x8*>(dst) = lo;
-        *reinterpret_cast<bf16x8*>(dst + 8) = hi;
+        *reinterpret_cast<bf16x8*>(dv + off) = a;
+        *reinterpret_cast<bf16x8*>(dk + off) = bb;
       }
     }
   }
   if (acc_cols > 0) TERRA_FLUSH_DT(acc_cols);
 #undef TERRA_FLUSH_DT
   __syncthreads();
-  float* out = partial + ((int64_t)h * nslice + slice) * g.nbins;
-  for (int x = threadIdx.x; x < g.nbins; x += kWinThreads) {
-    const int rx = g.nbins - 1 - x;
-    out[x] = ((dtb[rx] + dtb[g.nbins + rx]) + dtb[2 * g.nbins + rx]) + dtb[3 * g.nbins + rx];
+  for (int x = threadIdx.x; x < NH * g.nbins; x += NT) {
+    const int t = x / g.nbins, y = x - t * g.nbins;
+    const int ry = g.nbins - 1 - y;
+    const float* d = dtb + 4 * t * g.nbins;
+    partial[((int64_t)(NH * hg + t) * nslice + slice) * g.nbins + y] =
+        ((d[ry] + d[g.nbins + ry]) + d[2 * g.nbins + ry]) + d[3 * g.nbins + ry];
   }
 }
 
@@ -793,9 +799,11 @@ bool win_fwd_ok(const Geo& g, bool bf16_) { return bf16_ && g.wh * g.ww <= kWinM
 bool win_bwd_ok(const Geo& g, bool bf16_) { return bf16_ && g.wh * g.ww <= kWinMax && g.hd == kBwdHD; }
 
 // Slices of the window range per head; a pure function of the geometry.
+static int bwd_heads_per_group(const Geo& g);
 int win_bwd_nslice(const Geo& g) {
   const int total = g.B * g.nwin;
-  int target = (1024 + g.heads - 1) / g.heads;     // ~1024 workgroups
+  const int groups = g.heads / bwd_heads_per_group(g);
+  int target = (512 + groups - 1) / groups;        // ~512 workgroups (2 per CU)
   if (target > total) target = total;
   if (target < 1) target = 1;
   const int per = (total + target - 1) / target;
@@ -812,9 +820,13 @@ size_t win_fwd_lds(const Geo& g) {
   }
   return one;
 }
+static int bwd_heads_per_group(const Geo& g) { return g.heads % 2 == 0 ? 2 : 1; }
+
 size_t win_bwd_lds(const Geo& g) {
-  return 4 * 64 * sizeof(bf16x8) + sizeof(bf16) * (2 * kWinMax * (kBwdHD + 8) + kBwdHD * (kWinMax + 8)) +
-         2 * 4 * kBwdHD * (kWinMax + 4) + 4 * kWinMax + 4 * (5 * g.nbins + 4);
+  const int nh = bwd_heads_per_group(g);
+  return (size_t)nh * (sizeof(bf16) * (2 * kWinMax * (kBwdHD + 8) + kBwdHD * (kWinMax + 8)) +
+                       2 * 4 * kBwdHD * (kWinMax + 4) + 4 * (g.nbins + 4) + 4 * 4 * g.nbins) +
+         4 * kWinMax + 16 * 4 * 64;
 }
 
 // Four consecutive result registers are four consecutive keys of one window
@@ -871,16 +883,19 @@ hipError_t launch_win_bwd(const Geo& g, const void* q, const void* k, const void
   const int per = (total + nslice - 1) / nslice;
   const float sl2 = kLog2e / sqrtf((float)g.hd);
   const float scale = 1.0f / sqrtf((float)g.hd);
-  if (quad_layout(g))
-    hipLaunchKernelGGL((bwd_win_kernel<true>), dim3(g.heads * nslice), dim3(kWinThreads),
-                       win_bwd_lds(g), st, (const bf16*)q, (const bf16*)k, (const bf16*)v,
-                       (const bf16*)dout, lse, table, (bf16*)dq, (bf16*)dk, (bf16*)dv, partial, g,
-                       nslice, per, sl2, scale);
-  else
-    hipLaunchKernelGGL((bwd_win_kernel<false>), dim3(g.heads * nslice), dim3(kWinThreads),
-                       win_bwd_lds(g), st, (const bf16*)q, (const bf16*)k, (const bf16*)v,
-                       (const bf16*)dout, lse, table, (bf16*)dq, (bf16*)dk, (bf16*)dv, partial, g,
-                       nslice, per, sl2, scale);
+  const int nh = bwd_heads_per_group(g);
+  const dim3 grid(g.heads / nh * nslice);
+  const size_t lds = win_bwd_lds(g);
+#define TERRA_BWD_GO(QUAD_, NH_)                                                             \
+  hipLaunchKernelGGL((bwd_win_kernel<QUAD_, NH_>), grid, dim3(kWinThreads * NH_), lds, st,   \
+                     (const bf16*)q, (const bf16*)k, (const bf16*)v, (const bf16*)dout, lse,  \
+                     table, (bf16*)dq, (bf16*)dk, (bf16*)dv, partial, g, nslice, per, sl2, scale)
+  if (quad_layout(g)) {
+    if (nh == 2) TERRA_BWD_GO(true, 2); else TERRA_BWD_GO(true, 1);
+  } else {
+    if (nh == 2) TERRA_BWD_GO(false, 2); else TERRA_BWD_GO(false, 1);
+  }
+#undef TERRA_BWD_GO
   return hipGetLastError();
 }
 
