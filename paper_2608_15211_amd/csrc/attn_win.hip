@@ -444,16 +444,38 @@ __global__ __launch_bounds__(kPairThreads) void fwd_win_pair_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Backward (head_dim 32): one workgroup per (head, run of windows).  Per
-// window: wave w owns queries [32w, 32w+32) for P, dP, D, dS and dQ, then
-// the four waves rotate over the key blocks to sum dV and dK in LDS.
+// Backward (head_dim 32): one workgroup of 4 waves per (head, run of
+// consecutive windows), two workgroups resident per CU so that one's memory
+// phase overlaps the other's matrix work.  Per window, wave w owns queries
+// [32w, 32w+32) for P, dP, D, dS and dQ; the four waves then rotate over the
+// key blocks to sum dV and dK in LDS.
 // ---------------------------------------------------------------------------
 constexpr int kBwdHD = 32;
+constexpr int kBwdKS = kBwdHD + 8;     // LDS row stride (bf16) of K, V, Q, dO rows
+constexpr int kBwdRS = kWinMax + 4;    // LDS row stride (fp32) of the dV, dK sums
+constexpr int kBwdCPR = kBwdHD / 8;    // 16-byte chunks per token row of one head
+
+// Per-lane 0/1 factors of the bias-gradient fold for the window width cols
+// (a multiple of 4 that divides 32, so window rows never straddle a 32-lane
+// half): cq is the lane's query column.
+struct FoldMask {
+  float next;     // lane l+1 holds the next query of the same window row
+  float b0, b1, b2;
+};
+
+__device__ __forceinline__ FoldMask fold_mask(int cq, int cols) {
+  FoldMask m;
+  m.next = cq < cols - 1 ? 1.0f : 0.0f;
+  m.b0 = cq < 3 ? 1.0f : 0.0f;
+  m.b1 = (cq == 1 || cq == 2) ? 1.0f : 0.0f;
+  m.b2 = cq == 2 ? 1.0f : 0.0f;
+  return m;
+}
 
 // Per-wave state of the backward for one window.
 struct BwdWave {
-  const bf16* ks;       // K rows of the wave's head in LDS [128][HD+8]
-  const bf16* vs;       // V rows [128][HD+8]
+  const bf16* ks;       // K rows in LDS [128][KS]
+  const bf16* vs;       // V rows [128][KS]
   const bf16* kts;      // K^T [HD][128+8]
   const bf16x8* ident;  // 0/1 transpose operands [4][64]: (PERM, chunk)
   const int* kinfo;     // key words of the window
@@ -463,6 +485,7 @@ struct BwdWave {
   bf16x8 qop[2], dop[2];  // Q and dO of the wave's 32 queries (row operands)
   bf16x8 de[2], qe[2];    // dO and Q with lane = channel (column operands)
   float D, lse2, scale_log2;
+  FoldMask fold;
   int qrev, qlab, nbins, col, half;
 };
 
@@ -472,16 +495,42 @@ __device__ inline bf16x8 lds_ident(const bf16x8* ident, int which) {
   return ident[which * 64 + (threadIdx.x & 63)];
 }
 
+// Value of another lane by a DPP move (0 where the source lane is absent).
+template <int CTRL>
+__device__ __forceinline__ float dpp_lane(float x) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xF, 0xF, true));
+}
+constexpr int kDppNext = 0x130;    // wave_shl:1 - lane l reads lane l+1
+constexpr int kDppPrev1 = 0x111;   // row_shr:1  - lane l reads lane l-1 (same 16-lane row)
+constexpr int kDppPrev2 = 0x112;   // row_shr:2  - lane l reads lane l-2
+
+// dS summed along the bias diagonals of one register group: registers
+// 4g..4g+3 hold four consecutive keys k..k+3 of one window row, so (query q,
+// key k+x) and (q+1, k+x+1) share a bin when q+1 is in q's window row.  A
+// chain towards lower lanes leaves in lane q the sum of the bin of (q, k);
+// the pairs it cannot reach (query column cq < x) have the bins of
+// (q', k+3) for the three first queries q' of the row, summed into `b` there.
+// Group g4 updates a[g4] and b[g4].
+__device__ __forceinline__ void fold_diag(const f32x16& ds, int g4, const FoldMask& m, f32x4& a,
+                                          f32x4& b) {
+  float f = ds[4 * g4 + 3];
+  f = ds[4 * g4 + 2] + m.next * dpp_lane<kDppNext>(f);
+  f = ds[4 * g4 + 1] + m.next * dpp_lane<kDppNext>(f);
+  a[g4] += ds[4 * g4] + m.next * dpp_lane<kDppNext>(f);
+  b[g4] += m.b0 * ds[4 * g4 + 3];
+  b[g4] += m.b1 * dpp_lane<kDppPrev1>(ds[4 * g4 + 2]);
+  b[g4] += m.b2 * dpp_lane<kDppPrev2>(ds[4 * g4 + 1]);
+}
+
 // P of key block KB for the wave's queries (lane = query, registers = keys):
 // bias in the accumulator, S = K Q^T on the matrix cores, exp2 against the
 // saved log-sum-exp (+inf for padding queries, so their P is 0).
 template <int KB, bool QUAD, bool MASK>
 __device__ __forceinline__ f32x16 bwd_p(const BwdWave& st) {
-  constexpr int HD = kBwdHD;
   f32x16 p = bias_init<QUAD, MASK>(st.kinfo, st.tab, KB, st.half, st.qrev, st.qlab, st.nbins);
 #pragma unroll
   for (int c = 0; c < 2; ++c)
-    mma16(p, *reinterpret_cast<const bf16x8*>(st.ks + (32 * KB + st.col) * (HD + 8) + 16 * c + 8 * st.half),
+    mma16(p, *reinterpret_cast<const bf16x8*>(st.ks + (32 * KB + st.col) * kBwdKS + 16 * c + 8 * st.half),
           st.qop[c]);
 #pragma unroll
   for (int r = 0; r < 16; ++r) p[r] = __builtin_amdgcn_exp2f(p[r] * st.scale_log2 - st.lse2);
@@ -490,11 +539,10 @@ __device__ __forceinline__ f32x16 bwd_p(const BwdWave& st) {
 
 template <int KB>
 __device__ __forceinline__ f32x16 bwd_dp(const BwdWave& st) {
-  constexpr int HD = kBwdHD;
   f32x16 dp = f32x16{};
 #pragma unroll
   for (int c = 0; c < 2; ++c)
-    mma16(dp, *reinterpret_cast<const bf16x8*>(st.vs + (32 * KB + st.col) * (HD + 8) + 16 * c + 8 * st.half),
+    mma16(dp, *reinterpret_cast<const bf16x8*>(st.vs + (32 * KB + st.col) * kBwdKS + 16 * c + 8 * st.half),
           st.dop[c]);
   return dp;
 }
@@ -506,23 +554,21 @@ __device__ __forceinline__ f32x16 bwd_dp(const BwdWave& st) {
 // which are added to the running sums in LDS through the accumulator input.
 // Step T = 0 starts the sums.
 template <int KB, int T, bool QUAD, bool MASK>
-__device__ __forceinline__ void bwd_step(const BwdWave& st, f32x16& dtacc, f32x16& dqacc) {
-  constexpr int RS = kWinMax + 4;
+__device__ __forceinline__ void bwd_step(const BwdWave& st, f32x4& dta, f32x4& dtb, f32x16& dqacc) {
+  constexpr int RS = kBwdRS;
   bf16x8 pb0, pb1, db0, db1;
   {
     const f32x16 p = bwd_p<KB, QUAD, MASK>(st);
     f32x16 ds = bwd_dp<KB>(st);
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      ds[r] = p[r] * (ds[r] - st.D);
-      dtacc[r] += ds[r];
-    }
+    for (int r = 0; r < 16; ++r) ds[r] = p[r] * (ds[r] - st.D);
+#pragma unroll
+    for (int g4 = 0; g4 < 4; ++g4) fold_diag(ds, g4, st.fold, dta, dtb);
     pb0 = pack_bf16(p, 0); pb1 = pack_bf16(p, 8);
     db0 = pack_bf16(ds, 0); db1 = pack_bf16(ds, 8);
   }
   mma16(dqacc, lds_perm_op(st.kts + st.col * (kWinMax + 8) + 32 * KB, st.half), db0);
   mma16(dqacc, lds_perm_op(st.kts + st.col * (kWinMax + 8) + 32 * KB + 16, st.half), db1);
-  __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
   for (int which = 0; which < 2; ++which) {
     const bf16x8 ip0 = lds_ident(st.ident, 2), ip1 = lds_ident(st.ident, 3);
@@ -542,28 +588,29 @@ __device__ __forceinline__ void bwd_step(const BwdWave& st, f32x16& dtacc, f32x1
     for (int g4 = 0; g4 < 4; ++g4)
       *reinterpret_cast<f32x4*>(red + st.col * RS + 32 * KB + 8 * g4 + 4 * st.half) =
           f32x4{part[4 * g4], part[4 * g4 + 1], part[4 * g4 + 2], part[4 * g4 + 3]};
-    __builtin_amdgcn_sched_barrier(0);
   }
 }
 
 // The four steps of the wave with query block W: key blocks W, W+1, W+2,
-// W+3 (mod 4), so that at every step each block of the head is touched by
-// exactly one wave; a barrier ends each step, so the order of additions
-// into every block is fixed.
+// W+3 (mod 4), so that at every step each block is touched by exactly one
+// wave; a barrier ends each step, so the order of additions into every
+// block is fixed.
 template <int W, bool QUAD, bool MASK>
-__device__ __forceinline__ void bwd_rotation(const BwdWave& st, f32x16 (&dtacc)[4], f32x16& dqacc) {
-  bwd_step<(W + 0) & 3, 0, QUAD, MASK>(st, dtacc[(W + 0) & 3], dqacc);
+__device__ __forceinline__ void bwd_rotation(const BwdWave& st, f32x4 (&dta)[4], f32x4 (&dtb)[4],
+                                             f32x16& dqacc) {
+  bwd_step<(W + 0) & 3, 0, QUAD, MASK>(st, dta[(W + 0) & 3], dtb[(W + 0) & 3], dqacc);
   __syncthreads();
-  bwd_step<(W + 1) & 3, 1, QUAD, MASK>(st, dtacc[(W + 1) & 3], dqacc);
+  bwd_step<(W + 1) & 3, 1, QUAD, MASK>(st, dta[(W + 1) & 3], dtb[(W + 1) & 3], dqacc);
   __syncthreads();
-  bwd_step<(W + 2) & 3, 2, QUAD, MASK>(st, dtacc[(W + 2) & 3], dqacc);
+  bwd_step<(W + 2) & 3, 2, QUAD, MASK>(st, dta[(W + 2) & 3], dtb[(W + 2) & 3], dqacc);
   __syncthreads();
-  bwd_step<(W + 3) & 3, 3, QUAD, MASK>(st, dtacc[(W + 3) & 3], dqacc);
+  bwd_step<(W + 3) & 3, 3, QUAD, MASK>(st, dta[(W + 3) & 3], dtb[(W + 3) & 3], dqacc);
   __syncthreads();
 }
 
 template <bool QUAD, bool MASK>
-__device__ __forceinline__ void bwd_window_body(BwdWave& st, int qw, f32x16 (&dtacc)[4], f32x16& dqacc) {
+__device__ __forceinline__ void bwd_window_body(BwdWave& st, int qw, f32x4 (&dta)[4], f32x4 (&dtb)[4],
+                                                f32x16& dqacc) {
   // pass 1: D = sum_k P dP over the window
   float dsum = 0.0f;
 #define TERRA_DSUM(KB)                                                          \
@@ -571,7 +618,6 @@ __device__ __forceinline__ void bwd_window_body(BwdWave& st, int qw, f32x16 (&dt
     const f32x16 pk = bwd_p<KB, QUAD, MASK>(st);                                \
     const f32x16 dk = bwd_dp<KB>(st);                                           \
     _Pragma("unroll") for (int r = 0; r < 16; ++r) dsum += pk[r] * dk[r];       \
-    __builtin_amdgcn_sched_barrier(0);                                          \
   }
   TERRA_DSUM(0)
   TERRA_DSUM(1)
@@ -579,167 +625,185 @@ __device__ __forceinline__ void bwd_window_body(BwdWave& st, int qw, f32x16 (&dt
   TERRA_DSUM(3)
 #undef TERRA_DSUM
   st.D = dsum + __shfl_xor(dsum, 32);
-  __syncthreads();   // K^T of every key block is in LDS
+  __syncthreads();   // K^T of every key block is in LDS; Q, dO staging is dead
   switch (qw) {
-    case 0: bwd_rotation<0, QUAD, MASK>(st, dtacc, dqacc); break;
-    case 1: bwd_rotation<1, QUAD, MASK>(st, dtacc, dqacc); break;
-    case 2: bwd_rotation<2, QUAD, MASK>(st, dtacc, dqacc); break;
-    default: bwd_rotation<3, QUAD, MASK>(st, dtacc, dqacc); break;
+    case 0: bwd_rotation<0, QUAD, MASK>(st, dta, dtb, dqacc); break;
+    case 1: bwd_rotation<1, QUAD, MASK>(st, dta, dtb, dqacc); break;
+    case 2: bwd_rotation<2, QUAD, MASK>(st, dta, dtb, dqacc); break;
+    default: bwd_rotation<3, QUAD, MASK>(st, dta, dtb, dqacc); break;
   }
 }
 
-// Backward, head_dim 32.  One workgroup of 4*NH waves per (NH heads, run of
-// consecutive windows); wave w works on head NH*hg + (w >> 2) and queries
-// [32*(w&3), 32*(w&3)+32).  K and V are staged in LDS with row-contiguous
-// loads (NH*64-byte segments per token row); dQ, dK and dV leave the same
-// way.  The bias-gradient sums of every register run over windows of equal
-// width and are flushed to per-wave LDS bins when the width changes (a
-// register holds the same query/key slot pair, hence the same bin, in every
-// such window).
-template <bool QUAD, int NH>
-__global__ __launch_bounds__(kWinThreads * NH) void bwd_win_kernel(
+// Rows of one window held in registers between its prefetch and its
+// staging: thread t holds 16-byte chunks t and t+256 (row = chunk / 4) of
+// K, V, Q and dO, and the log-sum-exp (log2 units) of its wave's query.
+struct BwdRows {
+  uint4 k[2], v[2], q[2], d[2];
+  float lse2;
+};
+
+__device__ __forceinline__ void bwd_load_rows(BwdRows& r, const Geo& g, int wl, int h, int qi,
+                                              const bf16* __restrict__ q, const bf16* __restrict__ k,
+                                              const bf16* __restrict__ v, const bf16* __restrict__ dout,
+                                              const float* __restrict__ lse) {
+  const int b = wl / g.nwin;
+  const int w = wl - b * g.nwin;
+  const int wi = w / g.Mw, wj = w - (w / g.Mw) * g.Mw;
+  const int n = win_rows(g, wi) * win_cols(g, wj);
+  const int64_t img0 = (int64_t)b * g.HW;
+  const int64_t tok0 = img0 + win_offset(g, wi, wj);
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int idx = threadIdx.x + u * kWinThreads;
+    const int row = idx / kBwdCPR, ch = idx % kBwdCPR;
+    r.k[u] = r.v[u] = r.q[u] = r.d[u] = make_uint4(0, 0, 0, 0);
+    if (row < n) {
+      const int64_t off = (tok0 + row) * g.C + h * kBwdHD + ch * 8;
+      r.k[u] = *reinterpret_cast<const uint4*>(k + off);
+      r.v[u] = *reinterpret_cast<const uint4*>(v + off);
+      r.q[u] = *reinterpret_cast<const uint4*>(q + off);
+      r.d[u] = *reinterpret_cast<const uint4*>(dout + off);
+    }
+  }
+  r.lse2 = qi < n ? lse[img0 * g.heads + (int64_t)h * g.HW + (tok0 - img0) + qi] * kLog2e : INFINITY;
+}
+
+// Backward, head_dim 32, every window width a multiple of 4.  K, V, Q and dO
+// arrive with row-contiguous loads one window ahead (prefetched into
+// registers while the previous window computes); Q and dO are staged in the
+// dV/dK sum areas, which are free until the rotation starts.  dQ, dK and dV
+// leave with row-contiguous stores.  The bias-gradient sums of every
+// register run over windows of equal width and are flushed to per-wave LDS
+// bins when the width changes (a register holds the same query/key slot
+// pair, hence the same bin, in every such window).
+template <bool QUAD>
+__global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
     const bf16* __restrict__ q, const bf16* __restrict__ k, const bf16* __restrict__ v,
     const bf16* __restrict__ dout, const float* __restrict__ lse, const float* __restrict__ table,
     bf16* __restrict__ dq, bf16* __restrict__ dk, bf16* __restrict__ dv,
     float* __restrict__ partial, Geo g, int nslice, int per_slice, float scale_log2, float scale) {
   constexpr int HD = kBwdHD;
-  constexpr int KS = HD + 8;
-  constexpr int RS = kWinMax + 4;
-  constexpr int NT = kWinThreads * NH;
-  constexpr int CPR = 4 * NH;                                   // 16-byte chunks per row segment
+  constexpr int KS = kBwdKS;
+  constexpr int RS = kBwdRS;
   extern __shared__ __align__(16) char smem[];
   bf16x8* ident = reinterpret_cast<bf16x8*>(smem);              // [4][64]
-  // per head: K rows, V rows, K^T, dV sums, dK sums
-  bf16* ks = reinterpret_cast<bf16*>(ident + 4 * 64);           // [NH][128][KS]
-  bf16* vs = ks + NH * kWinMax * KS;                            // [NH][128][KS]
-  bf16* kts = vs + NH * kWinMax * KS;                           // [NH][HD][128+8]
-  float* redv = reinterpret_cast<float*>(kts + NH * HD * (kWinMax + 8));   // [NH][HD][RS]
-  float* redk = redv + NH * HD * RS;                            // [NH][HD][RS]
-  int* kinfo = reinterpret_cast<int*>(redk + NH * HD * RS);     // [128]
-  float* tab = reinterpret_cast<float*>(kinfo + kWinMax);       // [NH][nbins+4]
-  float* dtb = tab + NH * (g.nbins + 4);                        // [4*NH][nbins], reversed
+  bf16* ks = reinterpret_cast<bf16*>(ident + 4 * 64);           // [128][KS] K rows, then dQ
+  bf16* vs = ks + kWinMax * KS;                                 // [128][KS] V rows
+  bf16* kts = vs + kWinMax * KS;                                // [HD][128+8] K^T
+  float* redv = reinterpret_cast<float*>(kts + HD * (kWinMax + 8));   // [HD][RS] dV sums
+  float* redk = redv + HD * RS;                                 // [HD][RS] dK sums
+  int* kinfo = reinterpret_cast<int*>(redk + HD * RS);          // [128]
+  float* tab = reinterpret_cast<float*>(kinfo + kWinMax);       // [nbins+4]
+  float* bins = tab + (g.nbins + 4);                            // [4][nbins], reversed
+  bf16* qrows = reinterpret_cast<bf16*>(redv);                  // [128][KS] Q rows (staging)
+  bf16* drows = reinterpret_cast<bf16*>(redk);                  // [128][KS] dO rows (staging)
 
-  const int ngroups = g.heads / NH;
   const int work = xcd_work(blockIdx.x, gridDim.x);
-  const int slice = work / ngroups;
-  const int hg = work - slice * ngroups;
+  const int slice = work / g.heads;
+  const int h = work - slice * g.heads;
   const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int hs = wave >> 2, qw = wave & 3;
-  const int h = NH * hg + hs;
-  const int64_t cbase = (int64_t)NH * hg * HD;
-  const int hoff = h * HD;
+  const int qw = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int half = lane >> 5, col = lane & 31;
-  float* mybins = dtb + wave * g.nbins;
+  const int qi = 32 * qw + col;
+  float* mybins = bins + qw * g.nbins;
 
-  for (int x = threadIdx.x; x < 4 * NH * g.nbins; x += NT) dtb[x] = 0.0f;
-  if (wave < 4) ident[threadIdx.x] = (wave >> 1) ? ident_op<true>(wave & 1) : ident_op<false>(wave & 1);
-  for (int x = threadIdx.x; x < NH * (g.nbins + 4); x += NT) {
-    const int t = x / (g.nbins + 4), y = x - t * (g.nbins + 4);
-    tab[x] = y < g.nbins ? table[(g.nbins - 1 - y) * g.heads + NH * hg + t] * sqrtf((float)HD) : -INFINITY;
-  }
+  for (int x = threadIdx.x; x < 4 * g.nbins; x += kWinThreads) bins[x] = 0.0f;
+  ident[threadIdx.x] = (qw >> 1) ? ident_op<true>(qw & 1) : ident_op<false>(qw & 1);
+  for (int x = threadIdx.x; x < g.nbins + 4; x += kWinThreads)
+    tab[x] = x < g.nbins ? table[(g.nbins - 1 - x) * g.heads + h] * sqrtf((float)HD) : -INFINITY;
 
-  f32x16 dtacc[4];
+  f32x4 dta[4], dtb[4];
 #pragma unroll
-  for (int kb = 0; kb < 4; ++kb) dtacc[kb] = f32x16{};
+  for (int kb = 0; kb < 4; ++kb) dta[kb] = dtb[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
   int acc_cols = 0;
-  // (hh is made opaque so that the per-register slots are not hoisted out of
-  // the window loop into live registers)
+  // Register (kb, g4) of lane q holds, in dta, the bin of (q, k) with k the
+  // group's first key, and in dtb (query columns 0..2 only) the bin of
+  // (q, k+3); hh is made opaque so that the bins are not hoisted out of the
+  // window loop into live registers.
 #define TERRA_FLUSH_DT(cw)                                                              \
   {                                                                                     \
     const float rcw = 1.0f / (float)(cw);                                               \
-    const int qs_ = 32 * qw + col;                                                      \
-    const int aq = (int)(((float)qs_ + 0.5f) * rcw), cq = qs_ - aq * (cw);              \
+    const int aq = (int)(((float)qi + 0.5f) * rcw), cq = qi - aq * (cw);                \
     int hh = half;                                                                      \
     asm volatile("" : "+v"(hh));                                                        \
     _Pragma("unroll") for (int kb = 0; kb < 4; ++kb)                                    \
-    _Pragma("unroll") for (int r = 0; r < 16; ++r) {                                    \
-      const int kk = 32 * kb + acc_row(r, hh);                                          \
+    _Pragma("unroll") for (int g4 = 0; g4 < 4; ++g4) {                                  \
+      const int kk = 32 * kb + 8 * g4 + 4 * hh;                                         \
       const int ak = (int)(((float)kk + 0.5f) * rcw), ck = kk - ak * (cw);              \
-      if (aq < g.wh && ak < g.wh)                                                       \
-        atomicAdd(&mybins[g.nbins - 1 - ((aq - ak + g.wh - 1) * g.bstride +             \
-                                         (cq - ck + g.ww - 1))], dtacc[kb][r]);         \
-      dtacc[kb][r] = 0.0f;                                                              \
+      if (aq < g.wh && ak < g.wh) {                                                     \
+        const int bin = g.nbins - 1 - ((aq - ak + g.wh - 1) * g.bstride + (cq - ck + g.ww - 1)); \
+        atomicAdd(&mybins[bin], dta[kb][g4]);                                           \
+        if (cq < 3) atomicAdd(&mybins[bin + 3], dtb[kb][g4]);                           \
+      }                                                                                 \
+      dta[kb][g4] = 0.0f;                                                               \
+      dtb[kb][g4] = 0.0f;                                                               \
     }                                                                                   \
   }
 
   const int total = g.B * g.nwin;
   const int wbeg = slice * per_slice;
   const int wend = min(total, wbeg + per_slice);
+  BwdRows rows;
+  if (wbeg < wend) bwd_load_rows(rows, g, wbeg, h, qi, q, k, v, dout, lse);
   for (int wl = wbeg; wl < wend; ++wl) {
     const int b = wl / g.nwin;
     const int w = wl - b * g.nwin;
     const int wi = w / g.Mw, wj = w - (w / g.Mw) * g.Mw;
     const int cols = win_cols(g, wj);
     const int n = win_rows(g, wi) * cols;
-    const int64_t img0 = (int64_t)b * g.HW;
-    const int64_t tok0 = img0 + win_offset(g, wi, wj);
+    const int64_t tok0 = (int64_t)b * g.HW + win_offset(g, wi, wj);
     if (cols != acc_cols) {          // uniform across the workgroup
       if (acc_cols > 0) TERRA_FLUSH_DT(acc_cols);
       acc_cols = cols;
     }
-    const int qi = 32 * qw + col;
-    const bool qvalid = qi < n;
-    // global loads: K, V rows (row-contiguous), the wave's Q and dO rows, LSE
-    uint4 kr[2], vr[2];
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int idx = threadIdx.x + u * NT;
-      const int row = idx / CPR, ch = idx - (idx / CPR) * CPR;
-      kr[u] = vr[u] = make_uint4(0, 0, 0, 0);
-      if (row < n) {
-        const int64_t off = (tok0 + row) * g.C + cbase + ch * 8;
-        kr[u] = *reinterpret_cast<const uint4*>(k + off);
-        vr[u] = *reinterpret_cast<const uint4*>(v + off);
-      }
-    }
-    BwdWave st;
-#pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      st.qop[c] = qvalid ? *reinterpret_cast<const bf16x8*>(q + (tok0 + qi) * g.C + hoff + 16 * c + 8 * half)
-                         : zero8();
-      st.dop[c] = qvalid ? *reinterpret_cast<const bf16x8*>(dout + (tok0 + qi) * g.C + hoff + 16 * c + 8 * half)
-                         : zero8();
-    }
-    st.lse2 = qvalid ? lse[img0 * g.heads + (int64_t)h * g.HW + (tok0 - img0) + qi] * kLog2e : INFINITY;
 
     __syncthreads();   // the previous window is done with LDS
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
-      const int idx = threadIdx.x + u * NT;
-      const int row = idx / CPR, ch = idx - (idx / CPR) * CPR;
-      const int t = ch >> 2, c0 = (ch & 3) * 8;
-      *reinterpret_cast<uint4*>(ks + (t * kWinMax + row) * KS + c0) = kr[u];
-      *reinterpret_cast<uint4*>(vs + (t * kWinMax + row) * KS + c0) = vr[u];
+      const int idx = threadIdx.x + u * kWinThreads;
+      const int row = idx / kBwdCPR, c0 = (idx % kBwdCPR) * 8;
+      *reinterpret_cast<uint4*>(ks + row * KS + c0) = rows.k[u];
+      *reinterpret_cast<uint4*>(vs + row * KS + c0) = rows.v[u];
+      *reinterpret_cast<uint4*>(qrows + row * KS + c0) = rows.q[u];
+      *reinterpret_cast<uint4*>(drows + row * KS + c0) = rows.d[u];
     }
     if (threadIdx.x < kWinMax) kinfo[threadIdx.x] = win_token_info(g, wi, wj, cols, threadIdx.x, n);
+    BwdWave st;
+    st.lse2 = rows.lse2;
     __syncthreads();
+    if (wl + 1 < wend) bwd_load_rows(rows, g, wl + 1, h, qi, q, k, v, dout, lse);
 
-    st.ks = ks + hs * kWinMax * KS;
-    st.vs = vs + hs * kWinMax * KS;
-    st.kts = kts + hs * HD * (kWinMax + 8);
+    st.ks = ks;
+    st.vs = vs;
+    st.kts = kts;
     st.ident = ident;
     st.kinfo = kinfo;
-    st.tab = tab + hs * (g.nbins + 4);
-    st.redv = redv + hs * HD * RS;
-    st.redk = redk + hs * HD * RS;
+    st.tab = tab;
+    st.redv = redv;
+    st.redk = redk;
     st.scale_log2 = scale_log2;
     st.nbins = g.nbins;
     st.col = col;
     st.half = half;
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      st.qop[c] = *reinterpret_cast<const bf16x8*>(qrows + qi * KS + 16 * c + 8 * half);
+      st.dop[c] = *reinterpret_cast<const bf16x8*>(drows + qi * KS + 16 * c + 8 * half);
+    }
     {
-      // K^T: wave (hs, qw) transposes keys [32qw, 32qw+32) of its head
-      const bf16* r = st.ks + (32 * qw + col) * KS + 8 * half;
+      // K^T: wave qw transposes keys [32qw, 32qw+32)
+      const bf16* r = ks + qi * KS + 8 * half;
       const f32x16 t = mfma_transpose(*reinterpret_cast<const bf16x8*>(r),
                                       *reinterpret_cast<const bf16x8*>(r + 16),
                                       lds_ident(ident, 0), lds_ident(ident, 1));
 #pragma unroll
       for (int g4 = 0; g4 < 4; ++g4)
-        store4_bf16(kts + (hs * HD + col) * (kWinMax + 8) + 32 * qw + 8 * g4 + 4 * half, t, g4, 1.0f);
+        store4_bf16(kts + col * (kWinMax + 8) + 32 * qw + 8 * g4 + 4 * half, t, g4, 1.0f);
     }
-    const int qinf = qvalid ? win_token_info(g, wi, wj, cols, qi, n) : 0;
+    const int qinf = qi < n ? win_token_info(g, wi, wj, cols, qi, n) : 0;
     st.qlab = qinf >> 24;
     st.qrev = g.nbins - 1 - ((qinf & 0xFFFFFF) + (g.wh - 1) * g.bstride + (g.ww - 1));
+    st.fold = fold_mask(qi % cols, cols);
     {
       const bf16x8 in0 = lds_ident(ident, 0), in1 = lds_ident(ident, 1);
       const f32x16 te = mfma_transpose(st.dop[0], st.dop[1], in0, in1);
@@ -750,30 +814,26 @@ __global__ __launch_bounds__(kWinThreads * NH) void bwd_win_kernel(
       st.qe[1] = pack_bf16(tq, 8);
     }
     f32x16 dqacc = f32x16{};
-    if (window_needs_mask(g, wi, wj, n)) bwd_window_body<QUAD, true>(st, qw, dtacc, dqacc);
-    else bwd_window_body<QUAD, false>(st, qw, dtacc, dqacc);
+    if (window_needs_mask(g, wi, wj, n)) bwd_window_body<QUAD, true>(st, qw, dta, dtb, dqacc);
+    else bwd_window_body<QUAD, false>(st, qw, dta, dtb, dqacc);
 
-    // dQ rows of the wave into its head's K-row area (free after the
-    // rotation), then row-contiguous stores of dQ, dV and dK
+    // dQ rows of the wave into the K-row area (free after the rotation),
+    // then row-contiguous stores of dQ, dV and dK
 #pragma unroll
-    for (int g4 = 0; g4 < 4; ++g4)
-      store4_bf16(ks + (hs * kWinMax + 32 * qw + col) * KS + 8 * g4 + 4 * half, dqacc, g4, scale);
+    for (int g4 = 0; g4 < 4; ++g4) store4_bf16(ks + qi * KS + 8 * g4 + 4 * half, dqacc, g4, scale);
     __syncthreads();
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
-      const int idx = threadIdx.x + u * NT;
-      const int row = idx / CPR, ch = idx - (idx / CPR) * CPR;
+      const int idx = threadIdx.x + u * kWinThreads;
+      const int row = idx / kBwdCPR, c0 = (idx % kBwdCPR) * 8;
       if (row < n) {
-        const int t = ch >> 2, c0 = (ch & 3) * 8;
-        const int64_t off = (tok0 + row) * g.C + cbase + ch * 8;
-        *reinterpret_cast<uint4*>(dq + off) = *reinterpret_cast<const uint4*>(ks + (t * kWinMax + row) * KS + c0);
-        const float* rv = redv + t * HD * RS;
-        const float* rk = redk + t * HD * RS;
+        const int64_t off = (tok0 + row) * g.C + h * HD + c0;
+        *reinterpret_cast<uint4*>(dq + off) = *reinterpret_cast<const uint4*>(ks + row * KS + c0);
         bf16x8 a, bb;
 #pragma unroll
         for (int x = 0; x < 8; ++x) {
-          a[x] = (bf16)rv[(c0 + x) * RS + row];
-          bb[x] = (bf16)(rk[(c0 + x) * RS + row] * scale);
+          a[x] = (bf16)redv[(c0 + x) * RS + row];
+          bb[x] = (bf16)(redk[(c0 + x) * RS + row] * scale);
         }
         *reinterpret_cast<bf16x8*>(dv + off) = a;
         *reinterpret_cast<bf16x8*>(dk + off) = bb;
@@ -783,12 +843,10 @@ __global__ __launch_bounds__(kWinThreads * NH) void bwd_win_kernel(
   if (acc_cols > 0) TERRA_FLUSH_DT(acc_cols);
 #undef TERRA_FLUSH_DT
   __syncthreads();
-  for (int x = threadIdx.x; x < NH * g.nbins; x += NT) {
-    const int t = x / g.nbins, y = x - t * g.nbins;
+  for (int y = threadIdx.x; y < g.nbins; y += kWinThreads) {
     const int ry = g.nbins - 1 - y;
-    const float* d = dtb + 4 * t * g.nbins;
-    partial[((int64_t)(NH * hg + t) * nslice + slice) * g.nbins + y] =
-        ((d[ry] + d[g.nbins + ry]) + d[2 * g.nbins + ry]) + d[3 * g.nbins + ry];
+    partial[((int64_t)h * nslice + slice) * g.nbins + y] =
+        ((bins[ry] + bins[g.nbins + ry]) + bins[2 * g.nbins + ry]) + bins[3 * g.nbins + ry];
   }
 }
 
@@ -796,14 +854,26 @@ __global__ __launch_bounds__(kWinThreads * NH) void bwd_win_kernel(
 // Host side.
 // ---------------------------------------------------------------------------
 bool win_fwd_ok(const Geo& g, bool bf16_) { return bf16_ && g.wh * g.ww <= kWinMax && (g.hd == 32 || g.hd == 64); }
-bool win_bwd_ok(const Geo& g, bool bf16_) { return bf16_ && g.wh * g.ww <= kWinMax && g.hd == kBwdHD; }
+// The backward folds the bias gradient along groups of four keys of one
+// window row across lanes, so every window width must be a multiple of 4
+// that divides 32 (window rows never straddle a 32-lane half).
+static bool fold_width(int w) { return w == 4 || w == 8 || w == 16 || w == 32; }
+bool win_bwd_ok(const Geo& g, bool bf16_) {
+  return bf16_ && g.wh * g.ww <= kWinMax && g.hd == kBwdHD && fold_width(g.ww) &&
+         (g.W % g.ww == 0 || fold_width(g.W % g.ww));
+}
 
 // Slices of the window range per head; a pure function of the geometry.
-static int bwd_heads_per_group(const Geo& g);
+size_t win_bwd_lds(const Geo& g);
+
+// Slices of the window range per head: one round of workgroups over the 256
+// CUs, two resident per CU (two waves per SIMD; the LDS plan fits twice in
+// 160 KB), so that one workgroup's memory phase overlaps the other's matrix
+// work.  A pure function of the geometry.
 int win_bwd_nslice(const Geo& g) {
   const int total = g.B * g.nwin;
-  const int groups = g.heads / bwd_heads_per_group(g);
-  int target = (512 + groups - 1) / groups;        // ~512 workgroups (2 per CU)
+  const int per_cu = win_bwd_lds(g) * 2 <= 160 * 1024 ? 2 : 1;
+  int target = 256 * per_cu / g.heads;
   if (target > total) target = total;
   if (target < 1) target = 1;
   const int per = (total + target - 1) / target;
@@ -820,13 +890,9 @@ size_t win_fwd_lds(const Geo& g) {
   }
   return one;
 }
-static int bwd_heads_per_group(const Geo& g) { return g.heads % 2 == 0 ? 2 : 1; }
-
 size_t win_bwd_lds(const Geo& g) {
-  const int nh = bwd_heads_per_group(g);
-  return (size_t)nh * (sizeof(bf16) * (2 * kWinMax * (kBwdHD + 8) + kBwdHD * (kWinMax + 8)) +
-                       2 * 4 * kBwdHD * (kWinMax + 4) + 4 * (g.nbins + 4) + 4 * 4 * g.nbins) +
-         4 * kWinMax + 16 * 4 * 64;
+  return 16 * 4 * 64 + sizeof(bf16) * (2 * kWinMax * kBwdKS + kBwdHD * (kWinMax + 8)) +
+         sizeof(float) * 2 * kBwdHD * kBwdRS + 4 * kWinMax + 4 * (g.nbins + 4) + 4 * 4 * g.nbins;
 }
 
 // Four consecutive result registers are four consecutive keys of one window
@@ -883,19 +949,16 @@ hipError_t launch_win_bwd(const Geo& g, const void* q, const void* k, const void
   const int per = (total + nslice - 1) / nslice;
   const float sl2 = kLog2e / sqrtf((float)g.hd);
   const float scale = 1.0f / sqrtf((float)g.hd);
-  const int nh = bwd_heads_per_group(g);
-  const dim3 grid(g.heads / nh * nslice);
+  const dim3 grid(g.heads * nslice);
   const size_t lds = win_bwd_lds(g);
-#define TERRA_BWD_GO(QUAD_, NH_)                                                             \
-  hipLaunchKernelGGL((bwd_win_kernel<QUAD_, NH_>), grid, dim3(kWinThreads * NH_), lds, st,   \
-                     (const bf16*)q, (const bf16*)k, (const bf16*)v, (const bf16*)dout, lse,  \
-                     table, (bf16*)dq, (bf16*)dk, (bf16*)dv, partial, g, nslice, per, sl2, scale)
-  if (quad_layout(g)) {
-    if (nh == 2) TERRA_BWD_GO(true, 2); else TERRA_BWD_GO(true, 1);
-  } else {
-    if (nh == 2) TERRA_BWD_GO(false, 2); else TERRA_BWD_GO(false, 1);
-  }
-#undef TERRA_BWD_GO
+  if (quad_layout(g))
+    hipLaunchKernelGGL((bwd_win_kernel<true>), grid, dim3(kWinThreads), lds, st, (const bf16*)q,
+                       (const bf16*)k, (const bf16*)v, (const bf16*)dout, lse, table, (bf16*)dq,
+                       (bf16*)dk, (bf16*)dv, partial, g, nslice, per, sl2, scale);
+  else
+    hipLaunchKernelGGL((bwd_win_kernel<false>), grid, dim3(kWinThreads), lds, st, (const bf16*)q,
+                       (const bf16*)k, (const bf16*)v, (const bf16*)dout, lse, table, (bf16*)dq,
+                       (bf16*)dk, (bf16*)dv, partial, g, nslice, per, sl2, scale);
   return hipGetLastError();
 }
 

@@ -149,6 +149,16 @@ EDGE = [
     ("unit_windows", ts.small_config("e6", "bf16", 1, 4, 6, 1, 32, 1, 1, 0, 0, 0)),
     # periodic longitude only shift
     ("lon_shift", ts.small_config("e7", "f32", 1, 8, 24, 1, 32, 8, 8, 0, 5, 1)),
+    # window rows of 12 (query rows straddle 32-query blocks), ragged height, odd heads
+    ("w12_ragged_rows", ts.small_config("e8", "bf16", 1, 21, 60, 3, 32, 8, 12, 4, 6, 1)),
+    # widths 20 and 4, both wraps masked, two images
+    ("w20_both_masks", ts.small_config("e9", "bf16", 2, 12, 44, 2, 32, 4, 20, 2, 10, 3)),
+    # widths 16 and 4, ragged height, odd heads
+    ("w16_ragged", ts.small_config("e11", "bf16", 1, 21, 52, 3, 32, 8, 16, 4, 8, 1)),
+    # 8x8 windows with the longitude wrap masked too
+    ("w8_lon_mask", ts.small_config("e12", "bf16", 2, 16, 40, 2, 32, 8, 8, 4, 4, 3)),
+    # narrow 16x4 windows, ragged height
+    ("tall_w4", ts.small_config("e10", "bf16", 1, 37, 28, 2, 32, 16, 4, 8, 2, 1)),
 ]
 
 
@@ -182,8 +192,9 @@ def test_large_logits_stay_finite():
         _assert_close("LSE", _host(got["lse"][:, :, s:s + n]), ref[w][1], cfg)
 
 
-def test_bias_gradient_is_bit_reproducible():
-    cfg = ts.CONFIGS["c3_bf16_85x180_w12"]
+@pytest.mark.parametrize("name", ["c2_bf16_128x256_w8", "c3_bf16_85x180_w12"])
+def test_bias_gradient_is_bit_reproducible(name):
+    cfg = ts.CONFIGS[name]
     inp = ts.make_inputs(cfg)
     a = _run_gpu(cfg, inp)["dt"].cpu().numpy()
     b = _run_gpu(cfg, inp)["dt"].cpu().numpy()
