@@ -115,8 +115,8 @@ int terra_winattn_fwd(const terra_geom* g, int dtype, const void* q,
                       const void* k, const void* v, const float* bias_table,
                       void* o, float* lse, void* stream);
 
-/* Bytes of device workspace terra_winattn_bwd needs for this geometry
- * (0 on invalid input). */
+/* Bytes of device workspace terra_winattn_bwd (and terra_winattn_bwd_nhwc)
+ * needs for this geometry (0 on invalid input). */
 size_t terra_winattn_bwd_workspace_bytes(const terra_geom* g, int dtype);
 
 /* Shifted-window attention backward.  Inputs are the forward's inputs, its
@@ -136,6 +136,30 @@ int terra_winattn_bwd(const terra_geom* g, int dtype, const void* q,
                       const float* bias_table, void* dq, void* dk, void* dv,
                       float* dbias_table, void* workspace,
                       size_t workspace_bytes, void* stream);
+
+/* Fused route + attention forward: the same computation as
+ * terra_winattn_fwd with q, k, v and o as NHWC tensors read and written in
+ * place (Sec. IV-D route and its inverse folded into the kernels: row t of
+ * window (i, j) is read from, and its output written to, the grid point
+ * ((i*wh + t/cols + sh) mod H, (j*ww + t%cols + sw) mod W)).  lse is
+ * float32 B x heads x (H*W) in NHWC token order (index u*W + v).  Results
+ * equal terra_window_unroute of the window-major call's results, bit for
+ * bit. */
+int terra_winattn_fwd_nhwc(const terra_geom* g, int dtype, const void* q,
+                           const void* k, const void* v,
+                           const float* bias_table, void* o, float* lse,
+                           void* stream);
+
+/* Fused route + attention backward: terra_winattn_bwd with q, k, v, o,
+ * dout, dq, dk, dv as NHWC tensors and lse in NHWC token order, as written
+ * by terra_winattn_fwd_nhwc.  Needs the workspace of
+ * terra_winattn_bwd_workspace_bytes (the same size for both layouts). */
+int terra_winattn_bwd_nhwc(const terra_geom* g, int dtype, const void* q,
+                           const void* k, const void* v, const void* o,
+                           const void* dout, const float* lse,
+                           const float* bias_table, void* dq, void* dk,
+                           void* dv, float* dbias_table, void* workspace,
+                           size_t workspace_bytes, void* stream);
 
 /* Static string naming a status code. */
 const char* terra_status_string(int status);

@@ -9,7 +9,8 @@ the functions raise; there is no fallback.
 Entry points (same names as the C ABI):
     terra_validate_geometry, terra_window_count, terra_window_layout,
     terra_window_route, terra_window_unroute, terra_winattn_fwd,
-    terra_winattn_bwd_workspace_bytes, terra_winattn_bwd
+    terra_winattn_bwd_workspace_bytes, terra_winattn_bwd,
+    terra_winattn_fwd_nhwc, terra_winattn_bwd_nhwc (route fused in)
 """
 
 import ctypes
@@ -65,15 +66,17 @@ def lib():
     L.terra_window_route.argtypes = [G, i32, vp, vp, vp]
     L.terra_window_unroute.argtypes = [G, i32, vp, vp, vp]
     L.terra_winattn_fwd.argtypes = [G, i32, vp, vp, vp, vp, vp, vp, vp]
+    L.terra_winattn_fwd_nhwc.argtypes = [G, i32, vp, vp, vp, vp, vp, vp, vp]
     L.terra_winattn_bwd_workspace_bytes.argtypes = [G, i32]
     L.terra_winattn_bwd_workspace_bytes.restype = sz
     L.terra_winattn_bwd.argtypes = [G, i32] + [vp] * 12 + [sz, vp]
+    L.terra_winattn_bwd_nhwc.argtypes = [G, i32] + [vp] * 12 + [sz, vp]
     L.terra_status_string.argtypes = [i32]
     L.terra_status_string.restype = ctypes.c_char_p
     L.terra_last_error.restype = ctypes.c_char_p
     for name in ("terra_validate_geometry", "terra_window_count", "terra_window_layout",
                  "terra_window_route", "terra_window_unroute", "terra_winattn_fwd",
-                 "terra_winattn_bwd"):
+                 "terra_winattn_bwd", "terra_winattn_fwd_nhwc", "terra_winattn_bwd_nhwc"):
         getattr(L, name).restype = i32
     _lib = L
     return L
@@ -177,27 +180,22 @@ def terra_window_unroute(y_win, g, out=None):
     return out
 
 
-def terra_winattn_fwd(q, k, v, table, g, out=None, lse=None):
-    """Window-major q, k, v (B,H*W,C) and float32 bias table
-    (2wh-1,2ww-1,heads) -> (O (B,H*W,C), LSE float32 (B,heads,H*W))."""
+def _attn_fwd(fn, shape, q, k, v, table, g, out, lse):
     import torch
     gg = _geom(g)
     n, nl, nt = _sizes(gg)
     dt = q.dtype
     if out is None:
-        out = torch.empty((gg.B, gg.H * gg.W, gg.C), dtype=dt, device=q.device)
+        out = torch.empty(shape(gg), dtype=dt, device=q.device)
     if lse is None:
         lse = torch.empty((gg.B, gg.heads, gg.H * gg.W), dtype=torch.float32, device=q.device)
-    _check(lib().terra_winattn_fwd(
-        ctypes.byref(gg), _dtype_code(dt), _dev(q, "q", dt, n), _dev(k, "k", dt, n),
-        _dev(v, "v", dt, n), _dev(table, "table", torch.float32, nt), _dev(out, "o", dt, n),
-        _dev(lse, "lse", torch.float32, nl), _stream()))
+    _check(fn(ctypes.byref(gg), _dtype_code(dt), _dev(q, "q", dt, n), _dev(k, "k", dt, n),
+              _dev(v, "v", dt, n), _dev(table, "table", torch.float32, nt), _dev(out, "o", dt, n),
+              _dev(lse, "lse", torch.float32, nl), _stream()))
     return out, lse
 
 
-def terra_winattn_bwd(q, k, v, o, dout, lse, table, g, out=None, workspace=None):
-    """Returns (dQ, dK, dV, dTable).  `out` may hold preallocated
-    (dq, dk, dv, dtable); `workspace` a uint8 device tensor."""
+def _attn_bwd(fn, q, k, v, o, dout, lse, table, g, out, workspace):
     import torch
     gg = _geom(g)
     n, nl, nt = _sizes(gg)
@@ -210,10 +208,34 @@ def terra_winattn_bwd(q, k, v, o, dout, lse, table, g, out=None, workspace=None)
     need = terra_winattn_bwd_workspace_bytes(gg, code)
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
-    _check(lib().terra_winattn_bwd(
-        ctypes.byref(gg), code, _dev(q, "q", dt, n), _dev(k, "k", dt, n), _dev(v, "v", dt, n),
-        _dev(o, "o", dt, n), _dev(dout, "dout", dt, n), _dev(lse, "lse", torch.float32, nl),
-        _dev(table, "table", torch.float32, nt), _dev(dq, "dq", dt, n), _dev(dk, "dk", dt, n),
-        _dev(dv, "dv", dt, n), _dev(dtab, "dtable", torch.float32, nt),
-        _dev(workspace, "workspace"), ctypes.c_size_t(workspace.numel()), _stream()))
+    _check(fn(ctypes.byref(gg), code, _dev(q, "q", dt, n), _dev(k, "k", dt, n), _dev(v, "v", dt, n),
+              _dev(o, "o", dt, n), _dev(dout, "dout", dt, n), _dev(lse, "lse", torch.float32, nl),
+              _dev(table, "table", torch.float32, nt), _dev(dq, "dq", dt, n), _dev(dk, "dk", dt, n),
+              _dev(dv, "dv", dt, n), _dev(dtab, "dtable", torch.float32, nt),
+              _dev(workspace, "workspace"), ctypes.c_size_t(workspace.numel()), _stream()))
     return dq, dk, dv, dtab
+
+
+def terra_winattn_fwd(q, k, v, table, g, out=None, lse=None):
+    """Window-major q, k, v (B,H*W,C) and float32 bias table
+    (2wh-1,2ww-1,heads) -> (O (B,H*W,C), LSE float32 (B,heads,H*W))."""
+    return _attn_fwd(lib().terra_winattn_fwd, lambda gg: (gg.B, gg.H * gg.W, gg.C),
+                     q, k, v, table, g, out, lse)
+
+
+def terra_winattn_fwd_nhwc(q, k, v, table, g, out=None, lse=None):
+    """NHWC q, k, v (B,H,W,C), route fused in -> (O (B,H,W,C), LSE float32
+    (B,heads,H*W) in NHWC token order)."""
+    return _attn_fwd(lib().terra_winattn_fwd_nhwc, lambda gg: (gg.B, gg.H, gg.W, gg.C),
+                     q, k, v, table, g, out, lse)
+
+
+def terra_winattn_bwd(q, k, v, o, dout, lse, table, g, out=None, workspace=None):
+    """Window-major tensors.  Returns (dQ, dK, dV, dTable).  `out` may hold
+    preallocated (dq, dk, dv, dtable); `workspace` a uint8 device tensor."""
+    return _attn_bwd(lib().terra_winattn_bwd, q, k, v, o, dout, lse, table, g, out, workspace)
+
+
+def terra_winattn_bwd_nhwc(q, k, v, o, dout, lse, table, g, out=None, workspace=None):
+    """As terra_winattn_bwd with NHWC tensors and NHWC-ordered LSE."""
+    return _attn_bwd(lib().terra_winattn_bwd_nhwc, q, k, v, o, dout, lse, table, g, out, workspace)

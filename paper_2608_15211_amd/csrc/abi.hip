@@ -11,11 +11,12 @@
 namespace terra {
 hipError_t launch_route(const Geo& g, int row_bytes, const void* src, void* dst, bool forward,
                         hipStream_t stream);
-hipError_t launch_attn_fwd(const Geo& g, bool bf16, const void* q, const void* k, const void* v,
-                           const float* table, void* o, float* lse, hipStream_t st);
-hipError_t launch_attn_bwd(const Geo& g, bool bf16, const void* q, const void* k, const void* v,
-                           const void* o, const void* dout, const float* lse, const float* table,
-                           void* dq, void* dk, void* dv, float* dtab, void* ws, hipStream_t st);
+hipError_t launch_attn_fwd(const Geo& g, bool bf16, bool nhwc, const void* q, const void* k,
+                           const void* v, const float* table, void* o, float* lse, hipStream_t st);
+hipError_t launch_attn_bwd(const Geo& g, bool bf16, bool nhwc, const void* q, const void* k,
+                           const void* v, const void* o, const void* dout, const float* lse,
+                           const float* table, void* dq, void* dk, void* dv, float* dtab, void* ws,
+                           hipStream_t st);
 size_t bwd_workspace(const Geo& g, bool bf16);
 size_t attn_max_lds(const Geo& g, bool bf16);
 }  // namespace terra
@@ -182,16 +183,52 @@ int terra_window_unroute(const terra_geom* g, int dtype, const void* y_win, void
   return route_common(g, dtype, y_win, x_nhwc, false, stream);
 }
 
-int terra_winattn_fwd(const terra_geom* g, int dtype, const void* q, const void* k, const void* v,
-                      const float* bias_table, void* o, float* lse, void* stream) {
+}  // extern "C"
+
+static int attn_fwd_common(const terra_geom* g, int dtype, bool nhwc, const void* q, const void* k,
+                           const void* v, const float* bias_table, void* o, float* lse,
+                           void* stream) {
   int s = check_attn(g, dtype);
   if (s) return s;
   if (!q || !k || !v || !bias_table || !o || !lse)
     return fail(TERRA_ERR_INVALID, "tensor pointer is NULL");
   terra::Geo G = make_geo(g);
-  return hip_status(terra::launch_attn_fwd(G, dtype == TERRA_BF16, q, k, v, bias_table, o, lse,
+  return hip_status(terra::launch_attn_fwd(G, dtype == TERRA_BF16, nhwc, q, k, v, bias_table, o, lse,
                                            (hipStream_t)stream),
-                    "terra_winattn_fwd launch");
+                    nhwc ? "terra_winattn_fwd_nhwc launch" : "terra_winattn_fwd launch");
+}
+
+static int attn_bwd_common(const terra_geom* g, int dtype, bool nhwc, const void* q, const void* k,
+                           const void* v, const void* o, const void* dout, const float* lse,
+                           const float* bias_table, void* dq, void* dk, void* dv,
+                           float* dbias_table, void* workspace, size_t workspace_bytes,
+                           void* stream) {
+  int s = check_attn(g, dtype);
+  if (s) return s;
+  if (!q || !k || !v || !o || !dout || !lse || !bias_table || !dq || !dk || !dv || !dbias_table)
+    return fail(TERRA_ERR_INVALID, "tensor pointer is NULL");
+  terra::Geo G = make_geo(g);
+  const size_t need = terra::bwd_workspace(G, dtype == TERRA_BF16);
+  if (!workspace || workspace_bytes < need)
+    return fail(TERRA_ERR_WORKSPACE, "workspace of %zu bytes given, %zu needed",
+                workspace ? workspace_bytes : (size_t)0, need);
+  return hip_status(terra::launch_attn_bwd(G, dtype == TERRA_BF16, nhwc, q, k, v, o, dout, lse,
+                                           bias_table, dq, dk, dv, dbias_table, workspace,
+                                           (hipStream_t)stream),
+                    nhwc ? "terra_winattn_bwd_nhwc launch" : "terra_winattn_bwd launch");
+}
+
+extern "C" {
+
+int terra_winattn_fwd(const terra_geom* g, int dtype, const void* q, const void* k, const void* v,
+                      const float* bias_table, void* o, float* lse, void* stream) {
+  return attn_fwd_common(g, dtype, false, q, k, v, bias_table, o, lse, stream);
+}
+
+int terra_winattn_fwd_nhwc(const terra_geom* g, int dtype, const void* q, const void* k,
+                           const void* v, const float* bias_table, void* o, float* lse,
+                           void* stream) {
+  return attn_fwd_common(g, dtype, true, q, k, v, bias_table, o, lse, stream);
 }
 
 size_t terra_winattn_bwd_workspace_bytes(const terra_geom* g, int dtype) {
@@ -203,19 +240,17 @@ int terra_winattn_bwd(const terra_geom* g, int dtype, const void* q, const void*
                       const void* o, const void* dout, const float* lse, const float* bias_table,
                       void* dq, void* dk, void* dv, float* dbias_table, void* workspace,
                       size_t workspace_bytes, void* stream) {
-  int s = check_attn(g, dtype);
-  if (s) return s;
-  if (!q || !k || !v || !o || !dout || !lse || !bias_table || !dq || !dk || !dv || !dbias_table)
-    return fail(TERRA_ERR_INVALID, "tensor pointer is NULL");
-  terra::Geo G = make_geo(g);
-  const size_t need = terra::bwd_workspace(G, dtype == TERRA_BF16);
-  if (!workspace || workspace_bytes < need)
-    return fail(TERRA_ERR_WORKSPACE, "workspace of %zu bytes given, %zu needed",
-                workspace ? workspace_bytes : (size_t)0, need);
-  return hip_status(terra::launch_attn_bwd(G, dtype == TERRA_BF16, q, k, v, o, dout, lse,
-                                           bias_table, dq, dk, dv, dbias_table, workspace,
-                                           (hipStream_t)stream),
-                    "terra_winattn_bwd launch");
+  return attn_bwd_common(g, dtype, false, q, k, v, o, dout, lse, bias_table, dq, dk, dv,
+                         dbias_table, workspace, workspace_bytes, stream);
+}
+
+int terra_winattn_bwd_nhwc(const terra_geom* g, int dtype, const void* q, const void* k,
+                           const void* v, const void* o, const void* dout, const float* lse,
+                           const float* bias_table, void* dq, void* dk, void* dv,
+                           float* dbias_table, void* workspace, size_t workspace_bytes,
+                           void* stream) {
+  return attn_bwd_common(g, dtype, true, q, k, v, o, dout, lse, bias_table, dq, dk, dv,
+                         dbias_table, workspace, workspace_bytes, stream);
 }
 
 const char* terra_status_string(int status) {

@@ -36,9 +36,9 @@ bool win_bwd_ok(const Geo& g, bool bf16_);
 int win_bwd_nslice(const Geo& g);
 size_t win_fwd_lds(const Geo& g);
 size_t win_bwd_lds(const Geo& g);
-hipError_t launch_win_fwd(const Geo& g, const void* q, const void* k, const void* v,
+hipError_t launch_win_fwd(const Geo& g, bool nhwc, const void* q, const void* k, const void* v,
                           const float* table, void* o, float* lse, hipStream_t st);
-hipError_t launch_win_bwd(const Geo& g, const void* q, const void* k, const void* v,
+hipError_t launch_win_bwd(const Geo& g, bool nhwc, const void* q, const void* k, const void* v,
                           const void* dout, const float* lse, const float* table, void* dq,
                           void* dk, void* dv, float* partial, int nslice, hipStream_t st);
 
@@ -82,12 +82,12 @@ __device__ inline typename Operand<T>::type load_op_lds_perm(const T* row, int h
   return o;
 }
 
-// Copy rows [r0, r0+kTile) x HD of one head from a window-major tensor
-// into LDS, row-major (stride HD+kPad) and/or transposed (stride kTile+kPad).
-// Rows at or beyond n are zero.
-template <typename T, int HD, bool ROWMAJOR, bool TRANS>
-__device__ inline void stage_tile(const T* __restrict__ src, int64_t tok0, int r0, int n,
-                                  int C, int hoff, T* lds_rm, T* lds_tr) {
+// Copy rows [r0, r0+kTile) x HD of one head of one window into LDS,
+// row-major (stride HD+kPad) and/or transposed (stride kTile+kPad).  Rows at
+// or beyond n are zero.
+template <typename T, int HD, bool ROWMAJOR, bool TRANS, bool NHWC>
+__device__ inline void stage_tile(const T* __restrict__ src, const Geo& g, const WinTokens<NHWC>& wt,
+                                  int r0, int n, int hoff, T* lds_rm, T* lds_tr) {
   constexpr int kTile = tile_of<T, HD>();
   constexpr int kElemPerChunk = 16 / sizeof(T);
   constexpr int kCpr = HD / kElemPerChunk;
@@ -97,7 +97,7 @@ __device__ inline void stage_tile(const T* __restrict__ src, int64_t tok0, int r
     const int row = r0 + rr;
     uint4 raw = make_uint4(0, 0, 0, 0);
     if (row < n)
-      raw = *reinterpret_cast<const uint4*>(src + (tok0 + row) * C + hoff + ch * kElemPerChunk);
+      raw = *reinterpret_cast<const uint4*>(src + wt.tok(g, row) * g.C + hoff + ch * kElemPerChunk);
     if (ROWMAJOR)
       *reinterpret_cast<uint4*>(lds_rm + rr * (HD + kPad) + ch * kElemPerChunk) = raw;
     if (TRANS) {
@@ -122,7 +122,7 @@ __device__ inline int token_info(const Geo& g, int i, int j, int cols, int t, in
 // Forward.  Grid: B * nwin * heads * nqc workgroups (nqc query chunks of 128
 // per window, empty chunks of small windows exit at once).
 // ---------------------------------------------------------------------------
-template <typename T, int HD>
+template <typename T, int HD, bool NHWC>
 __global__ __launch_bounds__(kThreads) void fwd_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const float* __restrict__ table, T* __restrict__ o, float* __restrict__ lse,
@@ -144,7 +144,7 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(
   const int n = win_rows(g, i) * cols;
   const int q0 = qc * kChunk;
   if (q0 >= n) return;
-  const int64_t tok0 = (int64_t)b * g.HW + win_offset(g, i, j);
+  const WinTokens<NHWC> wt(g, b, i, j);
   const int hoff = h * HD;
 
   for (int x = threadIdx.x; x < g.nbins; x += kThreads) tab[x] = table[x * g.heads + h] * kLog2e;
@@ -160,7 +160,7 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(
   typename Operand<T>::type qop[HD / 16];
 #pragma unroll
   for (int c = 0; c < HD / 16; ++c)
-    qop[c] = qvalid ? load_op_global<T>(q + (tok0 + qi) * g.C + hoff + 16 * c + 8 * half)
+    qop[c] = qvalid ? load_op_global<T>(q + wt.tok(g, qi) * g.C + hoff + 16 * c + 8 * half)
                     : zero_op<T>();
 
   f32x16 oacc[HD / 32];
@@ -170,8 +170,8 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(
 
   for (int k0 = 0; k0 < n; k0 += kTile) {
     __syncthreads();
-    stage_tile<T, HD, true, false>(k, tok0, k0, n, g.C, hoff, kt, nullptr);
-    stage_tile<T, HD, false, true>(v, tok0, k0, n, g.C, hoff, nullptr, vt);
+    stage_tile<T, HD, true, false>(k, g, wt, k0, n, hoff, kt, nullptr);
+    stage_tile<T, HD, false, true>(v, g, wt, k0, n, hoff, nullptr, vt);
     if (threadIdx.x < kTile) kinfo[threadIdx.x] = token_info(g, i, j, cols, k0 + threadIdx.x, n);
     __syncthreads();
 
@@ -225,7 +225,7 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(
   l_run += __shfl_xor(l_run, 32);
   if (!qvalid) return;
   const float inv = 1.0f / l_run;
-  T* orow = o + (tok0 + qi) * g.C + hoff;
+  T* orow = o + wt.tok(g, qi) * g.C + hoff;
 #pragma unroll
   for (int eb = 0; eb < HD / 32; ++eb) {
 #pragma unroll
@@ -235,9 +235,7 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(
       for (int x = 0; x < 4; ++x) orow[e + x] = from_float<T>(oacc[eb][4 * grp + x] * inv);
     }
   }
-  if (half == 0)
-    lse[((int64_t)b * g.heads + h) * g.HW + (tok0 - (int64_t)b * g.HW) + qi] =
-        (m_run + __log2f(l_run)) * kLn2;
+  if (half == 0) lse[wt.lse_at(g, h, qi)] = (m_run + __log2f(l_run)) * kLn2;
 }
 
 // ---------------------------------------------------------------------------
@@ -248,7 +246,7 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(
 // fp32 (equal to <dO_q, O_q> for the unrounded O) and stores it for the
 // dK/dV kernel; the second sweep forms dS, dQ and the bias bins.
 // ---------------------------------------------------------------------------
-template <typename T, int HD>
+template <typename T, int HD, bool NHWC>
 __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const T* __restrict__ dout, const float* __restrict__ lse, float* __restrict__ D,
@@ -283,30 +281,29 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(
     const int n = win_rows(g, i) * cols;
     const int q0 = qc * kChunk;
     if (q0 >= n) continue;
-    const int64_t img0 = (int64_t)b * g.HW;
-    const int64_t tok0 = img0 + win_offset(g, i, j);
+    const WinTokens<NHWC> wt(g, b, i, j);
     const int qi = q0 + wave * kWaveQ + col;
     const bool qvalid = qi < n;
     const int qinf = token_info(g, i, j, cols, qvalid ? qi : 0, n);
     const int qlab = qinf >> 24;
     const int qoff = (qinf & 0xFFFFFF) + (g.wh - 1) * g.bstride + (g.ww - 1);
-    const int64_t lidx = (img0 * g.heads) + (int64_t)h * g.HW + (tok0 - img0) + (qvalid ? qi : 0);
+    const int64_t lidx = wt.lse_at(g, h, qvalid ? qi : 0);
     const float lse2 = lse[lidx] * kLog2e;
 
     typename Operand<T>::type qop[HD / 16], dop[HD / 16];
 #pragma unroll
     for (int c = 0; c < HD / 16; ++c) {
-      qop[c] = qvalid ? load_op_global<T>(q + (tok0 + qi) * g.C + hoff + 16 * c + 8 * half)
+      qop[c] = qvalid ? load_op_global<T>(q + wt.tok(g, qi) * g.C + hoff + 16 * c + 8 * half)
                       : zero_op<T>();
-      dop[c] = qvalid ? load_op_global<T>(dout + (tok0 + qi) * g.C + hoff + 16 * c + 8 * half)
+      dop[c] = qvalid ? load_op_global<T>(dout + wt.tok(g, qi) * g.C + hoff + 16 * c + 8 * half)
                       : zero_op<T>();
     }
     // sweep 1: D_q
     float dsum = 0.0f;
     for (int k0 = 0; k0 < n; k0 += kTile) {
       __syncthreads();
-      stage_tile<T, HD, true, false>(k, tok0, k0, n, g.C, hoff, kt, nullptr);
-      stage_tile<T, HD, true, false>(v, tok0, k0, n, g.C, hoff, vr, nullptr);
+      stage_tile<T, HD, true, false>(k, g, wt, k0, n, hoff, kt, nullptr);
+      stage_tile<T, HD, true, false>(v, g, wt, k0, n, hoff, vr, nullptr);
       if (threadIdx.x < kTile) kinfo[threadIdx.x] = token_info(g, i, j, cols, k0 + threadIdx.x, n);
       __syncthreads();
 #pragma unroll
@@ -335,8 +332,8 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(
 
     for (int k0 = 0; k0 < n; k0 += kTile) {
       __syncthreads();
-      stage_tile<T, HD, true, true>(k, tok0, k0, n, g.C, hoff, kt, ktt);
-      stage_tile<T, HD, true, false>(v, tok0, k0, n, g.C, hoff, vr, nullptr);
+      stage_tile<T, HD, true, true>(k, g, wt, k0, n, hoff, kt, ktt);
+      stage_tile<T, HD, true, false>(v, g, wt, k0, n, hoff, vr, nullptr);
       if (threadIdx.x < kTile) kinfo[threadIdx.x] = token_info(g, i, j, cols, k0 + threadIdx.x, n);
       __syncthreads();
       f32x16 dsb[kTile / 32];
@@ -391,7 +388,7 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(
       }
     }
     if (qvalid) {
-      T* row = dq + (tok0 + qi) * g.C + hoff;
+      T* row = dq + wt.tok(g, qi) * g.C + hoff;
 #pragma unroll
       for (int eb = 0; eb < HD / 32; ++eb)
 #pragma unroll
@@ -411,7 +408,7 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(
 // Backward, step 2: dK and dV.  Grid: B * nwin * heads * nkc (key chunks of
 // 128; a wave owns 32 keys and walks the window's queries in LDS tiles).
 // ---------------------------------------------------------------------------
-template <typename T, int HD>
+template <typename T, int HD, bool NHWC>
 __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const T* __restrict__ dout, const float* __restrict__ lse, const float* __restrict__ D,
@@ -438,8 +435,7 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(
   const int n = win_rows(g, i) * cols;
   const int kbase = kc * kChunk;
   if (kbase >= n) return;
-  const int64_t img0 = (int64_t)b * g.HW;
-  const int64_t tok0 = img0 + win_offset(g, i, j);
+  const WinTokens<NHWC> wt(g, b, i, j);
   const int hoff = h * HD;
   for (int x = threadIdx.x; x < g.nbins; x += kThreads) tab[x] = table[x * g.heads + h] * kLog2e;
 
@@ -454,27 +450,27 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(
   typename Operand<T>::type kop[HD / 16], vop[HD / 16];
 #pragma unroll
   for (int c = 0; c < HD / 16; ++c) {
-    kop[c] = kvalid ? load_op_global<T>(k + (tok0 + ki) * g.C + hoff + 16 * c + 8 * half)
+    kop[c] = kvalid ? load_op_global<T>(k + wt.tok(g, ki) * g.C + hoff + 16 * c + 8 * half)
                     : zero_op<T>();
-    vop[c] = kvalid ? load_op_global<T>(v + (tok0 + ki) * g.C + hoff + 16 * c + 8 * half)
+    vop[c] = kvalid ? load_op_global<T>(v + wt.tok(g, ki) * g.C + hoff + 16 * c + 8 * half)
                     : zero_op<T>();
   }
   f32x16 dkacc[HD / 32], dvacc[HD / 32];
 #pragma unroll
   for (int eb = 0; eb < HD / 32; ++eb) { dkacc[eb] = f32x16{}; dvacc[eb] = f32x16{}; }
-  const int64_t lbase = img0 * g.heads + (int64_t)h * g.HW + (tok0 - img0);
 
   for (int t0 = 0; t0 < n; t0 += kTile) {
     __syncthreads();
-    stage_tile<T, HD, true, true>(q, tok0, t0, n, g.C, hoff, qr, qtt);
-    stage_tile<T, HD, true, true>(dout, tok0, t0, n, g.C, hoff, dr, dtt);
+    stage_tile<T, HD, true, true>(q, g, wt, t0, n, hoff, qr, qtt);
+    stage_tile<T, HD, true, true>(dout, g, wt, t0, n, hoff, dr, dtt);
     if (threadIdx.x < kTile) {
       const int t = t0 + threadIdx.x;
       const int inf = token_info(g, i, j, cols, t, n);
       qinfo[threadIdx.x] = (inf & 0xFFFFFF) + (g.wh - 1) * g.bstride + (g.ww - 1) +
                            (t < n ? (inf & 0xFF000000) : (kLabBad << 24));
-      ql[threadIdx.x] = t < n ? lse[lbase + t] * kLog2e : 0.0f;
-      qd[threadIdx.x] = t < n ? D[lbase + t] : 0.0f;
+      const int64_t li = t < n ? wt.lse_at(g, h, t) : 0;
+      ql[threadIdx.x] = t < n ? lse[li] * kLog2e : 0.0f;
+      qd[threadIdx.x] = t < n ? D[li] : 0.0f;
     }
     __syncthreads();
 #pragma unroll
@@ -512,8 +508,8 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(
     }
   }
   if (!kvalid) return;
-  T* krow = dk + (tok0 + ki) * g.C + hoff;
-  T* vrow = dv + (tok0 + ki) * g.C + hoff;
+  T* krow = dk + wt.tok(g, ki) * g.C + hoff;
+  T* vrow = dv + wt.tok(g, ki) * g.C + hoff;
 #pragma unroll
   for (int eb = 0; eb < HD / 32; ++eb)
 #pragma unroll
@@ -573,14 +569,14 @@ static size_t dkdv_lds(const Geo& g) {
   return sizeof(T) * (2 * kTile * (HD + kPad) + 2 * HD * (kTile + kPad)) + 12 * kTile + 4 * g.nbins;
 }
 
-template <typename T, int HD>
+template <typename T, int HD, bool NHWC>
 static hipError_t fwd_impl(const Geo& g, const void* q, const void* k, const void* v,
                            const float* table, void* o, float* lse, hipStream_t st) {
   const int nqc = num_chunks(g);
   const int grid = g.B * g.nwin * g.heads * nqc;
   const float sl2 = kLog2e / sqrtf((float)HD);
   const size_t lds = fwd_lds<T, HD>(g);
-  hipLaunchKernelGGL((fwd_kernel<T, HD>), dim3(grid), dim3(kThreads), lds, st,
+  hipLaunchKernelGGL((fwd_kernel<T, HD, NHWC>), dim3(grid), dim3(kThreads), lds, st,
                      (const T*)q, (const T*)k, (const T*)v, table, (T*)o, lse, g, nqc, sl2);
   return hipGetLastError();
 }
@@ -592,7 +588,7 @@ size_t bwd_workspace(const Geo& g, bool bf16) {
   return ((dbytes + 255) / 256) * 256 + pbytes;
 }
 
-template <typename T, int HD>
+template <typename T, int HD, bool NHWC>
 static hipError_t bwd_impl(const Geo& g, const void* q, const void* k, const void* v,
                            const void* o, const void* dout, const float* lse,
                            const float* table, void* dq, void* dk, void* dv, float* dtab,
@@ -607,14 +603,14 @@ static hipError_t bwd_impl(const Geo& g, const void* q, const void* k, const voi
   const float sl2 = kLog2e / sqrtf((float)HD);
   const float scale = 1.0f / sqrtf((float)HD);
   const size_t lds_dq = dq_lds<T, HD>(g);
-  hipLaunchKernelGGL((bwd_dq_kernel<T, HD>), dim3(g.heads * nslice), dim3(kThreads),
+  hipLaunchKernelGGL((bwd_dq_kernel<T, HD, NHWC>), dim3(g.heads * nslice), dim3(kThreads),
                      lds_dq, st, (const T*)q, (const T*)k, (const T*)v,
                      (const T*)dout, lse, D, table, (T*)dq, partial, g, nqc, nslice, sl2, scale);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int grid = g.B * g.nwin * g.heads * nqc;
   const size_t lds_kv = dkdv_lds<T, HD>(g);
-  hipLaunchKernelGGL((bwd_dkdv_kernel<T, HD>), dim3(grid), dim3(kThreads), lds_kv, st,
+  hipLaunchKernelGGL((bwd_dkdv_kernel<T, HD, NHWC>), dim3(grid), dim3(kThreads), lds_kv, st,
                      (const T*)q, (const T*)k, (const T*)v, (const T*)dout, lse, D, table,
                      (T*)dk, (T*)dv, g, nqc, sl2, scale);
   e = hipGetLastError();
@@ -641,36 +637,55 @@ size_t attn_max_lds(const Geo& g, bool bf16) {
   return m;
 }
 
-hipError_t launch_attn_fwd(const Geo& g, bool bf16, const void* q, const void* k, const void* v,
-                           const float* table, void* o, float* lse, hipStream_t st) {
-  if (win_fwd_ok(g, bf16)) return launch_win_fwd(g, q, k, v, table, o, lse, st);
+template <bool NHWC>
+static hipError_t fwd_generic(const Geo& g, bool bf16, const void* q, const void* k, const void* v,
+                              const float* table, void* o, float* lse, hipStream_t st) {
   if (bf16)
-    return g.hd == 32 ? fwd_impl<__bf16, 32>(g, q, k, v, table, o, lse, st)
-                      : fwd_impl<__bf16, 64>(g, q, k, v, table, o, lse, st);
-  return g.hd == 32 ? fwd_impl<float, 32>(g, q, k, v, table, o, lse, st)
-                    : fwd_impl<float, 64>(g, q, k, v, table, o, lse, st);
+    return g.hd == 32 ? fwd_impl<__bf16, 32, NHWC>(g, q, k, v, table, o, lse, st)
+                      : fwd_impl<__bf16, 64, NHWC>(g, q, k, v, table, o, lse, st);
+  return g.hd == 32 ? fwd_impl<float, 32, NHWC>(g, q, k, v, table, o, lse, st)
+                    : fwd_impl<float, 64, NHWC>(g, q, k, v, table, o, lse, st);
 }
 
-hipError_t launch_attn_bwd(const Geo& g, bool bf16, const void* q, const void* k, const void* v,
-                           const void* o, const void* dout, const float* lse, const float* table,
-                           void* dq, void* dk, void* dv, float* dtab, void* ws, hipStream_t st) {
+template <bool NHWC>
+static hipError_t bwd_generic(const Geo& g, bool bf16, const void* q, const void* k, const void* v,
+                              const void* o, const void* dout, const float* lse, const float* table,
+                              void* dq, void* dk, void* dv, float* dtab, void* ws, hipStream_t st) {
+  if (bf16)
+    return g.hd == 32
+               ? bwd_impl<__bf16, 32, NHWC>(g, q, k, v, o, dout, lse, table, dq, dk, dv, dtab, ws, st)
+               : bwd_impl<__bf16, 64, NHWC>(g, q, k, v, o, dout, lse, table, dq, dk, dv, dtab, ws, st);
+  return g.hd == 32
+             ? bwd_impl<float, 32, NHWC>(g, q, k, v, o, dout, lse, table, dq, dk, dv, dtab, ws, st)
+             : bwd_impl<float, 64, NHWC>(g, q, k, v, o, dout, lse, table, dq, dk, dv, dtab, ws, st);
+}
+
+// nhwc: q, k, v, o (and dout, dq, dk, dv) are B x H x W x C read and written
+// in place (the token route fused into the kernels), LSE in the same token
+// order; otherwise they are window-major.
+hipError_t launch_attn_fwd(const Geo& g, bool bf16, bool nhwc, const void* q, const void* k,
+                           const void* v, const float* table, void* o, float* lse, hipStream_t st) {
+  if (win_fwd_ok(g, bf16)) return launch_win_fwd(g, nhwc, q, k, v, table, o, lse, st);
+  return nhwc ? fwd_generic<true>(g, bf16, q, k, v, table, o, lse, st)
+              : fwd_generic<false>(g, bf16, q, k, v, table, o, lse, st);
+}
+
+hipError_t launch_attn_bwd(const Geo& g, bool bf16, bool nhwc, const void* q, const void* k,
+                           const void* v, const void* o, const void* dout, const float* lse,
+                           const float* table, void* dq, void* dk, void* dv, float* dtab, void* ws,
+                           hipStream_t st) {
   if (win_bwd_ok(g, bf16)) {
     const int nslice = win_bwd_nslice(g);
     float* partial = reinterpret_cast<float*>(ws);
-    hipError_t e = launch_win_bwd(g, q, k, v, dout, lse, table, dq, dk, dv, partial, nslice, st);
+    hipError_t e = launch_win_bwd(g, nhwc, q, k, v, dout, lse, table, dq, dk, dv, partial, nslice, st);
     if (e != hipSuccess) return e;
     const int nred = g.nbins * g.heads;
     hipLaunchKernelGGL(dtab_reduce_kernel, dim3((nred + kThreads - 1) / kThreads), dim3(kThreads), 0,
                        st, partial, dtab, g, nslice);
     return hipGetLastError();
   }
-  if (bf16)
-    return g.hd == 32
-               ? bwd_impl<__bf16, 32>(g, q, k, v, o, dout, lse, table, dq, dk, dv, dtab, ws, st)
-               : bwd_impl<__bf16, 64>(g, q, k, v, o, dout, lse, table, dq, dk, dv, dtab, ws, st);
-  return g.hd == 32
-             ? bwd_impl<float, 32>(g, q, k, v, o, dout, lse, table, dq, dk, dv, dtab, ws, st)
-             : bwd_impl<float, 64>(g, q, k, v, o, dout, lse, table, dq, dk, dv, dtab, ws, st);
+  return nhwc ? bwd_generic<true>(g, bf16, q, k, v, o, dout, lse, table, dq, dk, dv, dtab, ws, st)
+              : bwd_generic<false>(g, bf16, q, k, v, o, dout, lse, table, dq, dk, dv, dtab, ws, st);
 }
 
 }  // namespace terra

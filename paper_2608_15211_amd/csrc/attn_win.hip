@@ -79,15 +79,15 @@ __device__ inline void store4_bf16(bf16* dst, const f32x16& acc, int g, float mu
 }
 
 // Stage rows [0, 128) x HD of one head into LDS row-major (zero beyond n).
-template <int HD>
-__device__ inline void stage_rows(const bf16* __restrict__ src, int64_t tok0, int n, int C,
+template <int HD, bool NHWC>
+__device__ inline void stage_rows(const bf16* __restrict__ src, const Geo& g, const WinTokens<NHWC>& wt, int n,
                                   int hoff, bf16* lds) {
   constexpr int kCpr = HD / 8;
   for (int idx = threadIdx.x; idx < kWinMax * kCpr; idx += kWinThreads) {
     const int row = idx / kCpr;
     const int ch = idx - row * kCpr;
     uint4 raw = make_uint4(0, 0, 0, 0);
-    if (row < n) raw = *reinterpret_cast<const uint4*>(src + (tok0 + row) * C + hoff + ch * 8);
+    if (row < n) raw = *reinterpret_cast<const uint4*>(src + wt.tok(g, row) * g.C + hoff + ch * 8);
     *reinterpret_cast<uint4*>(lds + row * (HD + 8) + ch * 8) = raw;
   }
 }
@@ -172,7 +172,7 @@ __device__ inline int xcd_work(int bid, int nblocks) {
 // Forward: one workgroup per (image, window, head); wave w owns queries
 // [32w, 32w+32).  Grid B * nwin * heads, head fastest.
 // ---------------------------------------------------------------------------
-template <int HD, bool QUAD>
+template <int HD, bool QUAD, bool NHWC>
 __global__ __launch_bounds__(kWinThreads) void fwd_win_kernel(
     const bf16* __restrict__ q, const bf16* __restrict__ k, const bf16* __restrict__ v,
     const float* __restrict__ table, bf16* __restrict__ o, float* __restrict__ lse, Geo g,
@@ -191,8 +191,7 @@ __global__ __launch_bounds__(kWinThreads) void fwd_win_kernel(
   const int cols = win_cols(g, wj);
   const int n = win_rows(g, wi) * cols;
   const int nkb = (n + 31) >> 5;
-  const int64_t img0 = (int64_t)b * g.HW;
-  const int64_t tok0 = img0 + win_offset(g, wi, wj);
+  const WinTokens<NHWC> wt(g, b, wi, wj);
   const int hoff = h * HD;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int half = lane >> 5, col = lane & 31;
@@ -204,7 +203,7 @@ __global__ __launch_bounds__(kWinThreads) void fwd_win_kernel(
   for (int x = threadIdx.x; x < g.nbins + 4; x += kWinThreads)
     tab[x] = x < g.nbins ? table[(g.nbins - 1 - x) * g.heads + h] * bscale : -INFINITY;
   if (threadIdx.x < kWinMax) kinfo[threadIdx.x] = win_token_info(g, wi, wj, cols, threadIdx.x, n);
-  stage_rows<HD>(k, tok0, n, g.C, hoff, ks);
+  stage_rows<HD>(k, g, wt, n, hoff, ks);
   // V^T through LDS: stage V rows into the vts area's tail is not possible
   // (different shapes), so each wave transposes its 32 rows straight from
   // memory.
@@ -215,7 +214,7 @@ __global__ __launch_bounds__(kWinThreads) void fwd_win_kernel(
     for (int eb = 0; eb < HD / 32; ++eb) {
       bf16x8 a0 = zero8(), a1 = zero8();
       if (row < n) {
-        const bf16* p = v + (tok0 + row) * g.C + hoff + 32 * eb + 8 * half;
+        const bf16* p = v + wt.tok(g, row) * g.C + hoff + 32 * eb + 8 * half;
         a0 = *reinterpret_cast<const bf16x8*>(p);
         a1 = *reinterpret_cast<const bf16x8*>(p + 16);
       }
@@ -237,7 +236,7 @@ __global__ __launch_bounds__(kWinThreads) void fwd_win_kernel(
   bf16x8 qop[HD / 16];
 #pragma unroll
   for (int c = 0; c < HD / 16; ++c)
-    qop[c] = qvalid ? *reinterpret_cast<const bf16x8*>(q + (tok0 + qi) * g.C + hoff + 16 * c + 8 * half)
+    qop[c] = qvalid ? *reinterpret_cast<const bf16x8*>(q + wt.tok(g, qi) * g.C + hoff + 16 * c + 8 * half)
                     : zero8();
 
   // raw scores with the bias folded into the accumulator: s = QK^T + bias*sqrt(hd)
@@ -286,12 +285,12 @@ __global__ __launch_bounds__(kWinThreads) void fwd_win_kernel(
   l += __shfl_xor(l, 32);
   if (!qvalid) return;
   const float inv = 1.0f / l;
-  bf16* orow = o + (tok0 + qi) * g.C + hoff;
+  bf16* orow = o + wt.tok(g, qi) * g.C + hoff;
 #pragma unroll
   for (int eb = 0; eb < HD / 32; ++eb)
 #pragma unroll
     for (int g4 = 0; g4 < 4; ++g4) store4_bf16(orow + 32 * eb + 8 * g4 + 4 * half, oacc[eb], g4, inv);
-  if (half == 0) lse[(img0 * g.heads) + (int64_t)h * g.HW + (tok0 - img0) + qi] = (m + __log2f(l)) * kLn2;
+  if (half == 0) lse[wt.lse_at(g, h, qi)] = (m + __log2f(l)) * kLn2;
 }
 
 // ---------------------------------------------------------------------------
@@ -304,7 +303,7 @@ __global__ __launch_bounds__(kWinThreads) void fwd_win_kernel(
 // ---------------------------------------------------------------------------
 constexpr int kPairThreads = 512;
 
-template <bool QUAD>
+template <bool QUAD, bool NHWC>
 __global__ __launch_bounds__(kPairThreads) void fwd_win_pair_kernel(
     const bf16* __restrict__ q, const bf16* __restrict__ k, const bf16* __restrict__ v,
     const float* __restrict__ table, bf16* __restrict__ o, float* __restrict__ lse, Geo g,
@@ -327,8 +326,7 @@ __global__ __launch_bounds__(kPairThreads) void fwd_win_pair_kernel(
   const int cols = win_cols(g, wj);
   const int n = win_rows(g, wi) * cols;
   const int nkb = (n + 31) >> 5;
-  const int64_t img0 = (int64_t)b * g.HW;
-  const int64_t tok0 = img0 + win_offset(g, wi, wj);
+  const WinTokens<NHWC> wt(g, b, wi, wj);
   const int64_t cbase = (int64_t)2 * hp * HD;          // first channel of the pair
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int half = lane >> 5, col = lane & 31;
@@ -345,7 +343,7 @@ __global__ __launch_bounds__(kPairThreads) void fwd_win_pair_kernel(
     const int row = idx >> 3, ch = idx & 7;
     kr[u] = qr[u] = vr[u] = make_uint4(0, 0, 0, 0);
     if (row < n) {
-      const int64_t off = (tok0 + row) * g.C + cbase + ch * 8;
+      const int64_t off = wt.tok(g, row) * g.C + cbase + ch * 8;
       kr[u] = *reinterpret_cast<const uint4*>(k + off);
       qr[u] = *reinterpret_cast<const uint4*>(q + off);
       vr[u] = *reinterpret_cast<const uint4*>(v + off);
@@ -428,7 +426,7 @@ __global__ __launch_bounds__(kPairThreads) void fwd_win_pair_kernel(
     for (int g4 = 0; g4 < 4; ++g4)
       store4_bf16(qs + (hs * kWinMax + qi) * KS + 8 * g4 + 4 * half, oacc, g4, inv);
     if (qvalid && half == 0)
-      lse[(img0 * g.heads) + (int64_t)h * g.HW + (tok0 - img0) + qi] = (m + __log2f(l)) * kLn2;
+      lse[wt.lse_at(g, h, qi)] = (m + __log2f(l)) * kLn2;
   }
   __syncthreads();
 #pragma unroll
@@ -437,7 +435,7 @@ __global__ __launch_bounds__(kPairThreads) void fwd_win_pair_kernel(
     const int row = idx >> 3, ch = idx & 7;
     if (row < n) {
       const int t = ch >> 2, e0 = (ch & 3) * 8;
-      *reinterpret_cast<uint4*>(o + (tok0 + row) * g.C + cbase + ch * 8) =
+      *reinterpret_cast<uint4*>(o + wt.tok(g, row) * g.C + cbase + ch * 8) =
           *reinterpret_cast<const uint4*>(qs + (t * kWinMax + row) * KS + e0);
     }
   }
@@ -642,6 +640,7 @@ struct BwdRows {
   float lse2;
 };
 
+template <bool NHWC>
 __device__ __forceinline__ void bwd_load_rows(BwdRows& r, const Geo& g, int wl, int h, int qi,
                                               const bf16* __restrict__ q, const bf16* __restrict__ k,
                                               const bf16* __restrict__ v, const bf16* __restrict__ dout,
@@ -650,22 +649,21 @@ __device__ __forceinline__ void bwd_load_rows(BwdRows& r, const Geo& g, int wl, 
   const int w = wl - b * g.nwin;
   const int wi = w / g.Mw, wj = w - (w / g.Mw) * g.Mw;
   const int n = win_rows(g, wi) * win_cols(g, wj);
-  const int64_t img0 = (int64_t)b * g.HW;
-  const int64_t tok0 = img0 + win_offset(g, wi, wj);
+  const WinTokens<NHWC> wt(g, b, wi, wj);
 #pragma unroll
   for (int u = 0; u < 2; ++u) {
     const int idx = threadIdx.x + u * kWinThreads;
     const int row = idx / kBwdCPR, ch = idx % kBwdCPR;
     r.k[u] = r.v[u] = r.q[u] = r.d[u] = make_uint4(0, 0, 0, 0);
     if (row < n) {
-      const int64_t off = (tok0 + row) * g.C + h * kBwdHD + ch * 8;
+      const int64_t off = wt.tok(g, row) * g.C + h * kBwdHD + ch * 8;
       r.k[u] = *reinterpret_cast<const uint4*>(k + off);
       r.v[u] = *reinterpret_cast<const uint4*>(v + off);
       r.q[u] = *reinterpret_cast<const uint4*>(q + off);
       r.d[u] = *reinterpret_cast<const uint4*>(dout + off);
     }
   }
-  r.lse2 = qi < n ? lse[img0 * g.heads + (int64_t)h * g.HW + (tok0 - img0) + qi] * kLog2e : INFINITY;
+  r.lse2 = qi < n ? lse[wt.lse_at(g, h, qi)] * kLog2e : INFINITY;
 }
 
 // Backward, head_dim 32, every window width a multiple of 4.  K, V, Q and dO
@@ -676,7 +674,7 @@ __device__ __forceinline__ void bwd_load_rows(BwdRows& r, const Geo& g, int wl, 
 // register run over windows of equal width and are flushed to per-wave LDS
 // bins when the width changes (a register holds the same query/key slot
 // pair, hence the same bin, in every such window).
-template <bool QUAD>
+template <bool QUAD, bool NHWC>
 __global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
     const bf16* __restrict__ q, const bf16* __restrict__ k, const bf16* __restrict__ v,
     const bf16* __restrict__ dout, const float* __restrict__ lse, const float* __restrict__ table,
@@ -744,14 +742,14 @@ __global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
   const int wbeg = slice * per_slice;
   const int wend = min(total, wbeg + per_slice);
   BwdRows rows;
-  if (wbeg < wend) bwd_load_rows(rows, g, wbeg, h, qi, q, k, v, dout, lse);
+  if (wbeg < wend) bwd_load_rows<NHWC>(rows, g, wbeg, h, qi, q, k, v, dout, lse);
   for (int wl = wbeg; wl < wend; ++wl) {
     const int b = wl / g.nwin;
     const int w = wl - b * g.nwin;
     const int wi = w / g.Mw, wj = w - (w / g.Mw) * g.Mw;
     const int cols = win_cols(g, wj);
     const int n = win_rows(g, wi) * cols;
-    const int64_t tok0 = (int64_t)b * g.HW + win_offset(g, wi, wj);
+    const WinTokens<NHWC> wt(g, b, wi, wj);
     if (cols != acc_cols) {          // uniform across the workgroup
       if (acc_cols > 0) TERRA_FLUSH_DT(acc_cols);
       acc_cols = cols;
@@ -771,7 +769,7 @@ __global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
     BwdWave st;
     st.lse2 = rows.lse2;
     __syncthreads();
-    if (wl + 1 < wend) bwd_load_rows(rows, g, wl + 1, h, qi, q, k, v, dout, lse);
+    if (wl + 1 < wend) bwd_load_rows<NHWC>(rows, g, wl + 1, h, qi, q, k, v, dout, lse);
 
     st.ks = ks;
     st.vs = vs;
@@ -827,7 +825,7 @@ __global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
       const int idx = threadIdx.x + u * kWinThreads;
       const int row = idx / kBwdCPR, c0 = (idx % kBwdCPR) * 8;
       if (row < n) {
-        const int64_t off = (tok0 + row) * g.C + h * HD + c0;
+        const int64_t off = wt.tok(g, row) * g.C + h * HD + c0;
         *reinterpret_cast<uint4*>(dq + off) = *reinterpret_cast<const uint4*>(ks + row * KS + c0);
         bf16x8 a, bb;
 #pragma unroll
@@ -902,12 +900,12 @@ static bool quad_layout(const Geo& g) {
   return g.ww % 4 == 0 && (g.W % g.ww) % 4 == 0 && (g.flags & 2) == 0;
 }
 
-template <int HD, bool QUAD>
+template <int HD, bool QUAD, bool NHWC>
 static void fwd_win_go(const Geo& g, const void* q, const void* k, const void* v,
                        const float* table, void* o, float* lse, hipStream_t st) {
   const int grid = g.B * g.nwin * g.heads;
   const float sl2 = kLog2e / sqrtf((float)g.hd);
-  hipLaunchKernelGGL((fwd_win_kernel<HD, QUAD>), dim3(grid), dim3(kWinThreads), win_fwd_lds(g), st,
+  hipLaunchKernelGGL((fwd_win_kernel<HD, QUAD, NHWC>), dim3(grid), dim3(kWinThreads), win_fwd_lds(g), st,
                      (const bf16*)q, (const bf16*)k, (const bf16*)v, table, (bf16*)o, lse, g, sl2);
 }
 
@@ -916,49 +914,64 @@ size_t win_fwd_pair_lds(const Geo& g) {
          4 * 2 * (g.nbins + 4);
 }
 
-hipError_t launch_win_fwd(const Geo& g, const void* q, const void* k, const void* v,
-                          const float* table, void* o, float* lse, hipStream_t st) {
+template <bool QUAD, bool NHWC>
+static void fwd_win_pair_go(const Geo& g, const void* q, const void* k, const void* v,
+                            const float* table, void* o, float* lse, hipStream_t st) {
+  const int grid = g.B * g.nwin * (g.heads / 2);
+  const float sl2 = kLog2e / sqrtf((float)g.hd);
+  hipLaunchKernelGGL((fwd_win_pair_kernel<QUAD, NHWC>), dim3(grid), dim3(kPairThreads),
+                     win_fwd_pair_lds(g), st, (const bf16*)q, (const bf16*)k, (const bf16*)v, table,
+                     (bf16*)o, lse, g, sl2);
+}
+
+template <bool NHWC>
+static void launch_win_fwd_t(const Geo& g, const void* q, const void* k, const void* v,
+                             const float* table, void* o, float* lse, hipStream_t st) {
   const bool quad = quad_layout(g);
   if (g.hd == 32 && g.heads % 2 == 0) {
-    const int grid = g.B * g.nwin * (g.heads / 2);
-    const float sl2 = kLog2e / sqrtf((float)g.hd);
-    if (quad)
-      hipLaunchKernelGGL((fwd_win_pair_kernel<true>), dim3(grid), dim3(kPairThreads),
-                         win_fwd_pair_lds(g), st, (const bf16*)q, (const bf16*)k, (const bf16*)v,
-                         table, (bf16*)o, lse, g, sl2);
-    else
-      hipLaunchKernelGGL((fwd_win_pair_kernel<false>), dim3(grid), dim3(kPairThreads),
-                         win_fwd_pair_lds(g), st, (const bf16*)q, (const bf16*)k, (const bf16*)v,
-                         table, (bf16*)o, lse, g, sl2);
-    return hipGetLastError();
-  }
-  if (g.hd == 32) {
-    if (quad) fwd_win_go<32, true>(g, q, k, v, table, o, lse, st);
-    else fwd_win_go<32, false>(g, q, k, v, table, o, lse, st);
+    if (quad) fwd_win_pair_go<true, NHWC>(g, q, k, v, table, o, lse, st);
+    else fwd_win_pair_go<false, NHWC>(g, q, k, v, table, o, lse, st);
+  } else if (g.hd == 32) {
+    if (quad) fwd_win_go<32, true, NHWC>(g, q, k, v, table, o, lse, st);
+    else fwd_win_go<32, false, NHWC>(g, q, k, v, table, o, lse, st);
   } else {
-    if (quad) fwd_win_go<64, true>(g, q, k, v, table, o, lse, st);
-    else fwd_win_go<64, false>(g, q, k, v, table, o, lse, st);
+    if (quad) fwd_win_go<64, true, NHWC>(g, q, k, v, table, o, lse, st);
+    else fwd_win_go<64, false, NHWC>(g, q, k, v, table, o, lse, st);
   }
+}
+
+hipError_t launch_win_fwd(const Geo& g, bool nhwc, const void* q, const void* k, const void* v,
+                          const float* table, void* o, float* lse, hipStream_t st) {
+  if (nhwc) launch_win_fwd_t<true>(g, q, k, v, table, o, lse, st);
+  else launch_win_fwd_t<false>(g, q, k, v, table, o, lse, st);
   return hipGetLastError();
 }
 
-hipError_t launch_win_bwd(const Geo& g, const void* q, const void* k, const void* v,
-                          const void* dout, const float* lse, const float* table, void* dq,
-                          void* dk, void* dv, float* partial, int nslice, hipStream_t st) {
+template <bool QUAD, bool NHWC>
+static void bwd_win_go(const Geo& g, const void* q, const void* k, const void* v, const void* dout,
+                       const float* lse, const float* table, void* dq, void* dk, void* dv,
+                       float* partial, int nslice, hipStream_t st) {
   const int total = g.B * g.nwin;
   const int per = (total + nslice - 1) / nslice;
   const float sl2 = kLog2e / sqrtf((float)g.hd);
   const float scale = 1.0f / sqrtf((float)g.hd);
-  const dim3 grid(g.heads * nslice);
-  const size_t lds = win_bwd_lds(g);
-  if (quad_layout(g))
-    hipLaunchKernelGGL((bwd_win_kernel<true>), grid, dim3(kWinThreads), lds, st, (const bf16*)q,
-                       (const bf16*)k, (const bf16*)v, (const bf16*)dout, lse, table, (bf16*)dq,
-                       (bf16*)dk, (bf16*)dv, partial, g, nslice, per, sl2, scale);
-  else
-    hipLaunchKernelGGL((bwd_win_kernel<false>), grid, dim3(kWinThreads), lds, st, (const bf16*)q,
-                       (const bf16*)k, (const bf16*)v, (const bf16*)dout, lse, table, (bf16*)dq,
-                       (bf16*)dk, (bf16*)dv, partial, g, nslice, per, sl2, scale);
+  hipLaunchKernelGGL((bwd_win_kernel<QUAD, NHWC>), dim3(g.heads * nslice), dim3(kWinThreads),
+                     win_bwd_lds(g), st, (const bf16*)q, (const bf16*)k, (const bf16*)v,
+                     (const bf16*)dout, lse, table, (bf16*)dq, (bf16*)dk, (bf16*)dv, partial, g,
+                     nslice, per, sl2, scale);
+}
+
+hipError_t launch_win_bwd(const Geo& g, bool nhwc, const void* q, const void* k, const void* v,
+                          const void* dout, const float* lse, const float* table, void* dq,
+                          void* dk, void* dv, float* partial, int nslice, hipStream_t st) {
+  const bool quad = quad_layout(g);
+  if (nhwc) {
+    if (quad) bwd_win_go<true, true>(g, q, k, v, dout, lse, table, dq, dk, dv, partial, nslice, st);
+    else bwd_win_go<false, true>(g, q, k, v, dout, lse, table, dq, dk, dv, partial, nslice, st);
+  } else {
+    if (quad) bwd_win_go<true, false>(g, q, k, v, dout, lse, table, dq, dk, dv, partial, nslice, st);
+    else bwd_win_go<false, false>(g, q, k, v, dout, lse, table, dq, dk, dv, partial, nslice, st);
+  }
   return hipGetLastError();
 }
 

@@ -64,6 +64,38 @@ __device__ inline int fast_div(int n, int d, float rcp) {
   return q;
 }
 
+// Token index of row t of window (b, i, j) in a B x H x W x C tensor read in
+// one of two layouts:
+// * window-major (routed): the window's first slot plus t;
+// * NHWC, in place: the grid point that the rolled coordinate
+//   (i*wh + a, j*ww + c), (a, c) = (t / cols, t % cols), was taken from,
+//   ((i*wh + a + sh) mod H, (j*ww + c + sw) mod W) - the cyclic shift of
+//   Sec. IV-D read as a roll by -shift, so reading in place fuses the token
+//   route (and writing in place its inverse) into the attention kernels.
+// The log-sum-exp (and the backward's D) of a token sits at
+// (b*heads + h)*HW + (token - b*HW) in either layout.
+template <bool NHWC>
+struct WinTokens {
+  int64_t img0, first;    // b*HW; window-major first slot of the window
+  int r0, c0, cols;       // i*wh + sh, j*ww + sw, window width
+  float rcols;
+  __device__ WinTokens(const Geo& g, int b, int i, int j)
+      : img0((int64_t)b * g.HW), first((int64_t)b * g.HW + win_offset(g, i, j)),
+        r0(i * g.wh + g.sh), c0(j * g.ww + g.sw), cols(win_cols(g, j)),
+        rcols(1.0f / (float)win_cols(g, j)) {}
+  __device__ int64_t tok(const Geo& g, int t) const {
+    if (!NHWC) return first + t;
+    const int a = fast_div(t, cols, rcols);
+    int u = r0 + a, v = c0 + (t - a * cols);
+    if (u >= g.H) u -= g.H;
+    if (v >= g.W) v -= g.W;
+    return img0 + (int64_t)u * g.W + v;
+  }
+  __device__ int64_t lse_at(const Geo& g, int h, int t) const {
+    return img0 * g.heads + (int64_t)h * g.HW + (tok(g, t) - img0);
+  }
+};
+
 // ---------------------------------------------------------------------------
 // Matrix-core tiles.  One MFMA "operand" is 8 consecutive contraction-dim
 // elements per lane: lane l supplies row/column (l % 32) and contraction

@@ -98,8 +98,15 @@ def test_device_calls_reject_bad_arguments_before_launch():
     args = [fake] * 11
     assert L.terra_winattn_bwd(ctypes.byref(g), 1, *args, fake, ctypes.c_size_t(need - 4), s) == 3
     assert L.terra_winattn_bwd(ctypes.byref(g), 1, *args, null, ctypes.c_size_t(need), s) == 3
+    # the fused (NHWC) entry points share the checks
+    assert L.terra_winattn_fwd_nhwc(ctypes.byref(g), 1, fake, fake, null, fake, fake, fake, s) == 1
+    assert L.terra_winattn_fwd_nhwc(ctypes.byref(g), 5, *([fake] * 6), s) == 1
+    assert L.terra_winattn_bwd_nhwc(ctypes.byref(g), 1, *args, fake, ctypes.c_size_t(need - 4), s) == 3
+    assert L.terra_winattn_bwd_nhwc(ctypes.byref(g), 1, null, *args[1:], fake, ctypes.c_size_t(need),
+                                    s) == 1
     g2 = P.terra_geom.make(1, 16, 32, 48, 3, 16, 8, 8, 4, 4, 1)
     assert L.terra_winattn_fwd(ctypes.byref(g2), 1, *([fake] * 6), s) == 2
+    assert L.terra_winattn_fwd_nhwc(ctypes.byref(g2), 1, *([fake] * 6), s) == 2
     assert L.terra_winattn_bwd_workspace_bytes(ctypes.byref(g2), 1) == 0
     for code in range(5):
         assert L.terra_status_string(code)
