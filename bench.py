@@ -1,19 +1,22 @@
 """Benchmark of the shifted-window attention hot path on one MI355X.
 
-One step = one pass of the whole path over one synthetic batch:
-  route Q, K, V (NHWC -> window-major)      terra_window_route x3
-  attention forward (O, LSE)                terra_winattn_fwd
-  route dOut                                terra_window_route
-  attention backward (dQ, dK, dV, dTable)   terra_winattn_bwd
-  inverse route O, dQ, dK, dV               terra_window_unroute x4
+One step = one pass of the whole path over one synthetic batch, with the
+token route fused into the attention kernels (NHWC read and written in
+place):
+  attention forward (O, LSE)                terra_winattn_fwd_nhwc
+  attention backward (dQ, dK, dV, dTable)   terra_winattn_bwd_nhwc
 Inputs are resident in HBM before timing starts.  W warm-up steps, then K
 timed steps between device synchronisations; every launch is bracketed by
-HIP events on the stream it runs on.
+HIP events on the stream it runs on.  The same K steps are then run with
+the unfused pipeline (route Q, K, V, dO; window-major forward and
+backward; inverse route of O, dQ, dK, dV), which also gives the standalone
+routing bandwidth.
 
 The printed JSON line's `value` is the attention forward+backward
-algorithmic TFLOP/s of the whole step (flops 12 n^2 hd per window and head,
-divided by the full step time including the routes); per-phase figures,
-the roofline of the dominant phase and the oracle CPU baseline ride along.
+algorithmic TFLOP/s of the fused step (flops 12 n^2 hd per window and
+head, divided by the full step time); per-phase figures, the roofline of
+the dominant kernel, the unfused pipeline and the oracle CPU baseline ride
+along.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--config NAME]
 """
@@ -65,19 +68,15 @@ def algorithmic(cfg):
 
 
 # HBM bytes per launch measured with two rocprofv3 passes (FETCH_SIZE, then
-# WRITE_SIZE; FETCH_SIZE scaled by 1.9994 and WRITE_SIZE by 1.0000, the
+# WRITE_SIZE; FETCH_SIZE scaled by 1.9995 and WRITE_SIZE by 1.0000, the
 # factors a plain copy of known size reads on the same run) on the 128x1080
-# workload.  A figure is reported only while the kernel source still has the
+# workload, for the fused kernels (backward: bwd_win_kernel + dtab_reduce).  A figure is reported only while the kernel source still has the
 # SHA-256 prefix it was measured with.
 MEASURED_TRAFFIC = {
-    ("c4_bf16_128x1080_w8x16", "bwd"): dict(source="attn_win.hip", sha256="8face7597e344b6b",
-                                           bytes=(422454 + 3593) * 1024 * 1.9994 + (623938 + 44) * 1024),
-    ("c4_bf16_128x1080_w8x16", "fwd"): dict(source="attn_win.hip", sha256="8face7597e344b6b",
-                                           bytes=311445 * 1024 * 1.9994 + 220332 * 1024),
-    ("c4_bf16_128x1080_w8x16", "route"): dict(source="route.hip", sha256="b90d28f25d7093a1",
-                                             bytes=103710 * 1024 * 1.9994 + 207361 * 1024),
-    ("c4_bf16_128x1080_w8x16", "unroute"): dict(source="route.hip", sha256="b90d28f25d7093a1",
-                                               bytes=103712 * 1024 * 1.9994 + 207360 * 1024),
+    ("c4_bf16_128x1080_w8x16", "bwd_nhwc"): dict(source="attn_win.hip", sha256="9851e6b1644e0b7f",
+                                                bytes=(437754 + 1802) * 1024 * 1.9995 + (624047 + 44) * 1024),
+    ("c4_bf16_128x1080_w8x16", "fwd_nhwc"): dict(source="attn_win.hip", sha256="9851e6b1644e0b7f",
+                                                bytes=311305 * 1024 * 1.9995 + 224419 * 1024),
 }
 
 
@@ -118,9 +117,9 @@ def cpu_baseline(cfg, seconds_target=15.0):
         dt = time.perf_counter() - t0
         n2 = sum(float(slots[w][2]) ** 2 for w in sel) * cfg.B * cfg.heads
         sample_time, sample_flops, used = dt, 12.0 * n2 * cfg.head_dim, len(sel)
-        if dt >= seconds_target / 3 or nsel >= len(slots):
+        if dt >= seconds_target * 0.6 or nsel >= len(slots):
             break
-        nsel = min(len(slots), int(nsel * max(2.0, seconds_target / 3 / max(dt, 1e-3))))
+        nsel = min(len(slots), int(nsel * max(1.2, seconds_target / max(dt, 1e-3))))
     e = 4 if cfg.dtype == "f32" else 2
     route_gbps = 2.0 * cfg.B * cfg.H * cfg.W * cfg.C * e / t_route / 1e9
     return {
@@ -171,44 +170,58 @@ def main():
             for n in ("o", "dq", "dk", "dv")}
     ws = torch.empty(max(1, P.terra_winattn_bwd_workspace_bytes(cfg, tdt)), dtype=torch.uint8, device=dev)
 
-    phases = ["route", "fwd", "bwd", "unroute"]
+    fused_phases = ["fwd", "bwd"]
+    unfused_phases = ["route", "fwd_wm", "bwd_wm", "unroute"]
+
+    def rec(ev, name, fn):
+        if ev is not None:
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            b.record()
+            ev[name].append((a, b))
+        else:
+            fn()
 
     def step(ev):
-        def rec(name, fn):
-            if ev is not None:
-                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                a.record()
-                fn()
-                b.record()
-                ev[name].append((a, b))
-            else:
-                fn()
-        for n in ("q", "k", "v"):
-            rec("route", lambda n=n: P.terra_window_route(x[n], cfg, out=w[n]))
-        rec("fwd", lambda: P.terra_winattn_fwd(w["q"], w["k"], w["v"], table, cfg, out=o, lse=lse))
-        rec("route", lambda: P.terra_window_route(x["dout"], cfg, out=w["dout"]))
-        rec("bwd", lambda: P.terra_winattn_bwd(w["q"], w["k"], w["v"], o, w["dout"], lse, table, cfg,
-                                               out=grads, workspace=ws))
-        for n, t in (("o", o), ("dq", grads[0]), ("dk", grads[1]), ("dv", grads[2])):
-            rec("unroute", lambda n=n, t=t: P.terra_window_unroute(t, cfg, out=back[n]))
+        rec(ev, "fwd", lambda: P.terra_winattn_fwd_nhwc(x["q"], x["k"], x["v"], table, cfg,
+                                                         out=back["o"], lse=lse))
+        rec(ev, "bwd", lambda: P.terra_winattn_bwd_nhwc(x["q"], x["k"], x["v"], back["o"], x["dout"],
+                                                         lse, table, cfg, workspace=ws,
+                                                         out=(back["dq"], back["dk"], back["dv"],
+                                                              grads[3])))
 
-    print("bench: warm-up %d steps" % args.warmup, file=sys.stderr, flush=True)
-    for _ in range(args.warmup):
-        step(None)
-    torch.cuda.synchronize()
-    ev = {p: [] for p in phases}
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    start.record()
-    for _ in range(args.steps):
-        step(ev)
-    stop.record()
-    torch.cuda.synchronize()
-    print("bench: timed %d steps" % args.steps, file=sys.stderr, flush=True)
-    total_ms = start.elapsed_time(stop)
-    ms_step = total_ms / args.steps
-    per_launch = {p: float(np.mean([a.elapsed_time(b) for a, b in ev[p]])) for p in phases}
-    per_step = {p: float(np.sum([a.elapsed_time(b) for a, b in ev[p]])) / args.steps for p in phases}
+    def step_unfused(ev):
+        for n in ("q", "k", "v"):
+            rec(ev, "route", lambda n=n: P.terra_window_route(x[n], cfg, out=w[n]))
+        rec(ev, "fwd_wm", lambda: P.terra_winattn_fwd(w["q"], w["k"], w["v"], table, cfg, out=o, lse=lse))
+        rec(ev, "route", lambda: P.terra_window_route(x["dout"], cfg, out=w["dout"]))
+        rec(ev, "bwd_wm", lambda: P.terra_winattn_bwd(w["q"], w["k"], w["v"], o, w["dout"], lse, table, cfg,
+                                                      out=grads, workspace=ws))
+        for n, t in (("o", o), ("dq", grads[0]), ("dk", grads[1]), ("dv", grads[2])):
+            rec(ev, "unroute", lambda n=n, t=t: P.terra_window_unroute(t, cfg, out=back[n]))
+
+    def timed(fn, phases):
+        print("bench: warm-up %d steps" % args.warmup, file=sys.stderr, flush=True)
+        for _ in range(args.warmup):
+            fn(None)
+        torch.cuda.synchronize()
+        ev = {p: [] for p in phases}
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        start.record()
+        for _ in range(args.steps):
+            fn(ev)
+        stop.record()
+        torch.cuda.synchronize()
+        print("bench: timed %d steps" % args.steps, file=sys.stderr, flush=True)
+        ms = start.elapsed_time(stop) / args.steps
+        per_launch = {p: float(np.mean([a.elapsed_time(b) for a, b in ev[p]])) for p in phases}
+        per_step = {p: float(np.sum([a.elapsed_time(b) for a, b in ev[p]])) / args.steps for p in phases}
+        return ms, per_launch, per_step
+
+    ms_step, per_launch, per_step = timed(step, fused_phases)
+    ms_unf, pl_unf, ps_unf = timed(step_unfused, unfused_phases)
 
     alg = algorithmic(cfg)
     attn_flops = alg["fwd_flops"] + alg["bwd_flops"]
@@ -218,22 +231,19 @@ def main():
     attn_tflops = attn_flops / (attn_ms * 1e-3) / 1e12
     ai = attn_flops / (alg["fwd_bytes"] + alg["bwd_bytes"])
     attainable = min(peak, ai * PEAK_HBM_GBPS / 1e3)
-    route_gbps = alg["route_bytes"] / (per_launch["route"] * 1e-3) / 1e9
-    unroute_gbps = alg["route_bytes"] / (per_launch["unroute"] * 1e-3) / 1e9
+    route_gbps = alg["route_bytes"] / (pl_unf["route"] * 1e-3) / 1e9
+    unroute_gbps = alg["route_bytes"] / (pl_unf["unroute"] * 1e-3) / 1e9
 
-    # dominant phase (by time per step) -> roofline object
-    unit_bytes = {"route": alg["route_bytes"], "unroute": alg["route_bytes"],
-                  "fwd": alg["fwd_bytes"], "bwd": alg["bwd_bytes"]}
-    dom = max(phases, key=lambda p: per_step[p])
+    # dominant kernel of the step (by time per step) -> roofline object
+    unit_bytes = {"fwd": alg["fwd_bytes"], "bwd": alg["bwd_bytes"]}
+    dom = max(fused_phases, key=lambda p: per_step[p])
     achieved = unit_bytes[dom] / (per_launch[dom] * 1e-3) / 1e9
-    traffic = measured_traffic(cfg.name, dom)
+    traffic = measured_traffic(cfg.name, dom + "_nhwc")
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS,
                 "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4),
                 "traffic": None if traffic is None else round(traffic),
-                "kernel": {"route": "terra_window_route (route_kernel)",
-                           "unroute": "terra_window_unroute (route_kernel)",
-                           "fwd": "terra_winattn_fwd (fwd_win_kernel)",
-                           "bwd": "terra_winattn_bwd (bwd_win_kernel + dtab_reduce_kernel)"}[dom],
+                "kernel": {"fwd": "terra_winattn_fwd_nhwc (fwd_win_pair_kernel)",
+                           "bwd": "terra_winattn_bwd_nhwc (bwd_win_kernel + dtab_reduce_kernel)"}[dom],
                 "algorithmic_bytes_per_launch": unit_bytes[dom],
                 "avg_launch_ms": round(per_launch[dom], 4)}
 
@@ -252,7 +262,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": cfg.name, "B": cfg.B, "grid": [cfg.H, cfg.W], "C": cfg.C,
                    "heads": cfg.heads, "head_dim": cfg.head_dim, "window": [cfg.wh, cfg.ww],
-                   "shift": [cfg.sh, cfg.sw], "parallelism": "single-gpu"},
+                   "shift": [cfg.sh, cfg.sw], "route": "fused", "parallelism": "single-gpu"},
         "roofline": roofline,
         "attn": {"fwd_ms": round(per_step["fwd"], 4), "bwd_ms": round(per_step["bwd"], 4),
                  "tflops_kernels_only": round(attn_tflops, 2),
@@ -261,11 +271,15 @@ def main():
                  "frac_attainable": round(attn_tflops / attainable, 4),
                  "fwd_hbm_GBps": round(alg["fwd_bytes"] / (per_launch["fwd"] * 1e-3) / 1e9, 1),
                  "bwd_hbm_GBps": round(alg["bwd_bytes"] / (per_launch["bwd"] * 1e-3) / 1e9, 1)},
-        "routing": {"route_ms": round(per_launch["route"], 4), "route_GBps": round(route_gbps, 1),
+        "routing": {"route_ms": round(pl_unf["route"], 4), "route_GBps": round(route_gbps, 1),
                     "route_frac_hbm": round(route_gbps / PEAK_HBM_GBPS, 4),
-                    "unroute_ms": round(per_launch["unroute"], 4),
+                    "unroute_ms": round(pl_unf["unroute"], 4),
                     "unroute_GBps": round(unroute_gbps, 1),
                     "unroute_frac_hbm": round(unroute_gbps / PEAK_HBM_GBPS, 4)},
+        "unfused": {"ms_per_step": round(ms_unf, 4),
+                    "value": round(attn_flops / (ms_unf * 1e-3) / 1e12, 2),
+                    "fwd_ms": round(ps_unf["fwd_wm"], 4), "bwd_ms": round(ps_unf["bwd_wm"], 4),
+                    "route_ms_per_step": round(ps_unf["route"] + ps_unf["unroute"], 4)},
     }
     if not args.no_cpu_baseline:
         print("bench: timing the oracle on a sample", file=sys.stderr, flush=True)

@@ -295,19 +295,50 @@ __global__ __launch_bounds__(kWinThreads) void fwd_win_kernel(
 
 // ---------------------------------------------------------------------------
 // Forward for head_dim 32 and an even head count: one workgroup of 8 waves
-// per (image, window, head pair).  Global memory is touched only in
-// row-contiguous 128-byte segments (8 lanes per token row): Q, K and V are
-// staged through LDS (V transposed by the staging stores) and O goes back
-// through LDS.  Wave w handles head 2*hp + (w >> 2) and queries
-// [32*(w&3), 32*(w&3)+32).
+// per (head pair, run of consecutive windows), two resident per CU.  Global
+// memory is touched only in row-contiguous 128-byte segments (8 lanes per
+// token row): Q, K and V of the next window are loaded into registers while
+// the current one computes, then staged through LDS (V transposed by the
+// staging stores); O goes back through LDS.  Wave w handles head
+// 2*hp + (w >> 2) and queries [32*(w&3), 32*(w&3)+32).
 // ---------------------------------------------------------------------------
 constexpr int kPairThreads = 512;
 
+// Rows of one window and head pair held in registers between their prefetch
+// and their staging: thread t holds 16-byte chunks t and t+512 (row =
+// chunk / 8) of K, Q and V.
+struct PairRows {
+  uint4 k[2], q[2], v[2];
+};
+
+template <bool NHWC>
+__device__ __forceinline__ void pair_load_rows(PairRows& r, const Geo& g, int wl, int64_t cbase,
+                                               const bf16* __restrict__ q, const bf16* __restrict__ k,
+                                               const bf16* __restrict__ v) {
+  const int b = wl / g.nwin;
+  const int w = wl - b * g.nwin;
+  const int wi = w / g.Mw, wj = w - (w / g.Mw) * g.Mw;
+  const int n = win_rows(g, wi) * win_cols(g, wj);
+  const WinTokens<NHWC> wt(g, b, wi, wj);
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int idx = threadIdx.x + u * kPairThreads;
+    const int row = idx >> 3, ch = idx & 7;
+    r.k[u] = r.q[u] = r.v[u] = make_uint4(0, 0, 0, 0);
+    if (row < n) {
+      const int64_t off = wt.tok(g, row) * g.C + cbase + ch * 8;
+      r.k[u] = *reinterpret_cast<const uint4*>(k + off);
+      r.q[u] = *reinterpret_cast<const uint4*>(q + off);
+      r.v[u] = *reinterpret_cast<const uint4*>(v + off);
+    }
+  }
+}
+
 template <bool QUAD, bool NHWC>
-__global__ __launch_bounds__(kPairThreads) void fwd_win_pair_kernel(
+__global__ __launch_bounds__(kPairThreads, 4) void fwd_win_pair_kernel(
     const bf16* __restrict__ q, const bf16* __restrict__ k, const bf16* __restrict__ v,
     const float* __restrict__ table, bf16* __restrict__ o, float* __restrict__ lse, Geo g,
-    float scale_log2) {
+    int per_slice, float scale_log2) {
   constexpr int HD = 32;
   constexpr int KS = HD + 8, VS = kWinMax + 8;
   extern __shared__ __align__(16) char smem[];
@@ -318,125 +349,136 @@ __global__ __launch_bounds__(kPairThreads) void fwd_win_pair_kernel(
   float* tab = reinterpret_cast<float*>(kinfo + kWinMax);          // [2][nbins+4]
 
   const int hpairs = g.heads >> 1;
-  int work = xcd_work(blockIdx.x, gridDim.x);
-  const int hp = work % hpairs; work /= hpairs;
-  const int w = work % g.nwin;
-  const int b = work / g.nwin;
-  const int wi = w / g.Mw, wj = w - (w / g.Mw) * g.Mw;
-  const int cols = win_cols(g, wj);
-  const int n = win_rows(g, wi) * cols;
-  const int nkb = (n + 31) >> 5;
-  const WinTokens<NHWC> wt(g, b, wi, wj);
+  const int work = xcd_work(blockIdx.x, gridDim.x);
+  const int slice = work / hpairs;
+  const int hp = work - slice * hpairs;
   const int64_t cbase = (int64_t)2 * hp * HD;          // first channel of the pair
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int half = lane >> 5, col = lane & 31;
   const int hs = wave >> 2, qb = wave & 3;
   const int h = 2 * hp + hs;
   const int qi = 32 * qb + col;
-  const bool qvalid = qi < n;
+  const bf16* ksh = ks + hs * kWinMax * KS;
+  const bf16* vth = vts + hs * HD * VS;
+  const float* tabh = tab + hs * (g.nbins + 4);
 
-  // ---- row-contiguous loads: thread -> (row, 16-byte chunk of the pair) ----
-  uint4 kr[2], qr[2], vr[2];
-#pragma unroll
-  for (int u = 0; u < 2; ++u) {
-    const int idx = threadIdx.x + u * kPairThreads;
-    const int row = idx >> 3, ch = idx & 7;
-    kr[u] = qr[u] = vr[u] = make_uint4(0, 0, 0, 0);
-    if (row < n) {
-      const int64_t off = wt.tok(g, row) * g.C + cbase + ch * 8;
-      kr[u] = *reinterpret_cast<const uint4*>(k + off);
-      qr[u] = *reinterpret_cast<const uint4*>(q + off);
-      vr[u] = *reinterpret_cast<const uint4*>(v + off);
-    }
-  }
+  // bias tables of the pair times sqrt(hd), reversed, then four -inf
   const float bscale = sqrtf((float)HD);
   for (int x = threadIdx.x; x < 2 * (g.nbins + 4); x += kPairThreads) {
     const int t = x / (g.nbins + 4), y = x - t * (g.nbins + 4);
     tab[x] = y < g.nbins ? table[(g.nbins - 1 - y) * g.heads + 2 * hp + t] * bscale : -INFINITY;
   }
-  if (threadIdx.x < kWinMax) kinfo[threadIdx.x] = win_token_info(g, wi, wj, cols, threadIdx.x, n);
-#pragma unroll
-  for (int u = 0; u < 2; ++u) {
-    const int idx = threadIdx.x + u * kPairThreads;
-    const int row = idx >> 3, ch = idx & 7;
-    const int t = ch >> 2, e0 = (ch & 3) * 8;
-    *reinterpret_cast<uint4*>(ks + (t * kWinMax + row) * KS + e0) = kr[u];
-    *reinterpret_cast<uint4*>(qs + (t * kWinMax + row) * KS + e0) = qr[u];
-    const bf16* ve = reinterpret_cast<const bf16*>(&vr[u]);
-#pragma unroll
-    for (int x = 0; x < 8; ++x) vts[(t * HD + e0 + x) * VS + row] = ve[x];
-  }
-  __syncthreads();
 
-  const bool active = qb < nkb;
-  const bf16* ksh = ks + hs * kWinMax * KS;
-  const bf16* vth = vts + hs * HD * VS;
-  const float* tabh = tab + hs * (g.nbins + 4);
-  f32x16 oacc = f32x16{};
-  float m = 0.0f, l = 1.0f;
-  if (active) {
-    bf16x8 qop[2];
+  const int total = g.B * g.nwin;
+  const int wbeg = slice * per_slice;
+  const int wend = min(total, wbeg + per_slice);
+  PairRows rows;
+  if (wbeg < wend) pair_load_rows<NHWC>(rows, g, wbeg, cbase, q, k, v);
+  for (int wl = wbeg; wl < wend; ++wl) {
+    const int b = wl / g.nwin;
+    const int w = wl - b * g.nwin;
+    const int wi = w / g.Mw, wj = w - (w / g.Mw) * g.Mw;
+    const int cols = win_cols(g, wj);
+    const int n = win_rows(g, wi) * cols;
+    const int nkb = (n + 31) >> 5;
+    const WinTokens<NHWC> wt(g, b, wi, wj);
+    const bool qvalid = qi < n;
+
+    __syncthreads();   // the previous window is done with LDS
 #pragma unroll
-    for (int c = 0; c < 2; ++c)
-      qop[c] = *reinterpret_cast<const bf16x8*>(qs + (hs * kWinMax + qi) * KS + 16 * c + 8 * half);
-    const int qinf = kinfo[qvalid ? qi : 0];
-    const int qlab = qinf >> 24;
-    const int qrev = g.nbins - 1 - ((qinf & 0xFFFFFF) + (g.wh - 1) * g.bstride + (g.ww - 1));
-    const bool mask = window_needs_mask(g, wi, wj, n);
-    f32x16 s[4];
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      if (kb < nkb) {
-        s[kb] = mask ? bias_init<QUAD, true>(kinfo, tabh, kb, half, qrev, qlab, g.nbins)
-                     : bias_init<QUAD, false>(kinfo, tabh, kb, half, qrev, qlab, g.nbins);
-#pragma unroll
-        for (int c = 0; c < 2; ++c)
-          mma16(s[kb], *reinterpret_cast<const bf16x8*>(ksh + (32 * kb + col) * KS + 16 * c + 8 * half), qop[c]);
-      }
-    }
-    float mr = -INFINITY;
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb)
-      if (kb < nkb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) mr = fmaxf(mr, s[kb][r]);
-    mr = fmaxf(mr, __shfl_xor(mr, 32));
-    m = mr * scale_log2;
-    l = 0.0f;
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      if (kb < nkb) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float p = __builtin_amdgcn_exp2f(s[kb][r] * scale_log2 - m);
-          s[kb][r] = p;
-          l += p;
-        }
-#pragma unroll
-        for (int c = 0; c < 2; ++c)
-          mma16(oacc, lds_perm_op(vth + col * VS + 32 * kb + 16 * c, half), pack_bf16(s[kb], 8 * c));
-      }
-    }
-    l += __shfl_xor(l, 32);
-  }
-  __syncthreads();   // every wave has read its Q rows; qs now takes O
-  if (active) {
-    const float inv = 1.0f / l;
-#pragma unroll
-    for (int g4 = 0; g4 < 4; ++g4)
-      store4_bf16(qs + (hs * kWinMax + qi) * KS + 8 * g4 + 4 * half, oacc, g4, inv);
-    if (qvalid && half == 0)
-      lse[wt.lse_at(g, h, qi)] = (m + __log2f(l)) * kLn2;
-  }
-  __syncthreads();
-#pragma unroll
-  for (int u = 0; u < 2; ++u) {
-    const int idx = threadIdx.x + u * kPairThreads;
-    const int row = idx >> 3, ch = idx & 7;
-    if (row < n) {
+    for (int u = 0; u < 2; ++u) {
+      const int idx = threadIdx.x + u * kPairThreads;
+      const int row = idx >> 3, ch = idx & 7;
       const int t = ch >> 2, e0 = (ch & 3) * 8;
-      *reinterpret_cast<uint4*>(o + wt.tok(g, row) * g.C + cbase + ch * 8) =
-          *reinterpret_cast<const uint4*>(qs + (t * kWinMax + row) * KS + e0);
+      *reinterpret_cast<uint4*>(ks + (t * kWinMax + row) * KS + e0) = rows.k[u];
+      *reinterpret_cast<uint4*>(qs + (t * kWinMax + row) * KS + e0) = rows.q[u];
+      const bf16* ve = reinterpret_cast<const bf16*>(&rows.v[u]);
+#pragma unroll
+      for (int x = 0; x < 8; ++x) vts[(t * HD + e0 + x) * VS + row] = ve[x];
+    }
+    if (threadIdx.x < kWinMax) kinfo[threadIdx.x] = win_token_info(g, wi, wj, cols, threadIdx.x, n);
+    __syncthreads();
+    if (wl + 1 < wend) pair_load_rows<NHWC>(rows, g, wl + 1, cbase, q, k, v);
+
+    // Softmax over the two halves of the window's keys in turn (running
+    // max and sum; a half with no allowed key for a query leaves it as it
+    // was), so that only 32 score registers are live.
+    const bool active = qb < nkb;
+    f32x16 oacc = f32x16{};
+    float m = -INFINITY, l = 0.0f;
+    if (active) {
+      bf16x8 qop[2];
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+        qop[c] = *reinterpret_cast<const bf16x8*>(qs + (hs * kWinMax + qi) * KS + 16 * c + 8 * half);
+      const int qinf = kinfo[qvalid ? qi : 0];
+      const int qlab = qinf >> 24;
+      const int qrev = g.nbins - 1 - ((qinf & 0xFFFFFF) + (g.wh - 1) * g.bstride + (g.ww - 1));
+      const bool mask = window_needs_mask(g, wi, wj, n);
+#pragma unroll
+      for (int hb = 0; hb < 2; ++hb) {
+        if (2 * hb < nkb) {
+          f32x16 s[2];
+          float mr = -INFINITY;
+#pragma unroll
+          for (int j = 0; j < 2; ++j) {
+            const int kb = 2 * hb + j;
+            if (kb < nkb) {
+              s[j] = mask ? bias_init<QUAD, true>(kinfo, tabh, kb, half, qrev, qlab, g.nbins)
+                          : bias_init<QUAD, false>(kinfo, tabh, kb, half, qrev, qlab, g.nbins);
+#pragma unroll
+              for (int c = 0; c < 2; ++c)
+                mma16(s[j], *reinterpret_cast<const bf16x8*>(ksh + (32 * kb + col) * KS + 16 * c + 8 * half),
+                      qop[c]);
+#pragma unroll
+              for (int r = 0; r < 16; ++r) mr = fmaxf(mr, s[j][r]);
+            }
+          }
+          mr = fmaxf(mr, __shfl_xor(mr, 32));
+          const float mnew = fmaxf(m, mr * scale_log2);
+          const float mref = mnew == -INFINITY ? 0.0f : mnew;   // nothing allowed yet
+          const float alpha = __builtin_amdgcn_exp2f(m - mref);
+          l *= alpha;
+#pragma unroll
+          for (int r = 0; r < 16; ++r) oacc[r] *= alpha;
+          m = mnew;
+#pragma unroll
+          for (int j = 0; j < 2; ++j) {
+            const int kb = 2 * hb + j;
+            if (kb < nkb) {
+#pragma unroll
+              for (int r = 0; r < 16; ++r) {
+                const float p = __builtin_amdgcn_exp2f(s[j][r] * scale_log2 - mref);
+                s[j][r] = p;
+                l += p;
+              }
+#pragma unroll
+              for (int c = 0; c < 2; ++c)
+                mma16(oacc, lds_perm_op(vth + col * VS + 32 * kb + 16 * c, half), pack_bf16(s[j], 8 * c));
+            }
+          }
+        }
+      }
+      l += __shfl_xor(l, 32);
+    }
+    __syncthreads();   // every wave has read its Q rows; qs now takes O
+    if (active) {
+      const float inv = 1.0f / l;
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4)
+        store4_bf16(qs + (hs * kWinMax + qi) * KS + 8 * g4 + 4 * half, oacc, g4, inv);
+      if (qvalid && half == 0) lse[wt.lse_at(g, h, qi)] = (m + __log2f(l)) * kLn2;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int idx = threadIdx.x + u * kPairThreads;
+      const int row = idx >> 3, ch = idx & 7;
+      if (row < n) {
+        const int t = ch >> 2, e0 = (ch & 3) * 8;
+        *reinterpret_cast<uint4*>(o + wt.tok(g, row) * g.C + cbase + ch * 8) =
+            *reinterpret_cast<const uint4*>(qs + (t * kWinMax + row) * KS + e0);
+      }
     }
   }
 }
@@ -914,14 +956,27 @@ size_t win_fwd_pair_lds(const Geo& g) {
          4 * 2 * (g.nbins + 4);
 }
 
+// Slices of the window range per head pair of the forward: one round of
+// workgroups, two resident per CU.
+static int win_fwd_pair_nslice(const Geo& g) {
+  const int total = g.B * g.nwin;
+  int target = 2 * 256 / (g.heads / 2);
+  if (target > total) target = total;
+  if (target < 1) target = 1;
+  return target;
+}
+
 template <bool QUAD, bool NHWC>
 static void fwd_win_pair_go(const Geo& g, const void* q, const void* k, const void* v,
                             const float* table, void* o, float* lse, hipStream_t st) {
-  const int grid = g.B * g.nwin * (g.heads / 2);
+  const int total = g.B * g.nwin;
+  const int nslice = win_fwd_pair_nslice(g);
+  const int per = (total + nslice - 1) / nslice;
+  const int grid = (g.heads / 2) * ((total + per - 1) / per);
   const float sl2 = kLog2e / sqrtf((float)g.hd);
   hipLaunchKernelGGL((fwd_win_pair_kernel<QUAD, NHWC>), dim3(grid), dim3(kPairThreads),
                      win_fwd_pair_lds(g), st, (const bf16*)q, (const bf16*)k, (const bf16*)v, table,
-                     (bf16*)o, lse, g, sl2);
+                     (bf16*)o, lse, g, per, sl2);
 }
 
 template <bool NHWC>
