@@ -295,18 +295,17 @@ __global__ __launch_bounds__(kWinThreads) void fwd_win_kernel(
 
 // ---------------------------------------------------------------------------
 // Forward for head_dim 32 and an even head count: one workgroup of 8 waves
-// per (head pair, run of consecutive windows), two resident per CU.  Global
-// memory is touched only in row-contiguous 128-byte segments (8 lanes per
-// token row): Q, K and V of the next window are loaded into registers while
-// the current one computes, then staged through LDS (V transposed by the
-// staging stores); O goes back through LDS.  Wave w handles head
+// per (head pair, run of consecutive windows), two resident per CU (one's
+// loads overlap the other's matrix work; loading one window ahead measured
+// slower).  Global memory is touched only in row-contiguous 128-byte
+// segments (8 lanes per token row): Q, K and V are staged through LDS (V
+// transposed by the staging stores) and O goes back through LDS.  Wave w handles head
 // 2*hp + (w >> 2) and queries [32*(w&3), 32*(w&3)+32).
 // ---------------------------------------------------------------------------
 constexpr int kPairThreads = 512;
 
-// Rows of one window and head pair held in registers between their prefetch
-// and their staging: thread t holds 16-byte chunks t and t+512 (row =
-// chunk / 8) of K, Q and V.
+// Rows of one window and head pair on their way from HBM to LDS: thread t
+// holds 16-byte chunks t and t+512 (row = chunk / 8) of K, Q and V.
 struct PairRows {
   uint4 k[2], q[2], v[2];
 };
@@ -373,7 +372,6 @@ __global__ __launch_bounds__(kPairThreads, 4) void fwd_win_pair_kernel(
   const int wbeg = slice * per_slice;
   const int wend = min(total, wbeg + per_slice);
   PairRows rows;
-  if (wbeg < wend) pair_load_rows<NHWC>(rows, g, wbeg, cbase, q, k, v);
   for (int wl = wbeg; wl < wend; ++wl) {
     const int b = wl / g.nwin;
     const int w = wl - b * g.nwin;
@@ -384,6 +382,7 @@ __global__ __launch_bounds__(kPairThreads, 4) void fwd_win_pair_kernel(
     const WinTokens<NHWC> wt(g, b, wi, wj);
     const bool qvalid = qi < n;
 
+    pair_load_rows<NHWC>(rows, g, wl, cbase, q, k, v);
     __syncthreads();   // the previous window is done with LDS
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
@@ -398,7 +397,6 @@ __global__ __launch_bounds__(kPairThreads, 4) void fwd_win_pair_kernel(
     }
     if (threadIdx.x < kWinMax) kinfo[threadIdx.x] = win_token_info(g, wi, wj, cols, threadIdx.x, n);
     __syncthreads();
-    if (wl + 1 < wend) pair_load_rows<NHWC>(rows, g, wl + 1, cbase, q, k, v);
 
     // Softmax over the two halves of the window's keys in turn (running
     // max and sum; a half with no allowed key for a query leaves it as it
@@ -577,9 +575,13 @@ __device__ __forceinline__ f32x16 bwd_p(const BwdWave& st) {
   return p;
 }
 
+// dP of key block KB (lane = query, registers = keys), plus `init` (the
+// accumulator's starting value: 0, or -D so that dP - D comes out directly).
 template <int KB>
-__device__ __forceinline__ f32x16 bwd_dp(const BwdWave& st) {
-  f32x16 dp = f32x16{};
+__device__ __forceinline__ f32x16 bwd_dp(const BwdWave& st, float init) {
+  f32x16 dp;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) dp[r] = init;
 #pragma unroll
   for (int c = 0; c < 2; ++c)
     mma16(dp, *reinterpret_cast<const bf16x8*>(st.vs + (32 * KB + st.col) * kBwdKS + 16 * c + 8 * st.half),
@@ -599,9 +601,9 @@ __device__ __forceinline__ void bwd_step(const BwdWave& st, f32x4& dta, f32x4& d
   bf16x8 pb0, pb1, db0, db1;
   {
     const f32x16 p = bwd_p<KB, QUAD, MASK>(st);
-    f32x16 ds = bwd_dp<KB>(st);
+    f32x16 ds = bwd_dp<KB>(st, -st.D);
 #pragma unroll
-    for (int r = 0; r < 16; ++r) ds[r] = p[r] * (ds[r] - st.D);
+    for (int r = 0; r < 16; ++r) ds[r] *= p[r];
 #pragma unroll
     for (int g4 = 0; g4 < 4; ++g4) fold_diag(ds, g4, st.fold, dta, dtb);
     pb0 = pack_bf16(p, 0); pb1 = pack_bf16(p, 8);
@@ -656,7 +658,7 @@ __device__ __forceinline__ void bwd_window_body(BwdWave& st, int qw, f32x4 (&dta
 #define TERRA_DSUM(KB)                                                          \
   {                                                                             \
     const f32x16 pk = bwd_p<KB, QUAD, MASK>(st);                                \
-    const f32x16 dk = bwd_dp<KB>(st);                                           \
+    const f32x16 dk = bwd_dp<KB>(st, 0.0f);                                     \
     _Pragma("unroll") for (int r = 0; r < 16; ++r) dsum += pk[r] * dk[r];       \
   }
   TERRA_DSUM(0)
@@ -674,9 +676,9 @@ __device__ __forceinline__ void bwd_window_body(BwdWave& st, int qw, f32x4 (&dta
   }
 }
 
-// Rows of one window held in registers between its prefetch and its
-// staging: thread t holds 16-byte chunks t and t+256 (row = chunk / 4) of
-// K, V, Q and dO, and the log-sum-exp (log2 units) of its wave's query.
+// Rows of one window on their way from HBM to LDS: thread t holds 16-byte
+// chunks t and t+256 (row = chunk / 4) of K, V, Q and dO, and the
+// log-sum-exp (log2 units) of its wave's query.
 struct BwdRows {
   uint4 k[2], v[2], q[2], d[2];
   float lse2;
@@ -708,10 +710,11 @@ __device__ __forceinline__ void bwd_load_rows(BwdRows& r, const Geo& g, int wl, 
   r.lse2 = qi < n ? lse[wt.lse_at(g, h, qi)] * kLog2e : INFINITY;
 }
 
-// Backward, head_dim 32, every window width a multiple of 4.  K, V, Q and dO
-// arrive with row-contiguous loads one window ahead (prefetched into
-// registers while the previous window computes); Q and dO are staged in the
-// dV/dK sum areas, which are free until the rotation starts.  dQ, dK and dV
+// Backward, head_dim 32, window widths in {4, 8, 16, 32}.  K, V, Q and dO
+// arrive with row-contiguous loads (the other workgroup resident on the CU
+// computes meanwhile; loading one window ahead measured slower); Q and dO
+// are staged in the dV/dK sum areas, which are free until the rotation
+// starts.  dQ, dK and dV
 // leave with row-contiguous stores.  The bias-gradient sums of every
 // register run over windows of equal width and are flushed to per-wave LDS
 // bins when the width changes (a register holds the same query/key slot
@@ -784,7 +787,6 @@ __global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
   const int wbeg = slice * per_slice;
   const int wend = min(total, wbeg + per_slice);
   BwdRows rows;
-  if (wbeg < wend) bwd_load_rows<NHWC>(rows, g, wbeg, h, qi, q, k, v, dout, lse);
   for (int wl = wbeg; wl < wend; ++wl) {
     const int b = wl / g.nwin;
     const int w = wl - b * g.nwin;
@@ -797,6 +799,7 @@ __global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
       acc_cols = cols;
     }
 
+    bwd_load_rows<NHWC>(rows, g, wl, h, qi, q, k, v, dout, lse);
     __syncthreads();   // the previous window is done with LDS
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
@@ -811,7 +814,6 @@ __global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
     BwdWave st;
     st.lse2 = rows.lse2;
     __syncthreads();
-    if (wl + 1 < wend) bwd_load_rows<NHWC>(rows, g, wl + 1, h, qi, q, k, v, dout, lse);
 
     st.ks = ks;
     st.vs = vs;
