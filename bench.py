@@ -36,7 +36,7 @@ sys.path.insert(0, ROOT)
 import terra_synth as ts  # noqa: E402
 
 METRIC = "Swin window-attn fwd+bwd TFLOP/s (% MFMA peak); routing GB/s (% HBM)"
-PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 / fp16 MFMA
 PEAK_F32_TFLOPS = 157.3       # MI355X fp32 matrix
 PEAK_HBM_GBPS = 8000.0        # MI355X HBM3E
 DEFAULT_CONFIG = "c4_bf16_128x1080_w8x16"
@@ -140,7 +140,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", default=DEFAULT_CONFIG, choices=ts.ORDER)
+    ap.add_argument("--config", default=DEFAULT_CONFIG, choices=list(ts.ALL))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -151,10 +151,10 @@ def main():
     import torch
     import paper_2608_15211_amd as P
 
-    cfg = ts.CONFIGS[args.config]
+    cfg = ts.ALL[args.config]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    tdt = torch.float32 if cfg.dtype == "f32" else torch.bfloat16
+    tdt = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[cfg.dtype]
     print("bench: generating %s inputs" % cfg.name, file=sys.stderr, flush=True)
     inp = ts.make_inputs(cfg)
     x = {n: torch.from_numpy(inp[n]).to(dev).to(tdt) for n in ("q", "k", "v", "dout")}
@@ -234,18 +234,26 @@ def main():
     route_gbps = alg["route_bytes"] / (pl_unf["route"] * 1e-3) / 1e9
     unroute_gbps = alg["route_bytes"] / (pl_unf["unroute"] * 1e-3) / 1e9
 
-    # dominant kernel of the step (by time per step) -> roofline object
+    # dominant kernel of the step (by time per step) -> roofline object: HBM
+    # bound below the ridge point (peak flops / peak bandwidth), matrix-core
+    # bound above it
     unit_bytes = {"fwd": alg["fwd_bytes"], "bwd": alg["bwd_bytes"]}
+    unit_flops = {"fwd": alg["fwd_flops"], "bwd": alg["bwd_flops"]}
     dom = max(fused_phases, key=lambda p: per_step[p])
-    achieved = unit_bytes[dom] / (per_launch[dom] * 1e-3) / 1e9
     traffic = measured_traffic(cfg.name, dom + "_nhwc")
-    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS,
-                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4),
-                "traffic": None if traffic is None else round(traffic),
-                "kernel": {"fwd": "terra_winattn_fwd_nhwc (fwd_win_pair_kernel)",
-                           "bwd": "terra_winattn_bwd_nhwc (bwd_win_kernel + dtab_reduce_kernel)"}[dom],
-                "algorithmic_bytes_per_launch": unit_bytes[dom],
-                "avg_launch_ms": round(per_launch[dom], 4)}
+    if unit_flops[dom] / unit_bytes[dom] > peak * 1e12 / (PEAK_HBM_GBPS * 1e9):
+        achieved = unit_flops[dom] / (per_launch[dom] * 1e-3) / 1e12
+        roofline = {"bound": "mfma", "achieved": round(achieved, 1), "peak": peak,
+                    "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
+                    "algorithmic_flops_per_launch": unit_flops[dom]}
+    else:
+        achieved = unit_bytes[dom] / (per_launch[dom] * 1e-3) / 1e9
+        roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS,
+                    "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBPS, 4),
+                    "algorithmic_bytes_per_launch": unit_bytes[dom]}
+    roofline.update({"traffic": None if traffic is None else round(traffic),
+                     "kernel": {"fwd": "terra_winattn_fwd_nhwc", "bwd": "terra_winattn_bwd_nhwc"}[dom],
+                     "avg_launch_ms": round(per_launch[dom], 4)})
 
     line = {
         "metric": METRIC,

@@ -29,9 +29,10 @@
  *   window-major token order.  Bias tables are float32
  *   [2wh-1][2ww-1][heads]; the bias of query q and key k is
  *   T[a_q - a_k + wh - 1][c_q - c_k + ww - 1][h], (a, c) = in-window offset.
- * Element types.  TERRA_F32 (float) or TERRA_BF16 (bfloat16 storage, float32
- *   accumulation, results rounded to nearest even).  Bias tables, LSE and the
- *   bias-table gradient are always float32.
+ * Element types.  TERRA_F32 (float), TERRA_BF16 (bfloat16 storage, float32
+ *   accumulation, results rounded to nearest even) or TERRA_F16 (IEEE half
+ *   storage, the paper's training precision, float32 accumulation).  Bias
+ *   tables, LSE and the bias-table gradient are always float32.
  * Memory.  Every tensor pointer is a DEVICE pointer allocated by the caller;
  *   the library allocates nothing and keeps no device state.  Geometry
  *   structs and host arrays stay owned by the caller.  Tensors of one call
@@ -61,7 +62,7 @@ typedef struct terra_geom {
   int32_t mask_flags;        /* TERRA_MASK_LAT | TERRA_MASK_LON           */
 } terra_geom;
 
-enum terra_dtype { TERRA_F32 = 0, TERRA_BF16 = 1 };
+enum terra_dtype { TERRA_F32 = 0, TERRA_BF16 = 1, TERRA_F16 = 2 };
 
 enum terra_status {
   TERRA_OK = 0,
@@ -79,8 +80,8 @@ int terra_version(void);
 
 /* Checks the geometry rules above (host only, no device call).  Returns
  * TERRA_OK, TERRA_ERR_INVALID, or TERRA_ERR_UNSUPPORTED when the attention
- * kernels cannot take it (head_dim not 32 or 64, more than 8192 bias bins
- * per head, more than 2^31 elements per tensor).  Routing accepts any
+ * kernels cannot take it (head_dim not 32, 64 or 128, more than 8192 bias
+ * bins per head, more than 2^31 elements per tensor).  Routing accepts any
  * geometry that is valid. */
 int terra_validate_geometry(const terra_geom* g);
 

@@ -21,6 +21,7 @@ LIB_PATH = os.path.join(_HERE, "libterra_swin.so")
 
 TERRA_F32 = 0
 TERRA_BF16 = 1
+TERRA_F16 = 2
 TERRA_MASK_LAT = 1
 TERRA_MASK_LON = 2
 STATUS = {0: "TERRA_OK", 1: "TERRA_ERR_INVALID", 2: "TERRA_ERR_UNSUPPORTED",
@@ -129,6 +130,8 @@ def _dtype_code(dtype):
         return TERRA_F32
     if dtype in (torch.bfloat16, "bf16"):
         return TERRA_BF16
+    if dtype in (torch.float16, "f16"):
+        return TERRA_F16
     raise TypeError("unsupported dtype %r" % (dtype,))
 
 

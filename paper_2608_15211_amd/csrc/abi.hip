@@ -11,14 +11,14 @@
 namespace terra {
 hipError_t launch_route(const Geo& g, int row_bytes, const void* src, void* dst, bool forward,
                         hipStream_t stream);
-hipError_t launch_attn_fwd(const Geo& g, bool bf16, bool nhwc, const void* q, const void* k,
+hipError_t launch_attn_fwd(const Geo& g, int dt, bool nhwc, const void* q, const void* k,
                            const void* v, const float* table, void* o, float* lse, hipStream_t st);
-hipError_t launch_attn_bwd(const Geo& g, bool bf16, bool nhwc, const void* q, const void* k,
+hipError_t launch_attn_bwd(const Geo& g, int dt, bool nhwc, const void* q, const void* k,
                            const void* v, const void* o, const void* dout, const float* lse,
                            const float* table, void* dq, void* dk, void* dv, float* dtab, void* ws,
                            hipStream_t st);
-size_t bwd_workspace(const Geo& g, bool bf16);
-size_t attn_max_lds(const Geo& g, bool bf16);
+size_t bwd_workspace(const Geo& g, int dt);
+size_t attn_max_lds(const Geo& g, int dt);
 }  // namespace terra
 
 namespace {
@@ -72,8 +72,8 @@ int check_geom(const terra_geom* g) {
 }
 
 int check_dtype(int dtype) {
-  if (dtype != TERRA_F32 && dtype != TERRA_BF16)
-    return fail(TERRA_ERR_INVALID, "dtype %d is neither TERRA_F32 nor TERRA_BF16", dtype);
+  if (dtype != TERRA_F32 && dtype != TERRA_BF16 && dtype != TERRA_F16)
+    return fail(TERRA_ERR_INVALID, "dtype %d is not TERRA_F32, TERRA_BF16 or TERRA_F16", dtype);
   return ok();
 }
 
@@ -95,8 +95,8 @@ int check_attn(const terra_geom* g, int dtype) {
   int s = check_geom(g);
   if (s) return s;
   if ((s = check_dtype(dtype))) return s;
-  if (g->head_dim != 32 && g->head_dim != 64)
-    return fail(TERRA_ERR_UNSUPPORTED, "head_dim %d: the attention kernels take 32 or 64",
+  if (g->head_dim != 32 && g->head_dim != 64 && g->head_dim != 128)
+    return fail(TERRA_ERR_UNSUPPORTED, "head_dim %d: the attention kernels take 32, 64 or 128",
                 g->head_dim);
   if ((int64_t)g->B * g->H * g->W * g->C >= kMaxElems)
     return fail(TERRA_ERR_UNSUPPORTED, "tensors above 2^31 elements are not supported");
@@ -104,7 +104,7 @@ int check_attn(const terra_geom* g, int dtype) {
   if (G.nbins > kMaxBins)
     return fail(TERRA_ERR_UNSUPPORTED, "(2wh-1)(2ww-1) = %d bias bins exceeds %d", G.nbins,
                 kMaxBins);
-  if (terra::attn_max_lds(G, dtype == TERRA_BF16) > kMaxLds)
+  if (terra::attn_max_lds(G, dtype) > kMaxLds)
     return fail(TERRA_ERR_UNSUPPORTED, "window needs more LDS than one workgroup has");
   return ok();
 }
@@ -118,8 +118,8 @@ int terra_version(void) { return 100; }
 int terra_validate_geometry(const terra_geom* g) {
   int s = check_geom(g);
   if (s) return s;
-  if (g->head_dim != 32 && g->head_dim != 64)
-    return fail(TERRA_ERR_UNSUPPORTED, "head_dim %d: the attention kernels take 32 or 64",
+  if (g->head_dim != 32 && g->head_dim != 64 && g->head_dim != 128)
+    return fail(TERRA_ERR_UNSUPPORTED, "head_dim %d: the attention kernels take 32, 64 or 128",
                 g->head_dim);
   terra::Geo G = make_geo(g);
   if (G.nbins > kMaxBins)
@@ -162,7 +162,7 @@ static int route_common(const terra_geom* g, int dtype, const void* src, void* d
   if ((s = check_dtype(dtype))) return s;
   if (!src || !dst) return fail(TERRA_ERR_INVALID, "tensor pointer is NULL");
   if (src == dst) return fail(TERRA_ERR_INVALID, "route source and destination must differ");
-  const int esize = dtype == TERRA_BF16 ? 2 : 4;
+  const int esize = dtype == TERRA_F32 ? 4 : 2;
   const int64_t row_bytes = (int64_t)g->C * esize;
   // The per-window chunk index must stay below 2^22 (worst case 2-byte chunks).
   if ((int64_t)g->wh * g->ww * (row_bytes / 2) >= ((int64_t)1 << 22))
@@ -193,7 +193,7 @@ static int attn_fwd_common(const terra_geom* g, int dtype, bool nhwc, const void
   if (!q || !k || !v || !bias_table || !o || !lse)
     return fail(TERRA_ERR_INVALID, "tensor pointer is NULL");
   terra::Geo G = make_geo(g);
-  return hip_status(terra::launch_attn_fwd(G, dtype == TERRA_BF16, nhwc, q, k, v, bias_table, o, lse,
+  return hip_status(terra::launch_attn_fwd(G, dtype, nhwc, q, k, v, bias_table, o, lse,
                                            (hipStream_t)stream),
                     nhwc ? "terra_winattn_fwd_nhwc launch" : "terra_winattn_fwd launch");
 }
@@ -208,11 +208,11 @@ static int attn_bwd_common(const terra_geom* g, int dtype, bool nhwc, const void
   if (!q || !k || !v || !o || !dout || !lse || !bias_table || !dq || !dk || !dv || !dbias_table)
     return fail(TERRA_ERR_INVALID, "tensor pointer is NULL");
   terra::Geo G = make_geo(g);
-  const size_t need = terra::bwd_workspace(G, dtype == TERRA_BF16);
+  const size_t need = terra::bwd_workspace(G, dtype);
   if (!workspace || workspace_bytes < need)
     return fail(TERRA_ERR_WORKSPACE, "workspace of %zu bytes given, %zu needed",
                 workspace ? workspace_bytes : (size_t)0, need);
-  return hip_status(terra::launch_attn_bwd(G, dtype == TERRA_BF16, nhwc, q, k, v, o, dout, lse,
+  return hip_status(terra::launch_attn_bwd(G, dtype, nhwc, q, k, v, o, dout, lse,
                                            bias_table, dq, dk, dv, dbias_table, workspace,
                                            (hipStream_t)stream),
                     nhwc ? "terra_winattn_bwd_nhwc launch" : "terra_winattn_bwd launch");
@@ -233,7 +233,7 @@ int terra_winattn_fwd_nhwc(const terra_geom* g, int dtype, const void* q, const 
 
 size_t terra_winattn_bwd_workspace_bytes(const terra_geom* g, int dtype) {
   if (check_attn(g, dtype)) return 0;
-  return terra::bwd_workspace(make_geo(g), dtype == TERRA_BF16);
+  return terra::bwd_workspace(make_geo(g), dtype);
 }
 
 int terra_winattn_bwd(const terra_geom* g, int dtype, const void* q, const void* k, const void* v,

@@ -45,9 +45,9 @@ hipError_t launch_win_bwd(const Geo& g, bool nhwc, const void* q, const void* k,
 constexpr int kThreads = 256;   // 4 waves
 constexpr int kWaveQ = 32;      // queries (or keys) per wave
 constexpr int kChunk = 128;     // queries (or keys) per workgroup
-// Keys (or queries) per LDS tile: 64, or 32 for fp32 with head_dim 64 so
-// that the staged tiles stay within 64 KB of LDS.
-template <typename T, int HD> constexpr int tile_of() { return (sizeof(T) == 4 && HD == 64) ? 32 : 64; }
+// Keys (or queries) per LDS tile: 64, or 32 for fp32 with head_dim 64 or 128
+// (so that a staged tile set stays within 80 KB of LDS).
+template <typename T, int HD> constexpr int tile_of() { return (sizeof(T) == 4 && HD >= 64) ? 32 : 64; }
 constexpr int kPad = 8;         // LDS row padding, elements
 constexpr int kLabBad = 0xFF;   // label of padding slots (never matches)
 
@@ -581,8 +581,8 @@ static hipError_t fwd_impl(const Geo& g, const void* q, const void* k, const voi
   return hipGetLastError();
 }
 
-size_t bwd_workspace(const Geo& g, bool bf16) {
-  if (win_bwd_ok(g, bf16)) return (size_t)g.heads * win_bwd_nslice(g) * g.nbins * sizeof(float);
+size_t bwd_workspace(const Geo& g, int dt) {
+  if (win_bwd_ok(g, dt == 1)) return (size_t)g.heads * win_bwd_nslice(g) * g.nbins * sizeof(float);
   const size_t dbytes = (size_t)g.B * g.heads * g.HW * sizeof(float);
   const size_t pbytes = (size_t)g.heads * bwd_nslice(g) * g.nbins * sizeof(float);
   return ((dbytes + 255) / 256) * 256 + pbytes;
@@ -621,60 +621,81 @@ static hipError_t bwd_impl(const Geo& g, const void* q, const void* k, const voi
   return hipGetLastError();
 }
 
-size_t attn_max_lds(const Geo& g, bool bf16) {
-  size_t m;
-  if (bf16) {
-    m = g.hd == 32 ? dkdv_lds<__bf16, 32>(g) : dkdv_lds<__bf16, 64>(g);
-    const size_t d = g.hd == 32 ? dq_lds<__bf16, 32>(g) : dq_lds<__bf16, 64>(g);
-    m = m > d ? m : d;
-  } else {
-    m = g.hd == 32 ? dkdv_lds<float, 32>(g) : dkdv_lds<float, 64>(g);
-    const size_t d = g.hd == 32 ? dq_lds<float, 32>(g) : dq_lds<float, 64>(g);
-    m = m > d ? m : d;
+// Element type codes of the C ABI: 0 float, 1 bfloat16, 2 float16.
+constexpr int kF32 = 0, kBF16 = 1;
+
+template <typename T>
+static size_t max_lds_t(const Geo& g) {
+  size_t m, d;
+  switch (g.hd) {
+    case 32: m = dkdv_lds<T, 32>(g); d = dq_lds<T, 32>(g); break;
+    case 64: m = dkdv_lds<T, 64>(g); d = dq_lds<T, 64>(g); break;
+    default: m = dkdv_lds<T, 128>(g); d = dq_lds<T, 128>(g); break;
   }
-  if (win_fwd_ok(g, bf16) && win_fwd_lds(g) > m) m = win_fwd_lds(g);
-  if (win_bwd_ok(g, bf16) && win_bwd_lds(g) > m) m = win_bwd_lds(g);
+  return m > d ? m : d;
+}
+
+size_t attn_max_lds(const Geo& g, int dt) {
+  size_t m = dt == kF32 ? max_lds_t<float>(g) : dt == kBF16 ? max_lds_t<__bf16>(g) : max_lds_t<_Float16>(g);
+  const bool bf = dt == kBF16;
+  if (win_fwd_ok(g, bf) && win_fwd_lds(g) > m) m = win_fwd_lds(g);
+  if (win_bwd_ok(g, bf) && win_bwd_lds(g) > m) m = win_bwd_lds(g);
   return m;
 }
 
-template <bool NHWC>
-static hipError_t fwd_generic(const Geo& g, bool bf16, const void* q, const void* k, const void* v,
+template <typename T, bool NHWC>
+static hipError_t fwd_generic(const Geo& g, const void* q, const void* k, const void* v,
                               const float* table, void* o, float* lse, hipStream_t st) {
-  if (bf16)
-    return g.hd == 32 ? fwd_impl<__bf16, 32, NHWC>(g, q, k, v, table, o, lse, st)
-                      : fwd_impl<__bf16, 64, NHWC>(g, q, k, v, table, o, lse, st);
-  return g.hd == 32 ? fwd_impl<float, 32, NHWC>(g, q, k, v, table, o, lse, st)
-                    : fwd_impl<float, 64, NHWC>(g, q, k, v, table, o, lse, st);
+  switch (g.hd) {
+    case 32: return fwd_impl<T, 32, NHWC>(g, q, k, v, table, o, lse, st);
+    case 64: return fwd_impl<T, 64, NHWC>(g, q, k, v, table, o, lse, st);
+    default: return fwd_impl<T, 128, NHWC>(g, q, k, v, table, o, lse, st);
+  }
 }
 
-template <bool NHWC>
-static hipError_t bwd_generic(const Geo& g, bool bf16, const void* q, const void* k, const void* v,
+template <typename T, bool NHWC>
+static hipError_t bwd_generic(const Geo& g, const void* q, const void* k, const void* v,
                               const void* o, const void* dout, const float* lse, const float* table,
                               void* dq, void* dk, void* dv, float* dtab, void* ws, hipStream_t st) {
-  if (bf16)
-    return g.hd == 32
-               ? bwd_impl<__bf16, 32, NHWC>(g, q, k, v, o, dout, lse, table, dq, dk, dv, dtab, ws, st)
-               : bwd_impl<__bf16, 64, NHWC>(g, q, k, v, o, dout, lse, table, dq, dk, dv, dtab, ws, st);
-  return g.hd == 32
-             ? bwd_impl<float, 32, NHWC>(g, q, k, v, o, dout, lse, table, dq, dk, dv, dtab, ws, st)
-             : bwd_impl<float, 64, NHWC>(g, q, k, v, o, dout, lse, table, dq, dk, dv, dtab, ws, st);
+  switch (g.hd) {
+    case 32: return bwd_impl<T, 32, NHWC>(g, q, k, v, o, dout, lse, table, dq, dk, dv, dtab, ws, st);
+    case 64: return bwd_impl<T, 64, NHWC>(g, q, k, v, o, dout, lse, table, dq, dk, dv, dtab, ws, st);
+    default: return bwd_impl<T, 128, NHWC>(g, q, k, v, o, dout, lse, table, dq, dk, dv, dtab, ws, st);
+  }
 }
 
-// nhwc: q, k, v, o (and dout, dq, dk, dv) are B x H x W x C read and written
-// in place (the token route fused into the kernels), LSE in the same token
-// order; otherwise they are window-major.
-hipError_t launch_attn_fwd(const Geo& g, bool bf16, bool nhwc, const void* q, const void* k,
+template <bool NHWC>
+static hipError_t fwd_dispatch(const Geo& g, int dt, const void* q, const void* k, const void* v,
+                               const float* table, void* o, float* lse, hipStream_t st) {
+  if (dt == kF32) return fwd_generic<float, NHWC>(g, q, k, v, table, o, lse, st);
+  if (dt == kBF16) return fwd_generic<__bf16, NHWC>(g, q, k, v, table, o, lse, st);
+  return fwd_generic<_Float16, NHWC>(g, q, k, v, table, o, lse, st);
+}
+
+template <bool NHWC>
+static hipError_t bwd_dispatch(const Geo& g, int dt, const void* q, const void* k, const void* v,
+                               const void* o, const void* dout, const float* lse, const float* table,
+                               void* dq, void* dk, void* dv, float* dtab, void* ws, hipStream_t st) {
+  if (dt == kF32) return bwd_generic<float, NHWC>(g, q, k, v, o, dout, lse, table, dq, dk, dv, dtab, ws, st);
+  if (dt == kBF16) return bwd_generic<__bf16, NHWC>(g, q, k, v, o, dout, lse, table, dq, dk, dv, dtab, ws, st);
+  return bwd_generic<_Float16, NHWC>(g, q, k, v, o, dout, lse, table, dq, dk, dv, dtab, ws, st);
+}
+
+// dt: element type code.  nhwc: q, k, v, o (and dout, dq, dk, dv) are
+// B x H x W x C read and written in place (the token route fused into the
+// kernels), LSE in the same token order; otherwise they are window-major.
+hipError_t launch_attn_fwd(const Geo& g, int dt, bool nhwc, const void* q, const void* k,
                            const void* v, const float* table, void* o, float* lse, hipStream_t st) {
-  if (win_fwd_ok(g, bf16)) return launch_win_fwd(g, nhwc, q, k, v, table, o, lse, st);
-  return nhwc ? fwd_generic<true>(g, bf16, q, k, v, table, o, lse, st)
-              : fwd_generic<false>(g, bf16, q, k, v, table, o, lse, st);
+  if (win_fwd_ok(g, dt == kBF16)) return launch_win_fwd(g, nhwc, q, k, v, table, o, lse, st);
+  return nhwc ? fwd_dispatch<true>(g, dt, q, k, v, table, o, lse, st)
+              : fwd_dispatch<false>(g, dt, q, k, v, table, o, lse, st);
 }
 
-hipError_t launch_attn_bwd(const Geo& g, bool bf16, bool nhwc, const void* q, const void* k,
+hipError_t launch_attn_bwd(const Geo& g, int dt, bool nhwc, const void* q, const void* k,
                            const void* v, const void* o, const void* dout, const float* lse,
                            const float* table, void* dq, void* dk, void* dv, float* dtab, void* ws,
                            hipStream_t st) {
-  if (win_bwd_ok(g, bf16)) {
+  if (win_bwd_ok(g, dt == kBF16)) {
     const int nslice = win_bwd_nslice(g);
     float* partial = reinterpret_cast<float*>(ws);
     hipError_t e = launch_win_bwd(g, nhwc, q, k, v, dout, lse, table, dq, dk, dv, partial, nslice, st);
@@ -684,8 +705,8 @@ hipError_t launch_attn_bwd(const Geo& g, bool bf16, bool nhwc, const void* q, co
                        st, partial, dtab, g, nslice);
     return hipGetLastError();
   }
-  return nhwc ? bwd_generic<true>(g, bf16, q, k, v, o, dout, lse, table, dq, dk, dv, dtab, ws, st)
-              : bwd_generic<false>(g, bf16, q, k, v, o, dout, lse, table, dq, dk, dv, dtab, ws, st);
+  return nhwc ? bwd_dispatch<true>(g, dt, q, k, v, o, dout, lse, table, dq, dk, dv, dtab, ws, st)
+              : bwd_dispatch<false>(g, dt, q, k, v, o, dout, lse, table, dq, dk, dv, dtab, ws, st);
 }
 
 }  // namespace terra

@@ -56,7 +56,7 @@ __device__ inline f32x16 mfma_transpose(const bf16x8& a0, const bf16x8& a1, cons
 
 __device__ inline int win_token_info(const Geo& g, int i, int j, int cols, int t, int n) {
   if (t >= n) return kLabBadW << 24;
-  const int a = t / cols;
+  const int a = fast_div(t, cols, 1.0f / (float)cols);
   const int c = t - a * cols;
   const int lab = row_label(g, i * g.wh + a) | col_label(g, j * g.ww + c);
   return (a * g.bstride + c) | (lab << 24);
@@ -491,6 +491,7 @@ __global__ __launch_bounds__(kPairThreads, 4) void fwd_win_pair_kernel(
 constexpr int kBwdHD = 32;
 constexpr int kBwdKS = kBwdHD + 8;     // LDS row stride (bf16) of K, V, Q, dO rows
 constexpr int kBwdRS = kWinMax + 4;    // LDS row stride (fp32) of the dV, dK sums
+constexpr int kBwdTS = kWinMax + 8;    // LDS row stride (bf16) of K^T
 constexpr int kBwdCPR = kBwdHD / 8;    // 16-byte chunks per token row of one head
 
 // Per-lane 0/1 factors of the bias-gradient fold for the window width cols
@@ -609,8 +610,8 @@ __device__ __forceinline__ void bwd_step(const BwdWave& st, f32x4& dta, f32x4& d
     pb0 = pack_bf16(p, 0); pb1 = pack_bf16(p, 8);
     db0 = pack_bf16(ds, 0); db1 = pack_bf16(ds, 8);
   }
-  mma16(dqacc, lds_perm_op(st.kts + st.col * (kWinMax + 8) + 32 * KB, st.half), db0);
-  mma16(dqacc, lds_perm_op(st.kts + st.col * (kWinMax + 8) + 32 * KB + 16, st.half), db1);
+  mma16(dqacc, lds_perm_op(st.kts + st.col * kBwdTS + 32 * KB, st.half), db0);
+  mma16(dqacc, lds_perm_op(st.kts + st.col * kBwdTS + 32 * KB + 16, st.half), db1);
 #pragma unroll
   for (int which = 0; which < 2; ++which) {
     const bf16x8 ip0 = lds_ident(st.ident, 2), ip1 = lds_ident(st.ident, 3);
@@ -733,7 +734,7 @@ __global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
   bf16* ks = reinterpret_cast<bf16*>(ident + 4 * 64);           // [128][KS] K rows, then dQ
   bf16* vs = ks + kWinMax * KS;                                 // [128][KS] V rows
   bf16* kts = vs + kWinMax * KS;                                // [HD][128+8] K^T
-  float* redv = reinterpret_cast<float*>(kts + HD * (kWinMax + 8));   // [HD][RS] dV sums
+  float* redv = reinterpret_cast<float*>(kts + HD * kBwdTS);    // [HD][RS] dV sums
   float* redk = redv + HD * RS;                                 // [HD][RS] dK sums
   int* kinfo = reinterpret_cast<int*>(redk + HD * RS);          // [128]
   float* tab = reinterpret_cast<float*>(kinfo + kWinMax);       // [nbins+4]
@@ -840,9 +841,9 @@ __global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
                                       lds_ident(ident, 0), lds_ident(ident, 1));
 #pragma unroll
       for (int g4 = 0; g4 < 4; ++g4)
-        store4_bf16(kts + col * (kWinMax + 8) + 32 * qw + 8 * g4 + 4 * half, t, g4, 1.0f);
+        store4_bf16(kts + col * kBwdTS + 32 * qw + 8 * g4 + 4 * half, t, g4, 1.0f);
     }
-    const int qinf = qi < n ? win_token_info(g, wi, wj, cols, qi, n) : 0;
+    const int qinf = qi < n ? kinfo[qi] : 0;
     st.qlab = qinf >> 24;
     st.qrev = g.nbins - 1 - ((qinf & 0xFFFFFF) + (g.wh - 1) * g.bstride + (g.ww - 1));
     st.fold = fold_mask(qi % cols, cols);
@@ -933,7 +934,7 @@ size_t win_fwd_lds(const Geo& g) {
   return one;
 }
 size_t win_bwd_lds(const Geo& g) {
-  return 16 * 4 * 64 + sizeof(bf16) * (2 * kWinMax * kBwdKS + kBwdHD * (kWinMax + 8)) +
+  return 16 * 4 * 64 + sizeof(bf16) * (2 * kWinMax * kBwdKS + kBwdHD * kBwdTS) +
          sizeof(float) * 2 * kBwdHD * kBwdRS + 4 * kWinMax + 4 * (g.nbins + 4) + 4 * 4 * g.nbins;
 }
 

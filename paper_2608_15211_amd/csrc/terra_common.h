@@ -12,6 +12,7 @@
 namespace terra {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -104,10 +105,14 @@ struct WinTokens {
 // ---------------------------------------------------------------------------
 template <typename T> struct Operand;
 template <> struct Operand<__bf16> { typedef bf16x8 type; };
+template <> struct Operand<_Float16> { typedef f16x8 type; };
 template <> struct Operand<float> { typedef f32x8 type; };
 
 __device__ inline void mma16(f32x16& acc, const bf16x8& a, const bf16x8& b) {
   acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc, 0, 0, 0);
+}
+__device__ inline void mma16(f32x16& acc, const f16x8& a, const f16x8& b) {
+  acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, acc, 0, 0, 0);
 }
 // fp32: eight 32x32x2 steps; step i contracts slot i of both lane halves, so
 // the slot numbering matches the bf16 instruction exactly.
@@ -123,10 +128,12 @@ __device__ __host__ constexpr int acc_row(int r, int h) { return 8 * (r / 4) + 4
 template <typename T> __device__ inline T from_float(float x);
 template <> __device__ inline float from_float<float>(float x) { return x; }
 template <> __device__ inline __bf16 from_float<__bf16>(float x) { return (__bf16)x; }
+template <> __device__ inline _Float16 from_float<_Float16>(float x) { return (_Float16)x; }
 
 template <typename T> __device__ inline float to_float(T x);
 template <> __device__ inline float to_float<float>(float x) { return x; }
 template <> __device__ inline float to_float<__bf16>(__bf16 x) { return (float)x; }
+template <> __device__ inline float to_float<_Float16>(_Float16 x) { return (float)x; }
 
 // Pack result registers r0..r0+7 (as float) into an operand.
 template <typename T>

@@ -11,9 +11,9 @@ down-sampling), with Gaussian activations in place of learned ones.
 
 Recipe (all configurations): ``numpy.random.default_rng(seed)`` (PCG64),
 draw order Q, K, V, dOut, each B x H x W x C standard normal in float64,
-cast to float32 and, for bf16 configurations, rounded to bf16 with
-round-to-nearest-even; then the relative-position bias table
-0.02 * N(0, 1) of shape (2wh-1, 2ww-1, heads), float32.
+cast to float32 and, for bf16 (fp16) configurations, rounded to bf16
+(IEEE half) with round-to-nearest-even; then the relative-position bias
+table 0.02 * N(0, 1) of shape (2wh-1, 2ww-1, heads), float32.
 """
 
 from dataclasses import dataclass
@@ -24,7 +24,7 @@ import numpy as np
 @dataclass(frozen=True)
 class Config:
     name: str
-    dtype: str          # "f32" or "bf16"
+    dtype: str          # "f32", "bf16" or "f16"
     B: int
     H: int
     W: int
@@ -63,6 +63,18 @@ CONFIGS = {
 
 ORDER = list(CONFIGS)
 
+# Paper-shaped variants (Table III models; Sec. VII-A: FP16 mixed precision).
+# Every model has head_dim d / N_h = 128; the Transformer-stage grid of the
+# 2041 x 4320 globe at patch 4 and one stride-2 down-sampling is 256 x 540.
+VARIANTS = {
+    # small model (d = 1024, 8 heads, w = 8), fp16
+    "p1_f16_256x540_hd128_w8": Config("p1_f16_256x540_hd128_w8", "f16", 1, 256, 540, 8, 128, 8, 8, 4, 4),
+    # large model (d = 8192, 64 heads, w = 32), fp16: 8 of its heads, one
+    # GPU's share under 8-way head sharding
+    "p2_f16_256x540_hd128_w32": Config("p2_f16_256x540_hd128_w32", "f16", 1, 256, 540, 8, 128, 32, 32, 16, 16),
+}
+ALL = dict(CONFIGS, **VARIANTS)
+
 
 def bf16_round(x):
     """Round float32 values to the nearest bf16 (ties to even).  Returns
@@ -87,8 +99,9 @@ def bf16_from_bits(b):
 
 
 def make_inputs(cfg, seed=0, q_scale=1.0):
-    """Q, K, V, dOut as B x H x W x C float32 arrays (bf16-exact for bf16
-    configurations) and the bias table, drawn in the documented order."""
+    """Q, K, V, dOut as B x H x W x C float32 arrays (exact in the storage
+    type of the configuration) and the bias table, drawn in the documented
+    order."""
     rng = np.random.default_rng(seed)
     shape = (cfg.B, cfg.H, cfg.W, cfg.C)
     out = {}
@@ -98,6 +111,8 @@ def make_inputs(cfg, seed=0, q_scale=1.0):
             x = (x * np.float32(q_scale)).astype(np.float32)
         if cfg.dtype == "bf16":
             x = bf16_round(x)
+        elif cfg.dtype == "f16":
+            x = x.astype(np.float16).astype(np.float32)
         out[name] = x
     tshape = (2 * cfg.wh - 1, 2 * cfg.ww - 1, cfg.heads)
     out["table"] = (0.02 * rng.standard_normal(tshape)).astype(np.float32)

@@ -1,4 +1,4 @@
-"""Write the oracle's bias-table gradient for the two full-size grids.
+"""Write the oracle's bias-table gradient for the full-size grids.
 
 Calls only the oracle (and the seeded input generator): route every input,
 run the fp64 backward over every window, and store dT as float64 .npy files
@@ -21,12 +21,13 @@ sys.path.insert(0, os.path.dirname(os.path.dirname(HERE)))
 import terra_synth as ts  # noqa: E402
 from oracle import Geometry, route, attn_bwd  # noqa: E402
 
-DEFAULT = ["c4_bf16_128x1080_w8x16", "c5_bf16_256x540_w24"]
+DEFAULT = ["c4_bf16_128x1080_w8x16", "c5_bf16_256x540_w24",
+           "p1_f16_256x540_hd128_w8", "p2_f16_256x540_hd128_w32"]
 
 
 def main(names):
     for name in names:
-        cfg = ts.CONFIGS[name]
+        cfg = ts.ALL[name]
         g = Geometry(**cfg.geom_kwargs())
         t0 = time.time()
         inp = ts.make_inputs(cfg)

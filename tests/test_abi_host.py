@@ -64,6 +64,7 @@ BAD = [
     (dict(mask_flags=4), 1),
     (dict(B=0), 1),
     (dict(heads=1, head_dim=64, C=64, wh=16, ww=32), 0),
+    (dict(heads=1, head_dim=128, C=128), 0),   # head_dim 128 (the paper's models)
     (dict(heads=4, head_dim=16, C=64), 2),    # head_dim outside {32, 64}
 ]
 
@@ -89,6 +90,8 @@ def test_device_calls_reject_bad_arguments_before_launch():
     null = ctypes.c_void_p(0)
     s = ctypes.c_void_p(0)
     assert L.terra_window_route(ctypes.byref(g), 7, fake, fake, s) == 1       # bad dtype
+    assert L.terra_winattn_fwd(ctypes.byref(g), 3, *([fake] * 6), s) == 1     # bad dtype
+    assert L.terra_winattn_bwd_workspace_bytes(ctypes.byref(g), 2) > 0       # fp16
     assert L.terra_window_route(ctypes.byref(g), 1, null, fake, s) == 1       # NULL
     assert L.terra_window_route(ctypes.byref(g), 1, fake, fake, s) == 1       # in place
     assert L.terra_winattn_fwd(ctypes.byref(g), 1, fake, fake, null, fake, fake, fake, s) == 1
