@@ -259,15 +259,13 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(
   T* ktt = vr + kTile * (HD + kPad);                  // K^T [HD][kTile+kPad]
   int* kinfo = reinterpret_cast<int*>(ktt + HD * (kTile + kPad));
   float* tab = reinterpret_cast<float*>(kinfo + kTile);
-  float* dtab = tab + g.nbins;
+  float* dtab = tab + g.nbins;                        // [4][nbins], one per wave
 
   const int h = blockIdx.x / nslice;
   const int slice = blockIdx.x - h * nslice;
   const int hoff = h * HD;
-  for (int x = threadIdx.x; x < g.nbins; x += kThreads) {
-    tab[x] = table[x * g.heads + h] * kLog2e;
-    dtab[x] = 0.0f;
-  }
+  for (int x = threadIdx.x; x < g.nbins; x += kThreads) tab[x] = table[x * g.heads + h] * kLog2e;
+  for (int x = threadIdx.x; x < 4 * g.nbins; x += kThreads) dtab[x] = 0.0f;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int half = lane >> 5, col = lane & 31;
   const int nitems = g.B * g.nwin * nqc;
@@ -326,6 +324,15 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(
     if (qvalid && half == 0) D[lidx] = Dq;
 
     // sweep 2: dS, dQ, bias bins
+    const bool fold = (g.ww % 4 == 0) && (g.W % g.ww) % 4 == 0;   // uniform
+    const int cq = qi - fast_div(qi, cols, 1.0f / (float)cols) * cols;
+    // runs: lanes of one 32-lane half holding consecutive queries of one
+    // window row; run = lanes before this one in its run, rest = lanes after
+    const int run = cq < col ? cq : col;
+    const int rest = (cols - 1 - cq) < (31 - col) ? (cols - 1 - cq) : (31 - col);
+    const float fnext = rest > 0 ? 1.0f : 0.0f;          // lane l+1 is in the run
+    const float fsend = fnext;                           // this lane may pass to l+1
+    const float fkeep = run < 3 ? 1.0f : 0.0f;           // one of the run's first three
     f32x16 dqacc[HD / 32];
 #pragma unroll
     for (int eb = 0; eb < HD / 32; ++eb) dqacc[eb] = f32x16{};
@@ -364,27 +371,69 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(
           }
         }
       }
-      // Bias bins in a fixed order: the waves take turns, and the two lane
-      // halves add with separate instructions (within one half, lanes hold
-      // distinct queries of the same key, hence distinct bins).
-#pragma unroll 1
-      for (int turn = 0; turn < kThreads / 64; ++turn) {
-        if (wave == turn) {
-#pragma unroll 1
-          for (int hh = 0; hh < 2; ++hh) {
-            if (half == hh) {
+      // Bias bins: each wave adds into its own copy, and the two lane halves
+      // add with separate instructions (within one half, lanes hold distinct
+      // queries of the same key, hence distinct bins), so every bin receives
+      // its additions in program order.  When every window width is a
+      // multiple of 4, registers 4g..4g+3 hold four consecutive keys k..k+3
+      // of one window row and (q, k+x), (q+1, k+x+1) share a bin.  Within a
+      // run of consecutive lanes holding consecutive queries of one window
+      // row, a DPP chain towards lower lanes folds each group into one value
+      // (bin of (q, k)); the pairs it cannot reach (fewer than x lanes
+      // before q in the run) move towards higher lanes into the run's first
+      // three lanes (bin of (q', k+3)), and the few that would leave a run
+      // shorter than three lanes are added on their own.
+      float* mybins = dtab + wave * g.nbins;
+      if (fold) {
+        float fa[kTile / 32][4], fb[kTile / 32][4];
 #pragma unroll
-              for (int kb = 0; kb < kTile / 32; ++kb)
+        for (int kb = 0; kb < kTile / 32; ++kb)
 #pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                  const int inf = kinfo[kb * 32 + acc_row(r, half)];
-                  if (dsb[kb][r] != 0.0f) atomicAdd(&dtab[qoff - (inf & 0xFFFFFF)], dsb[kb][r]);
-                }
-            }
-            __builtin_amdgcn_wave_barrier();
+          for (int g4 = 0; g4 < 4; ++g4) {
+            const float d0 = dsb[kb][4 * g4], d1 = dsb[kb][4 * g4 + 1];
+            const float d2 = dsb[kb][4 * g4 + 2], d3 = dsb[kb][4 * g4 + 3];
+            float f = d3;
+            f = d2 + fnext * dpp_lane<kDppNext>(f);
+            f = d1 + fnext * dpp_lane<kDppNext>(f);
+            fa[kb][g4] = d0 + fnext * dpp_lane<kDppNext>(f);
+            const float p1 = dpp_lane<kDppWavePrev>(d2 * fsend);
+            const float p2 = dpp_lane<kDppWavePrev>(dpp_lane<kDppWavePrev>(d1 * fsend) * fsend);
+            fb[kb][g4] = fkeep * (d3 + p1 + p2);
           }
+#pragma unroll 1
+        for (int hh = 0; hh < 2; ++hh) {
+          if (half == hh) {
+#pragma unroll
+            for (int kb = 0; kb < kTile / 32; ++kb)
+#pragma unroll
+              for (int g4 = 0; g4 < 4; ++g4) {
+                const int kk = kb * 32 + 8 * g4 + 4 * half;
+                if (fa[kb][g4] != 0.0f)
+                  atomicAdd(&mybins[qoff - (kinfo[kk] & 0xFFFFFF)], fa[kb][g4]);
+                if (fb[kb][g4] != 0.0f)
+                  atomicAdd(&mybins[qoff - (kinfo[kk + 3] & 0xFFFFFF)], fb[kb][g4]);
+#pragma unroll
+                for (int x = 1; x < 3; ++x)
+                  if (run < x && rest < 3 - x && dsb[kb][4 * g4 + x] != 0.0f)
+                    atomicAdd(&mybins[qoff - (kinfo[kk + x] & 0xFFFFFF)], dsb[kb][4 * g4 + x]);
+              }
+          }
+          __builtin_amdgcn_wave_barrier();
         }
-        __syncthreads();
+      } else {
+#pragma unroll 1
+        for (int hh = 0; hh < 2; ++hh) {
+          if (half == hh) {
+#pragma unroll
+            for (int kb = 0; kb < kTile / 32; ++kb)
+#pragma unroll
+              for (int r = 0; r < 16; ++r) {
+                const int inf = kinfo[kb * 32 + acc_row(r, half)];
+                if (dsb[kb][r] != 0.0f) atomicAdd(&mybins[qoff - (inf & 0xFFFFFF)], dsb[kb][r]);
+              }
+          }
+          __builtin_amdgcn_wave_barrier();
+        }
       }
     }
     if (qvalid) {
@@ -401,7 +450,8 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(
   }
   __syncthreads();
   float* out = partial + ((int64_t)h * nslice + slice) * g.nbins;
-  for (int x = threadIdx.x; x < g.nbins; x += kThreads) out[x] = dtab[x];
+  for (int x = threadIdx.x; x < g.nbins; x += kThreads)
+    out[x] = ((dtab[x] + dtab[g.nbins + x]) + dtab[2 * g.nbins + x]) + dtab[3 * g.nbins + x];
 }
 
 // ---------------------------------------------------------------------------
@@ -561,7 +611,7 @@ static size_t fwd_lds(const Geo& g) {
 template <typename T, int HD>
 static size_t dq_lds(const Geo& g) {
   constexpr int kTile = tile_of<T, HD>();
-  return sizeof(T) * (2 * kTile * (HD + kPad) + HD * (kTile + kPad)) + 4 * kTile + 8 * g.nbins;
+  return sizeof(T) * (2 * kTile * (HD + kPad) + HD * (kTile + kPad)) + 4 * kTile + 20 * g.nbins;
 }
 template <typename T, int HD>
 static size_t dkdv_lds(const Geo& g) {

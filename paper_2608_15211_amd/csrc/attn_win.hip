@@ -516,7 +516,6 @@ struct BwdWave {
   const bf16* ks;       // K rows in LDS [128][KS]
   const bf16* vs;       // V rows [128][KS]
   const bf16* kts;      // K^T [HD][128+8]
-  const bf16x8* ident;  // 0/1 transpose operands [4][64]: (PERM, chunk)
   const int* kinfo;     // key words of the window
   const float* tab;     // bias table times sqrt(hd), reversed, then -inf
   float* redv;          // dV partial sums [HD][RS]
@@ -528,20 +527,11 @@ struct BwdWave {
   int qrev, qlab, nbins, col, half;
 };
 
-// Transpose operand `which` = 2*PERM + chunk, read from LDS so that the
-// compiler does not keep all four resident in registers.
-__device__ inline bf16x8 lds_ident(const bf16x8* ident, int which) {
-  return ident[which * 64 + (threadIdx.x & 63)];
+// Row-to-column transpose operand of chunk c (ident_op<false>), read from
+// LDS: it is needed once per window, so it does not hold registers.
+__device__ inline bf16x8 lds_ident(const bf16x8* ident, int c) {
+  return ident[c * 64 + (threadIdx.x & 63)];
 }
-
-// Value of another lane by a DPP move (0 where the source lane is absent).
-template <int CTRL>
-__device__ __forceinline__ float dpp_lane(float x) {
-  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xF, 0xF, true));
-}
-constexpr int kDppNext = 0x130;    // wave_shl:1 - lane l reads lane l+1
-constexpr int kDppPrev1 = 0x111;   // row_shr:1  - lane l reads lane l-1 (same 16-lane row)
-constexpr int kDppPrev2 = 0x112;   // row_shr:2  - lane l reads lane l-2
 
 // dS summed along the bias diagonals of one register group: registers
 // 4g..4g+3 hold four consecutive keys k..k+3 of one window row, so (query q,
@@ -614,7 +604,7 @@ __device__ __forceinline__ void bwd_step(const BwdWave& st, f32x4& dta, f32x4& d
   mma16(dqacc, lds_perm_op(st.kts + st.col * kBwdTS + 32 * KB + 16, st.half), db1);
 #pragma unroll
   for (int which = 0; which < 2; ++which) {
-    const bf16x8 ip0 = lds_ident(st.ident, 2), ip1 = lds_ident(st.ident, 3);
+    const bf16x8 ip0 = ident_op<true>(0), ip1 = ident_op<true>(1);
     const f32x16 tr = which == 0 ? mfma_transpose(pb0, pb1, ip0, ip1) : mfma_transpose(db0, db1, ip0, ip1);
     float* red = which == 0 ? st.redv : st.redk;
     f32x16 part;
@@ -730,8 +720,8 @@ __global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
   constexpr int KS = kBwdKS;
   constexpr int RS = kBwdRS;
   extern __shared__ __align__(16) char smem[];
-  bf16x8* ident = reinterpret_cast<bf16x8*>(smem);              // [4][64]
-  bf16* ks = reinterpret_cast<bf16*>(ident + 4 * 64);           // [128][KS] K rows, then dQ
+  bf16x8* ident = reinterpret_cast<bf16x8*>(smem);              // [2][64]
+  bf16* ks = reinterpret_cast<bf16*>(ident + 2 * 64);           // [128][KS] K rows, then dQ
   bf16* vs = ks + kWinMax * KS;                                 // [128][KS] V rows
   bf16* kts = vs + kWinMax * KS;                                // [HD][128+8] K^T
   float* redv = reinterpret_cast<float*>(kts + HD * kBwdTS);    // [HD][RS] dV sums
@@ -752,7 +742,7 @@ __global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
   float* mybins = bins + qw * g.nbins;
 
   for (int x = threadIdx.x; x < 4 * g.nbins; x += kWinThreads) bins[x] = 0.0f;
-  ident[threadIdx.x] = (qw >> 1) ? ident_op<true>(qw & 1) : ident_op<false>(qw & 1);
+  if (qw < 2) ident[threadIdx.x] = ident_op<false>(qw);
   for (int x = threadIdx.x; x < g.nbins + 4; x += kWinThreads)
     tab[x] = x < g.nbins ? table[(g.nbins - 1 - x) * g.heads + h] * sqrtf((float)HD) : -INFINITY;
 
@@ -819,7 +809,6 @@ __global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
     st.ks = ks;
     st.vs = vs;
     st.kts = kts;
-    st.ident = ident;
     st.kinfo = kinfo;
     st.tab = tab;
     st.redv = redv;
@@ -934,7 +923,7 @@ size_t win_fwd_lds(const Geo& g) {
   return one;
 }
 size_t win_bwd_lds(const Geo& g) {
-  return 16 * 4 * 64 + sizeof(bf16) * (2 * kWinMax * kBwdKS + kBwdHD * kBwdTS) +
+  return 16 * 2 * 64 + sizeof(bf16) * (2 * kWinMax * kBwdKS + kBwdHD * kBwdTS) +
          sizeof(float) * 2 * kBwdHD * kBwdRS + 4 * kWinMax + 4 * (g.nbins + 4) + 4 * 4 * g.nbins;
 }
 

@@ -97,6 +97,16 @@ struct WinTokens {
   }
 };
 
+// Value of another lane by a DPP move (0 where the source lane is absent).
+template <int CTRL>
+__device__ __forceinline__ float dpp_lane(float x) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xF, 0xF, true));
+}
+constexpr int kDppNext = 0x130;    // wave_shl:1 - lane l reads lane l+1
+constexpr int kDppPrev1 = 0x111;   // row_shr:1  - lane l reads lane l-1 (same 16-lane row)
+constexpr int kDppPrev2 = 0x112;   // row_shr:2  - lane l reads lane l-2
+constexpr int kDppWavePrev = 0x138;  // wave_shr:1 - lane l reads lane l-1
+
 // ---------------------------------------------------------------------------
 // Matrix-core tiles.  One MFMA "operand" is 8 consecutive contraction-dim
 // elements per lane: lane l supplies row/column (l % 32) and contraction
