@@ -120,9 +120,12 @@ __device__ inline int token_info(const Geo& g, int i, int j, int cols, int t, in
 
 // ---------------------------------------------------------------------------
 // Forward.  Grid: B * nwin * heads * nqc workgroups (nqc query chunks of 128
-// per window, empty chunks of small windows exit at once).
+// per window, empty chunks of small windows exit at once).  The bias enters
+// the score accumulator before the QK^T product (table times sqrt(hd) in
+// reversed bin order, -inf entries for excluded pairs), so each score costs
+// one multiply-add and one exp2 outside the matrix cores.
 // ---------------------------------------------------------------------------
-template <typename T, int HD, bool NHWC>
+template <typename T, int HD, bool NHWC, bool QUAD>
 __global__ __launch_bounds__(kThreads) void fwd_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const float* __restrict__ table, T* __restrict__ o, float* __restrict__ lse,
@@ -132,7 +135,7 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(
   T* kt = reinterpret_cast<T*>(smem);                          // [kTile][HD+kPad]
   T* vt = kt + kTile * (HD + kPad);                            // [HD][kTile+kPad]
   int* kinfo = reinterpret_cast<int*>(vt + HD * (kTile + kPad));
-  float* tab = reinterpret_cast<float*>(kinfo + kTile);        // [nbins]
+  float* tab = reinterpret_cast<float*>(kinfo + kTile);        // [nbins+4], reversed
 
   int bid = blockIdx.x;
   const int qc = bid % nqc; bid /= nqc;
@@ -147,7 +150,9 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(
   const WinTokens<NHWC> wt(g, b, i, j);
   const int hoff = h * HD;
 
-  for (int x = threadIdx.x; x < g.nbins; x += kThreads) tab[x] = table[x * g.heads + h] * kLog2e;
+  const float bscale = sqrtf((float)HD);
+  for (int x = threadIdx.x; x < g.nbins + 4; x += kThreads)
+    tab[x] = x < g.nbins ? table[(g.nbins - 1 - x) * g.heads + h] * bscale : -INFINITY;
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int half = lane >> 5, col = lane & 31;
@@ -155,7 +160,8 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(
   const bool qvalid = qi < n;
   const int qinf = token_info(g, i, j, cols, qvalid ? qi : 0, n);
   const int qlab = qinf >> 24;
-  const int qoff = (qinf & 0xFFFFFF) + (g.wh - 1) * g.bstride + (g.ww - 1);
+  const int qrev = g.nbins - 1 - ((qinf & 0xFFFFFF) + (g.wh - 1) * g.bstride + (g.ww - 1));
+  const bool mask = window_has_labels(g, i, j) || (n % kTile) != 0;
 
   typename Operand<T>::type qop[HD / 16];
 #pragma unroll
@@ -166,7 +172,7 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(
   f32x16 oacc[HD / 32];
 #pragma unroll
   for (int eb = 0; eb < HD / 32; ++eb) oacc[eb] = f32x16{};
-  float m_run = -1e30f, l_run = 0.0f;
+  float m_run = -1e30f, l_run = 0.0f;     // running max (log2 units) and sum
 
   for (int k0 = 0; k0 < n; k0 += kTile) {
     __syncthreads();
@@ -176,28 +182,21 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(
     __syncthreads();
 
     f32x16 s[kTile / 32];
+    float mloc = -INFINITY;
 #pragma unroll
     for (int kb = 0; kb < kTile / 32; ++kb) {
-      s[kb] = f32x16{};
+      s[kb] = mask ? bias_init<QUAD, true>(kinfo, tab, kb, half, qrev, qlab, g.nbins)
+                   : bias_init<QUAD, false>(kinfo, tab, kb, half, qrev, qlab, g.nbins);
 #pragma unroll
       for (int c = 0; c < HD / 16; ++c)
         mma16(s[kb], load_op_lds<T>(kt + (kb * 32 + col) * (HD + kPad) + 16 * c + 8 * half), qop[c]);
-    }
-    float mloc = m_run;
 #pragma unroll
-    for (int kb = 0; kb < kTile / 32; ++kb) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int inf = kinfo[kb * 32 + acc_row(r, half)];
-        const float bias = tab[qoff - (inf & 0xFFFFFF)];
-        const float val = ((inf >> 24) == qlab) ? s[kb][r] * scale_log2 + bias : -INFINITY;
-        s[kb][r] = val;
-        mloc = fmaxf(mloc, val);
-      }
+      for (int r = 0; r < 16; ++r) mloc = fmaxf(mloc, s[kb][r]);
     }
     mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
-    const float alpha = exp2f(m_run - mloc);
-    m_run = mloc;
+    const float mnew = fmaxf(m_run, mloc * scale_log2);
+    const float alpha = exp2f(m_run - mnew);
+    m_run = mnew;
     l_run *= alpha;
 #pragma unroll
     for (int eb = 0; eb < HD / 32; ++eb) oacc[eb] *= alpha;
@@ -205,7 +204,7 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(
     for (int kb = 0; kb < kTile / 32; ++kb) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float p = exp2f(s[kb][r] - m_run);
+        const float p = __builtin_amdgcn_exp2f(s[kb][r] * scale_log2 - m_run);
         s[kb][r] = p;
         l_run += p;
       }
@@ -246,7 +245,7 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(
 // fp32 (equal to <dO_q, O_q> for the unrounded O) and stores it for the
 // dK/dV kernel; the second sweep forms dS, dQ and the bias bins.
 // ---------------------------------------------------------------------------
-template <typename T, int HD, bool NHWC>
+template <typename T, int HD, bool NHWC, bool QUAD>
 __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const T* __restrict__ dout, const float* __restrict__ lse, float* __restrict__ D,
@@ -258,13 +257,15 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(
   T* vr = kt + kTile * (HD + kPad);                   // V  [kTile][HD+kPad]
   T* ktt = vr + kTile * (HD + kPad);                  // K^T [HD][kTile+kPad]
   int* kinfo = reinterpret_cast<int*>(ktt + HD * (kTile + kPad));
-  float* tab = reinterpret_cast<float*>(kinfo + kTile);
-  float* dtab = tab + g.nbins;                        // [4][nbins], one per wave
+  float* tab = reinterpret_cast<float*>(kinfo + kTile);   // [nbins+4], reversed
+  float* dtab = tab + g.nbins + 4;                    // [4][nbins], one per wave
 
   const int h = blockIdx.x / nslice;
   const int slice = blockIdx.x - h * nslice;
   const int hoff = h * HD;
-  for (int x = threadIdx.x; x < g.nbins; x += kThreads) tab[x] = table[x * g.heads + h] * kLog2e;
+  const float bscale = sqrtf((float)HD);
+  for (int x = threadIdx.x; x < g.nbins + 4; x += kThreads)
+    tab[x] = x < g.nbins ? table[(g.nbins - 1 - x) * g.heads + h] * bscale : -INFINITY;
   for (int x = threadIdx.x; x < 4 * g.nbins; x += kThreads) dtab[x] = 0.0f;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int half = lane >> 5, col = lane & 31;
@@ -285,8 +286,11 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(
     const int qinf = token_info(g, i, j, cols, qvalid ? qi : 0, n);
     const int qlab = qinf >> 24;
     const int qoff = (qinf & 0xFFFFFF) + (g.wh - 1) * g.bstride + (g.ww - 1);
+    const int qrev = g.nbins - 1 - qoff;
     const int64_t lidx = wt.lse_at(g, h, qvalid ? qi : 0);
-    const float lse2 = lse[lidx] * kLog2e;
+    // +inf for padding queries: their P is exactly 0
+    const float lse2 = qvalid ? lse[lidx] * kLog2e : INFINITY;
+    const bool mask = window_has_labels(g, i, j) || (n % kTile) != 0;
 
     typename Operand<T>::type qop[HD / 16], dop[HD / 16];
 #pragma unroll
@@ -306,18 +310,17 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(
       __syncthreads();
 #pragma unroll
       for (int kb = 0; kb < kTile / 32; ++kb) {
-        f32x16 s = f32x16{}, dp = f32x16{};
+        f32x16 s = mask ? bias_init<QUAD, true>(kinfo, tab, kb, half, qrev, qlab, g.nbins)
+                        : bias_init<QUAD, false>(kinfo, tab, kb, half, qrev, qlab, g.nbins);
+        f32x16 dp = f32x16{};
 #pragma unroll
         for (int c = 0; c < HD / 16; ++c) {
           mma16(s, load_op_lds<T>(kt + (kb * 32 + col) * (HD + kPad) + 16 * c + 8 * half), qop[c]);
           mma16(dp, load_op_lds<T>(vr + (kb * 32 + col) * (HD + kPad) + 16 * c + 8 * half), dop[c]);
         }
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int inf = kinfo[kb * 32 + acc_row(r, half)];
-          if ((inf >> 24) == qlab)
-            dsum += exp2f(s[r] * scale_log2 + tab[qoff - (inf & 0xFFFFFF)] - lse2) * dp[r];
-        }
+        for (int r = 0; r < 16; ++r)
+          dsum += __builtin_amdgcn_exp2f(s[r] * scale_log2 - lse2) * dp[r];
       }
     }
     const float Dq = dsum + __shfl_xor(dsum, 32);
@@ -346,22 +349,18 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(
       f32x16 dsb[kTile / 32];
 #pragma unroll
       for (int kb = 0; kb < kTile / 32; ++kb) {
-        f32x16 s = f32x16{}, dp = f32x16{};
+        f32x16 s = mask ? bias_init<QUAD, true>(kinfo, tab, kb, half, qrev, qlab, g.nbins)
+                        : bias_init<QUAD, false>(kinfo, tab, kb, half, qrev, qlab, g.nbins);
+        f32x16 dp;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) dp[r] = -Dq;      // dP - D straight from the product
 #pragma unroll
         for (int c = 0; c < HD / 16; ++c) {
           mma16(s, load_op_lds<T>(kt + (kb * 32 + col) * (HD + kPad) + 16 * c + 8 * half), qop[c]);
           mma16(dp, load_op_lds<T>(vr + (kb * 32 + col) * (HD + kPad) + 16 * c + 8 * half), dop[c]);
         }
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int inf = kinfo[kb * 32 + acc_row(r, half)];
-          float ds = 0.0f;
-          if (((inf >> 24) == qlab) && qvalid) {
-            const float p = exp2f(s[r] * scale_log2 + tab[qoff - (inf & 0xFFFFFF)] - lse2);
-            ds = p * (dp[r] - Dq);
-          }
-          dsb[kb][r] = ds;
-        }
+        for (int r = 0; r < 16; ++r) dsb[kb][r] = __builtin_amdgcn_exp2f(s[r] * scale_log2 - lse2) * dp[r];
 #pragma unroll
         for (int eb = 0; eb < HD / 32; ++eb) {
 #pragma unroll
@@ -458,7 +457,7 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(
 // Backward, step 2: dK and dV.  Grid: B * nwin * heads * nkc (key chunks of
 // 128; a wave owns 32 keys and walks the window's queries in LDS tiles).
 // ---------------------------------------------------------------------------
-template <typename T, int HD, bool NHWC>
+template <typename T, int HD, bool NHWC, bool QUAD>
 __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const T* __restrict__ dout, const float* __restrict__ lse, const float* __restrict__ D,
@@ -473,7 +472,7 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(
   int* qinfo = reinterpret_cast<int*>(dtt + HD * (kTile + kPad));
   float* ql = reinterpret_cast<float*>(qinfo + kTile);   // lse2 per query
   float* qd = ql + kTile;                                 // D per query
-  float* tab = qd + kTile;
+  float* tab = qd + kTile;                                // [nbins+4], forward order
 
   int bid = blockIdx.x;
   const int kc = bid % nkc; bid /= nkc;
@@ -487,7 +486,10 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(
   if (kbase >= n) return;
   const WinTokens<NHWC> wt(g, b, i, j);
   const int hoff = h * HD;
-  for (int x = threadIdx.x; x < g.nbins; x += kThreads) tab[x] = table[x * g.heads + h] * kLog2e;
+  const float bscale = sqrtf((float)HD);
+  for (int x = threadIdx.x; x < g.nbins + 4; x += kThreads)
+    tab[x] = x < g.nbins ? table[x * g.heads + h] * bscale : -INFINITY;
+  const bool mask = window_has_labels(g, i, j) || (n % kTile) != 0;
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int half = lane >> 5, col = lane & 31;
@@ -495,7 +497,7 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(
   const bool kvalid = ki < n;
   const int kinf = token_info(g, i, j, cols, kvalid ? ki : 0, n);
   const int klab = kvalid ? (kinf >> 24) : 0xFE;
-  const int koff = kinf & 0xFFFFFF;
+  const int kfwd = (g.wh - 1) * g.bstride + (g.ww - 1) - (kinf & 0xFFFFFF);
 
   typename Operand<T>::type kop[HD / 16], vop[HD / 16];
 #pragma unroll
@@ -516,16 +518,29 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(
     if (threadIdx.x < kTile) {
       const int t = t0 + threadIdx.x;
       const int inf = token_info(g, i, j, cols, t, n);
-      qinfo[threadIdx.x] = (inf & 0xFFFFFF) + (g.wh - 1) * g.bstride + (g.ww - 1) +
-                           (t < n ? (inf & 0xFF000000) : (kLabBad << 24));
+      qinfo[threadIdx.x] = inf;
       const int64_t li = t < n ? wt.lse_at(g, h, t) : 0;
-      ql[threadIdx.x] = t < n ? lse[li] * kLog2e : 0.0f;
+      ql[threadIdx.x] = t < n ? lse[li] * kLog2e : INFINITY;   // padding queries: P = 0
       qd[threadIdx.x] = t < n ? D[li] : 0.0f;
     }
     __syncthreads();
 #pragma unroll
     for (int qb = 0; qb < kTile / 32; ++qb) {
-      f32x16 s = f32x16{}, dp = f32x16{};
+      // registers 4g..4g+3 hold queries 32qb + 8g + 4*half + 0..3: their
+      // log-sum-exp and D are four consecutive LDS words
+      f32x16 s = mask ? bias_init_t<QUAD, true>(qinfo, tab, qb, half, kfwd, klab, g.nbins)
+                      : bias_init_t<QUAD, false>(qinfo, tab, qb, half, kfwd, klab, g.nbins);
+      f32x16 dp, lq;
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        const f32x4 d4 = *reinterpret_cast<const f32x4*>(qd + qb * 32 + 8 * g4 + 4 * half);
+        const f32x4 l4 = *reinterpret_cast<const f32x4*>(ql + qb * 32 + 8 * g4 + 4 * half);
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+          dp[4 * g4 + x] = -d4[x];     // dP - D straight from the product
+          lq[4 * g4 + x] = l4[x];
+        }
+      }
 #pragma unroll
       for (int c = 0; c < HD / 16; ++c) {
         mma16(s, load_op_lds<T>(qr + (qb * 32 + col) * (HD + kPad) + 16 * c + 8 * half), kop[c]);
@@ -534,14 +549,8 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(
       f32x16 ds;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int t = qb * 32 + acc_row(r, half);
-        const int inf = qinfo[t];
-        float p = 0.0f;
-        if (((inf >> 24) & 0xFF) == klab) {
-          const float bias = tab[(inf & 0xFFFFFF) - koff];
-          p = exp2f(s[r] * scale_log2 + bias - ql[t]);
-        }
-        ds[r] = p * (dp[r] - qd[t]);
+        const float p = __builtin_amdgcn_exp2f(s[r] * scale_log2 - lq[r]);
+        ds[r] = p * dp[r];
         s[r] = p;
       }
 #pragma unroll
@@ -606,17 +615,18 @@ int bwd_nslice(const Geo& g) {
 template <typename T, int HD>
 static size_t fwd_lds(const Geo& g) {
   constexpr int kTile = tile_of<T, HD>();
-  return sizeof(T) * (kTile * (HD + kPad) + HD * (kTile + kPad)) + 4 * kTile + 4 * g.nbins;
+  return sizeof(T) * (kTile * (HD + kPad) + HD * (kTile + kPad)) + 4 * kTile + 4 * (g.nbins + 4);
 }
 template <typename T, int HD>
 static size_t dq_lds(const Geo& g) {
   constexpr int kTile = tile_of<T, HD>();
-  return sizeof(T) * (2 * kTile * (HD + kPad) + HD * (kTile + kPad)) + 4 * kTile + 20 * g.nbins;
+  return sizeof(T) * (2 * kTile * (HD + kPad) + HD * (kTile + kPad)) + 4 * kTile + 4 * (g.nbins + 4) +
+         16 * g.nbins;
 }
 template <typename T, int HD>
 static size_t dkdv_lds(const Geo& g) {
   constexpr int kTile = tile_of<T, HD>();
-  return sizeof(T) * (2 * kTile * (HD + kPad) + 2 * HD * (kTile + kPad)) + 12 * kTile + 4 * g.nbins;
+  return sizeof(T) * (2 * kTile * (HD + kPad) + 2 * HD * (kTile + kPad)) + 12 * kTile + 4 * (g.nbins + 4);
 }
 
 template <typename T, int HD, bool NHWC>
@@ -626,8 +636,12 @@ static hipError_t fwd_impl(const Geo& g, const void* q, const void* k, const voi
   const int grid = g.B * g.nwin * g.heads * nqc;
   const float sl2 = kLog2e / sqrtf((float)HD);
   const size_t lds = fwd_lds<T, HD>(g);
-  hipLaunchKernelGGL((fwd_kernel<T, HD, NHWC>), dim3(grid), dim3(kThreads), lds, st,
-                     (const T*)q, (const T*)k, (const T*)v, table, (T*)o, lse, g, nqc, sl2);
+  if (quad_layout(g))
+    hipLaunchKernelGGL((fwd_kernel<T, HD, NHWC, true>), dim3(grid), dim3(kThreads), lds, st,
+                       (const T*)q, (const T*)k, (const T*)v, table, (T*)o, lse, g, nqc, sl2);
+  else
+    hipLaunchKernelGGL((fwd_kernel<T, HD, NHWC, false>), dim3(grid), dim3(kThreads), lds, st,
+                       (const T*)q, (const T*)k, (const T*)v, table, (T*)o, lse, g, nqc, sl2);
   return hipGetLastError();
 }
 
@@ -653,16 +667,27 @@ static hipError_t bwd_impl(const Geo& g, const void* q, const void* k, const voi
   const float sl2 = kLog2e / sqrtf((float)HD);
   const float scale = 1.0f / sqrtf((float)HD);
   const size_t lds_dq = dq_lds<T, HD>(g);
-  hipLaunchKernelGGL((bwd_dq_kernel<T, HD, NHWC>), dim3(g.heads * nslice), dim3(kThreads),
-                     lds_dq, st, (const T*)q, (const T*)k, (const T*)v,
-                     (const T*)dout, lse, D, table, (T*)dq, partial, g, nqc, nslice, sl2, scale);
+  const bool quad = quad_layout(g);
+  if (quad)
+    hipLaunchKernelGGL((bwd_dq_kernel<T, HD, NHWC, true>), dim3(g.heads * nslice), dim3(kThreads),
+                       lds_dq, st, (const T*)q, (const T*)k, (const T*)v,
+                       (const T*)dout, lse, D, table, (T*)dq, partial, g, nqc, nslice, sl2, scale);
+  else
+    hipLaunchKernelGGL((bwd_dq_kernel<T, HD, NHWC, false>), dim3(g.heads * nslice), dim3(kThreads),
+                       lds_dq, st, (const T*)q, (const T*)k, (const T*)v,
+                       (const T*)dout, lse, D, table, (T*)dq, partial, g, nqc, nslice, sl2, scale);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int grid = g.B * g.nwin * g.heads * nqc;
   const size_t lds_kv = dkdv_lds<T, HD>(g);
-  hipLaunchKernelGGL((bwd_dkdv_kernel<T, HD, NHWC>), dim3(grid), dim3(kThreads), lds_kv, st,
-                     (const T*)q, (const T*)k, (const T*)v, (const T*)dout, lse, D, table,
-                     (T*)dk, (T*)dv, g, nqc, sl2, scale);
+  if (quad)
+    hipLaunchKernelGGL((bwd_dkdv_kernel<T, HD, NHWC, true>), dim3(grid), dim3(kThreads), lds_kv, st,
+                       (const T*)q, (const T*)k, (const T*)v, (const T*)dout, lse, D, table,
+                       (T*)dk, (T*)dv, g, nqc, sl2, scale);
+  else
+    hipLaunchKernelGGL((bwd_dkdv_kernel<T, HD, NHWC, false>), dim3(grid), dim3(kThreads), lds_kv, st,
+                       (const T*)q, (const T*)k, (const T*)v, (const T*)dout, lse, D, table,
+                       (T*)dk, (T*)dv, g, nqc, sl2, scale);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int nred = g.nbins * g.heads;

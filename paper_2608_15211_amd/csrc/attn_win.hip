@@ -133,32 +133,7 @@ __device__ inline bf16x8 pack_bf16(const f32x16& acc, int r0) {
 // True when some pair of the window must be excluded: a wrap label inside
 // the window or padding slots in its last 32-token block.
 __device__ inline bool window_needs_mask(const Geo& g, int wi, int wj, int n) {
-  const bool lat = (g.flags & 1) && g.sh > 0 && (wi * g.wh + win_rows(g, wi)) > g.H - g.sh;
-  const bool lon = (g.flags & 2) && g.sw > 0 && (wj * g.ww + win_cols(g, wj)) > g.W - g.sw;
-  return lat || lon || (n & 31) != 0;
-}
-
-// Accumulator initialiser of key block KB: the bias of each (query, key)
-// pair, pre-multiplied by sqrt(hd) so that one multiply by log2(e)/sqrt(hd)
-// after the QK^T product yields the log2-domain score; -inf for excluded
-// pairs (tab[nbins .. nbins+3] holds -inf).  qrev is the lane's reversed
-// bin offset, qlab its label.
-template <bool QUAD, bool MASK>
-__device__ inline f32x16 bias_init(const int* kinfo, const float* tab, int kb, int half, int qrev,
-                                   int qlab, int nbins) {
-  f32x16 c;
-#pragma unroll
-  for (int g4 = 0; g4 < 4; ++g4) {
-    int inf = kinfo[32 * kb + 8 * g4 + 4 * half];
-#pragma unroll
-    for (int x = 0; x < 4; ++x) {
-      if (!QUAD && x > 0) inf = kinfo[32 * kb + 8 * g4 + 4 * half + x];
-      int rb = qrev + (inf & 0xFFFFFF);
-      if (MASK && (inf >> 24) != qlab) rb = nbins - (QUAD ? x : 0);
-      c[4 * g4 + x] = tab[rb + (QUAD ? x : 0)];
-    }
-  }
-  return c;
+  return window_has_labels(g, wi, wj) || (n & 31) != 0;
 }
 
 // Map a linear block index to a work index so that consecutive work items
@@ -927,12 +902,6 @@ size_t win_bwd_lds(const Geo& g) {
          sizeof(float) * 2 * kBwdHD * kBwdRS + 4 * kWinMax + 4 * (g.nbins + 4) + 4 * 4 * g.nbins;
 }
 
-// Four consecutive result registers are four consecutive keys of one window
-// row, with one label, when every window width is a multiple of 4 and the
-// longitude wrap is not masked.
-static bool quad_layout(const Geo& g) {
-  return g.ww % 4 == 0 && (g.W % g.ww) % 4 == 0 && (g.flags & 2) == 0;
-}
 
 template <int HD, bool QUAD, bool NHWC>
 static void fwd_win_go(const Geo& g, const void* q, const void* k, const void* v,

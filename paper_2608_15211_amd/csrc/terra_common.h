@@ -97,6 +97,66 @@ struct WinTokens {
   }
 };
 
+// True when window (wi, wj) holds tokens of more than one wrap label (the
+// latitude rows or longitude columns that the shift moved across the edge).
+__device__ inline bool window_has_labels(const Geo& g, int wi, int wj) {
+  const bool lat = (g.flags & 1) && g.sh > 0 && (wi * g.wh + win_rows(g, wi)) > g.H - g.sh;
+  const bool lon = (g.flags & 2) && g.sw > 0 && (wj * g.ww + win_cols(g, wj)) > g.W - g.sw;
+  return lat || lon;
+}
+
+// Accumulator initialiser of key block KB: the bias of each (query, key)
+// pair, pre-multiplied by sqrt(hd) so that one multiply by log2(e)/sqrt(hd)
+// after the QK^T product yields the log2-domain score; -inf for excluded
+// pairs (tab[nbins .. nbins+3] holds -inf).  qrev is the lane's reversed
+// bin offset, qlab its label.
+template <bool QUAD, bool MASK>
+__device__ inline f32x16 bias_init(const int* kinfo, const float* tab, int kb, int half, int qrev,
+                                   int qlab, int nbins) {
+  f32x16 c;
+#pragma unroll
+  for (int g4 = 0; g4 < 4; ++g4) {
+    int inf = kinfo[32 * kb + 8 * g4 + 4 * half];
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+      if (!QUAD && x > 0) inf = kinfo[32 * kb + 8 * g4 + 4 * half + x];
+      int rb = qrev + (inf & 0xFFFFFF);
+      if (MASK && (inf >> 24) != qlab) rb = nbins - (QUAD ? x : 0);
+      c[4 * g4 + x] = tab[rb + (QUAD ? x : 0)];
+    }
+  }
+  return c;
+}
+
+// The same in the key-major form (lane = key, registers = queries of query
+// block QB): the table is in forward bin order, times sqrt(hd), with four
+// -inf entries after it; kfwd is the lane's key term of the bin index,
+// (wh-1)(2ww-1) + ww-1 - (a_k (2ww-1) + c_k), and klab its label.
+template <bool QUAD, bool MASK>
+__device__ inline f32x16 bias_init_t(const int* qinfo, const float* tabf, int qb, int half, int kfwd,
+                                     int klab, int nbins) {
+  f32x16 c;
+#pragma unroll
+  for (int g4 = 0; g4 < 4; ++g4) {
+    int inf = qinfo[32 * qb + 8 * g4 + 4 * half];
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+      if (!QUAD && x > 0) inf = qinfo[32 * qb + 8 * g4 + 4 * half + x];
+      int rb = kfwd + (inf & 0xFFFFFF);
+      if (MASK && (inf >> 24) != klab) rb = nbins - (QUAD ? x : 0);
+      c[4 * g4 + x] = tabf[rb + (QUAD ? x : 0)];
+    }
+  }
+  return c;
+}
+
+// Four consecutive result registers are four consecutive keys (queries) of
+// one window row, with one label, when every window width is a multiple of
+// 4 and the longitude wrap is not masked.
+__host__ inline bool quad_layout(const Geo& g) {
+  return g.ww % 4 == 0 && (g.W % g.ww) % 4 == 0 && (g.flags & 2) == 0;
+}
+
 // Value of another lane by a DPP move (0 where the source lane is absent).
 template <int CTRL>
 __device__ __forceinline__ float dpp_lane(float x) {
