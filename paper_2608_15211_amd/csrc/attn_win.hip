@@ -314,12 +314,14 @@ __global__ __launch_bounds__(kPairThreads, 4) void fwd_win_pair_kernel(
     const float* __restrict__ table, bf16* __restrict__ o, float* __restrict__ lse, Geo g,
     int per_slice, float scale_log2) {
   constexpr int HD = 32;
-  constexpr int KS = HD + 8, VS = kWinMax + 8;
+  // V^T rows of 132 elements, the second head 16 elements further: the
+  // staging stores of one instruction then fall in distinct LDS banks
+  constexpr int KS = HD + 8, VS = kWinMax + 4, VH = HD * VS + 16;
   extern __shared__ __align__(16) char smem[];
   bf16* ks = reinterpret_cast<bf16*>(smem);                        // [2][128][KS] K rows
   bf16* qs = ks + 2 * kWinMax * KS;                                // [2][128][KS] Q rows, then O
-  bf16* vts = qs + 2 * kWinMax * KS;                               // [2][HD][VS]  V^T
-  int* kinfo = reinterpret_cast<int*>(vts + 2 * HD * VS);          // [128]
+  bf16* vts = qs + 2 * kWinMax * KS;                               // [2][VH]  V^T
+  int* kinfo = reinterpret_cast<int*>(vts + 2 * VH);               // [128]
   float* tab = reinterpret_cast<float*>(kinfo + kWinMax);          // [2][nbins+4]
 
   const int hpairs = g.heads >> 1;
@@ -333,7 +335,7 @@ __global__ __launch_bounds__(kPairThreads, 4) void fwd_win_pair_kernel(
   const int h = 2 * hp + hs;
   const int qi = 32 * qb + col;
   const bf16* ksh = ks + hs * kWinMax * KS;
-  const bf16* vth = vts + hs * HD * VS;
+  const bf16* vth = vts + hs * VH;
   const float* tabh = tab + hs * (g.nbins + 4);
 
   // bias tables of the pair times sqrt(hd), reversed, then four -inf
@@ -368,7 +370,7 @@ __global__ __launch_bounds__(kPairThreads, 4) void fwd_win_pair_kernel(
       *reinterpret_cast<uint4*>(qs + (t * kWinMax + row) * KS + e0) = rows.q[u];
       const bf16* ve = reinterpret_cast<const bf16*>(&rows.v[u]);
 #pragma unroll
-      for (int x = 0; x < 8; ++x) vts[(t * HD + e0 + x) * VS + row] = ve[x];
+      for (int x = 0; x < 8; ++x) vts[t * VH + (e0 + x) * VS + row] = ve[x];
     }
     if (threadIdx.x < kWinMax) kinfo[threadIdx.x] = win_token_info(g, wi, wj, cols, threadIdx.x, n);
     __syncthreads();
@@ -913,7 +915,7 @@ static void fwd_win_go(const Geo& g, const void* q, const void* k, const void* v
 }
 
 size_t win_fwd_pair_lds(const Geo& g) {
-  return sizeof(bf16) * 2 * (2 * kWinMax * (32 + 8) + 32 * (kWinMax + 8)) + 4 * kWinMax +
+  return sizeof(bf16) * 2 * (2 * kWinMax * (32 + 8) + 32 * (kWinMax + 4) + 16) + 4 * kWinMax +
          4 * 2 * (g.nbins + 4);
 }
 
