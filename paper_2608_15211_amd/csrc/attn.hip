@@ -109,6 +109,50 @@ __device__ inline void stage_tile(const T* __restrict__ src, const Geo& g, const
   }
 }
 
+// One staged tile of one tensor held in registers between its load from HBM
+// and its store to LDS, so that the next tile's loads overlap the current
+// tile's matrix work: thread t holds 16-byte chunks t, t+256, ... (row =
+// chunk / chunks-per-row).
+template <typename T, int HD>
+struct TileRegs {
+  static constexpr int kCpr = HD * (int)sizeof(T) / 16;
+  static constexpr int kPer = tile_of<T, HD>() * kCpr / kThreads;
+  uint4 r[kPer];
+};
+
+template <typename T, int HD, bool NHWC>
+__device__ inline void tile_load(TileRegs<T, HD>& t, const T* __restrict__ src, const Geo& g,
+                                 const WinTokens<NHWC>& wt, int r0, int n, int hoff) {
+  constexpr int kCpr = TileRegs<T, HD>::kCpr;
+#pragma unroll
+  for (int u = 0; u < TileRegs<T, HD>::kPer; ++u) {
+    const int idx = threadIdx.x + u * kThreads;
+    const int rr = idx / kCpr, ch = idx % kCpr;
+    const int row = r0 + rr;
+    t.r[u] = make_uint4(0, 0, 0, 0);
+    if (row < n)
+      t.r[u] = *reinterpret_cast<const uint4*>(src + wt.tok(g, row) * g.C + hoff + ch * (16 / (int)sizeof(T)));
+  }
+}
+
+template <typename T, int HD, bool ROWMAJOR, bool TRANS>
+__device__ inline void tile_store(const TileRegs<T, HD>& t, T* lds_rm, T* lds_tr) {
+  constexpr int kTile = tile_of<T, HD>();
+  constexpr int kCpr = TileRegs<T, HD>::kCpr;
+  constexpr int kElemPerChunk = 16 / sizeof(T);
+#pragma unroll
+  for (int u = 0; u < TileRegs<T, HD>::kPer; ++u) {
+    const int idx = threadIdx.x + u * kThreads;
+    const int rr = idx / kCpr, ch = idx % kCpr;
+    if (ROWMAJOR) *reinterpret_cast<uint4*>(lds_rm + rr * (HD + kPad) + ch * kElemPerChunk) = t.r[u];
+    if (TRANS) {
+      const T* e = reinterpret_cast<const T*>(&t.r[u]);
+#pragma unroll
+      for (int x = 0; x < kElemPerChunk; ++x) lds_tr[(ch * kElemPerChunk + x) * (kTile + kPad) + rr] = e[x];
+    }
+  }
+}
+
 // Label/bias-offset word of in-window token t (t < n), or of a pad slot.
 __device__ inline int token_info(const Geo& g, int i, int j, int cols, int t, int n) {
   if (t >= n) return kLabBad << 24;
@@ -246,7 +290,7 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(
 // dK/dV kernel; the second sweep forms dS, dQ and the bias bins.
 // ---------------------------------------------------------------------------
 template <typename T, int HD, bool NHWC, bool QUAD>
-__global__ __launch_bounds__(kThreads) void bwd_dq_kernel(
+__global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const T* __restrict__ dout, const float* __restrict__ lse, float* __restrict__ D,
     const float* __restrict__ table, T* __restrict__ dq, float* __restrict__ partial,
@@ -300,14 +344,32 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(
       dop[c] = qvalid ? load_op_global<T>(dout + wt.tok(g, qi) * g.C + hoff + 16 * c + 8 * half)
                       : zero_op<T>();
     }
-    // sweep 1: D_q
+    // sweep 1: D_q.  The K, V tiles go HBM -> registers -> LDS; up to head
+    // dim 64 each tile's loads are issued while the previous tile computes
+    // (after the last tile of sweep 1 come the first tiles of sweep 2); at
+    // head dim 128 the registers this holds would halve the occupancy.
+    constexpr bool kPrefetch = HD <= 64;
+    TileRegs<T, HD> rk, rv;
+    if (kPrefetch) {
+      tile_load(rk, k, g, wt, 0, n, hoff);
+      tile_load(rv, v, g, wt, 0, n, hoff);
+    }
     float dsum = 0.0f;
     for (int k0 = 0; k0 < n; k0 += kTile) {
+      if (!kPrefetch) {
+        tile_load(rk, k, g, wt, k0, n, hoff);
+        tile_load(rv, v, g, wt, k0, n, hoff);
+      }
       __syncthreads();
-      stage_tile<T, HD, true, false>(k, g, wt, k0, n, hoff, kt, nullptr);
-      stage_tile<T, HD, true, false>(v, g, wt, k0, n, hoff, vr, nullptr);
+      tile_store<T, HD, true, false>(rk, kt, nullptr);
+      tile_store<T, HD, true, false>(rv, vr, nullptr);
       if (threadIdx.x < kTile) kinfo[threadIdx.x] = token_info(g, i, j, cols, k0 + threadIdx.x, n);
       __syncthreads();
+      if (kPrefetch) {
+        const int nk0 = k0 + kTile < n ? k0 + kTile : 0;
+        tile_load(rk, k, g, wt, nk0, n, hoff);
+        tile_load(rv, v, g, wt, nk0, n, hoff);
+      }
 #pragma unroll
       for (int kb = 0; kb < kTile / 32; ++kb) {
         f32x16 s = mask ? bias_init<QUAD, true>(kinfo, tab, kb, half, qrev, qlab, g.nbins)
@@ -341,11 +403,19 @@ __global__ __launch_bounds__(kThreads) void bwd_dq_kernel(
     for (int eb = 0; eb < HD / 32; ++eb) dqacc[eb] = f32x16{};
 
     for (int k0 = 0; k0 < n; k0 += kTile) {
+      if (!kPrefetch) {
+        tile_load(rk, k, g, wt, k0, n, hoff);
+        tile_load(rv, v, g, wt, k0, n, hoff);
+      }
       __syncthreads();
-      stage_tile<T, HD, true, true>(k, g, wt, k0, n, hoff, kt, ktt);
-      stage_tile<T, HD, true, false>(v, g, wt, k0, n, hoff, vr, nullptr);
+      tile_store<T, HD, true, true>(rk, kt, ktt);
+      tile_store<T, HD, true, false>(rv, vr, nullptr);
       if (threadIdx.x < kTile) kinfo[threadIdx.x] = token_info(g, i, j, cols, k0 + threadIdx.x, n);
       __syncthreads();
+      if (kPrefetch && k0 + kTile < n) {
+        tile_load(rk, k, g, wt, k0 + kTile, n, hoff);
+        tile_load(rv, v, g, wt, k0 + kTile, n, hoff);
+      }
       f32x16 dsb[kTile / 32];
 #pragma unroll
       for (int kb = 0; kb < kTile / 32; ++kb) {
