@@ -82,33 +82,6 @@ __device__ inline typename Operand<T>::type load_op_lds_perm(const T* row, int h
   return o;
 }
 
-// Copy rows [r0, r0+kTile) x HD of one head of one window into LDS,
-// row-major (stride HD+kPad) and/or transposed (stride kTile+kPad).  Rows at
-// or beyond n are zero.
-template <typename T, int HD, bool ROWMAJOR, bool TRANS, bool NHWC>
-__device__ inline void stage_tile(const T* __restrict__ src, const Geo& g, const WinTokens<NHWC>& wt,
-                                  int r0, int n, int hoff, T* lds_rm, T* lds_tr) {
-  constexpr int kTile = tile_of<T, HD>();
-  constexpr int kElemPerChunk = 16 / sizeof(T);
-  constexpr int kCpr = HD / kElemPerChunk;
-  for (int idx = threadIdx.x; idx < kTile * kCpr; idx += kThreads) {
-    const int rr = idx / kCpr;
-    const int ch = idx - rr * kCpr;
-    const int row = r0 + rr;
-    uint4 raw = make_uint4(0, 0, 0, 0);
-    if (row < n)
-      raw = *reinterpret_cast<const uint4*>(src + wt.tok(g, row) * g.C + hoff + ch * kElemPerChunk);
-    if (ROWMAJOR)
-      *reinterpret_cast<uint4*>(lds_rm + rr * (HD + kPad) + ch * kElemPerChunk) = raw;
-    if (TRANS) {
-      const T* e = reinterpret_cast<const T*>(&raw);
-#pragma unroll
-      for (int x = 0; x < kElemPerChunk; ++x)
-        lds_tr[(ch * kElemPerChunk + x) * (kTile + kPad) + rr] = e[x];
-    }
-  }
-}
-
 // One staged tile of one tensor held in registers between its load from HBM
 // and its store to LDS, so that the next tile's loads overlap the current
 // tile's matrix work: thread t holds 16-byte chunks t, t+256, ... (row =
@@ -218,12 +191,27 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(
   for (int eb = 0; eb < HD / 32; ++eb) oacc[eb] = f32x16{};
   float m_run = -1e30f, l_run = 0.0f;     // running max (log2 units) and sum
 
+  // K, V tiles go HBM -> registers -> LDS, one tile ahead up to head dim 64
+  constexpr bool kPrefetch = HD <= 64;
+  TileRegs<T, HD> rk, rv;
+  if (kPrefetch) {
+    tile_load(rk, k, g, wt, 0, n, hoff);
+    tile_load(rv, v, g, wt, 0, n, hoff);
+  }
   for (int k0 = 0; k0 < n; k0 += kTile) {
+    if (!kPrefetch) {
+      tile_load(rk, k, g, wt, k0, n, hoff);
+      tile_load(rv, v, g, wt, k0, n, hoff);
+    }
     __syncthreads();
-    stage_tile<T, HD, true, false>(k, g, wt, k0, n, hoff, kt, nullptr);
-    stage_tile<T, HD, false, true>(v, g, wt, k0, n, hoff, nullptr, vt);
+    tile_store<T, HD, true, false>(rk, kt, nullptr);
+    tile_store<T, HD, false, true>(rv, nullptr, vt);
     if (threadIdx.x < kTile) kinfo[threadIdx.x] = token_info(g, i, j, cols, k0 + threadIdx.x, n);
     __syncthreads();
+    if (kPrefetch && k0 + kTile < n) {
+      tile_load(rk, k, g, wt, k0 + kTile, n, hoff);
+      tile_load(rv, v, g, wt, k0 + kTile, n, hoff);
+    }
 
     f32x16 s[kTile / 32];
     float mloc = -INFINITY;
@@ -581,10 +569,21 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(
 #pragma unroll
   for (int eb = 0; eb < HD / 32; ++eb) { dkacc[eb] = f32x16{}; dvacc[eb] = f32x16{}; }
 
+  // Q, dO tiles go HBM -> registers -> LDS, one tile ahead up to head dim 64
+  constexpr bool kPrefetch = HD <= 64;
+  TileRegs<T, HD> rq, rd;
+  if (kPrefetch) {
+    tile_load(rq, q, g, wt, 0, n, hoff);
+    tile_load(rd, dout, g, wt, 0, n, hoff);
+  }
   for (int t0 = 0; t0 < n; t0 += kTile) {
+    if (!kPrefetch) {
+      tile_load(rq, q, g, wt, t0, n, hoff);
+      tile_load(rd, dout, g, wt, t0, n, hoff);
+    }
     __syncthreads();
-    stage_tile<T, HD, true, true>(q, g, wt, t0, n, hoff, qr, qtt);
-    stage_tile<T, HD, true, true>(dout, g, wt, t0, n, hoff, dr, dtt);
+    tile_store<T, HD, true, true>(rq, qr, qtt);
+    tile_store<T, HD, true, true>(rd, dr, dtt);
     if (threadIdx.x < kTile) {
       const int t = t0 + threadIdx.x;
       const int inf = token_info(g, i, j, cols, t, n);
@@ -594,6 +593,10 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(
       qd[threadIdx.x] = t < n ? D[li] : 0.0f;
     }
     __syncthreads();
+    if (kPrefetch && t0 + kTile < n) {
+      tile_load(rq, q, g, wt, t0 + kTile, n, hoff);
+      tile_load(rd, dout, g, wt, t0 + kTile, n, hoff);
+    }
 #pragma unroll
     for (int qb = 0; qb < kTile / 32; ++qb) {
       // registers 4g..4g+3 hold queries 32qb + 8g + 4*half + 0..3: their
