@@ -51,6 +51,15 @@ template <typename T, int HD> constexpr int tile_of() { return (sizeof(T) == 4 &
 constexpr int kPad = 8;         // LDS row padding, elements
 constexpr int kLabBad = 0xFF;   // label of padding slots (never matches)
 
+// Transposed tiles (head-dim rows e, token columns): row e starts at
+// e * (kTile + kPad) plus 4 elements per group of 8 rows, so that the
+// transposing staging stores of one instruction (8 rows of one chunk, the
+// chunks 8 rows apart) fall in distinct LDS banks.
+template <typename T, int HD>
+__device__ __host__ constexpr int tr_row(int e) { return e * (tile_of<T, HD>() + kPad) + (e >> 3) * 4; }
+template <typename T, int HD>
+__device__ __host__ constexpr int tr_size() { return tr_row<T, HD>(HD); }
+
 // Slot s (0..7) of lane half h inside a 16-deep contraction chunk, when the
 // operand comes from 32x32 result registers 8c..8c+7: row acc_row(s, h).
 __device__ inline int perm_slot(int s, int h) { return 8 * (s / 4) + 4 * h + (s % 4); }
@@ -121,7 +130,7 @@ __device__ inline void tile_store(const TileRegs<T, HD>& t, T* lds_rm, T* lds_tr
     if (TRANS) {
       const T* e = reinterpret_cast<const T*>(&t.r[u]);
 #pragma unroll
-      for (int x = 0; x < kElemPerChunk; ++x) lds_tr[(ch * kElemPerChunk + x) * (kTile + kPad) + rr] = e[x];
+      for (int x = 0; x < kElemPerChunk; ++x) lds_tr[tr_row<T, HD>(ch * kElemPerChunk + x) + rr] = e[x];
     }
   }
 }
@@ -151,7 +160,7 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(
   extern __shared__ __align__(16) char smem[];
   T* kt = reinterpret_cast<T*>(smem);                          // [kTile][HD+kPad]
   T* vt = kt + kTile * (HD + kPad);                            // [HD][kTile+kPad]
-  int* kinfo = reinterpret_cast<int*>(vt + HD * (kTile + kPad));
+  int* kinfo = reinterpret_cast<int*>(vt + tr_size<T, HD>());
   float* tab = reinterpret_cast<float*>(kinfo + kTile);        // [nbins+4], reversed
 
   int bid = blockIdx.x;
@@ -247,7 +256,7 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(
       for (int kb = 0; kb < kTile / 32; ++kb) {
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
-          const T* row = vt + (eb * 32 + col) * (kTile + kPad) + kb * 32 + 16 * c;
+          const T* row = vt + tr_row<T, HD>(eb * 32 + col) + kb * 32 + 16 * c;
           mma16(oacc[eb], load_op_lds_perm<T>(row, half), pack8<T>(s[kb], 8 * c));
         }
       }
@@ -287,8 +296,8 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
   extern __shared__ __align__(16) char smem[];
   T* kt = reinterpret_cast<T*>(smem);                 // K  [kTile][HD+kPad]
   T* vr = kt + kTile * (HD + kPad);                   // V  [kTile][HD+kPad]
-  T* ktt = vr + kTile * (HD + kPad);                  // K^T [HD][kTile+kPad]
-  int* kinfo = reinterpret_cast<int*>(ktt + HD * (kTile + kPad));
+  T* ktt = vr + kTile * (HD + kPad);                  // K^T (transposed tile)
+  int* kinfo = reinterpret_cast<int*>(ktt + tr_size<T, HD>());
   float* tab = reinterpret_cast<float*>(kinfo + kTile);   // [nbins+4], reversed
   float* dtab = tab + g.nbins + 4;                    // [4][nbins], one per wave
 
@@ -423,7 +432,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
         for (int eb = 0; eb < HD / 32; ++eb) {
 #pragma unroll
           for (int c = 0; c < 2; ++c) {
-            const T* row = ktt + (eb * 32 + col) * (kTile + kPad) + kb * 32 + 16 * c;
+            const T* row = ktt + tr_row<T, HD>(eb * 32 + col) + kb * 32 + 16 * c;
             mma16(dqacc[eb], load_op_lds_perm<T>(row, half), pack8<T>(dsb[kb], 8 * c));
           }
         }
@@ -525,9 +534,9 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(
   extern __shared__ __align__(16) char smem[];
   T* qr = reinterpret_cast<T*>(smem);                 // Q  [kTile][HD+kPad]
   T* dr = qr + kTile * (HD + kPad);                   // dO [kTile][HD+kPad]
-  T* qtt = dr + kTile * (HD + kPad);                  // Q^T  [HD][kTile+kPad]
-  T* dtt = qtt + HD * (kTile + kPad);                 // dO^T [HD][kTile+kPad]
-  int* qinfo = reinterpret_cast<int*>(dtt + HD * (kTile + kPad));
+  T* qtt = dr + kTile * (HD + kPad);                  // Q^T (transposed tile)
+  T* dtt = qtt + tr_size<T, HD>();                   // dO^T
+  int* qinfo = reinterpret_cast<int*>(dtt + tr_size<T, HD>());
   float* ql = reinterpret_cast<float*>(qinfo + kTile);   // lse2 per query
   float* qd = ql + kTile;                                 // D per query
   float* tab = qd + kTile;                                // [nbins+4], forward order
@@ -631,9 +640,9 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
           const int cofs = qb * 32 + 16 * c;
-          mma16(dvacc[eb], load_op_lds_perm<T>(dtt + (eb * 32 + col) * (kTile + kPad) + cofs, half),
+          mma16(dvacc[eb], load_op_lds_perm<T>(dtt + tr_row<T, HD>(eb * 32 + col) + cofs, half),
                 pack8<T>(s, 8 * c));
-          mma16(dkacc[eb], load_op_lds_perm<T>(qtt + (eb * 32 + col) * (kTile + kPad) + cofs, half),
+          mma16(dkacc[eb], load_op_lds_perm<T>(qtt + tr_row<T, HD>(eb * 32 + col) + cofs, half),
                 pack8<T>(ds, 8 * c));
         }
       }
@@ -688,18 +697,18 @@ int bwd_nslice(const Geo& g) {
 template <typename T, int HD>
 static size_t fwd_lds(const Geo& g) {
   constexpr int kTile = tile_of<T, HD>();
-  return sizeof(T) * (kTile * (HD + kPad) + HD * (kTile + kPad)) + 4 * kTile + 4 * (g.nbins + 4);
+  return sizeof(T) * (kTile * (HD + kPad) + tr_size<T, HD>()) + 4 * kTile + 4 * (g.nbins + 4);
 }
 template <typename T, int HD>
 static size_t dq_lds(const Geo& g) {
   constexpr int kTile = tile_of<T, HD>();
-  return sizeof(T) * (2 * kTile * (HD + kPad) + HD * (kTile + kPad)) + 4 * kTile + 4 * (g.nbins + 4) +
+  return sizeof(T) * (2 * kTile * (HD + kPad) + tr_size<T, HD>()) + 4 * kTile + 4 * (g.nbins + 4) +
          16 * g.nbins;
 }
 template <typename T, int HD>
 static size_t dkdv_lds(const Geo& g) {
   constexpr int kTile = tile_of<T, HD>();
-  return sizeof(T) * (2 * kTile * (HD + kPad) + 2 * HD * (kTile + kPad)) + 12 * kTile + 4 * (g.nbins + 4);
+  return sizeof(T) * (2 * kTile * (HD + kPad) + 2 * tr_size<T, HD>()) + 12 * kTile + 4 * (g.nbins + 4);
 }
 
 template <typename T, int HD, bool NHWC>
