@@ -471,6 +471,15 @@ constexpr int kBwdRS = kWinMax + 4;    // LDS row stride (fp32) of the dV, dK su
 constexpr int kBwdTS = kWinMax + 8;    // LDS row stride (bf16) of K^T
 constexpr int kBwdCPR = kBwdHD / 8;    // 16-byte chunks per token row of one head
 
+// Token row of 16-byte chunk idx (chunk idx % 4 of its row) in the
+// row-contiguous staging of one head: the 16 lanes of a group take rows
+// r, r+4, r+8, r+12 of a 16-row band, whose 64-byte LDS row segments
+// (80-byte row stride) then fall in distinct banks.
+__device__ __forceinline__ int bwd_stage_row(int idx) {
+  const int blk = idx >> 4;
+  return ((blk >> 2) << 4) + (blk & 3) + 4 * ((idx >> 2) & 3);
+}
+
 // Per-lane 0/1 factors of the bias-gradient fold for the window width cols
 // (a multiple of 4 that divides 32, so window rows never straddle a 32-lane
 // half): cq is the lane's query column.
@@ -645,7 +654,7 @@ __device__ __forceinline__ void bwd_window_body(BwdWave& st, int qw, f32x4 (&dta
 }
 
 // Rows of one window on their way from HBM to LDS: thread t holds 16-byte
-// chunks t and t+256 (row = chunk / 4) of K, V, Q and dO, and the
+// chunks t and t+256 (row bwd_stage_row(chunk)) of K, V, Q and dO, and the
 // log-sum-exp (log2 units) of its wave's query.
 struct BwdRows {
   uint4 k[2], v[2], q[2], d[2];
@@ -665,7 +674,7 @@ __device__ __forceinline__ void bwd_load_rows(BwdRows& r, const Geo& g, int wl, 
 #pragma unroll
   for (int u = 0; u < 2; ++u) {
     const int idx = threadIdx.x + u * kWinThreads;
-    const int row = idx / kBwdCPR, ch = idx % kBwdCPR;
+    const int row = bwd_stage_row(idx), ch = idx % kBwdCPR;
     r.k[u] = r.v[u] = r.q[u] = r.d[u] = make_uint4(0, 0, 0, 0);
     if (row < n) {
       const int64_t off = wt.tok(g, row) * g.C + h * kBwdHD + ch * 8;
@@ -772,7 +781,7 @@ __global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
       const int idx = threadIdx.x + u * kWinThreads;
-      const int row = idx / kBwdCPR, c0 = (idx % kBwdCPR) * 8;
+      const int row = bwd_stage_row(idx), c0 = (idx % kBwdCPR) * 8;
       *reinterpret_cast<uint4*>(ks + row * KS + c0) = rows.k[u];
       *reinterpret_cast<uint4*>(vs + row * KS + c0) = rows.v[u];
       *reinterpret_cast<uint4*>(qrows + row * KS + c0) = rows.q[u];
@@ -834,7 +843,7 @@ __global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
       const int idx = threadIdx.x + u * kWinThreads;
-      const int row = idx / kBwdCPR, c0 = (idx % kBwdCPR) * 8;
+      const int row = bwd_stage_row(idx), c0 = (idx % kBwdCPR) * 8;
       if (row < n) {
         const int64_t off = wt.tok(g, row) * g.C + h * HD + c0;
         *reinterpret_cast<uint4*>(dq + off) = *reinterpret_cast<const uint4*>(ks + row * KS + c0);
