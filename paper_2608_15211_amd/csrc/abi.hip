@@ -87,6 +87,7 @@ terra::Geo make_geo(const terra_geom* g) {
   G.HW = g->H * g->W;
   G.bstride = 2 * g->ww - 1;
   G.nbins = (2 * g->wh - 1) * G.bstride;
+  terra::set_table_stride(G);
   return G;
 }
 

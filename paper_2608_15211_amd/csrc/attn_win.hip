@@ -59,7 +59,23 @@ __device__ inline int win_token_info(const Geo& g, int i, int j, int cols, int t
   const int a = fast_div(t, cols, 1.0f / (float)cols);
   const int c = t - a * cols;
   const int lab = row_label(g, i * g.wh + a) | col_label(g, j * g.ww + c);
-  return (a * g.bstride + c) | (lab << 24);
+  return (a * g.tstride + c) | (lab << 24);
+}
+
+// Entry x of the LDS bias table of head h: bins in reversed order, rows of
+// tstride entries (the padding entries are never read), times `scale`; four
+// -inf entries at ntab .. ntab+3 serve excluded pairs.
+__device__ inline float table_entry(const Geo& g, const float* __restrict__ table, int h, int x,
+                                    float scale) {
+  if (x >= g.ntab) return -INFINITY;
+  const int y = g.ntab - 1 - x;
+  const int da = y / g.tstride, dc = y - da * g.tstride;
+  return dc < g.bstride ? table[(da * g.bstride + dc) * g.heads + h] * scale : 0.0f;
+}
+
+// Reversed table index of query word qinf against key offset 0.
+__device__ inline int table_qrev(const Geo& g, int qinf) {
+  return g.ntab - 1 - ((qinf & 0xFFFFFF) + (g.wh - 1) * g.tstride + (g.ww - 1));
 }
 
 __device__ inline bf16x8 zero8() {
@@ -156,7 +172,7 @@ __global__ __launch_bounds__(kWinThreads) void fwd_win_kernel(
   bf16* ks = reinterpret_cast<bf16*>(smem);                       // [128][HD+8]
   bf16* vts = ks + kWinMax * (HD + 8);                            // [HD][128+8]
   int* kinfo = reinterpret_cast<int*>(vts + HD * (kWinMax + 8));  // [128]
-  float* tab = reinterpret_cast<float*>(kinfo + kWinMax);         // [nbins]
+  float* tab = reinterpret_cast<float*>(kinfo + kWinMax);         // [ntab+4]
 
   int work = xcd_work(blockIdx.x, gridDim.x);
   const int h = work % g.heads; work /= g.heads;
@@ -175,8 +191,7 @@ __global__ __launch_bounds__(kWinThreads) void fwd_win_kernel(
   // consecutive keys of a window row read consecutive addresses; four -inf
   // entries after it serve excluded pairs
   const float bscale = sqrtf((float)HD);
-  for (int x = threadIdx.x; x < g.nbins + 4; x += kWinThreads)
-    tab[x] = x < g.nbins ? table[(g.nbins - 1 - x) * g.heads + h] * bscale : -INFINITY;
+  for (int x = threadIdx.x; x < g.ntab + 4; x += kWinThreads) tab[x] = table_entry(g, table, h, x, bscale);
   if (threadIdx.x < kWinMax) kinfo[threadIdx.x] = win_token_info(g, wi, wj, cols, threadIdx.x, n);
   stage_rows<HD>(k, g, wt, n, hoff, ks);
   // V^T through LDS: stage V rows into the vts area's tail is not possible
@@ -207,7 +222,7 @@ __global__ __launch_bounds__(kWinThreads) void fwd_win_kernel(
   const int qinf = kinfo[qvalid ? qi : 0];
   const int qlab = qinf >> 24;
   // reversed bin of (q, k) = qrev + koff(k)
-  const int qrev = g.nbins - 1 - ((qinf & 0xFFFFFF) + (g.wh - 1) * g.bstride + (g.ww - 1));
+  const int qrev = table_qrev(g, qinf);
   bf16x8 qop[HD / 16];
 #pragma unroll
   for (int c = 0; c < HD / 16; ++c)
@@ -220,8 +235,8 @@ __global__ __launch_bounds__(kWinThreads) void fwd_win_kernel(
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb) {
     if (kb < nkb) {
-      s[kb] = mask ? bias_init<QUAD, true>(kinfo, tab, kb, half, qrev, qlab, g.nbins)
-                   : bias_init<QUAD, false>(kinfo, tab, kb, half, qrev, qlab, g.nbins);
+      s[kb] = mask ? bias_init<QUAD, true>(kinfo, tab, kb, half, qrev, qlab, g.ntab)
+                   : bias_init<QUAD, false>(kinfo, tab, kb, half, qrev, qlab, g.ntab);
 #pragma unroll
       for (int c = 0; c < HD / 16; ++c)
         mma16(s[kb], *reinterpret_cast<const bf16x8*>(ks + (32 * kb + col) * (HD + 8) + 16 * c + 8 * half),
@@ -322,7 +337,7 @@ __global__ __launch_bounds__(kPairThreads, 4) void fwd_win_pair_kernel(
   bf16* qs = ks + 2 * kWinMax * KS;                                // [2][128][KS] Q rows, then O
   bf16* vts = qs + 2 * kWinMax * KS;                               // [2][VH]  V^T
   int* kinfo = reinterpret_cast<int*>(vts + 2 * VH);               // [128]
-  float* tab = reinterpret_cast<float*>(kinfo + kWinMax);          // [2][nbins+4]
+  float* tab = reinterpret_cast<float*>(kinfo + kWinMax);          // [2][ntab+4]
 
   const int hpairs = g.heads >> 1;
   const int work = xcd_work(blockIdx.x, gridDim.x);
@@ -336,13 +351,13 @@ __global__ __launch_bounds__(kPairThreads, 4) void fwd_win_pair_kernel(
   const int qi = 32 * qb + col;
   const bf16* ksh = ks + hs * kWinMax * KS;
   const bf16* vth = vts + hs * VH;
-  const float* tabh = tab + hs * (g.nbins + 4);
+  const float* tabh = tab + hs * (g.ntab + 4);
 
   // bias tables of the pair times sqrt(hd), reversed, then four -inf
   const float bscale = sqrtf((float)HD);
-  for (int x = threadIdx.x; x < 2 * (g.nbins + 4); x += kPairThreads) {
-    const int t = x / (g.nbins + 4), y = x - t * (g.nbins + 4);
-    tab[x] = y < g.nbins ? table[(g.nbins - 1 - y) * g.heads + 2 * hp + t] * bscale : -INFINITY;
+  for (int x = threadIdx.x; x < 2 * (g.ntab + 4); x += kPairThreads) {
+    const int t = x / (g.ntab + 4), y = x - t * (g.ntab + 4);
+    tab[x] = table_entry(g, table, 2 * hp + t, y, bscale);
   }
 
   const int total = g.B * g.nwin;
@@ -388,7 +403,7 @@ __global__ __launch_bounds__(kPairThreads, 4) void fwd_win_pair_kernel(
         qop[c] = *reinterpret_cast<const bf16x8*>(qs + (hs * kWinMax + qi) * KS + 16 * c + 8 * half);
       const int qinf = kinfo[qvalid ? qi : 0];
       const int qlab = qinf >> 24;
-      const int qrev = g.nbins - 1 - ((qinf & 0xFFFFFF) + (g.wh - 1) * g.bstride + (g.ww - 1));
+      const int qrev = table_qrev(g, qinf);
       const bool mask = window_needs_mask(g, wi, wj, n);
 #pragma unroll
       for (int hb = 0; hb < 2; ++hb) {
@@ -399,8 +414,8 @@ __global__ __launch_bounds__(kPairThreads, 4) void fwd_win_pair_kernel(
           for (int j = 0; j < 2; ++j) {
             const int kb = 2 * hb + j;
             if (kb < nkb) {
-              s[j] = mask ? bias_init<QUAD, true>(kinfo, tabh, kb, half, qrev, qlab, g.nbins)
-                          : bias_init<QUAD, false>(kinfo, tabh, kb, half, qrev, qlab, g.nbins);
+              s[j] = mask ? bias_init<QUAD, true>(kinfo, tabh, kb, half, qrev, qlab, g.ntab)
+                          : bias_init<QUAD, false>(kinfo, tabh, kb, half, qrev, qlab, g.ntab);
 #pragma unroll
               for (int c = 0; c < 2; ++c)
                 mma16(s[j], *reinterpret_cast<const bf16x8*>(ksh + (32 * kb + col) * KS + 16 * c + 8 * half),
@@ -510,7 +525,7 @@ struct BwdWave {
   bf16x8 de[2], qe[2];    // dO and Q with lane = channel (column operands)
   float D, lse2, scale_log2;
   FoldMask fold;
-  int qrev, qlab, nbins, col, half;
+  int qrev, qlab, ntab, col, half;
 };
 
 // Row-to-column transpose operand of chunk c (ident_op<false>), read from
@@ -542,7 +557,7 @@ __device__ __forceinline__ void fold_diag(const f32x16& ds, int g4, const FoldMa
 // saved log-sum-exp (+inf for padding queries, so their P is 0).
 template <int KB, bool QUAD, bool MASK>
 __device__ __forceinline__ f32x16 bwd_p(const BwdWave& st) {
-  f32x16 p = bias_init<QUAD, MASK>(st.kinfo, st.tab, KB, st.half, st.qrev, st.qlab, st.nbins);
+  f32x16 p = bias_init<QUAD, MASK>(st.kinfo, st.tab, KB, st.half, st.qrev, st.qlab, st.ntab);
 #pragma unroll
   for (int c = 0; c < 2; ++c)
     mma16(p, *reinterpret_cast<const bf16x8*>(st.ks + (32 * KB + st.col) * kBwdKS + 16 * c + 8 * st.half),
@@ -713,8 +728,8 @@ __global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
   float* redv = reinterpret_cast<float*>(kts + HD * kBwdTS);    // [HD][RS] dV sums
   float* redk = redv + HD * RS;                                 // [HD][RS] dK sums
   int* kinfo = reinterpret_cast<int*>(redk + HD * RS);          // [128]
-  float* tab = reinterpret_cast<float*>(kinfo + kWinMax);       // [nbins+4]
-  float* bins = tab + (g.nbins + 4);                            // [4][nbins], reversed
+  float* tab = reinterpret_cast<float*>(kinfo + kWinMax);       // [ntab+4]
+  float* bins = tab + (g.ntab + 4);                             // [4][nbins], reversed
   bf16* qrows = reinterpret_cast<bf16*>(redv);                  // [128][KS] Q rows (staging)
   bf16* drows = reinterpret_cast<bf16*>(redk);                  // [128][KS] dO rows (staging)
 
@@ -729,8 +744,8 @@ __global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
 
   for (int x = threadIdx.x; x < 4 * g.nbins; x += kWinThreads) bins[x] = 0.0f;
   if (qw < 2) ident[threadIdx.x] = ident_op<false>(qw);
-  for (int x = threadIdx.x; x < g.nbins + 4; x += kWinThreads)
-    tab[x] = x < g.nbins ? table[(g.nbins - 1 - x) * g.heads + h] * sqrtf((float)HD) : -INFINITY;
+  for (int x = threadIdx.x; x < g.ntab + 4; x += kWinThreads)
+    tab[x] = table_entry(g, table, h, x, sqrtf((float)HD));
 
   f32x4 dta[4], dtb[4];
 #pragma unroll
@@ -800,7 +815,7 @@ __global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
     st.redv = redv;
     st.redk = redk;
     st.scale_log2 = scale_log2;
-    st.nbins = g.nbins;
+    st.ntab = g.ntab;
     st.col = col;
     st.half = half;
 #pragma unroll
@@ -820,7 +835,7 @@ __global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
     }
     const int qinf = qi < n ? kinfo[qi] : 0;
     st.qlab = qinf >> 24;
-    st.qrev = g.nbins - 1 - ((qinf & 0xFFFFFF) + (g.wh - 1) * g.bstride + (g.ww - 1));
+    st.qrev = table_qrev(g, qinf);
     st.fold = fold_mask(qi % cols, cols);
     {
       const bf16x8 in0 = lds_ident(ident, 0), in1 = lds_ident(ident, 1);
@@ -901,7 +916,7 @@ int win_bwd_nslice(const Geo& g) {
 size_t win_fwd_pair_lds(const Geo& g);
 size_t win_fwd_lds(const Geo& g) {
   const size_t one = sizeof(bf16) * (kWinMax * (g.hd + 8) + g.hd * (kWinMax + 8)) + 4 * kWinMax +
-                     4 * (g.nbins + 4);
+                     4 * (g.ntab + 4);
   if (g.hd == 32 && g.heads % 2 == 0) {
     const size_t pair = win_fwd_pair_lds(g);
     return pair > one ? pair : one;
@@ -910,7 +925,7 @@ size_t win_fwd_lds(const Geo& g) {
 }
 size_t win_bwd_lds(const Geo& g) {
   return 16 * 2 * 64 + sizeof(bf16) * (2 * kWinMax * kBwdKS + kBwdHD * kBwdTS) +
-         sizeof(float) * 2 * kBwdHD * kBwdRS + 4 * kWinMax + 4 * (g.nbins + 4) + 4 * 4 * g.nbins;
+         sizeof(float) * 2 * kBwdHD * kBwdRS + 4 * kWinMax + 4 * (g.ntab + 4) + 4 * 4 * g.nbins;
 }
 
 
@@ -925,7 +940,7 @@ static void fwd_win_go(const Geo& g, const void* q, const void* k, const void* v
 
 size_t win_fwd_pair_lds(const Geo& g) {
   return sizeof(bf16) * 2 * (2 * kWinMax * (32 + 8) + 32 * (kWinMax + 4) + 16) + 4 * kWinMax +
-         4 * 2 * (g.nbins + 4);
+         4 * 2 * (g.ntab + 4);
 }
 
 // Slices of the window range per head pair of the forward: one round of

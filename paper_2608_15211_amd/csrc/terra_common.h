@@ -30,7 +30,16 @@ struct Geo {
   int HW;
   int nbins;          // (2wh-1)(2ww-1)
   int bstride;        // 2ww-1
+  // Row stride and size of the window kernels' LDS bias table: rows padded
+  // to a stride of 16 mod 32 so that the table reads of two window rows of
+  // queries fall in distinct LDS banks.
+  int tstride, ntab;  // ntab = (2wh-1) * tstride
 };
+
+__host__ inline void set_table_stride(Geo& g) {
+  g.tstride = g.bstride + ((48 - g.bstride % 32) % 32);
+  g.ntab = (2 * g.wh - 1) * g.tstride;
+}
 
 // Extent of window row i / column j (partial at the far edge).
 __device__ __host__ inline int win_rows(const Geo& g, int i) {
