@@ -88,6 +88,7 @@ terra::Geo make_geo(const terra_geom* g) {
   G.bstride = 2 * g->ww - 1;
   G.nbins = (2 * g->wh - 1) * G.bstride;
   terra::set_table_stride(G);
+  terra::set_col_recips(G);
   return G;
 }
 

@@ -138,7 +138,7 @@ __device__ inline void tile_store(const TileRegs<T, HD>& t, T* lds_rm, T* lds_tr
 // Label/bias-offset word of in-window token t (t < n), or of a pad slot.
 __device__ inline int token_info(const Geo& g, int i, int j, int cols, int t, int n) {
   if (t >= n) return kLabBad << 24;
-  const int a = t / cols;
+  const int a = fast_div(t, cols, win_rcols(g, j));
   const int c = t - a * cols;
   const int lab = row_label(g, i * g.wh + a) | col_label(g, j * g.ww + c);
   return (a * g.bstride + c) | (lab << 24);
@@ -387,7 +387,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
 
     // sweep 2: dS, dQ, bias bins
     const bool fold = (g.ww % 4 == 0) && (g.W % g.ww) % 4 == 0;   // uniform
-    const int cq = qi - fast_div(qi, cols, 1.0f / (float)cols) * cols;
+    const int cq = qi - fast_div(qi, cols, win_rcols(g, j)) * cols;
     // runs: lanes of one 32-lane half holding consecutive queries of one
     // window row; run = lanes before this one in its run, rest = lanes after
     const int run = cq < col ? cq : col;

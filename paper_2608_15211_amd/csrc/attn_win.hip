@@ -56,7 +56,7 @@ __device__ inline f32x16 mfma_transpose(const bf16x8& a0, const bf16x8& a1, cons
 
 __device__ inline int win_token_info(const Geo& g, int i, int j, int cols, int t, int n) {
   if (t >= n) return kLabBadW << 24;
-  const int a = fast_div(t, cols, 1.0f / (float)cols);
+  const int a = fast_div(t, cols, win_rcols(g, j));
   const int c = t - a * cols;
   const int lab = row_label(g, i * g.wh + a) | col_label(g, j * g.ww + c);
   return (a * g.tstride + c) | (lab << 24);

@@ -34,6 +34,9 @@ struct Geo {
   // to a stride of 16 mod 32 so that the table reads of two window rows of
   // queries fall in distinct LDS banks.
   int tstride, ntab;  // ntab = (2wh-1) * tstride
+  // 1 / width of full-width windows and of the last column's windows (the
+  // float reciprocals fast_div starts from), set on the host.
+  float rcols[2];
 };
 
 __host__ inline void set_table_stride(Geo& g) {
@@ -50,6 +53,14 @@ __device__ __host__ inline int win_cols(const Geo& g, int j) {
   int c = g.W - j * g.ww;
   return c < g.ww ? c : g.ww;
 }
+
+__host__ inline void set_col_recips(Geo& g) {
+  g.rcols[0] = 1.0f / (float)win_cols(g, 0);
+  g.rcols[1] = 1.0f / (float)win_cols(g, g.Mw - 1);
+}
+
+// Reciprocal of the width of window column j.
+__device__ inline float win_rcols(const Geo& g, int j) { return j == g.Mw - 1 ? g.rcols[1] : g.rcols[0]; }
 // First window-major slot of window (i, j) within its image: all window rows
 // above i are full (wh rows each), and the windows to the left in row i hold
 // rows_i * ww tokens each.
@@ -86,23 +97,27 @@ __device__ inline int fast_div(int n, int d, float rcp) {
 // (b*heads + h)*HW + (token - b*HW) in either layout.
 template <bool NHWC>
 struct WinTokens {
-  int64_t img0, first;    // b*HW; window-major first slot of the window
+  // Attention tensors hold fewer than 2^31 elements, so token indices and
+  // element offsets fit 32 bits.
+  uint32_t img0, first;   // b*HW; window-major first slot of the window
   int r0, c0, cols;       // i*wh + sh, j*ww + sw, window width
   float rcols;
   __device__ WinTokens(const Geo& g, int b, int i, int j)
-      : img0((int64_t)b * g.HW), first((int64_t)b * g.HW + win_offset(g, i, j)),
-        r0(i * g.wh + g.sh), c0(j * g.ww + g.sw), cols(win_cols(g, j)),
-        rcols(1.0f / (float)win_cols(g, j)) {}
-  __device__ int64_t tok(const Geo& g, int t) const {
+      : img0((uint32_t)(b * g.HW)), first((uint32_t)(b * g.HW + win_offset(g, i, j))),
+        r0(i * g.wh + g.sh), c0(j * g.ww + g.sw), cols(win_cols(g, j)), rcols(win_rcols(g, j)) {}
+  // Both wraps subtract once: the rolled coordinate is below twice the
+  // extent, and for x < 2 L, min(x, x - L) over unsigned is x mod L.
+  __device__ uint32_t tok(const Geo& g, int t) const {
     if (!NHWC) return first + t;
     const int a = fast_div(t, cols, rcols);
-    int u = r0 + a, v = c0 + (t - a * cols);
-    if (u >= g.H) u -= g.H;
-    if (v >= g.W) v -= g.W;
-    return img0 + (int64_t)u * g.W + v;
+    uint32_t u = (uint32_t)(r0 + a);
+    u = min(u, u - (uint32_t)g.H);
+    uint32_t v = (uint32_t)(c0 + (t - a * cols));
+    v = min(v, v - (uint32_t)g.W);
+    return img0 + u * (uint32_t)g.W + v;
   }
-  __device__ int64_t lse_at(const Geo& g, int h, int t) const {
-    return img0 * g.heads + (int64_t)h * g.HW + (tok(g, t) - img0);
+  __device__ uint32_t lse_at(const Geo& g, int h, int t) const {
+    return img0 * (uint32_t)g.heads + (uint32_t)(h * g.HW) + (tok(g, t) - img0);
   }
 };
 
