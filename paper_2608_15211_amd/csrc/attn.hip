@@ -234,7 +234,7 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(
 #pragma unroll
       for (int r = 0; r < 16; ++r) mloc = fmaxf(mloc, s[kb][r]);
     }
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
+    mloc = halves_max(mloc);
     const float mnew = fmaxf(m_run, mloc * scale_log2);
     const float alpha = exp2f(m_run - mnew);
     m_run = mnew;
@@ -262,7 +262,7 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(
       }
     }
   }
-  l_run += __shfl_xor(l_run, 32);
+  l_run = halves_sum(l_run);
   if (!qvalid) return;
   const float inv = 1.0f / l_run;
   T* orow = o + wt.tok(g, qi) * g.C + hoff;
@@ -382,7 +382,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
           dsum += __builtin_amdgcn_exp2f(s[r] * scale_log2 - lse2) * dp[r];
       }
     }
-    const float Dq = dsum + __shfl_xor(dsum, 32);
+    const float Dq = halves_sum(dsum);
     if (qvalid && half == 0) D[lidx] = Dq;
 
     // sweep 2: dS, dQ, bias bins

@@ -249,7 +249,7 @@ __global__ __launch_bounds__(kWinThreads) void fwd_win_kernel(
     if (kb < nkb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) mr = fmaxf(mr, s[kb][r]);
-  mr = fmaxf(mr, __shfl_xor(mr, 32));
+  mr = halves_max(mr);
   const float m = mr * scale_log2;            // row max, log2 domain
   float l = 0.0f;
   f32x16 oacc[HD / 32];
@@ -272,7 +272,7 @@ __global__ __launch_bounds__(kWinThreads) void fwd_win_kernel(
                 pack_bf16(s[kb], 8 * c));
     }
   }
-  l += __shfl_xor(l, 32);
+  l = halves_sum(l);
   if (!qvalid) return;
   const float inv = 1.0f / l;
   bf16* orow = o + wt.tok(g, qi) * g.C + hoff;
@@ -424,13 +424,15 @@ __global__ __launch_bounds__(kPairThreads, 4) void fwd_win_pair_kernel(
               for (int r = 0; r < 16; ++r) mr = fmaxf(mr, s[j][r]);
             }
           }
-          mr = fmaxf(mr, __shfl_xor(mr, 32));
+          mr = halves_max(mr);
           const float mnew = fmaxf(m, mr * scale_log2);
           const float mref = mnew == -INFINITY ? 0.0f : mnew;   // nothing allowed yet
-          const float alpha = __builtin_amdgcn_exp2f(m - mref);
-          l *= alpha;
+          if (hb > 0) {   // the first half starts from l = 0, O = 0
+            const float alpha = __builtin_amdgcn_exp2f(m - mref);
+            l *= alpha;
 #pragma unroll
-          for (int r = 0; r < 16; ++r) oacc[r] *= alpha;
+            for (int r = 0; r < 16; ++r) oacc[r] *= alpha;
+          }
           m = mnew;
 #pragma unroll
           for (int j = 0; j < 2; ++j) {
@@ -449,7 +451,7 @@ __global__ __launch_bounds__(kPairThreads, 4) void fwd_win_pair_kernel(
           }
         }
       }
-      l += __shfl_xor(l, 32);
+      l = halves_sum(l);
     }
     __syncthreads();   // every wave has read its Q rows; qs now takes O
     if (active) {
@@ -658,7 +660,7 @@ __device__ __forceinline__ void bwd_window_body(BwdWave& st, int qw, f32x4 (&dta
   TERRA_DSUM(2)
   TERRA_DSUM(3)
 #undef TERRA_DSUM
-  st.D = dsum + __shfl_xor(dsum, 32);
+  st.D = halves_sum(dsum);
   __syncthreads();   // K^T of every key block is in LDS; Q, dO staging is dead
   switch (qw) {
     case 0: bwd_rotation<0, QUAD, MASK>(st, dta, dtb, dqacc); break;

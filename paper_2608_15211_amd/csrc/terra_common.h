@@ -59,6 +59,25 @@ __host__ inline void set_col_recips(Geo& g) {
   g.rcols[1] = 1.0f / (float)win_cols(g, g.Mw - 1);
 }
 
+// Sum and maximum over the two 32-lane halves of a wave, in every lane:
+// swapping the upper half of x with the lower half of a copy of x leaves
+// the lower half's value in one and the upper half's in the other.  Written
+// as assembly (with wait states around it) because the compiler folds the
+// two results of the built-in swap of equal operands into one.
+__device__ __forceinline__ float2 halves_pair(float x) {
+  float y = x;
+  asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1\n\ts_nop 1" : "+v"(x), "+v"(y));
+  return float2{x, y};
+}
+__device__ __forceinline__ float halves_sum(float x) {
+  const float2 p = halves_pair(x);
+  return p.x + p.y;
+}
+__device__ __forceinline__ float halves_max(float x) {
+  const float2 p = halves_pair(x);
+  return fmaxf(p.x, p.y);
+}
+
 // Reciprocal of the width of window column j.
 __device__ inline float win_rcols(const Geo& g, int j) { return j == g.Mw - 1 ? g.rcols[1] : g.rcols[0]; }
 // First window-major slot of window (i, j) within its image: all window rows
