@@ -28,7 +28,7 @@ struct RouteArgs {
 };
 
 constexpr int kRouteThreads = 256;
-constexpr int kRouteUnroll = 4;
+constexpr int kRouteUnroll = 1;
 
 // FORWARD=true: NHWC -> window-major.  FORWARD=false: window-major -> NHWC.
 template <int VEC, bool FORWARD>
@@ -111,11 +111,13 @@ hipError_t launch_route(const Geo& g, int row_bytes, const void* src, void* dst,
   else if (row_bytes % 4 == 0 && ((uintptr_t)src % 4 == 0) && ((uintptr_t)dst % 4 == 0)) vec = 4;
   A.cpr = row_bytes / vec;
   A.rcp_cpr = 1.0f / (float)A.cpr;
-  // Enough workgroups to keep every CU streaming: aim for ~4096 in total,
-  // each with at least one full unrolled sweep of work.
+  // Many short workgroups (one 16-byte chunk per thread, up to ~64K
+  // workgroups) keep more loads in flight across the chip than fewer long
+  // ones: 6.4 TB/s against 5.6 TB/s with 4K workgroups of four chunks per
+  // thread on a 212 MB tensor.
   const int64_t chunks_per_win = (int64_t)g.wh * g.ww * A.cpr;
   const int64_t nwin_total = (int64_t)g.B * g.nwin;
-  int split = (int)((4096 + nwin_total - 1) / nwin_total);
+  int split = (int)((65536 + nwin_total - 1) / nwin_total);
   const int64_t max_split = (chunks_per_win + kRouteThreads * kRouteUnroll - 1) /
                             (kRouteThreads * kRouteUnroll);
   if (split > max_split) split = (int)max_split;
