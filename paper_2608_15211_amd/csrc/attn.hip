@@ -438,9 +438,12 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
         }
       }
       // Bias bins: each wave adds into its own copy, and the two lane halves
-      // add with separate instructions (within one half, lanes hold distinct
-      // queries of the same key, hence distinct bins), so every bin receives
-      // its additions in program order.  When every window width is a
+      // add with separate instructions.  Within one half, lanes hold distinct
+      // queries of the same key, hence distinct bins, so the additions are
+      // plain read-modify-writes (an LDS float atomic costs about three
+      // clocks per lane, some 170 times a store) and every bin receives them
+      // in program order; lanes with nothing to add (padding queries,
+      // excluded pairs) stay out.  When every window width is a
       // multiple of 4, registers 4g..4g+3 hold four consecutive keys k..k+3
       // of one window row and (q, k+x), (q+1, k+x+1) share a bin.  Within a
       // run of consecutive lanes holding consecutive queries of one window
@@ -475,13 +478,13 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
               for (int g4 = 0; g4 < 4; ++g4) {
                 const int kk = kb * 32 + 8 * g4 + 4 * half;
                 if (fa[kb][g4] != 0.0f)
-                  atomicAdd(&mybins[qoff - (kinfo[kk] & 0xFFFFFF)], fa[kb][g4]);
+                  mybins[qoff - (kinfo[kk] & 0xFFFFFF)] += fa[kb][g4];
                 if (fb[kb][g4] != 0.0f)
-                  atomicAdd(&mybins[qoff - (kinfo[kk + 3] & 0xFFFFFF)], fb[kb][g4]);
+                  mybins[qoff - (kinfo[kk + 3] & 0xFFFFFF)] += fb[kb][g4];
 #pragma unroll
                 for (int x = 1; x < 3; ++x)
                   if (run < x && rest < 3 - x && dsb[kb][4 * g4 + x] != 0.0f)
-                    atomicAdd(&mybins[qoff - (kinfo[kk + x] & 0xFFFFFF)], dsb[kb][4 * g4 + x]);
+                    mybins[qoff - (kinfo[kk + x] & 0xFFFFFF)] += dsb[kb][4 * g4 + x];
               }
           }
           __builtin_amdgcn_wave_barrier();
@@ -495,7 +498,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
 #pragma unroll
               for (int r = 0; r < 16; ++r) {
                 const int inf = kinfo[kb * 32 + acc_row(r, half)];
-                if (dsb[kb][r] != 0.0f) atomicAdd(&mybins[qoff - (inf & 0xFFFFFF)], dsb[kb][r]);
+                if (dsb[kb][r] != 0.0f) mybins[qoff - (inf & 0xFFFFFF)] += dsb[kb][r];
               }
           }
           __builtin_amdgcn_wave_barrier();
