@@ -755,26 +755,30 @@ __global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
   int acc_cols = 0;
   // Register (kb, g4) of lane q holds, in dta, the bin of (q, k) with k the
   // group's first key, and in dtb (query columns 0..2 only) the bin of
-  // (q, k+3); hh is made opaque so that the bins are not hoisted out of the
-  // window loop into live registers.
+  // (q, k+3).  The two lane halves flush with separate instructions: within
+  // one half the lanes hold distinct queries of the same key, hence distinct
+  // bins, so the additions are plain read-modify-writes in program order (an
+  // LDS float atomic costs about three clocks per lane).
 #define TERRA_FLUSH_DT(cw)                                                              \
   {                                                                                     \
     const float rcw = 1.0f / (float)(cw);                                               \
     const int aq = (int)(((float)qi + 0.5f) * rcw), cq = qi - aq * (cw);                \
-    int hh = half;                                                                      \
-    asm volatile("" : "+v"(hh));                                                        \
-    _Pragma("unroll") for (int kb = 0; kb < 4; ++kb)                                    \
-    _Pragma("unroll") for (int g4 = 0; g4 < 4; ++g4) {                                  \
-      const int kk = 32 * kb + 8 * g4 + 4 * hh;                                         \
-      const int ak = (int)(((float)kk + 0.5f) * rcw), ck = kk - ak * (cw);              \
-      if (aq < g.wh && ak < g.wh) {                                                     \
-        const int bin = g.nbins - 1 - ((aq - ak + g.wh - 1) * g.bstride + (cq - ck + g.ww - 1)); \
-        atomicAdd(&mybins[bin], dta[kb][g4]);                                           \
-        if (cq < 3) atomicAdd(&mybins[bin + 3], dtb[kb][g4]);                           \
+    _Pragma("unroll 1") for (int hh = 0; hh < 2; ++hh) {                                \
+      if (half == hh) {                                                                 \
+        _Pragma("unroll") for (int kb = 0; kb < 4; ++kb)                                \
+        _Pragma("unroll") for (int g4 = 0; g4 < 4; ++g4) {                              \
+          const int kk = 32 * kb + 8 * g4 + 4 * hh;                                     \
+          const int ak = (int)(((float)kk + 0.5f) * rcw), ck = kk - ak * (cw);          \
+          if (aq < g.wh && ak < g.wh) {                                                 \
+            const int bin = g.nbins - 1 - ((aq - ak + g.wh - 1) * g.bstride + (cq - ck + g.ww - 1)); \
+            mybins[bin] += dta[kb][g4];                                                 \
+            if (cq < 3) mybins[bin + 3] += dtb[kb][g4];                                 \
+          }                                                                             \
+        }                                                                               \
       }                                                                                 \
-      dta[kb][g4] = 0.0f;                                                               \
-      dtb[kb][g4] = 0.0f;                                                               \
+      __builtin_amdgcn_wave_barrier();                                                  \
     }                                                                                   \
+    _Pragma("unroll") for (int kb = 0; kb < 4; ++kb) dta[kb] = dtb[kb] = f32x4{0.f, 0.f, 0.f, 0.f}; \
   }
 
   const int total = g.B * g.nwin;
