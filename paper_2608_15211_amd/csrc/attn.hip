@@ -60,6 +60,37 @@ __device__ __host__ constexpr int tr_row(int e) { return e * (tile_of<T, HD>() +
 template <typename T, int HD>
 __device__ __host__ constexpr int tr_size() { return tr_row<T, HD>(HD); }
 
+// 16-bit V tiles stay row-major and give their transposed operands through
+// the LDS transpose read: in each 16-lane group G of that read, lane i
+// receives element i % 4 of the 8 bytes addressed by lane 16 G + 4 x + i / 4,
+// x = 0..3.  Row stride 16 mod 64 dwords, so the 4 rows x 64 bytes of two
+// groups fall in distinct LDS banks.
+template <int HD> constexpr int tr16_stride() { return HD == 32 ? 32 : HD == 64 ? 96 : 160; }
+template <typename T, int HD>
+__device__ __host__ constexpr int vtile_size() {
+  return sizeof(T) == 2 ? tile_of<T, HD>() * tr16_stride<HD>() : tr_size<T, HD>();
+}
+
+// Transposed operand of channel block eb, key block kb, chunk c2 from a
+// row-major 16-bit tile V: lane (channel col, half) receives
+// V[32 kb + 16 c2 + 4 half + x][32 eb + col] and the same 8 rows further,
+// x = 0..3 (the slot order of load_op_lds_perm).  Lane L therefore
+// addresses row 32 kb + 16 c2 + 4 (G / 2) + (L / 4) % 4, channels
+// 32 eb + 16 (G % 2) + 4 (L % 4).
+template <typename T, int HD>
+__device__ inline typename Operand<T>::type lds_tr_op(const T* V, int kb, int c2, int eb, int lane) {
+  typedef short v4s __attribute__((ext_vector_type(4)));
+  typedef short v8s __attribute__((ext_vector_type(8)));
+  typedef __attribute__((address_space(3))) v4s lds_v4s;
+  constexpr int VS = tr16_stride<HD>();
+  const int G = lane >> 4, x = (lane >> 2) & 3, m = lane & 3;
+  const T* p = V + (32 * kb + 16 * c2 + 4 * (G >> 1) + x) * VS + 32 * eb + 16 * (G & 1) + 4 * m;
+  const v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)p);
+  const v4s hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(p + 8 * VS));
+  const v8s o = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  return __builtin_bit_cast(typename Operand<T>::type, o);
+}
+
 // Slot s (0..7) of lane half h inside a 16-deep contraction chunk, when the
 // operand comes from 32x32 result registers 8c..8c+7: row acc_row(s, h).
 __device__ inline int perm_slot(int s, int h) { return 8 * (s / 4) + 4 * h + (s % 4); }
@@ -117,6 +148,18 @@ __device__ inline void tile_load(TileRegs<T, HD>& t, const T* __restrict__ src, 
   }
 }
 
+// Row-major store of a staged tile with row stride RS elements.
+template <typename T, int HD, int RS>
+__device__ inline void tile_store_rows(const TileRegs<T, HD>& t, T* lds) {
+  constexpr int kCpr = TileRegs<T, HD>::kCpr;
+#pragma unroll
+  for (int u = 0; u < TileRegs<T, HD>::kPer; ++u) {
+    const int idx = threadIdx.x + u * kThreads;
+    const int rr = idx / kCpr, ch = idx % kCpr;
+    *reinterpret_cast<uint4*>(lds + rr * RS + ch * (16 / (int)sizeof(T))) = t.r[u];
+  }
+}
+
 template <typename T, int HD, bool ROWMAJOR, bool TRANS>
 __device__ inline void tile_store(const TileRegs<T, HD>& t, T* lds_rm, T* lds_tr) {
   constexpr int kTile = tile_of<T, HD>();
@@ -159,8 +202,8 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(
   constexpr int kTile = tile_of<T, HD>();
   extern __shared__ __align__(16) char smem[];
   T* kt = reinterpret_cast<T*>(smem);                          // [kTile][HD+kPad]
-  T* vt = kt + kTile * (HD + kPad);                            // [HD][kTile+kPad]
-  int* kinfo = reinterpret_cast<int*>(vt + tr_size<T, HD>());
+  T* vt = kt + kTile * (HD + kPad);                            // V^T, or V rows (16-bit)
+  int* kinfo = reinterpret_cast<int*>(vt + vtile_size<T, HD>());
   float* tab = reinterpret_cast<float*>(kinfo + kTile);        // [nbins+4], reversed
 
   int bid = blockIdx.x;
@@ -214,7 +257,8 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(
     }
     __syncthreads();
     tile_store<T, HD, true, false>(rk, kt, nullptr);
-    tile_store<T, HD, false, true>(rv, nullptr, vt);
+    if (sizeof(T) == 2) tile_store_rows<T, HD, tr16_stride<HD>()>(rv, vt);
+    else tile_store<T, HD, false, true>(rv, nullptr, vt);
     if (threadIdx.x < kTile) kinfo[threadIdx.x] = token_info(g, i, j, cols, k0 + threadIdx.x, n);
     __syncthreads();
     if (kPrefetch && k0 + kTile < n) {
@@ -256,8 +300,12 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(
       for (int kb = 0; kb < kTile / 32; ++kb) {
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
-          const T* row = vt + tr_row<T, HD>(eb * 32 + col) + kb * 32 + 16 * c;
-          mma16(oacc[eb], load_op_lds_perm<T>(row, half), pack8<T>(s[kb], 8 * c));
+          if constexpr (sizeof(T) == 2) {
+            mma16(oacc[eb], lds_tr_op<T, HD>(vt, kb, c, eb, lane), pack8<T>(s[kb], 8 * c));
+          } else {
+            const T* row = vt + tr_row<T, HD>(eb * 32 + col) + kb * 32 + 16 * c;
+            mma16(oacc[eb], load_op_lds_perm<T>(row, half), pack8<T>(s[kb], 8 * c));
+          }
         }
       }
     }
@@ -700,7 +748,7 @@ int bwd_nslice(const Geo& g) {
 template <typename T, int HD>
 static size_t fwd_lds(const Geo& g) {
   constexpr int kTile = tile_of<T, HD>();
-  return sizeof(T) * (kTile * (HD + kPad) + tr_size<T, HD>()) + 4 * kTile + 4 * (g.nbins + 4);
+  return sizeof(T) * (kTile * (HD + kPad) + vtile_size<T, HD>()) + 4 * kTile + 4 * (g.nbins + 4);
 }
 template <typename T, int HD>
 static size_t dq_lds(const Geo& g) {
