@@ -70,19 +70,22 @@ template <typename T, int HD>
 __device__ __host__ constexpr int vtile_size() {
   return sizeof(T) == 2 ? tile_of<T, HD>() * tr16_stride<HD>() : tr_size<T, HD>();
 }
+// Transposed copy of a tile: needed for fp32 only (16-bit tiles are read
+// transposed straight from their row-major copy).
+template <typename T, int HD>
+__device__ __host__ constexpr int ttile_size() { return sizeof(T) == 2 ? 0 : tr_size<T, HD>(); }
 
 // Transposed operand of channel block eb, key block kb, chunk c2 from a
-// row-major 16-bit tile V: lane (channel col, half) receives
+// row-major 16-bit tile V of row stride RS: lane (channel col, half) receives
 // V[32 kb + 16 c2 + 4 half + x][32 eb + col] and the same 8 rows further,
 // x = 0..3 (the slot order of load_op_lds_perm).  Lane L therefore
 // addresses row 32 kb + 16 c2 + 4 (G / 2) + (L / 4) % 4, channels
 // 32 eb + 16 (G % 2) + 4 (L % 4).
-template <typename T, int HD>
+template <typename T, int VS>
 __device__ inline typename Operand<T>::type lds_tr_op(const T* V, int kb, int c2, int eb, int lane) {
   typedef short v4s __attribute__((ext_vector_type(4)));
   typedef short v8s __attribute__((ext_vector_type(8)));
   typedef __attribute__((address_space(3))) v4s lds_v4s;
-  constexpr int VS = tr16_stride<HD>();
   const int G = lane >> 4, x = (lane >> 2) & 3, m = lane & 3;
   const T* p = V + (32 * kb + 16 * c2 + 4 * (G >> 1) + x) * VS + 32 * eb + 16 * (G & 1) + 4 * m;
   const v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)p);
@@ -301,7 +304,7 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
           if constexpr (sizeof(T) == 2) {
-            mma16(oacc[eb], lds_tr_op<T, HD>(vt, kb, c, eb, lane), pack8<T>(s[kb], 8 * c));
+            mma16(oacc[eb], lds_tr_op<T, tr16_stride<HD>()>(vt, kb, c, eb, lane), pack8<T>(s[kb], 8 * c));
           } else {
             const T* row = vt + tr_row<T, HD>(eb * 32 + col) + kb * 32 + 16 * c;
             mma16(oacc[eb], load_op_lds_perm<T>(row, half), pack8<T>(s[kb], 8 * c));
@@ -344,8 +347,8 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
   extern __shared__ __align__(16) char smem[];
   T* kt = reinterpret_cast<T*>(smem);                 // K  [kTile][HD+kPad]
   T* vr = kt + kTile * (HD + kPad);                   // V  [kTile][HD+kPad]
-  T* ktt = vr + kTile * (HD + kPad);                  // K^T (transposed tile)
-  int* kinfo = reinterpret_cast<int*>(ktt + tr_size<T, HD>());
+  T* ktt = vr + kTile * (HD + kPad);                  // K^T (transposed tile, fp32)
+  int* kinfo = reinterpret_cast<int*>(ktt + ttile_size<T, HD>());
   float* tab = reinterpret_cast<float*>(kinfo + kTile);   // [nbins+4], reversed
   float* dtab = tab + g.nbins + 4;                    // [4][nbins], one per wave
 
@@ -453,7 +456,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
         tile_load(rv, v, g, wt, k0, n, hoff);
       }
       __syncthreads();
-      tile_store<T, HD, true, true>(rk, kt, ktt);
+      tile_store<T, HD, true, sizeof(T) == 4>(rk, kt, ktt);
       tile_store<T, HD, true, false>(rv, vr, nullptr);
       if (threadIdx.x < kTile) kinfo[threadIdx.x] = token_info(g, i, j, cols, k0 + threadIdx.x, n);
       __syncthreads();
@@ -480,8 +483,12 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
         for (int eb = 0; eb < HD / 32; ++eb) {
 #pragma unroll
           for (int c = 0; c < 2; ++c) {
-            const T* row = ktt + tr_row<T, HD>(eb * 32 + col) + kb * 32 + 16 * c;
-            mma16(dqacc[eb], load_op_lds_perm<T>(row, half), pack8<T>(dsb[kb], 8 * c));
+            if constexpr (sizeof(T) == 2) {
+              mma16(dqacc[eb], lds_tr_op<T, HD + kPad>(kt, kb, c, eb, lane), pack8<T>(dsb[kb], 8 * c));
+            } else {
+              const T* row = ktt + tr_row<T, HD>(eb * 32 + col) + kb * 32 + 16 * c;
+              mma16(dqacc[eb], load_op_lds_perm<T>(row, half), pack8<T>(dsb[kb], 8 * c));
+            }
           }
         }
       }
@@ -585,9 +592,9 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(
   extern __shared__ __align__(16) char smem[];
   T* qr = reinterpret_cast<T*>(smem);                 // Q  [kTile][HD+kPad]
   T* dr = qr + kTile * (HD + kPad);                   // dO [kTile][HD+kPad]
-  T* qtt = dr + kTile * (HD + kPad);                  // Q^T (transposed tile)
-  T* dtt = qtt + tr_size<T, HD>();                   // dO^T
-  int* qinfo = reinterpret_cast<int*>(dtt + tr_size<T, HD>());
+  T* qtt = dr + kTile * (HD + kPad);                  // Q^T (transposed tile, fp32)
+  T* dtt = qtt + ttile_size<T, HD>();                // dO^T (fp32)
+  int* qinfo = reinterpret_cast<int*>(dtt + ttile_size<T, HD>());
   float* ql = reinterpret_cast<float*>(qinfo + kTile);   // lse2 per query
   float* qd = ql + kTile;                                 // D per query
   float* tab = qd + kTile;                                // [nbins+4], forward order
@@ -642,8 +649,8 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(
       tile_load(rd, dout, g, wt, t0, n, hoff);
     }
     __syncthreads();
-    tile_store<T, HD, true, true>(rq, qr, qtt);
-    tile_store<T, HD, true, true>(rd, dr, dtt);
+    tile_store<T, HD, true, sizeof(T) == 4>(rq, qr, qtt);
+    tile_store<T, HD, true, sizeof(T) == 4>(rd, dr, dtt);
     if (threadIdx.x < kTile) {
       const int t = t0 + threadIdx.x;
       const int inf = token_info(g, i, j, cols, t, n);
@@ -690,11 +697,16 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(
       for (int eb = 0; eb < HD / 32; ++eb) {
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
-          const int cofs = qb * 32 + 16 * c;
-          mma16(dvacc[eb], load_op_lds_perm<T>(dtt + tr_row<T, HD>(eb * 32 + col) + cofs, half),
-                pack8<T>(s, 8 * c));
-          mma16(dkacc[eb], load_op_lds_perm<T>(qtt + tr_row<T, HD>(eb * 32 + col) + cofs, half),
-                pack8<T>(ds, 8 * c));
+          if constexpr (sizeof(T) == 2) {
+            mma16(dvacc[eb], lds_tr_op<T, HD + kPad>(dr, qb, c, eb, lane), pack8<T>(s, 8 * c));
+            mma16(dkacc[eb], lds_tr_op<T, HD + kPad>(qr, qb, c, eb, lane), pack8<T>(ds, 8 * c));
+          } else {
+            const int cofs = qb * 32 + 16 * c;
+            mma16(dvacc[eb], load_op_lds_perm<T>(dtt + tr_row<T, HD>(eb * 32 + col) + cofs, half),
+                  pack8<T>(s, 8 * c));
+            mma16(dkacc[eb], load_op_lds_perm<T>(qtt + tr_row<T, HD>(eb * 32 + col) + cofs, half),
+                  pack8<T>(ds, 8 * c));
+          }
         }
       }
     }
@@ -753,13 +765,13 @@ static size_t fwd_lds(const Geo& g) {
 template <typename T, int HD>
 static size_t dq_lds(const Geo& g) {
   constexpr int kTile = tile_of<T, HD>();
-  return sizeof(T) * (2 * kTile * (HD + kPad) + tr_size<T, HD>()) + 4 * kTile + 4 * (g.nbins + 4) +
+  return sizeof(T) * (2 * kTile * (HD + kPad) + ttile_size<T, HD>()) + 4 * kTile + 4 * (g.nbins + 4) +
          16 * g.nbins;
 }
 template <typename T, int HD>
 static size_t dkdv_lds(const Geo& g) {
   constexpr int kTile = tile_of<T, HD>();
-  return sizeof(T) * (2 * kTile * (HD + kPad) + 2 * tr_size<T, HD>()) + 12 * kTile + 4 * (g.nbins + 4);
+  return sizeof(T) * (2 * kTile * (HD + kPad) + 2 * ttile_size<T, HD>()) + 12 * kTile + 4 * (g.nbins + 4);
 }
 
 template <typename T, int HD, bool NHWC>
