@@ -75,25 +75,6 @@ __device__ __host__ constexpr int vtile_size() {
 template <typename T, int HD>
 __device__ __host__ constexpr int ttile_size() { return sizeof(T) == 2 ? 0 : tr_size<T, HD>(); }
 
-// Transposed operand of channel block eb, key block kb, chunk c2 from a
-// row-major 16-bit tile V of row stride RS: lane (channel col, half) receives
-// V[32 kb + 16 c2 + 4 half + x][32 eb + col] and the same 8 rows further,
-// x = 0..3 (the slot order of load_op_lds_perm).  Lane L therefore
-// addresses row 32 kb + 16 c2 + 4 (G / 2) + (L / 4) % 4, channels
-// 32 eb + 16 (G % 2) + 4 (L % 4).
-template <typename T, int VS>
-__device__ inline typename Operand<T>::type lds_tr_op(const T* V, int kb, int c2, int eb, int lane) {
-  typedef short v4s __attribute__((ext_vector_type(4)));
-  typedef short v8s __attribute__((ext_vector_type(8)));
-  typedef __attribute__((address_space(3))) v4s lds_v4s;
-  const int G = lane >> 4, x = (lane >> 2) & 3, m = lane & 3;
-  const T* p = V + (32 * kb + 16 * c2 + 4 * (G >> 1) + x) * VS + 32 * eb + 16 * (G & 1) + 4 * m;
-  const v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)p);
-  const v4s hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(p + 8 * VS));
-  const v8s o = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-  return __builtin_bit_cast(typename Operand<T>::type, o);
-}
-
 // Slot s (0..7) of lane half h inside a 16-deep contraction chunk, when the
 // operand comes from 32x32 result registers 8c..8c+7: row acc_row(s, h).
 __device__ inline int perm_slot(int s, int h) { return 8 * (s / 4) + 4 * h + (s % 4); }

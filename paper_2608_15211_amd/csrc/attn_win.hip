@@ -329,14 +329,15 @@ __global__ __launch_bounds__(kPairThreads, 4) void fwd_win_pair_kernel(
     const float* __restrict__ table, bf16* __restrict__ o, float* __restrict__ lse, Geo g,
     int per_slice, float scale_log2) {
   constexpr int HD = 32;
-  // V^T rows of 132 elements, the second head 16 elements further: the
-  // staging stores of one instruction then fall in distinct LDS banks
-  constexpr int KS = HD + 8, VS = kWinMax + 4, VH = HD * VS + 16;
+  // V stays row-major (64-byte rows): its transposed operands come through
+  // the LDS transpose read, 4 rows x 64 bytes of two lane groups in
+  // distinct banks
+  constexpr int KS = HD + 8, VH = kWinMax * HD;
   extern __shared__ __align__(16) char smem[];
   bf16* ks = reinterpret_cast<bf16*>(smem);                        // [2][128][KS] K rows
   bf16* qs = ks + 2 * kWinMax * KS;                                // [2][128][KS] Q rows, then O
-  bf16* vts = qs + 2 * kWinMax * KS;                               // [2][VH]  V^T
-  int* kinfo = reinterpret_cast<int*>(vts + 2 * VH);               // [128]
+  bf16* vrs = qs + 2 * kWinMax * KS;                               // [2][128][HD] V rows
+  int* kinfo = reinterpret_cast<int*>(vrs + 2 * VH);               // [128]
   float* tab = reinterpret_cast<float*>(kinfo + kWinMax);          // [2][ntab+4]
 
   const int hpairs = g.heads >> 1;
@@ -350,7 +351,7 @@ __global__ __launch_bounds__(kPairThreads, 4) void fwd_win_pair_kernel(
   const int h = 2 * hp + hs;
   const int qi = 32 * qb + col;
   const bf16* ksh = ks + hs * kWinMax * KS;
-  const bf16* vth = vts + hs * VH;
+  const bf16* vth = vrs + hs * VH;
   const float* tabh = tab + hs * (g.ntab + 4);
 
   // bias tables of the pair times sqrt(hd), reversed, then four -inf
@@ -383,9 +384,7 @@ __global__ __launch_bounds__(kPairThreads, 4) void fwd_win_pair_kernel(
       const int t = ch >> 2, e0 = (ch & 3) * 8;
       *reinterpret_cast<uint4*>(ks + (t * kWinMax + row) * KS + e0) = rows.k[u];
       *reinterpret_cast<uint4*>(qs + (t * kWinMax + row) * KS + e0) = rows.q[u];
-      const bf16* ve = reinterpret_cast<const bf16*>(&rows.v[u]);
-#pragma unroll
-      for (int x = 0; x < 8; ++x) vts[t * VH + (e0 + x) * VS + row] = ve[x];
+      *reinterpret_cast<uint4*>(vrs + t * VH + row * HD + e0) = rows.v[u];
     }
     if (threadIdx.x < kWinMax) kinfo[threadIdx.x] = win_token_info(g, wi, wj, cols, threadIdx.x, n);
     __syncthreads();
@@ -446,7 +445,7 @@ __global__ __launch_bounds__(kPairThreads, 4) void fwd_win_pair_kernel(
               }
 #pragma unroll
               for (int c = 0; c < 2; ++c)
-                mma16(oacc, lds_perm_op(vth + col * VS + 32 * kb + 16 * c, half), pack_bf16(s[j], 8 * c));
+                mma16(oacc, lds_tr_op<bf16, HD>(vth, kb, c, 0, lane), pack_bf16(s[j], 8 * c));
             }
           }
         }
@@ -945,8 +944,7 @@ static void fwd_win_go(const Geo& g, const void* q, const void* k, const void* v
 }
 
 size_t win_fwd_pair_lds(const Geo& g) {
-  return sizeof(bf16) * 2 * (2 * kWinMax * (32 + 8) + 32 * (kWinMax + 4) + 16) + 4 * kWinMax +
-         4 * 2 * (g.ntab + 4);
+  return sizeof(bf16) * 2 * (2 * kWinMax * (32 + 8) + kWinMax * 32) + 4 * kWinMax + 4 * 2 * (g.ntab + 4);
 }
 
 // Slices of the window range per head pair of the forward: one round of

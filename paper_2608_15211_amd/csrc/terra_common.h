@@ -221,6 +221,27 @@ template <> struct Operand<__bf16> { typedef bf16x8 type; };
 template <> struct Operand<_Float16> { typedef f16x8 type; };
 template <> struct Operand<float> { typedef f32x8 type; };
 
+// Transposed operand of channel block eb, key block kb, chunk c2 from a
+// row-major 16-bit tile V in LDS of row stride VS (elements): lane
+// (channel col, half) receives V[32 kb + 16 c2 + 4 half + x][32 eb + col]
+// and the same 8 rows further, x = 0..3 (two runs of 4 keys, the slot order
+// of the 32x32 result registers).  In each 16-lane group G of the LDS
+// transpose read, lane i receives element i % 4 of the 8 bytes addressed by
+// lane 16 G + 4 x + i / 4, x = 0..3; so lane L addresses row
+// 32 kb + 16 c2 + 4 (G / 2) + (L / 4) % 4, channels 32 eb + 16 (G % 2) + 4 (L % 4).
+template <typename T, int VS>
+__device__ inline typename Operand<T>::type lds_tr_op(const T* V, int kb, int c2, int eb, int lane) {
+  typedef short v4s __attribute__((ext_vector_type(4)));
+  typedef short v8s __attribute__((ext_vector_type(8)));
+  typedef __attribute__((address_space(3))) v4s lds_v4s;
+  const int G = lane >> 4, x = (lane >> 2) & 3, m = lane & 3;
+  const T* p = V + (32 * kb + 16 * c2 + 4 * (G >> 1) + x) * VS + 32 * eb + 16 * (G & 1) + 4 * m;
+  const v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)p);
+  const v4s hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(p + 8 * VS));
+  const v8s o = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  return __builtin_bit_cast(typename Operand<T>::type, o);
+}
+
 __device__ inline void mma16(f32x16& acc, const bf16x8& a, const bf16x8& b) {
   acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc, 0, 0, 0);
 }
