@@ -484,7 +484,6 @@ __global__ __launch_bounds__(kPairThreads, 4) void fwd_win_pair_kernel(
 constexpr int kBwdHD = 32;
 constexpr int kBwdKS = kBwdHD + 8;     // LDS row stride (bf16) of K, V, Q, dO rows
 constexpr int kBwdRS = kWinMax + 4;    // LDS row stride (fp32) of the dV, dK sums
-constexpr int kBwdTS = kWinMax + 8;    // LDS row stride (bf16) of K^T
 constexpr int kBwdCPR = kBwdHD / 8;    // 16-byte chunks per token row of one head
 
 // Token row of 16-byte chunk idx (chunk idx % 4 of its row) in the
@@ -517,7 +516,6 @@ __device__ __forceinline__ FoldMask fold_mask(int cq, int cols) {
 struct BwdWave {
   const bf16* ks;       // K rows in LDS [128][KS]
   const bf16* vs;       // V rows [128][KS]
-  const bf16* kts;      // K^T [HD][128+8]
   const int* kinfo;     // key words of the window
   const float* tab;     // bias table times sqrt(hd), reversed, then -inf
   float* redv;          // dV partial sums [HD][RS]
@@ -584,7 +582,8 @@ __device__ __forceinline__ f32x16 bwd_dp(const BwdWave& st, float init) {
 
 // One rotation step: key block KB.  P and dP are recomputed (so that P does
 // not occupy 64 registers across the steps), dS = P (dP - D) goes into the
-// bias accumulators and into dQ += dS K (K^T from LDS); P^T and dS^T (by
+// bias accumulators and into dQ += dS K (K^T operands by the LDS transpose
+// read of the K rows); P^T and dS^T (by
 // matrix-core transpose) times dO and Q give the block's dV and dK partials,
 // which are added to the running sums in LDS through the accumulator input.
 // Step T = 0 starts the sums.
@@ -602,8 +601,9 @@ __device__ __forceinline__ void bwd_step(const BwdWave& st, f32x4& dta, f32x4& d
     pb0 = pack_bf16(p, 0); pb1 = pack_bf16(p, 8);
     db0 = pack_bf16(ds, 0); db1 = pack_bf16(ds, 8);
   }
-  mma16(dqacc, lds_perm_op(st.kts + st.col * kBwdTS + 32 * KB, st.half), db0);
-  mma16(dqacc, lds_perm_op(st.kts + st.col * kBwdTS + 32 * KB + 16, st.half), db1);
+  const int lane = threadIdx.x & 63;
+  mma16(dqacc, lds_tr_op<bf16, kBwdKS>(st.ks, KB, 0, 0, lane), db0);
+  mma16(dqacc, lds_tr_op<bf16, kBwdKS>(st.ks, KB, 1, 0, lane), db1);
 #pragma unroll
   for (int which = 0; which < 2; ++which) {
     const bf16x8 ip0 = ident_op<true>(0), ip1 = ident_op<true>(1);
@@ -660,7 +660,7 @@ __device__ __forceinline__ void bwd_window_body(BwdWave& st, int qw, f32x4 (&dta
   TERRA_DSUM(3)
 #undef TERRA_DSUM
   st.D = halves_sum(dsum);
-  __syncthreads();   // K^T of every key block is in LDS; Q, dO staging is dead
+  __syncthreads();   // every wave has its Q and dO operands; the staging is dead
   switch (qw) {
     case 0: bwd_rotation<0, QUAD, MASK>(st, dta, dtb, dqacc); break;
     case 1: bwd_rotation<1, QUAD, MASK>(st, dta, dtb, dqacc); break;
@@ -725,8 +725,7 @@ __global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
   bf16x8* ident = reinterpret_cast<bf16x8*>(smem);              // [2][64]
   bf16* ks = reinterpret_cast<bf16*>(ident + 2 * 64);           // [128][KS] K rows, then dQ
   bf16* vs = ks + kWinMax * KS;                                 // [128][KS] V rows
-  bf16* kts = vs + kWinMax * KS;                                // [HD][128+8] K^T
-  float* redv = reinterpret_cast<float*>(kts + HD * kBwdTS);    // [HD][RS] dV sums
+  float* redv = reinterpret_cast<float*>(vs + kWinMax * KS);    // [HD][RS] dV sums
   float* redk = redv + HD * RS;                                 // [HD][RS] dK sums
   int* kinfo = reinterpret_cast<int*>(redk + HD * RS);          // [128]
   float* tab = reinterpret_cast<float*>(kinfo + kWinMax);       // [ntab+4]
@@ -814,7 +813,6 @@ __global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
 
     st.ks = ks;
     st.vs = vs;
-    st.kts = kts;
     st.kinfo = kinfo;
     st.tab = tab;
     st.redv = redv;
@@ -827,16 +825,6 @@ __global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
     for (int c = 0; c < 2; ++c) {
       st.qop[c] = *reinterpret_cast<const bf16x8*>(qrows + qi * KS + 16 * c + 8 * half);
       st.dop[c] = *reinterpret_cast<const bf16x8*>(drows + qi * KS + 16 * c + 8 * half);
-    }
-    {
-      // K^T: wave qw transposes keys [32qw, 32qw+32)
-      const bf16* r = ks + qi * KS + 8 * half;
-      const f32x16 t = mfma_transpose(*reinterpret_cast<const bf16x8*>(r),
-                                      *reinterpret_cast<const bf16x8*>(r + 16),
-                                      lds_ident(ident, 0), lds_ident(ident, 1));
-#pragma unroll
-      for (int g4 = 0; g4 < 4; ++g4)
-        store4_bf16(kts + col * kBwdTS + 32 * qw + 8 * g4 + 4 * half, t, g4, 1.0f);
     }
     const int qinf = qi < n ? kinfo[qi] : 0;
     st.qlab = qinf >> 24;
@@ -929,7 +917,7 @@ size_t win_fwd_lds(const Geo& g) {
   return one;
 }
 size_t win_bwd_lds(const Geo& g) {
-  return 16 * 2 * 64 + sizeof(bf16) * (2 * kWinMax * kBwdKS + kBwdHD * kBwdTS) +
+  return 16 * 2 * 64 + sizeof(bf16) * (2 * kWinMax * kBwdKS) +
          sizeof(float) * 2 * kBwdHD * kBwdRS + 4 * kWinMax + 4 * (g.ntab + 4) + 4 * 4 * g.nbins;
 }
 
