@@ -484,6 +484,13 @@ __global__ __launch_bounds__(kPairThreads, 4) void fwd_win_pair_kernel(
 constexpr int kBwdHD = 32;
 constexpr int kBwdKS = kBwdHD + 8;     // LDS row stride (bf16) of K, V, Q, dO rows
 constexpr int kBwdRS = kWinMax + 4;    // LDS row stride (fp32) of the dV, dK sums
+constexpr int kBwdRed = 32 * kBwdRS + 16;   // floats of one sum array
+
+// Row of channel e in the dV/dK sum arrays: channels 16..31 sit 16 words
+// further, so that the output stage's transposing reads (16 token rows of
+// four 8-channel groups per instruction) fall in distinct LDS banks; the
+// rotation's 16-byte accesses of 16 channels stay in distinct banks too.
+__device__ __forceinline__ int red_row(int e) { return e * kBwdRS + (e >> 4) * 16; }
 constexpr int kBwdCPR = kBwdHD / 8;    // 16-byte chunks per token row of one head
 
 // Token row of 16-byte chunk idx (chunk idx % 4 of its row) in the
@@ -612,7 +619,7 @@ __device__ __forceinline__ void bwd_step(const BwdWave& st, f32x4& dta, f32x4& d
     f32x16 part;
 #pragma unroll
     for (int g4 = 0; g4 < 4; ++g4) {
-      const f32x4 a = T > 0 ? *reinterpret_cast<const f32x4*>(red + st.col * RS + 32 * KB + 8 * g4 + 4 * st.half)
+      const f32x4 a = T > 0 ? *reinterpret_cast<const f32x4*>(red + red_row(st.col) + 32 * KB + 8 * g4 + 4 * st.half)
                             : f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int x = 0; x < 4; ++x) part[4 * g4 + x] = a[x];
@@ -621,7 +628,7 @@ __device__ __forceinline__ void bwd_step(const BwdWave& st, f32x4& dta, f32x4& d
     mma16(part, pack_bf16(tr, 8), which == 0 ? st.de[1] : st.qe[1]);
 #pragma unroll
     for (int g4 = 0; g4 < 4; ++g4)
-      *reinterpret_cast<f32x4*>(red + st.col * RS + 32 * KB + 8 * g4 + 4 * st.half) =
+      *reinterpret_cast<f32x4*>(red + red_row(st.col) + 32 * KB + 8 * g4 + 4 * st.half) =
           f32x4{part[4 * g4], part[4 * g4 + 1], part[4 * g4 + 2], part[4 * g4 + 3]};
   }
 }
@@ -726,8 +733,8 @@ __global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
   bf16* ks = reinterpret_cast<bf16*>(ident + 2 * 64);           // [128][KS] K rows, then dQ
   bf16* vs = ks + kWinMax * KS;                                 // [128][KS] V rows
   float* redv = reinterpret_cast<float*>(vs + kWinMax * KS);    // [HD][RS] dV sums
-  float* redk = redv + HD * RS;                                 // [HD][RS] dK sums
-  int* kinfo = reinterpret_cast<int*>(redk + HD * RS);          // [128]
+  float* redk = redv + kBwdRed;                                 // [HD][RS] dK sums
+  int* kinfo = reinterpret_cast<int*>(redk + kBwdRed);          // [128]
   float* tab = reinterpret_cast<float*>(kinfo + kWinMax);       // [ntab+4]
   float* bins = tab + (g.ntab + 4);                             // [4][nbins], reversed
   bf16* qrows = reinterpret_cast<bf16*>(redv);                  // [128][KS] Q rows (staging)
@@ -858,8 +865,8 @@ __global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
         bf16x8 a, bb;
 #pragma unroll
         for (int x = 0; x < 8; ++x) {
-          a[x] = (bf16)redv[(c0 + x) * RS + row];
-          bb[x] = (bf16)(redk[(c0 + x) * RS + row] * scale);
+          a[x] = (bf16)redv[red_row(c0 + x) + row];
+          bb[x] = (bf16)(redk[red_row(c0 + x) + row] * scale);
         }
         *reinterpret_cast<bf16x8*>(dv + off) = a;
         *reinterpret_cast<bf16x8*>(dk + off) = bb;
@@ -918,7 +925,7 @@ size_t win_fwd_lds(const Geo& g) {
 }
 size_t win_bwd_lds(const Geo& g) {
   return 16 * 2 * 64 + sizeof(bf16) * (2 * kWinMax * kBwdKS) +
-         sizeof(float) * 2 * kBwdHD * kBwdRS + 4 * kWinMax + 4 * (g.ntab + 4) + 4 * 4 * g.nbins;
+         sizeof(float) * 2 * kBwdRed + 4 * kWinMax + 4 * (g.ntab + 4) + 4 * 4 * g.nbins;
 }
 
 
