@@ -467,8 +467,11 @@ __global__ __launch_bounds__(kPairThreads, 4) void fwd_win_pair_kernel(
       const int row = idx >> 3, ch = idx & 7;
       if (row < n) {
         const int t = ch >> 2, e0 = (ch & 3) * 8;
-        *reinterpret_cast<uint4*>(o + wt.tok(g, row) * g.C + cbase + ch * 8) =
-            *reinterpret_cast<const uint4*>(qs + (t * kWinMax + row) * KS + e0);
+        // streaming store: O is not read again by this path (the backward
+        // recomputes P), so it should not displace the inputs in the caches
+        typedef unsigned int u32x4n __attribute__((ext_vector_type(4)));
+        __builtin_nontemporal_store(*reinterpret_cast<const u32x4n*>(qs + (t * kWinMax + row) * KS + e0),
+                                    reinterpret_cast<u32x4n*>(o + wt.tok(g, row) * g.C + cbase + ch * 8));
       }
     }
   }
