@@ -591,26 +591,20 @@ __device__ __forceinline__ f32x16 bwd_dp(const BwdWave& st, float init) {
 }
 
 // One rotation step: key block KB.  P and dP are recomputed (so that P does
-// not occupy 64 registers across the steps), dS = P (dP - D) goes into the
-// bias accumulators and into dQ += dS K (K^T operands by the LDS transpose
-// read of the K rows); P^T and dS^T (by
-// matrix-core transpose) times dO and Q give the block's dV and dK partials,
-// which are added to the running sums in LDS through the accumulator input.
-// Step T = 0 starts the sums.
-template <int KB, int T, bool QUAD, bool MASK>
-__device__ __forceinline__ void bwd_step(const BwdWave& st, f32x4& dta, f32x4& dtb, f32x16& dqacc) {
-  constexpr int RS = kBwdRS;
+// not occupy 64 registers across the steps; step 0 takes them from the D
+// pass), dS = P (dP - D) goes into the bias accumulators and into
+// dQ += dS K (K^T operands by the LDS transpose read of the K rows); P^T and
+// dS^T (by matrix-core transpose) times dO and Q give the block's dV and dK
+// partials, which are added to the running sums in LDS through the
+// accumulator input.  Step T = 0 starts the sums.
+template <int KB, int T>
+__device__ __forceinline__ void bwd_step_tail(const BwdWave& st, const f32x16& p, const f32x16& ds, f32x4& dta,
+                                              f32x4& dtb, f32x16& dqacc) {
   bf16x8 pb0, pb1, db0, db1;
-  {
-    const f32x16 p = bwd_p<KB, QUAD, MASK>(st);
-    f32x16 ds = bwd_dp<KB>(st, -st.D);
 #pragma unroll
-    for (int r = 0; r < 16; ++r) ds[r] *= p[r];
-#pragma unroll
-    for (int g4 = 0; g4 < 4; ++g4) fold_diag(ds, g4, st.fold, dta, dtb);
-    pb0 = pack_bf16(p, 0); pb1 = pack_bf16(p, 8);
-    db0 = pack_bf16(ds, 0); db1 = pack_bf16(ds, 8);
-  }
+  for (int g4 = 0; g4 < 4; ++g4) fold_diag(ds, g4, st.fold, dta, dtb);
+  pb0 = pack_bf16(p, 0); pb1 = pack_bf16(p, 8);
+  db0 = pack_bf16(ds, 0); db1 = pack_bf16(ds, 8);
   const int lane = threadIdx.x & 63;
   mma16(dqacc, lds_tr_op<bf16, kBwdKS>(st.ks, KB, 0, 0, lane), db0);
   mma16(dqacc, lds_tr_op<bf16, kBwdKS>(st.ks, KB, 1, 0, lane), db1);
@@ -636,14 +630,42 @@ __device__ __forceinline__ void bwd_step(const BwdWave& st, f32x4& dta, f32x4& d
   }
 }
 
-// The four steps of the wave with query block W: key blocks W, W+1, W+2,
-// W+3 (mod 4), so that at every step each block is touched by exactly one
-// wave; a barrier ends each step, so the order of additions into every
-// block is fixed.
+template <int KB, int T, bool QUAD, bool MASK>
+__device__ __forceinline__ void bwd_step(const BwdWave& st, f32x4& dta, f32x4& dtb, f32x16& dqacc) {
+  const f32x16 p = bwd_p<KB, QUAD, MASK>(st);
+  f32x16 ds = bwd_dp<KB>(st, -st.D);
+#pragma unroll
+  for (int r = 0; r < 16; ++r) ds[r] *= p[r];
+  bwd_step_tail<KB, T>(st, p, ds, dta, dtb, dqacc);
+}
+
+// The wave with query block W: pass 1 forms D = sum_k P dP over key blocks
+// W+1, W+2, W+3, W (mod 4), the last one's P and dP kept for step 0; then
+// the four steps over key blocks W, W+1, W+2, W+3, so that at every step
+// each block is touched by exactly one wave; a barrier ends each step, so
+// the order of additions into every block is fixed.
 template <int W, bool QUAD, bool MASK>
-__device__ __forceinline__ void bwd_rotation(const BwdWave& st, f32x4 (&dta)[4], f32x4 (&dtb)[4],
-                                             f32x16& dqacc) {
-  bwd_step<(W + 0) & 3, 0, QUAD, MASK>(st, dta[(W + 0) & 3], dtb[(W + 0) & 3], dqacc);
+__device__ __forceinline__ void bwd_rotation(BwdWave& st, f32x4 (&dta)[4], f32x4 (&dtb)[4], f32x16& dqacc) {
+  float dsum = 0.0f;
+#define TERRA_DSUM(KB)                                                          \
+  {                                                                             \
+    const f32x16 pk = bwd_p<KB, QUAD, MASK>(st);                                \
+    const f32x16 dk = bwd_dp<KB>(st, 0.0f);                                     \
+    _Pragma("unroll") for (int r = 0; r < 16; ++r) dsum += pk[r] * dk[r];       \
+  }
+  TERRA_DSUM((W + 1) & 3)
+  TERRA_DSUM((W + 2) & 3)
+  TERRA_DSUM((W + 3) & 3)
+#undef TERRA_DSUM
+  const f32x16 p0 = bwd_p<W, QUAD, MASK>(st);
+  f32x16 ds0 = bwd_dp<W>(st, 0.0f);
+#pragma unroll
+  for (int r = 0; r < 16; ++r) dsum += p0[r] * ds0[r];
+  st.D = halves_sum(dsum);
+#pragma unroll
+  for (int r = 0; r < 16; ++r) ds0[r] = p0[r] * (ds0[r] - st.D);
+  __syncthreads();   // every wave has its Q and dO operands; the staging is dead
+  bwd_step_tail<W, 0>(st, p0, ds0, dta[W], dtb[W], dqacc);
   __syncthreads();
   bwd_step<(W + 1) & 3, 1, QUAD, MASK>(st, dta[(W + 1) & 3], dtb[(W + 1) & 3], dqacc);
   __syncthreads();
@@ -656,21 +678,6 @@ __device__ __forceinline__ void bwd_rotation(const BwdWave& st, f32x4 (&dta)[4],
 template <bool QUAD, bool MASK>
 __device__ __forceinline__ void bwd_window_body(BwdWave& st, int qw, f32x4 (&dta)[4], f32x4 (&dtb)[4],
                                                 f32x16& dqacc) {
-  // pass 1: D = sum_k P dP over the window
-  float dsum = 0.0f;
-#define TERRA_DSUM(KB)                                                          \
-  {                                                                             \
-    const f32x16 pk = bwd_p<KB, QUAD, MASK>(st);                                \
-    const f32x16 dk = bwd_dp<KB>(st, 0.0f);                                     \
-    _Pragma("unroll") for (int r = 0; r < 16; ++r) dsum += pk[r] * dk[r];       \
-  }
-  TERRA_DSUM(0)
-  TERRA_DSUM(1)
-  TERRA_DSUM(2)
-  TERRA_DSUM(3)
-#undef TERRA_DSUM
-  st.D = halves_sum(dsum);
-  __syncthreads();   // every wave has its Q and dO operands; the staging is dead
   switch (qw) {
     case 0: bwd_rotation<0, QUAD, MASK>(st, dta, dtb, dqacc); break;
     case 1: bwd_rotation<1, QUAD, MASK>(st, dta, dtb, dqacc); break;
