@@ -591,8 +591,8 @@ __device__ __forceinline__ f32x16 bwd_dp(const BwdWave& st, float init) {
 }
 
 // One rotation step: key block KB.  P and dP are recomputed (so that P does
-// not occupy 64 registers across the steps; step 0 takes them from the D
-// pass), dS = P (dP - D) goes into the bias accumulators and into
+// not occupy 64 registers across the steps; steps 0 and 1 take them from
+// the D pass), dS = P (dP - D) goes into the bias accumulators and into
 // dQ += dS K (K^T operands by the LDS transpose read of the K rows); P^T and
 // dS^T (by matrix-core transpose) times dO and Q give the block's dV and dK
 // partials, which are added to the running sums in LDS through the
@@ -640,7 +640,7 @@ __device__ __forceinline__ void bwd_step(const BwdWave& st, f32x4& dta, f32x4& d
 }
 
 // The wave with query block W: pass 1 forms D = sum_k P dP over key blocks
-// W+1, W+2, W+3, W (mod 4), the last one's P and dP kept for step 0; then
+// W+2, W+3, W+1, W (mod 4), the last two P and dP kept for steps 1 and 0; then
 // the four steps over key blocks W, W+1, W+2, W+3, so that at every step
 // each block is touched by exactly one wave; a barrier ends each step, so
 // the order of additions into every block is fixed.
@@ -653,10 +653,13 @@ __device__ __forceinline__ void bwd_rotation(BwdWave& st, f32x4 (&dta)[4], f32x4
     const f32x16 dk = bwd_dp<KB>(st, 0.0f);                                     \
     _Pragma("unroll") for (int r = 0; r < 16; ++r) dsum += pk[r] * dk[r];       \
   }
-  TERRA_DSUM((W + 1) & 3)
   TERRA_DSUM((W + 2) & 3)
   TERRA_DSUM((W + 3) & 3)
 #undef TERRA_DSUM
+  const f32x16 p1 = bwd_p<(W + 1) & 3, QUAD, MASK>(st);
+  f32x16 ds1 = bwd_dp<(W + 1) & 3>(st, 0.0f);
+#pragma unroll
+  for (int r = 0; r < 16; ++r) dsum += p1[r] * ds1[r];
   const f32x16 p0 = bwd_p<W, QUAD, MASK>(st);
   f32x16 ds0 = bwd_dp<W>(st, 0.0f);
 #pragma unroll
@@ -664,10 +667,12 @@ __device__ __forceinline__ void bwd_rotation(BwdWave& st, f32x4 (&dta)[4], f32x4
   st.D = halves_sum(dsum);
 #pragma unroll
   for (int r = 0; r < 16; ++r) ds0[r] = p0[r] * (ds0[r] - st.D);
+#pragma unroll
+  for (int r = 0; r < 16; ++r) ds1[r] = p1[r] * (ds1[r] - st.D);
   __syncthreads();   // every wave has its Q and dO operands; the staging is dead
   bwd_step_tail<W, 0>(st, p0, ds0, dta[W], dtb[W], dqacc);
   __syncthreads();
-  bwd_step<(W + 1) & 3, 1, QUAD, MASK>(st, dta[(W + 1) & 3], dtb[(W + 1) & 3], dqacc);
+  bwd_step_tail<(W + 1) & 3, 1>(st, p1, ds1, dta[(W + 1) & 3], dtb[(W + 1) & 3], dqacc);
   __syncthreads();
   bwd_step<(W + 2) & 3, 2, QUAD, MASK>(st, dta[(W + 2) & 3], dtb[(W + 2) & 3], dqacc);
   __syncthreads();
