@@ -4,15 +4,14 @@
 // Same mathematics as attn.hip (W-MSA / SW-MSA of the Swin blocks,
 // Sec. IV-A, on the window-major layout of Sec. IV-D), organised so that a
 // workgroup holds one whole window of one head:
-// * every key of the window is in LDS at once, so the forward needs no
-//   online rescaling and the backward has all of P and dP of a query in
-//   registers: D_q = sum_k P dP is a register sum, and exp() runs once per
-//   score in the backward;
-// * 32x32 blocks are transposed ON THE MATRIX CORES: multiplying a block by
-//   a 0/1 permutation operand returns it in the transposed register layout
-//   (values are exact bf16, so the copy is exact).  This gives K^T and V^T
-//   for LDS, the query-major Q and dO operands, and P^T, dS^T for dK/dV
-//   without recomputing the scores;
+// * every key of the window is in LDS at once: D_q = sum_k P dP is a
+//   register sum over the window in the backward;
+// * row-major tiles in LDS give their transposed operands through the LDS
+//   transpose read (V for PV, K for dQ, Q and dO for dK and dV), and blocks
+//   held in registers (P^T, dS^T for dV/dK) are transposed ON THE MATRIX
+//   CORES: multiplying a block by a 0/1 permutation operand returns it in
+//   the transposed register layout (values are exact bf16, so the copy is
+//   exact);
 // * the backward walks many windows of one head per workgroup, sums the
 //   per-key partial dK/dV of its four waves in LDS in a fixed rotation, and
 //   keeps per-wave bias-gradient bins in LDS, so that every result is
@@ -530,18 +529,13 @@ struct BwdWave {
   const float* tab;     // bias table times sqrt(hd), reversed, then -inf
   float* redv;          // dV partial sums [HD][RS]
   float* redk;          // dK partial sums [HD][RS]
+  const bf16* qr;       // Q rows [128][HD] (transposed operands read from here)
+  const bf16* dr;       // dO rows [128][HD]
   bf16x8 qop[2], dop[2];  // Q and dO of the wave's 32 queries (row operands)
-  bf16x8 de[2], qe[2];    // dO and Q with lane = channel (column operands)
   float D, lse2, scale_log2;
   FoldMask fold;
-  int qrev, qlab, ntab, col, half;
+  int qrev, qlab, ntab, col, half, qw;
 };
-
-// Row-to-column transpose operand of chunk c (ident_op<false>), read from
-// LDS: it is needed once per window, so it does not hold registers.
-__device__ inline bf16x8 lds_ident(const bf16x8* ident, int c) {
-  return ident[c * 64 + (threadIdx.x & 63)];
-}
 
 // dS summed along the bias diagonals of one register group: registers
 // 4g..4g+3 hold four consecutive keys k..k+3 of one window row, so (query q,
@@ -591,8 +585,8 @@ __device__ __forceinline__ f32x16 bwd_dp(const BwdWave& st, float init) {
 }
 
 // One rotation step: key block KB.  P and dP are recomputed (so that P does
-// not occupy 64 registers across the steps; steps 0 and 1 take them from
-// the D pass), dS = P (dP - D) goes into the bias accumulators and into
+// not occupy 64 registers across the steps; steps 0, 1 and 2 take them
+// from the D pass), dS = P (dP - D) goes into the bias accumulators and into
 // dQ += dS K (K^T operands by the LDS transpose read of the K rows); P^T and
 // dS^T (by matrix-core transpose) times dO and Q give the block's dV and dK
 // partials, which are added to the running sums in LDS through the
@@ -621,8 +615,11 @@ __device__ __forceinline__ void bwd_step_tail(const BwdWave& st, const f32x16& p
 #pragma unroll
       for (int x = 0; x < 4; ++x) part[4 * g4 + x] = a[x];
     }
-    mma16(part, pack_bf16(tr, 0), which == 0 ? st.de[0] : st.qe[0]);
-    mma16(part, pack_bf16(tr, 8), which == 0 ? st.de[1] : st.qe[1]);
+    // dO or Q of the wave's queries with lane = channel, by the LDS
+    // transpose read of their rows
+    const bf16* rows = which == 0 ? st.dr : st.qr;
+    mma16(part, pack_bf16(tr, 0), lds_tr_op<bf16, kBwdHD>(rows, st.qw, 0, 0, lane));
+    mma16(part, pack_bf16(tr, 8), lds_tr_op<bf16, kBwdHD>(rows, st.qw, 1, 0, lane));
 #pragma unroll
     for (int g4 = 0; g4 < 4; ++g4)
       *reinterpret_cast<f32x4*>(red + red_row(st.col) + 32 * KB + 8 * g4 + 4 * st.half) =
@@ -640,7 +637,8 @@ __device__ __forceinline__ void bwd_step(const BwdWave& st, f32x4& dta, f32x4& d
 }
 
 // The wave with query block W: pass 1 forms D = sum_k P dP over key blocks
-// W+2, W+3, W+1, W (mod 4), the last two P and dP kept for steps 1 and 0; then
+// W+3, W+2, W+1, W (mod 4), the last three P and dP kept for steps 2, 1
+// and 0; then
 // the four steps over key blocks W, W+1, W+2, W+3, so that at every step
 // each block is touched by exactly one wave; a barrier ends each step, so
 // the order of additions into every block is fixed.
@@ -653,9 +651,12 @@ __device__ __forceinline__ void bwd_rotation(BwdWave& st, f32x4 (&dta)[4], f32x4
     const f32x16 dk = bwd_dp<KB>(st, 0.0f);                                     \
     _Pragma("unroll") for (int r = 0; r < 16; ++r) dsum += pk[r] * dk[r];       \
   }
-  TERRA_DSUM((W + 2) & 3)
   TERRA_DSUM((W + 3) & 3)
 #undef TERRA_DSUM
+  const f32x16 p2 = bwd_p<(W + 2) & 3, QUAD, MASK>(st);
+  f32x16 ds2 = bwd_dp<(W + 2) & 3>(st, 0.0f);
+#pragma unroll
+  for (int r = 0; r < 16; ++r) dsum += p2[r] * ds2[r];
   const f32x16 p1 = bwd_p<(W + 1) & 3, QUAD, MASK>(st);
   f32x16 ds1 = bwd_dp<(W + 1) & 3>(st, 0.0f);
 #pragma unroll
@@ -669,12 +670,13 @@ __device__ __forceinline__ void bwd_rotation(BwdWave& st, f32x4 (&dta)[4], f32x4
   for (int r = 0; r < 16; ++r) ds0[r] = p0[r] * (ds0[r] - st.D);
 #pragma unroll
   for (int r = 0; r < 16; ++r) ds1[r] = p1[r] * (ds1[r] - st.D);
-  __syncthreads();   // every wave has its Q and dO operands; the staging is dead
+#pragma unroll
+  for (int r = 0; r < 16; ++r) ds2[r] = p2[r] * (ds2[r] - st.D);
   bwd_step_tail<W, 0>(st, p0, ds0, dta[W], dtb[W], dqacc);
   __syncthreads();
   bwd_step_tail<(W + 1) & 3, 1>(st, p1, ds1, dta[(W + 1) & 3], dtb[(W + 1) & 3], dqacc);
   __syncthreads();
-  bwd_step<(W + 2) & 3, 2, QUAD, MASK>(st, dta[(W + 2) & 3], dtb[(W + 2) & 3], dqacc);
+  bwd_step_tail<(W + 2) & 3, 2>(st, p2, ds2, dta[(W + 2) & 3], dtb[(W + 2) & 3], dqacc);
   __syncthreads();
   bwd_step<(W + 3) & 3, 3, QUAD, MASK>(st, dta[(W + 3) & 3], dtb[(W + 3) & 3], dqacc);
   __syncthreads();
@@ -727,10 +729,9 @@ __device__ __forceinline__ void bwd_load_rows(BwdRows& r, const Geo& g, int wl, 
 
 // Backward, head_dim 32, window widths in {4, 8, 16, 32}.  K, V, Q and dO
 // arrive with row-contiguous loads (the other workgroup resident on the CU
-// computes meanwhile; loading one window ahead measured slower); Q and dO
-// are staged in the dV/dK sum areas, which are free until the rotation
-// starts.  dQ, dK and dV
-// leave with row-contiguous stores.  The bias-gradient sums of every
+// computes meanwhile; loading one window ahead measured slower) and stay in
+// LDS for the whole window (80 KB in all, two workgroups per CU).  dQ, dK
+// and dV leave with row-contiguous stores.  The bias-gradient sums of every
 // register run over windows of equal width and are flushed to per-wave LDS
 // bins when the width changes (a register holds the same query/key slot
 // pair, hence the same bin, in every such window).
@@ -744,16 +745,15 @@ __global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
   constexpr int KS = kBwdKS;
   constexpr int RS = kBwdRS;
   extern __shared__ __align__(16) char smem[];
-  bf16x8* ident = reinterpret_cast<bf16x8*>(smem);              // [2][64]
-  bf16* ks = reinterpret_cast<bf16*>(ident + 2 * 64);           // [128][KS] K rows, then dQ
+  bf16* ks = reinterpret_cast<bf16*>(smem);                     // [128][KS] K rows, then dQ
   bf16* vs = ks + kWinMax * KS;                                 // [128][KS] V rows
-  float* redv = reinterpret_cast<float*>(vs + kWinMax * KS);    // [HD][RS] dV sums
+  bf16* qr = vs + kWinMax * KS;                                 // [128][HD] Q rows
+  bf16* dr = qr + kWinMax * HD;                                 // [128][HD] dO rows
+  float* redv = reinterpret_cast<float*>(dr + kWinMax * HD);    // [HD][RS] dV sums
   float* redk = redv + kBwdRed;                                 // [HD][RS] dK sums
   int* kinfo = reinterpret_cast<int*>(redk + kBwdRed);          // [128]
   float* tab = reinterpret_cast<float*>(kinfo + kWinMax);       // [ntab+4]
   float* bins = tab + (g.ntab + 4);                             // [4][nbins], reversed
-  bf16* qrows = reinterpret_cast<bf16*>(redv);                  // [128][KS] Q rows (staging)
-  bf16* drows = reinterpret_cast<bf16*>(redk);                  // [128][KS] dO rows (staging)
 
   const int work = xcd_work(blockIdx.x, gridDim.x);
   const int slice = work / g.heads;
@@ -765,7 +765,6 @@ __global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
   float* mybins = bins + qw * g.nbins;
 
   for (int x = threadIdx.x; x < 4 * g.nbins; x += kWinThreads) bins[x] = 0.0f;
-  if (qw < 2) ident[threadIdx.x] = ident_op<false>(qw);
   for (int x = threadIdx.x; x < g.ntab + 4; x += kWinThreads)
     tab[x] = table_entry(g, table, h, x, sqrtf((float)HD));
 
@@ -825,8 +824,8 @@ __global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
       const int row = bwd_stage_row(idx), c0 = (idx % kBwdCPR) * 8;
       *reinterpret_cast<uint4*>(ks + row * KS + c0) = rows.k[u];
       *reinterpret_cast<uint4*>(vs + row * KS + c0) = rows.v[u];
-      *reinterpret_cast<uint4*>(qrows + row * KS + c0) = rows.q[u];
-      *reinterpret_cast<uint4*>(drows + row * KS + c0) = rows.d[u];
+      *reinterpret_cast<uint4*>(qr + row * HD + c0) = rows.q[u];
+      *reinterpret_cast<uint4*>(dr + row * HD + c0) = rows.d[u];
     }
     if (threadIdx.x < kWinMax) kinfo[threadIdx.x] = win_token_info(g, wi, wj, cols, threadIdx.x, n);
     BwdWave st;
@@ -839,28 +838,22 @@ __global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
     st.tab = tab;
     st.redv = redv;
     st.redk = redk;
+    st.qr = qr;
+    st.dr = dr;
+    st.qw = qw;
     st.scale_log2 = scale_log2;
     st.ntab = g.ntab;
     st.col = col;
     st.half = half;
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
-      st.qop[c] = *reinterpret_cast<const bf16x8*>(qrows + qi * KS + 16 * c + 8 * half);
-      st.dop[c] = *reinterpret_cast<const bf16x8*>(drows + qi * KS + 16 * c + 8 * half);
+      st.qop[c] = *reinterpret_cast<const bf16x8*>(qr + qi * HD + 16 * c + 8 * half);
+      st.dop[c] = *reinterpret_cast<const bf16x8*>(dr + qi * HD + 16 * c + 8 * half);
     }
     const int qinf = qi < n ? kinfo[qi] : 0;
     st.qlab = qinf >> 24;
     st.qrev = table_qrev(g, qinf);
     st.fold = fold_mask(qi % cols, cols);
-    {
-      const bf16x8 in0 = lds_ident(ident, 0), in1 = lds_ident(ident, 1);
-      const f32x16 te = mfma_transpose(st.dop[0], st.dop[1], in0, in1);
-      st.de[0] = pack_bf16(te, 0);
-      st.de[1] = pack_bf16(te, 8);
-      const f32x16 tq = mfma_transpose(st.qop[0], st.qop[1], in0, in1);
-      st.qe[0] = pack_bf16(tq, 0);
-      st.qe[1] = pack_bf16(tq, 8);
-    }
     f32x16 dqacc = f32x16{};
     if (window_needs_mask(g, wi, wj, n)) bwd_window_body<QUAD, true>(st, qw, dta, dtb, dqacc);
     else bwd_window_body<QUAD, false>(st, qw, dta, dtb, dqacc);
@@ -939,7 +932,7 @@ size_t win_fwd_lds(const Geo& g) {
   return one;
 }
 size_t win_bwd_lds(const Geo& g) {
-  return 16 * 2 * 64 + sizeof(bf16) * (2 * kWinMax * kBwdKS) +
+  return sizeof(bf16) * (2 * kWinMax * kBwdKS + 2 * kWinMax * kBwdHD) +
          sizeof(float) * 2 * kBwdRed + 4 * kWinMax + 4 * (g.ntab + 4) + 4 * 4 * g.nbins;
 }
 
