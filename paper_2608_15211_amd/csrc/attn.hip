@@ -211,6 +211,9 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(
   const int half = lane >> 5, col = lane & 31;
   const int qi = q0 + wave * kWaveQ + col;
   const bool qvalid = qi < n;
+  // waves whose 32 queries all lie past the window's end (last chunk of a
+  // window that is not a multiple of 128 tokens) skip the matrix work
+  const bool wactive = q0 + wave * kWaveQ < n;
   const int qinf = token_info(g, i, j, cols, qvalid ? qi : 0, n);
   const int qlab = qinf >> 24;
   const int qrev = g.nbins - 1 - ((qinf & 0xFFFFFF) + (g.wh - 1) * g.bstride + (g.ww - 1));
@@ -249,6 +252,7 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(
       tile_load(rk, k, g, wt, k0 + kTile, n, hoff);
       tile_load(rv, v, g, wt, k0 + kTile, n, hoff);
     }
+    if (!wactive) continue;     // staging and barriers only
 
     f32x16 s[kTile / 32];
     float mloc = -INFINITY;
@@ -356,6 +360,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
     const WinTokens<NHWC> wt(g, b, i, j);
     const int qi = q0 + wave * kWaveQ + col;
     const bool qvalid = qi < n;
+    const bool wactive = q0 + wave * kWaveQ < n;   // else staging and barriers only
     const int qinf = token_info(g, i, j, cols, qvalid ? qi : 0, n);
     const int qlab = qinf >> 24;
     const int qoff = (qinf & 0xFFFFFF) + (g.wh - 1) * g.bstride + (g.ww - 1);
@@ -399,6 +404,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
         tile_load(rk, k, g, wt, nk0, n, hoff);
         tile_load(rv, v, g, wt, nk0, n, hoff);
       }
+      if (!wactive) continue;
 #pragma unroll
       for (int kb = 0; kb < kTile / 32; ++kb) {
         f32x16 s = mask ? bias_init<QUAD, true>(kinfo, tab, kb, half, qrev, qlab, g.nbins)
@@ -445,6 +451,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
         tile_load(rk, k, g, wt, k0 + kTile, n, hoff);
         tile_load(rv, v, g, wt, k0 + kTile, n, hoff);
       }
+      if (!wactive) continue;
       f32x16 dsb[kTile / 32];
 #pragma unroll
       for (int kb = 0; kb < kTile / 32; ++kb) {
@@ -601,6 +608,7 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(
   const int half = lane >> 5, col = lane & 31;
   const int ki = kbase + wave * kWaveQ + col;
   const bool kvalid = ki < n;
+  const bool wactive = kbase + wave * kWaveQ < n;   // else staging and barriers only
   const int kinf = token_info(g, i, j, cols, kvalid ? ki : 0, n);
   const int klab = kvalid ? (kinf >> 24) : 0xFE;
   const int kfwd = (g.wh - 1) * g.bstride + (g.ww - 1) - (kinf & 0xFFFFFF);
@@ -645,6 +653,7 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(
       tile_load(rq, q, g, wt, t0 + kTile, n, hoff);
       tile_load(rd, dout, g, wt, t0 + kTile, n, hoff);
     }
+    if (!wactive) continue;
 #pragma unroll
     for (int qb = 0; qb < kTile / 32; ++qb) {
       // registers 4g..4g+3 hold queries 32qb + 8g + 4*half + 0..3: their
