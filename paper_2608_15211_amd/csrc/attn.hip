@@ -512,25 +512,63 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
             const float p2 = dpp_lane<kDppWavePrev>(dpp_lane<kDppWavePrev>(d1 * fsend) * fsend);
             fb[kb][g4] = fkeep * (d3 + p1 + p2);
           }
-#pragma unroll 1
-        for (int hh = 0; hh < 2; ++hh) {
-          if (half == hh) {
+        // One update of this lane: the folded pair sums of key block kb,
+        // group g4 (fa at (q, k), fb at (q, k+3)).
+        auto upd = [&](int kb, int g4, float va, float vb) {
+          const int kk = kb * 32 + 8 * g4 + 4 * half;
+          if (va != 0.0f) mybins[qoff - (kinfo[kk] & 0xFFFFFF)] += va;
+          if (vb != 0.0f) mybins[qoff - (kinfo[kk + 3] & 0xFFFFFF)] += vb;
+        };
+        if constexpr (kTile == 64) {
+          // Both halves update with one instruction when their keys are at
+          // least 32 tokens apart: the 32 queries of a half are consecutive
+          // tokens, so (q, k) and (q', k') share a bin only if |k - k'| =
+          // |q - q'| < 32.  Half 0 takes block 0 group t while half 1 takes
+          // block 1 group t (keys 32 + 4 or more apart), then half 0 takes
+          // block 1 group t while half 1 takes block 0 group t - 1 (36 or
+          // more), and the two updates left over go alone.
 #pragma unroll
-            for (int kb = 0; kb < kTile / 32; ++kb)
-#pragma unroll
-              for (int g4 = 0; g4 < 4; ++g4) {
-                const int kk = kb * 32 + 8 * g4 + 4 * half;
-                if (fa[kb][g4] != 0.0f)
-                  mybins[qoff - (kinfo[kk] & 0xFFFFFF)] += fa[kb][g4];
-                if (fb[kb][g4] != 0.0f)
-                  mybins[qoff - (kinfo[kk + 3] & 0xFFFFFF)] += fb[kb][g4];
-#pragma unroll
-                for (int x = 1; x < 3; ++x)
-                  if (run < x && rest < 3 - x && dsb[kb][4 * g4 + x] != 0.0f)
-                    mybins[qoff - (kinfo[kk + x] & 0xFFFFFF)] += dsb[kb][4 * g4 + x];
-              }
+          for (int t = 0; t < 4; ++t) {
+            const int kb = half, gt = t;
+            upd(kb, gt, half ? fa[1][t] : fa[0][t], half ? fb[1][t] : fb[0][t]);
           }
+#pragma unroll
+          for (int t = 1; t < 4; ++t) {
+            const int kb = 1 - half, gt = t - half;
+            upd(kb, gt, half ? fa[0][t - 1] : fa[1][t], half ? fb[0][t - 1] : fb[1][t]);
+          }
+          if (half == 0) upd(1, 0, fa[1][0], fb[1][0]);
           __builtin_amdgcn_wave_barrier();
+          if (half == 1) upd(0, 3, fa[0][3], fb[0][3]);
+          __builtin_amdgcn_wave_barrier();
+        } else {
+#pragma unroll 1
+          for (int hh = 0; hh < 2; ++hh) {
+            if (half == hh) {
+#pragma unroll
+              for (int g4 = 0; g4 < 4; ++g4) upd(0, g4, fa[0][g4], fb[0][g4]);
+            }
+            __builtin_amdgcn_wave_barrier();
+          }
+        }
+        // pairs of runs shorter than three lanes that the fold left out
+        if (__builtin_amdgcn_ballot_w64((run < 1 && rest < 2) || (run < 2 && rest < 1)) != 0) {
+#pragma unroll 1
+          for (int hh = 0; hh < 2; ++hh) {
+            if (half == hh) {
+#pragma unroll
+              for (int kb = 0; kb < kTile / 32; ++kb)
+#pragma unroll
+                for (int g4 = 0; g4 < 4; ++g4) {
+                  const int kk = kb * 32 + 8 * g4 + 4 * half;
+#pragma unroll
+                  for (int x = 1; x < 3; ++x)
+                    if (run < x && rest < 3 - x && dsb[kb][4 * g4 + x] != 0.0f)
+                      mybins[qoff - (kinfo[kk + x] & 0xFFFFFF)] += dsb[kb][4 * g4 + x];
+                }
+            }
+            __builtin_amdgcn_wave_barrier();
+          }
         }
       } else {
 #pragma unroll 1
