@@ -267,12 +267,19 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(
       for (int r = 0; r < 16; ++r) mloc = fmaxf(mloc, s[kb][r]);
     }
     mloc = halves_max(mloc);
-    const float mnew = fmaxf(m_run, mloc * scale_log2);
-    const float alpha = exp2f(m_run - mnew);
-    m_run = mnew;
-    l_run *= alpha;
+    // The running maximum moves (and O and the sum are rescaled) only when
+    // some query of the wave sees a score more than 2^8 above it: between
+    // moves the weights stay below 256, which the fp32 sums and the 16-bit
+    // operands carry as exactly as weights below 1.
+    const float mt = mloc * scale_log2;
+    if (__builtin_amdgcn_ballot_w64(mt > m_run + 8.0f) != 0) {
+      const float mnew = fmaxf(m_run, mt);
+      const float alpha = exp2f(m_run - mnew);
+      m_run = mnew;
+      l_run *= alpha;
 #pragma unroll
-    for (int eb = 0; eb < HD / 32; ++eb) oacc[eb] *= alpha;
+      for (int eb = 0; eb < HD / 32; ++eb) oacc[eb] *= alpha;
+    }
 #pragma unroll
     for (int kb = 0; kb < kTile / 32; ++kb) {
 #pragma unroll
@@ -622,7 +629,7 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(
   T* dtt = qtt + ttile_size<T, HD>();                // dO^T (fp32)
   int* qinfo = reinterpret_cast<int*>(dtt + ttile_size<T, HD>());
   float* ql = reinterpret_cast<float*>(qinfo + kTile);   // lse2 per query
-  float* qd = ql + kTile;                                 // D per query
+  float* qd = ql + kTile;                                 // -D per query
   float* tab = qd + kTile;                                // [nbins+4], forward order
 
   int bid = blockIdx.x;
@@ -684,7 +691,7 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(
       qinfo[threadIdx.x] = inf;
       const int64_t li = t < n ? wt.lse_at(g, h, t) : 0;
       ql[threadIdx.x] = t < n ? lse[li] * kLog2e : INFINITY;   // padding queries: P = 0
-      qd[threadIdx.x] = t < n ? D[li] : 0.0f;
+      qd[threadIdx.x] = t < n ? -D[li] : 0.0f;                 // -D: the dP accumulator's start
     }
     __syncthreads();
     if (kPrefetch && t0 + kTile < n) {
@@ -705,7 +712,7 @@ __global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(
         const f32x4 l4 = *reinterpret_cast<const f32x4*>(ql + qb * 32 + 8 * g4 + 4 * half);
 #pragma unroll
         for (int x = 0; x < 4; ++x) {
-          dp[4 * g4 + x] = -d4[x];     // dP - D straight from the product
+          dp[4 * g4 + x] = d4[x];      // dP - D straight from the product
           lq[4 * g4 + x] = l4[x];
         }
       }
