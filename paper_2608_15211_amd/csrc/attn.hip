@@ -534,20 +534,61 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
           // block 1 group t (keys 32 + 4 or more apart), then half 0 takes
           // block 1 group t while half 1 takes block 0 group t - 1 (36 or
           // more), and the two updates left over go alone.
+          if (q0 + wave * kWaveQ + kWaveQ <= n && k0 + kTile <= n) {
+            // Every query of the wave and every key of the tile is a window
+            // token: the updates need no guard (adding 0 to a bin that no
+            // other lane of the instruction touches changes nothing), and
+            // the key words are read before the first update.  Word index of
+            // this lane's group: 36 half + 8t in the first round, 32 - 36 half
+            // + 8t in the second, 32 (half 0) or 28 (half 1) left over.
+            int w1[4][2], w2[3][2], wl[2];
 #pragma unroll
-          for (int t = 0; t < 4; ++t) {
-            const int kb = half, gt = t;
-            upd(kb, gt, half ? fa[1][t] : fa[0][t], half ? fb[1][t] : fb[0][t]);
-          }
+            for (int t = 0; t < 4; ++t) {
+              const int kk = 36 * half + 8 * t;
+              w1[t][0] = qoff - (kinfo[kk] & 0xFFFFFF);
+              w1[t][1] = qoff - (kinfo[kk + 3] & 0xFFFFFF);
+            }
 #pragma unroll
-          for (int t = 1; t < 4; ++t) {
-            const int kb = 1 - half, gt = t - half;
-            upd(kb, gt, half ? fa[0][t - 1] : fa[1][t], half ? fb[0][t - 1] : fb[1][t]);
+            for (int t = 1; t < 4; ++t) {
+              const int kk = 32 - 36 * half + 8 * t;
+              w2[t - 1][0] = qoff - (kinfo[kk] & 0xFFFFFF);
+              w2[t - 1][1] = qoff - (kinfo[kk + 3] & 0xFFFFFF);
+            }
+            {
+              const int kk = half ? 28 : 32;
+              wl[0] = qoff - (kinfo[kk] & 0xFFFFFF);
+              wl[1] = qoff - (kinfo[kk + 3] & 0xFFFFFF);
+            }
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+              mybins[w1[t][0]] += half ? fa[1][t] : fa[0][t];
+              mybins[w1[t][1]] += half ? fb[1][t] : fb[0][t];
+            }
+#pragma unroll
+            for (int t = 1; t < 4; ++t) {
+              mybins[w2[t - 1][0]] += half ? fa[0][t - 1] : fa[1][t];
+              mybins[w2[t - 1][1]] += half ? fb[0][t - 1] : fb[1][t];
+            }
+            if (half == 0) { mybins[wl[0]] += fa[1][0]; mybins[wl[1]] += fb[1][0]; }
+            __builtin_amdgcn_wave_barrier();
+            if (half == 1) { mybins[wl[0]] += fa[0][3]; mybins[wl[1]] += fb[0][3]; }
+            __builtin_amdgcn_wave_barrier();
+          } else {
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+              const int kb = half, gt = t;
+              upd(kb, gt, half ? fa[1][t] : fa[0][t], half ? fb[1][t] : fb[0][t]);
+            }
+#pragma unroll
+            for (int t = 1; t < 4; ++t) {
+              const int kb = 1 - half, gt = t - half;
+              upd(kb, gt, half ? fa[0][t - 1] : fa[1][t], half ? fb[0][t - 1] : fb[1][t]);
+            }
+            if (half == 0) upd(1, 0, fa[1][0], fb[1][0]);
+            __builtin_amdgcn_wave_barrier();
+            if (half == 1) upd(0, 3, fa[0][3], fb[0][3]);
+            __builtin_amdgcn_wave_barrier();
           }
-          if (half == 0) upd(1, 0, fa[1][0], fb[1][0]);
-          __builtin_amdgcn_wave_barrier();
-          if (half == 1) upd(0, 3, fa[0][3], fb[0][3]);
-          __builtin_amdgcn_wave_barrier();
         } else {
 #pragma unroll 1
           for (int hh = 0; hh < 2; ++hh) {
