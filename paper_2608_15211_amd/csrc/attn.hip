@@ -51,6 +51,15 @@ template <typename T, int HD> constexpr int tile_of() { return (sizeof(T) == 4 &
 constexpr int kPad = 8;         // LDS row padding, elements
 constexpr int kLabBad = 0xFF;   // label of padding slots (never matches)
 
+// Work item of a forward workgroup.  The hardware hands consecutive
+// workgroups to the 8 XCDs in turn; giving each XCD one contiguous range of
+// items puts the query chunks of one window and head, which stage the same
+// K/V tiles, behind the same L2 (forward -2 to -4 %; measured no better or
+// slower for the dK/dV and dQ kernels, which keep the plain order).  The grid
+// is rounded up to a multiple of 8 and the padding workgroups exit at once.
+__device__ inline int xcd_item(int bid, int nblocks) { return (bid & 7) * (nblocks >> 3) + (bid >> 3); }
+static inline int grid8(int n) { return (n + 7) & ~7; }
+
 // Transposed tiles (head-dim rows e, token columns): row e starts at
 // e * (kTile + kPad) plus 4 elements per group of 8 rows, so that the
 // transposing staging stores of one instruction (8 rows of one chunk, the
@@ -190,7 +199,8 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(
   int* kinfo = reinterpret_cast<int*>(vt + vtile_size<T, HD>());
   float* tab = reinterpret_cast<float*>(kinfo + kTile);        // [nbins+4], reversed
 
-  int bid = blockIdx.x;
+  int bid = xcd_item(blockIdx.x, gridDim.x);
+  if (bid >= g.B * g.nwin * g.heads * nqc) return;
   const int qc = bid % nqc; bid /= nqc;
   const int h = bid % g.heads; bid /= g.heads;
   const int w = bid % g.nwin;
@@ -854,7 +864,7 @@ template <typename T, int HD, bool NHWC>
 static hipError_t fwd_impl(const Geo& g, const void* q, const void* k, const void* v,
                            const float* table, void* o, float* lse, hipStream_t st) {
   const int nqc = num_chunks(g);
-  const int grid = g.B * g.nwin * g.heads * nqc;
+  const int grid = grid8(g.B * g.nwin * g.heads * nqc);
   const float sl2 = kLog2e / sqrtf((float)HD);
   const size_t lds = fwd_lds<T, HD>(g);
   if (quad_layout(g))
