@@ -665,9 +665,13 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
 // ---------------------------------------------------------------------------
 // Backward, step 2: dK and dV.  Grid: B * nwin * heads * nkc (key chunks of
 // 128; a wave owns 32 keys and walks the window's queries in LDS tiles).
+// 16-bit types ask for two resident workgroups per CU: at head_dim 128 the
+// compiler otherwise takes 280 registers (one wave per SIMD); capped at 256
+// it spills 13 words and runs 10 % faster.  Three per CU (168 registers)
+// spill inside the loop at head_dim 64 and run 25 % slower.
 // ---------------------------------------------------------------------------
 template <typename T, int HD, bool NHWC, bool QUAD>
-__global__ __launch_bounds__(kThreads) void bwd_dkdv_kernel(
+__global__ __launch_bounds__(kThreads, sizeof(T) == 2 ? 2 : 1) void bwd_dkdv_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const T* __restrict__ dout, const float* __restrict__ lse, const float* __restrict__ D,
     const float* __restrict__ table, T* __restrict__ dk, T* __restrict__ dv,
