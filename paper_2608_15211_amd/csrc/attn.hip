@@ -838,14 +838,6 @@ __global__ __launch_bounds__(kThreads) void dtab_reduce_kernel(
 // ---------------------------------------------------------------------------
 static inline int num_chunks(const Geo& g) { return (g.wh * g.ww + kChunk - 1) / kChunk; }
 
-// Number of per-head slices of the dQ / bias-gradient kernel; a pure
-// function of the geometry so that the workspace size can be queried.
-int bwd_nslice(const Geo& g) {
-  const int items = g.B * g.nwin * num_chunks(g);
-  int target = (2048 + g.heads - 1) / g.heads;
-  if (target > items) target = items;
-  return target < 1 ? 1 : target;
-}
 
 template <typename T, int HD>
 static size_t fwd_lds(const Geo& g) {
@@ -862,6 +854,29 @@ template <typename T, int HD>
 static size_t dkdv_lds(const Geo& g) {
   constexpr int kTile = tile_of<T, HD>();
   return sizeof(T) * (2 * kTile * (HD + kPad) + 2 * ttile_size<T, HD>()) + 12 * kTile + 4 * (g.nbins + 4);
+}
+
+// Number of per-head slices of the dQ / bias-gradient kernel: a pure
+// function of the geometry and element type, so that the workspace size can
+// be queried.  The grid is one round of resident workgroups (two per CU by
+// the kernel's launch bound, one if its LDS does not leave room for two),
+// rounded down to whole heads: a grid a few workgroups past a round leaves
+// those few to run alone at the end (24 heads with ceil(2048 / 24) slices
+// each made 2064 workgroups, 4 rounds and 16 more).  Measured against 2, 4
+// and 8 rounds, one was fastest or level on every workload.
+constexpr int kF32 = 0, kBF16 = 1;
+constexpr int kDqRounds = 1;
+template <typename T>
+static int bwd_nslice_t(const Geo& g) {
+  const size_t lds = g.hd == 32 ? dq_lds<T, 32>(g) : g.hd == 64 ? dq_lds<T, 64>(g) : dq_lds<T, 128>(g);
+  const int per_cu = lds * 2 <= 160 * 1024 ? 2 : 1;
+  const int items = g.B * g.nwin * num_chunks(g);
+  int n = kDqRounds * 256 * per_cu / g.heads;
+  if (n > items) n = items;
+  return n < 1 ? 1 : n;
+}
+int bwd_nslice(const Geo& g, int dt) {
+  return dt == kF32 ? bwd_nslice_t<float>(g) : dt == kBF16 ? bwd_nslice_t<__bf16>(g) : bwd_nslice_t<_Float16>(g);
 }
 
 template <typename T, int HD, bool NHWC>
@@ -883,7 +898,7 @@ static hipError_t fwd_impl(const Geo& g, const void* q, const void* k, const voi
 size_t bwd_workspace(const Geo& g, int dt) {
   if (win_bwd_ok(g, dt == 1)) return (size_t)g.heads * win_bwd_nslice(g) * g.nbins * sizeof(float);
   const size_t dbytes = (size_t)g.B * g.heads * g.HW * sizeof(float);
-  const size_t pbytes = (size_t)g.heads * bwd_nslice(g) * g.nbins * sizeof(float);
+  const size_t pbytes = (size_t)g.heads * bwd_nslice(g, dt) * g.nbins * sizeof(float);
   return ((dbytes + 255) / 256) * 256 + pbytes;
 }
 
@@ -898,7 +913,7 @@ static hipError_t bwd_impl(const Geo& g, const void* q, const void* k, const voi
   (void)o;  // D is recomputed in-window from P and dP (see the dQ kernel)
   hipError_t e;
   const int nqc = num_chunks(g);
-  const int nslice = bwd_nslice(g);
+  const int nslice = bwd_nslice_t<T>(g);
   const float sl2 = kLog2e / sqrtf((float)HD);
   const float scale = 1.0f / sqrtf((float)HD);
   const size_t lds_dq = dq_lds<T, HD>(g);
@@ -932,7 +947,6 @@ static hipError_t bwd_impl(const Geo& g, const void* q, const void* k, const voi
 }
 
 // Element type codes of the C ABI: 0 float, 1 bfloat16, 2 float16.
-constexpr int kF32 = 0, kBF16 = 1;
 
 template <typename T>
 static size_t max_lds_t(const Geo& g) {
