@@ -819,18 +819,21 @@ __global__ __launch_bounds__(kThreads, sizeof(T) == 2 ? 2 : 1) void bwd_dkdv_ker
 
 // ---------------------------------------------------------------------------
 // Backward, step 3: dT[bin][h] = sum over slices of the partials, in slice
-// order (deterministic).
+// order (deterministic).  Consecutive threads take consecutive bins of one
+// head, so each slice's loads are contiguous, and the loop is unrolled so
+// that loads issue ahead of the additions, which stay in slice order.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kThreads) void dtab_reduce_kernel(
     const float* __restrict__ partial, float* __restrict__ dtab, Geo g, int nslice) {
   const int idx = blockIdx.x * kThreads + threadIdx.x;
   if (idx >= g.nbins * g.heads) return;
-  const int bin = idx / g.heads;
-  const int h = idx - bin * g.heads;
+  const int h = idx / g.nbins;
+  const int bin = idx - h * g.nbins;
   const float* p = partial + (int64_t)h * nslice * g.nbins + bin;
   float acc = 0.0f;
+#pragma unroll 8
   for (int s = 0; s < nslice; ++s) acc += p[(int64_t)s * g.nbins];
-  dtab[idx] = acc;
+  dtab[bin * g.heads + h] = acc;
 }
 
 // ---------------------------------------------------------------------------
