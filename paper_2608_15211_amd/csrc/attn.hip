@@ -859,27 +859,31 @@ static size_t dkdv_lds(const Geo& g) {
   return sizeof(T) * (2 * kTile * (HD + kPad) + 2 * ttile_size<T, HD>()) + 12 * kTile + 4 * (g.nbins + 4);
 }
 
-// Number of per-head slices of the dQ / bias-gradient kernel: a pure
-// function of the geometry and element type, so that the workspace size can
-// be queried.  The grid is one round of resident workgroups (two per CU by
-// the kernel's launch bound, one if its LDS does not leave room for two),
-// rounded down to whole heads: a grid a few workgroups past a round leaves
-// those few to run alone at the end (24 heads with ceil(2048 / 24) slices
-// each made 2064 workgroups, 4 rounds and 16 more).  Measured against 2, 4
-// and 8 rounds, one was fastest or level on every workload.
+// Per-head slices of the dQ / bias-gradient kernel.  The grid is one round
+// of resident workgroups rounded down to whole heads: a grid a few
+// workgroups past a round leaves those few to run alone at the end (24 heads
+// with ceil(2048 / 24) slices each made 2064 workgroups, 4 rounds and 16
+// more).  Measured against 2, 4 and 8 rounds, one was fastest or level on
+// every workload.  The launcher asks the runtime how many workgroups one CU
+// holds; the workspace (a pure function of the geometry and element type, so
+// that it can be queried) is sized for the most the kernel's LDS allows.
 constexpr int kF32 = 0, kBF16 = 1;
-constexpr int kDqRounds = 1;
-template <typename T>
-static int bwd_nslice_t(const Geo& g) {
-  const size_t lds = g.hd == 32 ? dq_lds<T, 32>(g) : g.hd == 64 ? dq_lds<T, 64>(g) : dq_lds<T, 128>(g);
-  const int per_cu = lds * 2 <= 160 * 1024 ? 2 : 1;
+static int slices_for(const Geo& g, int per_cu) {
   const int items = g.B * g.nwin * num_chunks(g);
-  int n = kDqRounds * 256 * per_cu / g.heads;
+  int n = 256 * per_cu / g.heads;
   if (n > items) n = items;
   return n < 1 ? 1 : n;
 }
+template <typename T>
+static int bwd_nslice_max_t(const Geo& g) {
+  const size_t lds = g.hd == 32 ? dq_lds<T, 32>(g) : g.hd == 64 ? dq_lds<T, 64>(g) : dq_lds<T, 128>(g);
+  int per_cu = (int)((160 * 1024) / lds);            // four waves a workgroup, at most 32 a CU
+  if (per_cu > 8) per_cu = 8;
+  return slices_for(g, per_cu < 1 ? 1 : per_cu);
+}
 int bwd_nslice(const Geo& g, int dt) {
-  return dt == kF32 ? bwd_nslice_t<float>(g) : dt == kBF16 ? bwd_nslice_t<__bf16>(g) : bwd_nslice_t<_Float16>(g);
+  return dt == kF32 ? bwd_nslice_max_t<float>(g) : dt == kBF16 ? bwd_nslice_max_t<__bf16>(g)
+                                                               : bwd_nslice_max_t<_Float16>(g);
 }
 
 template <typename T, int HD, bool NHWC>
@@ -916,11 +920,20 @@ static hipError_t bwd_impl(const Geo& g, const void* q, const void* k, const voi
   (void)o;  // D is recomputed in-window from P and dP (see the dQ kernel)
   hipError_t e;
   const int nqc = num_chunks(g);
-  const int nslice = bwd_nslice_t<T>(g);
   const float sl2 = kLog2e / sqrtf((float)HD);
   const float scale = 1.0f / sqrtf((float)HD);
   const size_t lds_dq = dq_lds<T, HD>(g);
   const bool quad = quad_layout(g);
+  int resident = 0;
+  const void* dq_fn = quad ? reinterpret_cast<const void*>(&bwd_dq_kernel<T, HD, NHWC, true>)
+                           : reinterpret_cast<const void*>(&bwd_dq_kernel<T, HD, NHWC, false>);
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&resident, dq_fn, kThreads, lds_dq) != hipSuccess) {
+    (void)hipGetLastError();
+    resident = 2;
+  }
+  int nslice = slices_for(g, resident < 1 ? 1 : resident);
+  const int nmax = bwd_nslice_max_t<T>(g);
+  if (nslice > nmax) nslice = nmax;
   if (quad)
     hipLaunchKernelGGL((bwd_dq_kernel<T, HD, NHWC, true>), dim3(g.heads * nslice), dim3(kThreads),
                        lds_dq, st, (const T*)q, (const T*)k, (const T*)v,
