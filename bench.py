@@ -68,15 +68,17 @@ def algorithmic(cfg):
 
 
 # HBM bytes per launch measured with two rocprofv3 passes (FETCH_SIZE, then
-# WRITE_SIZE; FETCH_SIZE scaled by 1.9995 and WRITE_SIZE by 1.0000, the
+# WRITE_SIZE; FETCH_SIZE scaled by 1.9996 and WRITE_SIZE by 1.0000, the
 # factors a plain copy of known size reads on the same run) on the 128x1080
-# workload, for the fused kernels (backward: bwd_win_kernel + dtab_reduce).  A figure is reported only while the kernel source still has the
-# SHA-256 prefix it was measured with.
+# workload, for the fused kernels (backward: bwd_win_kernel + dtab_reduce).
+# A figure is reported only while the kernel sources (the window kernels and
+# the file holding the bias-table reduction) still have the SHA-256 prefixes
+# they were measured with.
 MEASURED_TRAFFIC = {
-    ("c4_bf16_128x1080_w8x16", "bwd_nhwc"): dict(source="attn_win.hip", sha256="d67c70435fe25d4e",
-                                                bytes=(440302 + 1802) * 1024 * 1.9996 + (629779 + 44) * 1024),
-    ("c4_bf16_128x1080_w8x16", "fwd_nhwc"): dict(source="attn_win.hip", sha256="d67c70435fe25d4e",
-                                                bytes=311294 * 1024 * 1.9996 + 225031 * 1024),
+    ("c4_bf16_128x1080_w8x16", "bwd_nhwc"): dict(sources={"attn_win.hip": "d67c70435fe25d4e", "attn.hip": "70a26736f661b4cb"},
+                                                bytes=(440375 + 556) * 1024 * 1.9996 + (629886 + 304) * 1024),
+    ("c4_bf16_128x1080_w8x16", "fwd_nhwc"): dict(sources={"attn_win.hip": "d67c70435fe25d4e"},
+                                                bytes=311295 * 1024 * 1.9996 + 225342 * 1024),
 }
 
 
@@ -85,9 +87,11 @@ def measured_traffic(cfg_name, phase):
     ent = MEASURED_TRAFFIC.get((cfg_name, phase))
     if ent is None:
         return None
-    path = os.path.join(ROOT, "paper_2608_15211_amd", "csrc", ent["source"])
-    sha = hashlib.sha256(open(path, "rb").read()).hexdigest()
-    return ent["bytes"] if sha.startswith(ent["sha256"]) else None
+    for name, prefix in ent["sources"].items():
+        path = os.path.join(ROOT, "paper_2608_15211_amd", "csrc", name)
+        if not hashlib.sha256(open(path, "rb").read()).hexdigest().startswith(prefix):
+            return None
+    return ent["bytes"]
 
 
 def cpu_baseline(cfg, seconds_target=15.0):
