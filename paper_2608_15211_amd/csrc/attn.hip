@@ -339,19 +339,22 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(
 // fp32 (equal to <dO_q, O_q> for the unrounded O) and stores it for the
 // dK/dV kernel; the second sweep forms dS, dQ and the bias bins.
 // ---------------------------------------------------------------------------
-template <typename T, int HD, bool NHWC, bool QUAD>
+template <typename T, int HD, bool NHWC, bool QUAD, bool RES>
 __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const T* __restrict__ dout, const float* __restrict__ lse, float* __restrict__ D,
     const float* __restrict__ table, T* __restrict__ dq, float* __restrict__ partial,
     Geo g, int nqc, int nslice, float scale_log2, float scale) {
   constexpr int kTile = tile_of<T, HD>();
+  constexpr int kTE = kTile * (HD + kPad);            // elements of one staged tile
+  // RES: every tile of the window stays in LDS for the whole item (nt tiles)
+  const int nt = RES ? (g.wh * g.ww + kTile - 1) / kTile : 1;
   extern __shared__ __align__(16) char smem[];
-  T* kt = reinterpret_cast<T*>(smem);                 // K  [kTile][HD+kPad]
-  T* vr = kt + kTile * (HD + kPad);                   // V  [kTile][HD+kPad]
-  T* ktt = vr + kTile * (HD + kPad);                  // K^T (transposed tile, fp32)
-  int* kinfo = reinterpret_cast<int*>(ktt + ttile_size<T, HD>());
-  float* tab = reinterpret_cast<float*>(kinfo + kTile);   // [nbins+4], reversed
+  T* kt0 = reinterpret_cast<T*>(smem);                // K  nt x [kTile][HD+kPad]
+  T* vr0 = kt0 + nt * kTE;                            // V  nt x [kTile][HD+kPad]
+  T* ktt = vr0 + nt * kTE;                            // K^T (transposed tile, fp32)
+  int* kinfo0 = reinterpret_cast<int*>(ktt + ttile_size<T, HD>());   // nt x [kTile]
+  float* tab = reinterpret_cast<float*>(kinfo0 + nt * kTile);   // [nbins+4], reversed
   float* dtab = tab + g.nbins + 4;                    // [4][nbins], one per wave
 
   const int h = blockIdx.x / nslice;
@@ -401,25 +404,53 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
     // head dim 128 the registers this holds would halve the occupancy.
     constexpr bool kPrefetch = HD <= 64;
     TileRegs<T, HD> rk, rv;
-    if (kPrefetch) {
+    if constexpr (RES) {
+      // all tiles of the window into LDS once per item (each tile's loads
+      // issued before the previous tile is stored); both sweeps then read
+      // them without staging or barriers
+      tile_load(rk, k, g, wt, 0, n, hoff);
+      tile_load(rv, v, g, wt, 0, n, hoff);
+      __syncthreads();                  // the previous item is done with the tiles
+      for (int t0 = 0; t0 < n; t0 += kTile) {
+        TileRegs<T, HD> nk = rk, nv = rv;
+        if (t0 + kTile < n) {
+          tile_load(nk, k, g, wt, t0 + kTile, n, hoff);
+          tile_load(nv, v, g, wt, t0 + kTile, n, hoff);
+        }
+        const int tix = t0 / kTile;
+        tile_store<T, HD, true, false>(rk, kt0 + tix * kTE, nullptr);
+        tile_store<T, HD, true, false>(rv, vr0 + tix * kTE, nullptr);
+        if (threadIdx.x < kTile)
+          kinfo0[tix * kTile + threadIdx.x] = token_info(g, i, j, cols, t0 + threadIdx.x, n);
+        rk = nk;
+        rv = nv;
+      }
+      __syncthreads();
+    } else if (kPrefetch) {
       tile_load(rk, k, g, wt, 0, n, hoff);
       tile_load(rv, v, g, wt, 0, n, hoff);
     }
     float dsum = 0.0f;
     for (int k0 = 0; k0 < n; k0 += kTile) {
-      if (!kPrefetch) {
-        tile_load(rk, k, g, wt, k0, n, hoff);
-        tile_load(rv, v, g, wt, k0, n, hoff);
-      }
-      __syncthreads();
-      tile_store<T, HD, true, false>(rk, kt, nullptr);
-      tile_store<T, HD, true, false>(rv, vr, nullptr);
-      if (threadIdx.x < kTile) kinfo[threadIdx.x] = token_info(g, i, j, cols, k0 + threadIdx.x, n);
-      __syncthreads();
-      if (kPrefetch) {
-        const int nk0 = k0 + kTile < n ? k0 + kTile : 0;
-        tile_load(rk, k, g, wt, nk0, n, hoff);
-        tile_load(rv, v, g, wt, nk0, n, hoff);
+      const int tix = RES ? k0 / kTile : 0;
+      T* kt = kt0 + tix * kTE;
+      T* vr = vr0 + tix * kTE;
+      int* kinfo = kinfo0 + tix * kTile;
+      if constexpr (!RES) {
+        if (!kPrefetch) {
+          tile_load(rk, k, g, wt, k0, n, hoff);
+          tile_load(rv, v, g, wt, k0, n, hoff);
+        }
+        __syncthreads();
+        tile_store<T, HD, true, false>(rk, kt, nullptr);
+        tile_store<T, HD, true, false>(rv, vr, nullptr);
+        if (threadIdx.x < kTile) kinfo[threadIdx.x] = token_info(g, i, j, cols, k0 + threadIdx.x, n);
+        __syncthreads();
+        if (kPrefetch) {
+          const int nk0 = k0 + kTile < n ? k0 + kTile : 0;
+          tile_load(rk, k, g, wt, nk0, n, hoff);
+          tile_load(rv, v, g, wt, nk0, n, hoff);
+        }
       }
       if (!wactive) continue;
 #pragma unroll
@@ -455,18 +486,24 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
     for (int eb = 0; eb < HD / 32; ++eb) dqacc[eb] = f32x16{};
 
     for (int k0 = 0; k0 < n; k0 += kTile) {
-      if (!kPrefetch) {
-        tile_load(rk, k, g, wt, k0, n, hoff);
-        tile_load(rv, v, g, wt, k0, n, hoff);
-      }
-      __syncthreads();
-      tile_store<T, HD, true, sizeof(T) == 4>(rk, kt, ktt);
-      tile_store<T, HD, true, false>(rv, vr, nullptr);
-      if (threadIdx.x < kTile) kinfo[threadIdx.x] = token_info(g, i, j, cols, k0 + threadIdx.x, n);
-      __syncthreads();
-      if (kPrefetch && k0 + kTile < n) {
-        tile_load(rk, k, g, wt, k0 + kTile, n, hoff);
-        tile_load(rv, v, g, wt, k0 + kTile, n, hoff);
+      const int tix = RES ? k0 / kTile : 0;
+      T* kt = kt0 + tix * kTE;
+      T* vr = vr0 + tix * kTE;
+      int* kinfo = kinfo0 + tix * kTile;
+      if constexpr (!RES) {
+        if (!kPrefetch) {
+          tile_load(rk, k, g, wt, k0, n, hoff);
+          tile_load(rv, v, g, wt, k0, n, hoff);
+        }
+        __syncthreads();
+        tile_store<T, HD, true, sizeof(T) == 4>(rk, kt, ktt);
+        tile_store<T, HD, true, false>(rv, vr, nullptr);
+        if (threadIdx.x < kTile) kinfo[threadIdx.x] = token_info(g, i, j, cols, k0 + threadIdx.x, n);
+        __syncthreads();
+        if (kPrefetch && k0 + kTile < n) {
+          tile_load(rk, k, g, wt, k0 + kTile, n, hoff);
+          tile_load(rv, v, g, wt, k0 + kTile, n, hoff);
+        }
       }
       if (!wactive) continue;
       f32x16 dsb[kTile / 32];
@@ -847,11 +884,22 @@ static size_t fwd_lds(const Geo& g) {
   constexpr int kTile = tile_of<T, HD>();
   return sizeof(T) * (kTile * (HD + kPad) + vtile_size<T, HD>()) + 4 * kTile + 4 * (g.nbins + 4);
 }
+// Key tiles the dQ kernel keeps resident for a whole item: every tile of the
+// window for 16-bit types, head_dim up to 64 and windows of up to 256 tokens
+// (the staging then happens once per item instead of once per tile and
+// sweep), else 1 (tiles streamed through one staging buffer).
+template <typename T, int HD>
+static int dq_tiles(const Geo& g) {
+  constexpr int kTile = tile_of<T, HD>();
+  if (sizeof(T) != 2 || HD > 64 || g.wh * g.ww > 256) return 1;
+  return (g.wh * g.ww + kTile - 1) / kTile;
+}
 template <typename T, int HD>
 static size_t dq_lds(const Geo& g) {
   constexpr int kTile = tile_of<T, HD>();
-  return sizeof(T) * (2 * kTile * (HD + kPad) + ttile_size<T, HD>()) + 4 * kTile + 4 * (g.nbins + 4) +
-         16 * g.nbins;
+  const int nt = dq_tiles<T, HD>(g);
+  return sizeof(T) * (2 * nt * kTile * (HD + kPad) + ttile_size<T, HD>()) + 4 * nt * kTile +
+         4 * (g.nbins + 4) + 16 * g.nbins;
 }
 template <typename T, int HD>
 static size_t dkdv_lds(const Geo& g) {
@@ -924,9 +972,18 @@ static hipError_t bwd_impl(const Geo& g, const void* q, const void* k, const voi
   const float scale = 1.0f / sqrtf((float)HD);
   const size_t lds_dq = dq_lds<T, HD>(g);
   const bool quad = quad_layout(g);
+  const bool res = dq_tiles<T, HD>(g) > 1;
+  const void* dq_fn;
+  if constexpr (sizeof(T) == 2 && HD <= 64) {
+    dq_fn = quad ? (res ? reinterpret_cast<const void*>(&bwd_dq_kernel<T, HD, NHWC, true, true>)
+                        : reinterpret_cast<const void*>(&bwd_dq_kernel<T, HD, NHWC, true, false>))
+                 : (res ? reinterpret_cast<const void*>(&bwd_dq_kernel<T, HD, NHWC, false, true>)
+                        : reinterpret_cast<const void*>(&bwd_dq_kernel<T, HD, NHWC, false, false>));
+  } else {
+    dq_fn = quad ? reinterpret_cast<const void*>(&bwd_dq_kernel<T, HD, NHWC, true, false>)
+                 : reinterpret_cast<const void*>(&bwd_dq_kernel<T, HD, NHWC, false, false>);
+  }
   int resident = 0;
-  const void* dq_fn = quad ? reinterpret_cast<const void*>(&bwd_dq_kernel<T, HD, NHWC, true>)
-                           : reinterpret_cast<const void*>(&bwd_dq_kernel<T, HD, NHWC, false>);
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&resident, dq_fn, kThreads, lds_dq) != hipSuccess) {
     (void)hipGetLastError();
     resident = 2;
@@ -934,14 +991,20 @@ static hipError_t bwd_impl(const Geo& g, const void* q, const void* k, const voi
   int nslice = slices_for(g, resident < 1 ? 1 : resident);
   const int nmax = bwd_nslice_max_t<T>(g);
   if (nslice > nmax) nslice = nmax;
-  if (quad)
-    hipLaunchKernelGGL((bwd_dq_kernel<T, HD, NHWC, true>), dim3(g.heads * nslice), dim3(kThreads),
-                       lds_dq, st, (const T*)q, (const T*)k, (const T*)v,
-                       (const T*)dout, lse, D, table, (T*)dq, partial, g, nqc, nslice, sl2, scale);
-  else
-    hipLaunchKernelGGL((bwd_dq_kernel<T, HD, NHWC, false>), dim3(g.heads * nslice), dim3(kThreads),
-                       lds_dq, st, (const T*)q, (const T*)k, (const T*)v,
-                       (const T*)dout, lse, D, table, (T*)dq, partial, g, nqc, nslice, sl2, scale);
+#define TERRA_LAUNCH_DQ(QD, RS)                                                                 \
+  hipLaunchKernelGGL((bwd_dq_kernel<T, HD, NHWC, QD, RS>), dim3(g.heads * nslice), dim3(kThreads),  \
+                     lds_dq, st, (const T*)q, (const T*)k, (const T*)v, (const T*)dout, lse, D, table, \
+                     (T*)dq, partial, g, nqc, nslice, sl2, scale)
+  if constexpr (sizeof(T) == 2 && HD <= 64) {
+    if (quad && res) TERRA_LAUNCH_DQ(true, true);
+    else if (quad) TERRA_LAUNCH_DQ(true, false);
+    else if (res) TERRA_LAUNCH_DQ(false, true);
+    else TERRA_LAUNCH_DQ(false, false);
+  } else {
+    if (quad) TERRA_LAUNCH_DQ(true, false);
+    else TERRA_LAUNCH_DQ(false, false);
+  }
+#undef TERRA_LAUNCH_DQ
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int grid = g.B * g.nwin * g.heads * nqc;
