@@ -151,6 +151,16 @@ __device__ inline bool window_needs_mask(const Geo& g, int wi, int wj, int n) {
   return window_has_labels(g, wi, wj) || (n & 31) != 0;
 }
 
+// The same for the backward, whose rotation always covers all four 32-key
+// blocks: the padding keys past n also need excluding whenever the window
+// is shorter than wh rows, because the bias-gradient flush keeps every key
+// whose row (key index / width) lies inside the window height, and padding
+// keys of a short window do.  (In a full-height window they sit at row wh
+// or beyond and the flush drops them.)
+__device__ inline bool window_needs_mask_bwd(const Geo& g, int wi, int wj, int n) {
+  return window_needs_mask(g, wi, wj, n) || (n < kWinMax && win_rows(g, wi) < g.wh);
+}
+
 // Map a linear block index to a work index so that consecutive work items
 // run on the same XCD (blocks are dealt to the 8 XCDs round-robin).
 __device__ inline int xcd_work(int bid, int nblocks) {
@@ -855,7 +865,7 @@ __global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
     st.qrev = table_qrev(g, qinf);
     st.fold = fold_mask(qi % cols, cols);
     f32x16 dqacc = f32x16{};
-    if (window_needs_mask(g, wi, wj, n)) bwd_window_body<QUAD, true>(st, qw, dta, dtb, dqacc);
+    if (window_needs_mask_bwd(g, wi, wj, n)) bwd_window_body<QUAD, true>(st, qw, dta, dtb, dqacc);
     else bwd_window_body<QUAD, false>(st, qw, dta, dtb, dqacc);
 
     // dQ rows of the wave into the K-row area (free after the rotation),

@@ -80,10 +80,14 @@ def bf16_round(x):
     """Round float32 values to the nearest bf16 (ties to even).  Returns
     float32 values that are exactly representable in bf16."""
     x = np.ascontiguousarray(x, np.float32)
-    bits = x.view(np.uint32).astype(np.uint64)
-    lsb = (bits >> 16) & 1
-    rounded = ((bits + 0x7FFF + lsb) >> 16) << 16
-    return rounded.astype(np.uint32).view(np.float32).reshape(x.shape)
+    assert np.isfinite(x).all(), "bf16_round takes finite values only"
+    bits = x.view(np.uint32)
+    # finite values have bits <= 0xFF7FFFFF, so the sum stays below 2^32
+    r = (bits >> np.uint32(16)) & np.uint32(1)
+    r += bits
+    r += np.uint32(0x7FFF)
+    r &= np.uint32(0xFFFF0000)
+    return r.view(np.float32).reshape(x.shape)
 
 
 def bf16_bits(x):

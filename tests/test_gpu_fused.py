@@ -31,6 +31,12 @@ EDGE = [
     ts.small_config("f3", "bf16", 2, 16, 40, 2, 32, 8, 8, 4, 4, 3),
     ts.small_config("f4", "bf16", 1, 30, 20, 2, 64, 15, 12, 7, 5, 1),
     ts.small_config("f5", "f32", 1, 8, 24, 1, 32, 8, 8, 0, 5, 1),
+    # unshifted 8x16 / 16x8 windows on ragged heights (short last window row
+    # without wrap labels), no mask at all, and both wraps masked
+    ts.small_config("f6", "bf16", 1, 20, 32, 2, 32, 8, 16, 0, 0, 1),
+    ts.small_config("f7", "bf16", 1, 36, 24, 2, 32, 16, 8, 0, 0, 1),
+    ts.small_config("f8", "bf16", 1, 20, 40, 2, 32, 8, 16, 4, 8, 0),
+    ts.small_config("f9", "bf16", 1, 24, 48, 2, 32, 8, 16, 4, 8, 3),
 ]
 
 

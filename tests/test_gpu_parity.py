@@ -2,10 +2,11 @@
 
 Routing must match bit for bit.  Attention must match within max abs 1e-5
 (fp32) or max abs 2e-2 and relative L2 5e-3 (bf16, fp32 accumulation), on O,
-LSE, dQ, dK, dV and the bias-table gradient.  Small configurations are
-compared everywhere; the two full-size ones on sampled windows (first, last,
-latitude-seam, partial-column and random windows) plus the whole bias-table
-gradient from stored oracle values.
+LSE, dQ, dK, dV and the bias-table gradient.  Small configurations and the
+128 x 1080 workload are compared on every window against the whole oracle;
+the 256 x 540 workload (whose whole oracle takes minutes on the host) on 22
+sampled windows of every class plus the whole bias-table gradient from
+stored oracle values.
 """
 
 import os
@@ -26,7 +27,6 @@ pytestmark = pytest.mark.gpu
 
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
 SMALL = ["c1_f32_16x32_w8", "c2_bf16_128x256_w8", "c3_bf16_85x180_w12"]
-LARGE = ["c4_bf16_128x1080_w8x16", "c5_bf16_256x540_w24"]
 
 
 def _say(msg):
@@ -159,6 +159,17 @@ EDGE = [
     ("w8_lon_mask", ts.small_config("e12", "bf16", 2, 16, 40, 2, 32, 8, 8, 4, 4, 3)),
     # narrow 16x4 windows, ragged height
     ("tall_w4", ts.small_config("e10", "bf16", 1, 37, 28, 2, 32, 16, 4, 8, 2, 1)),
+    # unshifted (W-MSA) 8x16 windows on a ragged height: the last window row
+    # holds 4 x 16 = 64 tokens with no wrap label, so the window backward
+    # must still exclude the 64 padding keys of its rotation
+    ("w8x16_noshift_ragged", ts.small_config("e13", "bf16", 1, 20, 32, 2, 32, 8, 16, 0, 0, 1)),
+    # the same for 16x8 windows (last window row 4 x 8 = 32 tokens)
+    ("w16x8_noshift_ragged", ts.small_config("e14", "bf16", 1, 36, 24, 2, 32, 16, 8, 0, 0, 1)),
+    # shifted 8x16 windows with no mask at all (mask_flags 0), ragged both ways
+    ("w8x16_no_mask", ts.small_config("e15", "bf16", 1, 20, 40, 2, 32, 8, 16, 4, 8, 0)),
+    # shifted 8x16 windows with both wraps masked: the window backward's
+    # instance without the four-key quad layout
+    ("w8x16_both_masks", ts.small_config("e16", "bf16", 1, 24, 48, 2, 32, 8, 16, 4, 8, 3)),
 ]
 
 
@@ -176,20 +187,44 @@ def test_attention_edge_cases(label, cfg):
         _assert_close(nm, _host(a), b, cfg)
 
 
-def test_large_logits_stay_finite():
-    # Q scaled by 4 -> logits of several units; exercises the running max.
-    cfg = ts.CONFIGS["c2_bf16_128x256_w8"]
+@pytest.mark.parametrize("name", ["c2_bf16_128x256_w8", "c4_small_bf16_24x80_w8x16"])
+def test_large_logits_stay_finite(name):
+    # Q scaled by 4 -> logits of several units; exercises the running max of
+    # the forward and the recomputed P of the backward (c2's 8x8 windows take
+    # the generic backward, the 8x16 windows the window-resident one).
+    cfg = ts.CONFIGS.get(name) or ts.small_config(name, "bf16", 1, 24, 80, 4, 32, 8, 16, 4, 8)
     g = Geometry(**cfg.geom_kwargs())
+    _say("large logits %s" % name)
     inp = ts.make_inputs(cfg, seed=5, q_scale=4.0)
     got = _run_gpu(cfg, inp)
-    sel = [0, 31, 480, 511]
+    mh, mw = -(-cfg.H // cfg.wh), -(-cfg.W // cfg.ww)
+    sel = sorted({0, mw - 1, mw + 2, (mh - 1) * mw, mh * mw - 1})
     q, k, v, do = (o_route(inp[n], g) for n in ("q", "k", "v", "dout"))
     ref = attn_fwd_windows(q, k, v, inp["table"], g, sel)
+    bref = attn_bwd_windows(q, k, v, do, inp["table"], g, sel)
     slots = {w: (s, n) for w, s, n in window_slots(g)}
     for w in sel:
         s, n = slots[w]
+        for nm, t in (("O", got["o"]), ("dQ", got["dq"]), ("dK", got["dk"]), ("dV", got["dv"])):
+            assert torch.isfinite(t[:, s:s + n]).all(), nm
         _assert_close("O", _host(got["o"][:, s:s + n]), ref[w][0], cfg)
         _assert_close("LSE", _host(got["lse"][:, :, s:s + n]), ref[w][1], cfg)
+        for i, nm in enumerate(("dQ", "dK", "dV")):
+            # The 2e-2 max-abs bar is set for unit-scale inputs, where the
+            # gradients peak near 2.  With logits four times larger dK peaks
+            # near 15 (its bf16 storage alone moves it by up to 0.03), and the
+            # bf16 dS operands (reading 10) err in proportion to the terms
+            # summed, not to the result: rounding only dS to bf16 and summing
+            # exactly gives dQ errors of 3.8e-3 to 5.6e-3 of max |dQ| on these
+            # windows.  So here the max-abs error is taken relative to the
+            # largest reference magnitude, with a bar of 1e-2, beside the
+            # unchanged 5e-3 relative L2 bar.
+            gref = bref[w][i]
+            got_w = _host(got[nm.lower()][:, s:s + n])
+            err = float(np.abs(got_w - gref).max()) / float(np.abs(gref).max())
+            assert err <= 1e-2, "%s max abs err / max |ref| = %.3g > 1e-2" % (nm, err)
+            rel = np.linalg.norm(got_w - gref) / np.linalg.norm(gref)
+            assert rel <= 5e-3, "%s rel L2 err %.3g > 5e-3" % (nm, rel)
 
 
 @pytest.mark.parametrize("name", ["c2_bf16_128x256_w8", "c3_bf16_85x180_w12"])
@@ -202,23 +237,91 @@ def test_bias_gradient_is_bit_reproducible(name):
 
 
 # ------------------------------------------------------------------ full-size configs
-def _sample_windows(cfg, g, seed=0):
+def _sample_windows(cfg, g, seed=0, extra=4):
     mh, mw = -(-cfg.H // cfg.wh), -(-cfg.W // cfg.ww)
     last = mh * mw - 1
     pick = {0, mw - 1, (mh - 1) * mw, last, (mh - 2) * mw + 3, mw + mw - 1}
     rng = np.random.default_rng(seed)
-    pick.update(int(x) for x in rng.integers(0, last + 1, 4))
+    pick.update(int(x) for x in rng.integers(0, last + 1, extra))
     return sorted(pick)
 
 
-@pytest.mark.parametrize("name", LARGE)
-def test_attention_full_size_sampled(name):
-    cfg = ts.CONFIGS[name]
+def _close_chunked(name, got_t, ref, cfg, chunk=1 << 22):
+    """max abs and relative L2 of a whole device tensor against an fp64
+    reference, moved to the host in chunks of rows."""
+    got_t = got_t.reshape(-1)
+    ref = np.asarray(ref).reshape(-1)
+    err = 0.0
+    diff2 = 0.0
+    ref2 = 0.0
+    for lo in range(0, ref.size, chunk):
+        a = got_t[lo:lo + chunk].float().cpu().numpy().astype(np.float64)
+        b = ref[lo:lo + chunk]
+        d = a - b
+        err = max(err, float(np.abs(d).max()))
+        diff2 += float((d * d).sum())
+        ref2 += float((b * b).sum())
+    assert err <= 2e-2, "%s max abs err %.3g > 2e-2" % (name, err)
+    rel = np.sqrt(diff2 / ref2)
+    assert rel <= 5e-3, "%s rel L2 err %.3g > 5e-3" % (name, rel)
+    return err, rel
+
+
+@pytest.fixture(scope="module")
+def c4_full():
+    """The 128 x 1080 workload (24 heads x 32, 8 x 16 windows, shift (4, 8))
+    run once through the window-major entry points, with the routed inputs
+    kept for the oracle."""
+    cfg = ts.CONFIGS["c4_bf16_128x1080_w8x16"]
     g = Geometry(**cfg.geom_kwargs())
-    _say("full-size attention %s" % name)
+    _say("c4 full: inputs and GPU run")
     inp = ts.make_inputs(cfg)
     got = _run_gpu(cfg, inp)
-    sel = _sample_windows(cfg, g)
+    routed = {n: o_route(inp[n], g) for n in ("q", "k", "v", "dout")}
+    table = inp["table"]
+    del inp
+    yield cfg, g, got, routed, table
+    del got
+    torch.cuda.empty_cache()
+
+
+def test_c4_forward_every_window(c4_full):
+    # O and LSE of all 1088 windows against the whole oracle forward.
+    cfg, g, got, r, table = c4_full
+    _say("c4 full: oracle forward")
+    o, lse = attn_fwd(r["q"], r["k"], r["v"], table, g)
+    _close_chunked("O", got["o"], o, cfg)
+    _close_chunked("LSE", got["lse"], lse, cfg)
+
+
+def test_c4_backward_every_window(c4_full):
+    # dQ, dK, dV of all 1088 windows and the whole bias-table gradient
+    # against the whole oracle backward (and the stored oracle dT).
+    cfg, g, got, r, table = c4_full
+    _say("c4 full: oracle backward")
+    dq, dk, dv, dt = attn_bwd(r["q"], r["k"], r["v"], r["dout"], table, g)
+    _close_chunked("dQ", got["dq"], dq, cfg)
+    _close_chunked("dK", got["dk"], dk, cfg)
+    _close_chunked("dV", got["dv"], dv, cfg)
+    _assert_close("dT", _host(got["dt"]), dt, cfg)
+    gold = np.load(os.path.join(GOLDEN, "dtable_%s.npy" % cfg.name))
+    assert np.abs(gold - dt).max() < 1e-9      # the stored oracle value is the oracle's
+    sums = _host(got["dt"]).sum(axis=(0, 1))
+    assert np.abs(sums).max() < 1e-2
+
+
+def test_c5_attention_sampled_windows():
+    # 256 x 540, 24 heads x 64, 24 x 24 windows: the whole oracle takes
+    # minutes here, so O, LSE, dQ, dK and dV are compared on 22 windows (every
+    # window class: 576, 384, 288 and 192 tokens, the seams, and runs of
+    # neighbouring windows that the persistent kernels walk in sequence),
+    # plus the whole bias-table gradient from stored oracle values.
+    cfg = ts.CONFIGS["c5_bf16_256x540_w24"]
+    g = Geometry(**cfg.geom_kwargs())
+    _say("full-size attention %s" % cfg.name)
+    inp = ts.make_inputs(cfg)
+    got = _run_gpu(cfg, inp)
+    sel = sorted(set(_sample_windows(cfg, g, extra=6)) | {40, 41, 42, 43, 44, 45, 120, 121})
     q, k, v, do = (o_route(inp[n], g) for n in ("q", "k", "v", "dout"))
     fw = attn_fwd_windows(q, k, v, inp["table"], g, sel)
     bw = attn_bwd_windows(q, k, v, do, inp["table"], g, sel)
@@ -230,9 +333,7 @@ def test_attention_full_size_sampled(name):
         _assert_close("dQ[w%d]" % w, _host(got["dq"][:, s:s + n]), bw[w][0], cfg)
         _assert_close("dK[w%d]" % w, _host(got["dk"][:, s:s + n]), bw[w][1], cfg)
         _assert_close("dV[w%d]" % w, _host(got["dv"][:, s:s + n]), bw[w][2], cfg)
-    # whole bias-table gradient against the stored oracle result
-    gold = np.load(os.path.join(GOLDEN, "dtable_%s.npy" % name))
+    gold = np.load(os.path.join(GOLDEN, "dtable_%s.npy" % cfg.name))
     _assert_close("dT", _host(got["dt"]), gold, cfg)
-    # every head's bias gradient sums to zero (each row of dS sums to zero)
     sums = _host(got["dt"]).sum(axis=(0, 1))
     assert np.abs(sums).max() < 1e-2
