@@ -162,6 +162,95 @@ int terra_winattn_bwd_nhwc(const terra_geom* g, int dtype, const void* q,
                            void* dv, float* dbias_table, void* workspace,
                            size_t workspace_bytes, void* stream);
 
+/* ---------------------------------------------------------------------------
+ * Window assignment across ranks and the per-rank token route.
+ *
+ * On a multi-GPU run the token grid is held in DMP height stripes (the I/O
+ * topology, Sec. IV-B) and attention runs on complete windows owned by WP
+ * ranks (Sec. IV-C).  The calls below plan the ragged row-major ownership of
+ * Sec. V-A (Eq. (4)), list for one rank the rectangles of the grid it must
+ * receive from other ranks for its route (the boundary fragments of the
+ * shift route, Sec. IV-D), and run that rank's route and its inverse from
+ * its own stripe plus a buffer holding those fragments.  On one GPU the
+ * ranks are run one after another, and the fragment copy stands in for the
+ * point-to-point exchange.
+ *
+ * Stripes.  Rank r of P holds grid rows [floor(r H / P), floor((r+1) H / P))
+ *   of every image, as a B x rows x W x C tensor (the floor rule of Eq. (4)
+ *   applied to rows; equal stripes when P divides H, as on the paper's
+ *   padded grids).
+ * Windows.  Rank r owns windows [L_r, R_r), L_r = floor(r M / P), of every
+ *   image, M = Mh * Mw in row-major order (Eq. (4)); its window-major
+ *   tensor is B x (slot_end - slot_begin) x C, the slots of those windows in
+ *   the layout of terra_window_route.
+ * Fragments.  Rows [u0, u1) x columns [v0, v1) of the original grid held by
+ *   rank src_rank, stored row-major from token `offset` of the receiving
+ *   rank's fragment buffer (B x frag_tokens x C, image-major).  They are
+ *   sorted by source rank, so everything one rank sends to another is one
+ *   contiguous run of the buffer.
+ * ------------------------------------------------------------------------- */
+
+#define TERRA_MAX_FRAGMENTS 64
+
+typedef struct terra_rank_plan {
+  int32_t win_begin, win_end;     /* Eq. (4) window range [L_r, R_r)          */
+  int32_t slot_begin, slot_end;   /* its window-major slots, per image        */
+  int32_t row_begin, row_end;     /* DMP stripe rows held by the rank         */
+  int32_t nfrag;                  /* fragments received from other ranks      */
+  int32_t frag_tokens;            /* tokens per image in the fragment buffer  */
+} terra_rank_plan;
+
+typedef struct terra_fragment {
+  int32_t src_rank;               /* rank whose stripe holds the rectangle    */
+  int32_t u0, u1, v0, v1;         /* grid rows [u0, u1), columns [v0, v1)     */
+  int32_t offset;                 /* first token in the fragment buffer       */
+} terra_fragment;
+
+/* Eq. (3): padded input size of the fixed window assignment on an m x n WP
+ * mesh, Hhat = ceil(H / (p alpha w m)) p alpha w m (What likewise with n),
+ * for patch size p, down-sampling stride alpha and window w.  m = n = 1
+ * gives the least padding to whole windows.  overhead (nullable) receives
+ * Hhat What / (H W) - 1.  Host only. */
+int terra_plan_padded_grid(int32_t H, int32_t W, int32_t p, int32_t alpha, int32_t w, int32_t m,
+                           int32_t n, int32_t* Hhat, int32_t* What, double* overhead);
+
+/* Eq. (4): bounds[r] = floor(r M / ranks) for r = 0 .. ranks (ranks + 1
+ * host entries); rank r owns windows [bounds[r], bounds[r+1]).  Host only. */
+int terra_plan_window_ranges(int64_t M, int32_t ranks, int64_t* bounds);
+
+/* Plan of rank `rank` among `ranks` for the geometry g (its window range,
+ * slots, stripe and received fragments).  frags (nullable) receives
+ * plan->nfrag entries, at most TERRA_MAX_FRAGMENTS.  TERRA_ERR_UNSUPPORTED
+ * when the rank would receive more fragments (stripes far thinner than a
+ * window).  Host only. */
+int terra_plan_rank(const terra_geom* g, int32_t ranks, int32_t rank, terra_rank_plan* plan,
+                    terra_fragment* frags);
+
+/* Route of one rank: its window-major tensor y_win (B x (slot_end -
+ * slot_begin) x C) gathered from its stripe and its fragment buffer
+ * (layouts above).  Equals the corresponding slots of terra_window_route of
+ * the whole grid, bit for bit.  Device pointers; frag_buf may be NULL when
+ * the plan has no fragments. */
+int terra_window_route_rank(const terra_geom* g, int dtype, int32_t ranks, int32_t rank,
+                            const void* stripe, const void* frag_buf, void* y_win, void* stream);
+
+/* Inverse of terra_window_route_rank (its backward, Sec. IV-D): scatters
+ * y_win back to the rank's stripe and its fragment buffer.  Every element
+ * of the stripe that the rank's windows cover, and every fragment token, is
+ * overwritten; the rest is left as it was. */
+int terra_window_unroute_rank(const terra_geom* g, int dtype, int32_t ranks, int32_t rank,
+                              const void* y_win, void* stripe, void* frag_buf, void* stream);
+
+/* The exchange of the fragments of rank dst_rank's plan whose source is
+ * src_rank: pack copies them from src_rank's stripe into dst_rank's
+ * fragment buffer (the send and the receive of the point-to-point exchange
+ * in one copy), unpack copies them back (the backward).  Nothing is done
+ * when dst_rank receives nothing from src_rank. */
+int terra_fragment_pack(const terra_geom* g, int dtype, int32_t ranks, int32_t dst_rank,
+                        int32_t src_rank, const void* src_stripe, void* frag_buf, void* stream);
+int terra_fragment_unpack(const terra_geom* g, int dtype, int32_t ranks, int32_t dst_rank,
+                          int32_t src_rank, const void* frag_buf, void* src_stripe, void* stream);
+
 /* Static string naming a status code. */
 const char* terra_status_string(int status);
 

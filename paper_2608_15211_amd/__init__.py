@@ -10,7 +10,10 @@ Entry points (same names as the C ABI):
     terra_validate_geometry, terra_window_count, terra_window_layout,
     terra_window_route, terra_window_unroute, terra_winattn_fwd,
     terra_winattn_bwd_workspace_bytes, terra_winattn_bwd,
-    terra_winattn_fwd_nhwc, terra_winattn_bwd_nhwc (route fused in)
+    terra_winattn_fwd_nhwc, terra_winattn_bwd_nhwc (route fused in),
+    terra_plan_padded_grid, terra_plan_window_ranges, terra_plan_rank,
+    terra_window_route_rank, terra_window_unroute_rank, terra_fragment_pack,
+    terra_fragment_unpack (ragged window assignment and per-rank route)
 """
 
 import ctypes
@@ -46,6 +49,24 @@ class terra_geom(ctypes.Structure):
         return {n: getattr(self, n) for n, _ in self._fields_}
 
 
+class terra_rank_plan(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in
+                ("win_begin", "win_end", "slot_begin", "slot_end", "row_begin", "row_end",
+                 "nfrag", "frag_tokens")]
+
+    def as_dict(self):
+        return {n: getattr(self, n) for n, _ in self._fields_}
+
+
+class terra_fragment(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("src_rank", "u0", "u1", "v0", "v1", "offset")]
+
+    def as_dict(self):
+        return {n: getattr(self, n) for n, _ in self._fields_}
+
+
+TERRA_MAX_FRAGMENTS = 64
+
 _lib = None
 
 
@@ -72,12 +93,25 @@ def lib():
     L.terra_winattn_bwd_workspace_bytes.restype = sz
     L.terra_winattn_bwd.argtypes = [G, i32] + [vp] * 12 + [sz, vp]
     L.terra_winattn_bwd_nhwc.argtypes = [G, i32] + [vp] * 12 + [sz, vp]
+    i64 = ctypes.c_int64
+    L.terra_plan_padded_grid.argtypes = [i32] * 7 + [ctypes.POINTER(ctypes.c_int32)] * 2 + \
+        [ctypes.POINTER(ctypes.c_double)]
+    L.terra_plan_window_ranges.argtypes = [i64, i32, ctypes.POINTER(ctypes.c_int64)]
+    L.terra_plan_rank.argtypes = [G, i32, i32, ctypes.POINTER(terra_rank_plan),
+                                  ctypes.POINTER(terra_fragment)]
+    L.terra_window_route_rank.argtypes = [G, i32, i32, i32, vp, vp, vp, vp]
+    L.terra_window_unroute_rank.argtypes = [G, i32, i32, i32, vp, vp, vp, vp]
+    L.terra_fragment_pack.argtypes = [G, i32, i32, i32, i32, vp, vp, vp]
+    L.terra_fragment_unpack.argtypes = [G, i32, i32, i32, i32, vp, vp, vp]
     L.terra_status_string.argtypes = [i32]
     L.terra_status_string.restype = ctypes.c_char_p
     L.terra_last_error.restype = ctypes.c_char_p
     for name in ("terra_validate_geometry", "terra_window_count", "terra_window_layout",
                  "terra_window_route", "terra_window_unroute", "terra_winattn_fwd",
-                 "terra_winattn_bwd", "terra_winattn_fwd_nhwc", "terra_winattn_bwd_nhwc"):
+                 "terra_winattn_bwd", "terra_winattn_fwd_nhwc", "terra_winattn_bwd_nhwc",
+                 "terra_plan_padded_grid", "terra_plan_window_ranges", "terra_plan_rank",
+                 "terra_window_route_rank", "terra_window_unroute_rank", "terra_fragment_pack",
+                 "terra_fragment_unpack"):
         getattr(L, name).restype = i32
     _lib = L
     return L
@@ -242,3 +276,98 @@ def terra_winattn_bwd(q, k, v, o, dout, lse, table, g, out=None, workspace=None)
 def terra_winattn_bwd_nhwc(q, k, v, o, dout, lse, table, g, out=None, workspace=None):
     """As terra_winattn_bwd with NHWC tensors and NHWC-ordered LSE."""
     return _attn_bwd(lib().terra_winattn_bwd_nhwc, q, k, v, o, dout, lse, table, g, out, workspace)
+
+
+# ---------------------------------------------------------------- ranks
+def terra_plan_padded_grid(H, W, p, alpha, w, m=1, n=1):
+    """Eq. (3): (H_hat, W_hat, overhead) of the fixed assignment on an m x n mesh."""
+    hh, ww, ov = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_double()
+    _check(lib().terra_plan_padded_grid(H, W, p, alpha, w, m, n, ctypes.byref(hh), ctypes.byref(ww),
+                                        ctypes.byref(ov)))
+    return hh.value, ww.value, ov.value
+
+
+def terra_plan_window_ranges(M, ranks):
+    """Eq. (4): [L_0, L_1, ..., L_ranks = M]."""
+    out = (ctypes.c_int64 * (ranks + 1))()
+    _check(lib().terra_plan_window_ranges(M, ranks, out))
+    return list(out)
+
+
+def terra_plan_rank(g, ranks, rank):
+    """(plan dict, [fragment dicts]) of one rank."""
+    plan = terra_rank_plan()
+    frags = (terra_fragment * TERRA_MAX_FRAGMENTS)()
+    _check(lib().terra_plan_rank(ctypes.byref(_geom(g)), ranks, rank, ctypes.byref(plan), frags))
+    return plan.as_dict(), [frags[i].as_dict() for i in range(plan.nfrag)]
+
+
+def _opt(t, name, dtype):
+    return ctypes.c_void_p(0) if t is None else _dev(t, name, dtype)
+
+
+def terra_window_route_rank(stripe, frag_buf, g, ranks, rank, out=None):
+    """Rank `rank`'s window-major tensor (B, slot_end - slot_begin, C) from
+    its stripe (B, rows, W, C) and fragment buffer (B, frag_tokens, C)."""
+    import torch
+    gg = _geom(g)
+    plan, _ = terra_plan_rank(gg, ranks, rank)
+    dt = stripe.dtype
+    if stripe.numel() != gg.B * (plan["row_end"] - plan["row_begin"]) * gg.W * gg.C:
+        raise ValueError("stripe has %d elements, expected B*rows*W*C" % stripe.numel())
+    if frag_buf is not None and frag_buf.numel() != gg.B * plan["frag_tokens"] * gg.C:
+        raise ValueError("fragment buffer has %d elements, expected B*frag_tokens*C" % frag_buf.numel())
+    ntok = plan["slot_end"] - plan["slot_begin"]
+    if out is None:
+        out = torch.empty((gg.B, ntok, gg.C), dtype=dt, device=stripe.device)
+    elif out.numel() != gg.B * ntok * gg.C:
+        raise ValueError("out has %d elements, expected B*tokens*C" % out.numel())
+    _check(lib().terra_window_route_rank(ctypes.byref(gg), _dtype_code(dt), ranks, rank,
+                                         _dev(stripe, "stripe", dt), _opt(frag_buf, "frag_buf", dt),
+                                         _dev(out, "out", dt), _stream()))
+    return out
+
+
+def terra_window_unroute_rank(y_win, g, ranks, rank, stripe, frag_buf):
+    """Inverse of terra_window_route_rank: y_win back into stripe and frag_buf."""
+    gg = _geom(g)
+    plan, _ = terra_plan_rank(gg, ranks, rank)
+    dt = y_win.dtype
+    if y_win.numel() != gg.B * (plan["slot_end"] - plan["slot_begin"]) * gg.C:
+        raise ValueError("y_win has %d elements, expected B*tokens*C" % y_win.numel())
+    if stripe.numel() != gg.B * (plan["row_end"] - plan["row_begin"]) * gg.W * gg.C:
+        raise ValueError("stripe has %d elements, expected B*rows*W*C" % stripe.numel())
+    if frag_buf is not None and frag_buf.numel() != gg.B * plan["frag_tokens"] * gg.C:
+        raise ValueError("fragment buffer has %d elements, expected B*frag_tokens*C" % frag_buf.numel())
+    _check(lib().terra_window_unroute_rank(ctypes.byref(gg), _dtype_code(dt), ranks, rank,
+                                           _dev(y_win, "y_win", dt), _dev(stripe, "stripe", dt),
+                                           _opt(frag_buf, "frag_buf", dt), _stream()))
+
+
+def _frag_sizes(gg, ranks, dst_rank, src_rank, stripe, frag_buf):
+    plan, _ = terra_plan_rank(gg, ranks, dst_rank)
+    rows = (src_rank + 1) * gg.H // ranks - src_rank * gg.H // ranks
+    if stripe.numel() != gg.B * rows * gg.W * gg.C:
+        raise ValueError("source stripe has %d elements, expected B*rows*W*C" % stripe.numel())
+    if frag_buf.numel() != gg.B * plan["frag_tokens"] * gg.C:
+        raise ValueError("fragment buffer has %d elements, expected B*frag_tokens*C" % frag_buf.numel())
+
+
+def terra_fragment_pack(src_stripe, frag_buf, g, ranks, dst_rank, src_rank):
+    """Copy the fragments dst_rank receives from src_rank into its buffer."""
+    gg = _geom(g)
+    _frag_sizes(gg, ranks, dst_rank, src_rank, src_stripe, frag_buf)
+    dt = src_stripe.dtype
+    _check(lib().terra_fragment_pack(ctypes.byref(gg), _dtype_code(dt), ranks, dst_rank, src_rank,
+                                     _dev(src_stripe, "src_stripe", dt), _dev(frag_buf, "frag_buf", dt),
+                                     _stream()))
+
+
+def terra_fragment_unpack(frag_buf, src_stripe, g, ranks, dst_rank, src_rank):
+    """Copy those fragments back into src_rank's stripe (the backward)."""
+    gg = _geom(g)
+    _frag_sizes(gg, ranks, dst_rank, src_rank, src_stripe, frag_buf)
+    dt = src_stripe.dtype
+    _check(lib().terra_fragment_unpack(ctypes.byref(gg), _dtype_code(dt), ranks, dst_rank, src_rank,
+                                       _dev(frag_buf, "frag_buf", dt), _dev(src_stripe, "src_stripe", dt),
+                                       _stream()))

@@ -2,10 +2,12 @@
 // include/terra_swin.h): host-side argument checks, geometry set-up and
 // dispatch to the gfx950 kernels.  No allocation, no synchronisation.
 #include <stdarg.h>
+#include <stdint.h>
 #include <stdio.h>
 #include <string>
 
 #include "terra_common.h"
+#include "terra_plan.h"
 #include "../../include/terra_swin.h"
 
 namespace terra {
@@ -19,6 +21,11 @@ hipError_t launch_attn_bwd(const Geo& g, int dt, bool nhwc, const void* q, const
                            hipStream_t st);
 size_t bwd_workspace(const Geo& g, int dt);
 size_t attn_max_lds(const Geo& g, int dt);
+hipError_t launch_route_rank(const Geo& g, int row_bytes, const RankPlan& plan, const Frag* frags,
+                             void* stripe, void* fbuf, void* y, bool forward, hipStream_t st);
+hipError_t launch_frag_copy(const Geo& g, int row_bytes, const RankPlan& plan, const Frag* frags,
+                            int src, int src_row_begin, int src_row_end, void* stripe, void* fbuf,
+                            bool pack, hipStream_t st);
 }  // namespace terra
 
 namespace {
@@ -253,6 +260,134 @@ int terra_winattn_bwd_nhwc(const terra_geom* g, int dtype, const void* q, const 
                            void* stream) {
   return attn_bwd_common(g, dtype, true, q, k, v, o, dout, lse, bias_table, dq, dk, dv,
                          dbias_table, workspace, workspace_bytes, stream);
+}
+
+int terra_plan_padded_grid(int32_t H, int32_t W, int32_t p, int32_t alpha, int32_t w, int32_t m,
+                           int32_t n, int32_t* Hhat, int32_t* What, double* overhead) {
+  if (H < 1 || W < 1 || p < 1 || alpha < 1 || w < 1 || m < 1 || n < 1)
+    return fail(TERRA_ERR_INVALID, "H, W, p, alpha, w, m and n must be >= 1");
+  if (!Hhat || !What) return fail(TERRA_ERR_INVALID, "output pointer is NULL");
+  int64_t hh, ww;
+  terra::plan_padded(H, W, p, alpha, w, m, n, &hh, &ww);
+  if (hh > INT32_MAX || ww > INT32_MAX) return fail(TERRA_ERR_UNSUPPORTED, "padded size exceeds 2^31-1");
+  *Hhat = (int32_t)hh;
+  *What = (int32_t)ww;
+  if (overhead) *overhead = (double)hh * (double)ww / ((double)H * (double)W) - 1.0;
+  return ok();
+}
+
+int terra_plan_window_ranges(int64_t M, int32_t ranks, int64_t* bounds) {
+  if (M < 0 || ranks < 1) return fail(TERRA_ERR_INVALID, "need M >= 0 and ranks >= 1");
+  if (!bounds) return fail(TERRA_ERR_INVALID, "output pointer is NULL");
+  if (M > ((int64_t)1 << 40) || ranks > (1 << 20))
+    return fail(TERRA_ERR_UNSUPPORTED, "M above 2^40 or more than 2^20 ranks");
+  for (int32_t r = 0; r <= ranks; ++r) bounds[r] = terra::range_begin(M, ranks, r);
+  return ok();
+}
+
+static int plan_common(const terra_geom* g, int32_t ranks, int32_t rank, terra::RankPlan* plan,
+                       terra::Frag* frags) {
+  int s = check_geom(g);
+  if (s) return s;
+  if (ranks < 1 || rank < 0 || rank >= ranks)
+    return fail(TERRA_ERR_INVALID, "need ranks >= 1 and 0 <= rank (%d) < ranks (%d)", rank, ranks);
+  if (ranks > 65536) return fail(TERRA_ERR_UNSUPPORTED, "more than 65536 ranks");
+  terra::Geo G = make_geo(g);
+  if (terra::plan_rank(G, ranks, rank, plan, frags, terra::kMaxFrags) < 0)
+    return fail(TERRA_ERR_UNSUPPORTED,
+                "rank %d of %d receives more than %d fragments (stripes much thinner than a window)",
+                rank, ranks, terra::kMaxFrags);
+  return ok();
+}
+
+int terra_plan_rank(const terra_geom* g, int32_t ranks, int32_t rank, terra_rank_plan* plan,
+                    terra_fragment* frags) {
+  if (!plan) return fail(TERRA_ERR_INVALID, "plan pointer is NULL");
+  terra::RankPlan P;
+  terra::Frag F[terra::kMaxFrags];
+  int s = plan_common(g, ranks, rank, &P, F);
+  if (s) return s;
+  plan->win_begin = P.win_begin; plan->win_end = P.win_end;
+  plan->slot_begin = P.slot_begin; plan->slot_end = P.slot_end;
+  plan->row_begin = P.row_begin; plan->row_end = P.row_end;
+  plan->nfrag = P.nfrag; plan->frag_tokens = P.frag_tokens;
+  if (frags)
+    for (int f = 0; f < P.nfrag; ++f) {
+      frags[f].src_rank = F[f].src;
+      frags[f].u0 = F[f].u0; frags[f].u1 = F[f].u1;
+      frags[f].v0 = F[f].v0; frags[f].v1 = F[f].v1;
+      frags[f].offset = F[f].offset;
+    }
+  return ok();
+}
+
+static int rank_route_common(const terra_geom* g, int dtype, int32_t ranks, int32_t rank,
+                             void* stripe, void* frag_buf, void* y_win, bool forward, void* stream) {
+  terra::RankPlan P;
+  terra::Frag F[terra::kMaxFrags];
+  int s = plan_common(g, ranks, rank, &P, F);
+  if (s) return s;
+  if ((s = check_dtype(dtype))) return s;
+  const bool need_y = P.slot_end > P.slot_begin;
+  if ((need_y && !y_win) || (P.row_end > P.row_begin && need_y && !stripe) ||
+      (P.frag_tokens > 0 && !frag_buf))
+    return fail(TERRA_ERR_INVALID, "tensor pointer is NULL");
+  const int esize = dtype == TERRA_F32 ? 4 : 2;
+  const int64_t row_bytes = (int64_t)g->C * esize;
+  if ((int64_t)g->wh * g->ww * (row_bytes / 2) >= ((int64_t)1 << 22))
+    return fail(TERRA_ERR_UNSUPPORTED, "window of %d tokens x %lld bytes is too large to route",
+                g->wh * g->ww, (long long)row_bytes);
+  terra::Geo G = make_geo(g);
+  return hip_status(terra::launch_route_rank(G, (int)row_bytes, P, F, stripe, frag_buf, y_win, forward,
+                                             (hipStream_t)stream),
+                    forward ? "terra_window_route_rank launch" : "terra_window_unroute_rank launch");
+}
+
+int terra_window_route_rank(const terra_geom* g, int dtype, int32_t ranks, int32_t rank,
+                            const void* stripe, const void* frag_buf, void* y_win, void* stream) {
+  return rank_route_common(g, dtype, ranks, rank, const_cast<void*>(stripe),
+                           const_cast<void*>(frag_buf), y_win, true, stream);
+}
+
+int terra_window_unroute_rank(const terra_geom* g, int dtype, int32_t ranks, int32_t rank,
+                              const void* y_win, void* stripe, void* frag_buf, void* stream) {
+  return rank_route_common(g, dtype, ranks, rank, stripe, frag_buf, const_cast<void*>(y_win), false,
+                           stream);
+}
+
+static int frag_common(const terra_geom* g, int dtype, int32_t ranks, int32_t dst_rank,
+                       int32_t src_rank, void* src_stripe, void* frag_buf, bool pack, void* stream) {
+  terra::RankPlan P;
+  terra::Frag F[terra::kMaxFrags];
+  int s = plan_common(g, ranks, dst_rank, &P, F);
+  if (s) return s;
+  if ((s = check_dtype(dtype))) return s;
+  if (src_rank < 0 || src_rank >= ranks)
+    return fail(TERRA_ERR_INVALID, "src_rank %d outside [0, %d)", src_rank, ranks);
+  bool any = false;
+  for (int f = 0; f < P.nfrag; ++f) any = any || F[f].src == src_rank;
+  if (!any) return ok();
+  if (!src_stripe || !frag_buf) return fail(TERRA_ERR_INVALID, "tensor pointer is NULL");
+  if (src_stripe == frag_buf) return fail(TERRA_ERR_INVALID, "stripe and fragment buffer must differ");
+  const int esize = dtype == TERRA_F32 ? 4 : 2;
+  terra::Geo G = make_geo(g);
+  return hip_status(terra::launch_frag_copy(G, g->C * esize, P, F, src_rank,
+                                            terra::stripe_begin(g->H, ranks, src_rank),
+                                            terra::stripe_begin(g->H, ranks, src_rank + 1), src_stripe,
+                                            frag_buf, pack, (hipStream_t)stream),
+                    pack ? "terra_fragment_pack launch" : "terra_fragment_unpack launch");
+}
+
+int terra_fragment_pack(const terra_geom* g, int dtype, int32_t ranks, int32_t dst_rank,
+                        int32_t src_rank, const void* src_stripe, void* frag_buf, void* stream) {
+  return frag_common(g, dtype, ranks, dst_rank, src_rank, const_cast<void*>(src_stripe), frag_buf,
+                     true, stream);
+}
+
+int terra_fragment_unpack(const terra_geom* g, int dtype, int32_t ranks, int32_t dst_rank,
+                          int32_t src_rank, const void* frag_buf, void* src_stripe, void* stream) {
+  return frag_common(g, dtype, ranks, dst_rank, src_rank, src_stripe, const_cast<void*>(frag_buf),
+                     false, stream);
 }
 
 const char* terra_status_string(int status) {
