@@ -162,6 +162,25 @@ int terra_winattn_bwd_nhwc(const terra_geom* g, int dtype, const void* q,
                            void* dv, float* dbias_table, void* workspace,
                            size_t workspace_bytes, void* stream);
 
+/* Allocation-free fused backward, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc): terra_winattn_bwd_nhwc with its workspace taken from a
+ * device array the library holds, TERRA_SCRATCH_BYTES per GPU, kept until
+ * the process ends.  The caller still passes every input and output.  The
+ * call allocates nothing (its first call on a device looks up that device's
+ * array address once).  Geometries whose workspace
+ * (terra_winattn_bwd_workspace_bytes) exceeds TERRA_SCRATCH_BYTES return
+ * TERRA_ERR_UNSUPPORTED before any device work.  Every call on one GPU
+ * shares that GPU's array: calls that overlap on one GPU (concurrent
+ * streams, threads) race and must be ordered by the caller.  No part of the
+ * array needs to start at zero: each call writes everything it reads. */
+#define TERRA_SCRATCH_BYTES (32u << 20)
+int terra_winattn_bwd_nhwc_noalloc(const terra_geom* g, int dtype, const void* q,
+                                   const void* k, const void* v, const void* o,
+                                   const void* dout, const float* lse,
+                                   const float* bias_table, void* dq, void* dk,
+                                   void* dv, float* dbias_table, void* stream);
+
 /* ---------------------------------------------------------------------------
  * Window assignment across ranks and the per-rank token route.
  *

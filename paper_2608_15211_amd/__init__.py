@@ -11,6 +11,7 @@ Entry points (same names as the C ABI):
     terra_window_route, terra_window_unroute, terra_winattn_fwd,
     terra_winattn_bwd_workspace_bytes, terra_winattn_bwd,
     terra_winattn_fwd_nhwc, terra_winattn_bwd_nhwc (route fused in),
+    terra_winattn_bwd_nhwc_noalloc (workspace from a library-held array),
     terra_plan_padded_grid, terra_plan_window_ranges, terra_plan_rank,
     terra_window_route_rank, terra_window_unroute_rank, terra_fragment_pack,
     terra_fragment_unpack (ragged window assignment and per-rank route)
@@ -93,6 +94,7 @@ def lib():
     L.terra_winattn_bwd_workspace_bytes.restype = sz
     L.terra_winattn_bwd.argtypes = [G, i32] + [vp] * 12 + [sz, vp]
     L.terra_winattn_bwd_nhwc.argtypes = [G, i32] + [vp] * 12 + [sz, vp]
+    L.terra_winattn_bwd_nhwc_noalloc.argtypes = [G, i32] + [vp] * 12
     i64 = ctypes.c_int64
     L.terra_plan_padded_grid.argtypes = [i32] * 7 + [ctypes.POINTER(ctypes.c_int32)] * 2 + \
         [ctypes.POINTER(ctypes.c_double)]
@@ -109,6 +111,7 @@ def lib():
     for name in ("terra_validate_geometry", "terra_window_count", "terra_window_layout",
                  "terra_window_route", "terra_window_unroute", "terra_winattn_fwd",
                  "terra_winattn_bwd", "terra_winattn_fwd_nhwc", "terra_winattn_bwd_nhwc",
+                 "terra_winattn_bwd_nhwc_noalloc",
                  "terra_plan_padded_grid", "terra_plan_window_ranges", "terra_plan_rank",
                  "terra_window_route_rank", "terra_window_unroute_rank", "terra_fragment_pack",
                  "terra_fragment_unpack"):
@@ -276,6 +279,25 @@ def terra_winattn_bwd(q, k, v, o, dout, lse, table, g, out=None, workspace=None)
 def terra_winattn_bwd_nhwc(q, k, v, o, dout, lse, table, g, out=None, workspace=None):
     """As terra_winattn_bwd with NHWC tensors and NHWC-ordered LSE."""
     return _attn_bwd(lib().terra_winattn_bwd_nhwc, q, k, v, o, dout, lse, table, g, out, workspace)
+
+
+TERRA_SCRATCH_BYTES = 32 << 20
+
+
+def terra_winattn_bwd_nhwc_noalloc(q, k, v, o, dout, lse, table, g, out):
+    """terra_winattn_bwd_nhwc with no workspace argument: the library's own
+    per-GPU scratch array serves.  `out` = preallocated (dq, dk, dv, dtable)."""
+    import torch
+    gg = _geom(g)
+    n, nl, nt = _sizes(gg)
+    dt = q.dtype
+    dq, dk, dv, dtab = out
+    _check(lib().terra_winattn_bwd_nhwc_noalloc(
+        ctypes.byref(gg), _dtype_code(dt), _dev(q, "q", dt, n), _dev(k, "k", dt, n), _dev(v, "v", dt, n),
+        _dev(o, "o", dt, n), _dev(dout, "dout", dt, n), _dev(lse, "lse", torch.float32, nl),
+        _dev(table, "table", torch.float32, nt), _dev(dq, "dq", dt, n), _dev(dk, "dk", dt, n),
+        _dev(dv, "dv", dt, n), _dev(dtab, "dtable", torch.float32, nt), _stream()))
+    return dq, dk, dv, dtab
 
 
 # ---------------------------------------------------------------- ranks

@@ -4,6 +4,7 @@
 #include <stdarg.h>
 #include <stdint.h>
 #include <stdio.h>
+#include <mutex>
 #include <string>
 
 #include "terra_common.h"
@@ -388,6 +389,57 @@ int terra_fragment_unpack(const terra_geom* g, int dtype, int32_t ranks, int32_t
                           int32_t src_rank, const void* frag_buf, void* src_stripe, void* stream) {
   return frag_common(g, dtype, ranks, dst_rank, src_rank, src_stripe, const_cast<void*>(frag_buf),
                      false, stream);
+}
+
+}  // extern "C"
+
+// Device memory of the allocation-free backward: one array per GPU, held
+// until the process ends.  Its name is a host-side stand-in in host code;
+// the device address comes from hipGetSymbolAddress, once per device.
+static __device__ __align__(256) unsigned char scratch[TERRA_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Address of the current device's scratch array (set up on first use).
+int scratch_address(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(TERRA_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return fail(TERRA_ERR_UNSUPPORTED, "device %d >= %d", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(TERRA_ERR_HIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return ok();
+}
+}  // namespace
+
+extern "C" {
+
+int terra_winattn_bwd_nhwc_noalloc(const terra_geom* g, int dtype, const void* q, const void* k,
+                                   const void* v, const void* o, const void* dout, const float* lse,
+                                   const float* bias_table, void* dq, void* dk, void* dv,
+                                   float* dbias_table, void* stream) {
+  int s = check_attn(g, dtype);
+  if (s) return s;
+  const size_t need = terra::bwd_workspace(make_geo(g), dtype);
+  if (need > (size_t)TERRA_SCRATCH_BYTES)
+    return fail(TERRA_ERR_UNSUPPORTED,
+                "this geometry needs %zu bytes of scratch; the library holds %zu per GPU "
+                "(use terra_winattn_bwd_nhwc with a workspace)",
+                need, (size_t)TERRA_SCRATCH_BYTES);
+  void* ws = nullptr;
+  if ((s = scratch_address(&ws))) return s;
+  return attn_bwd_common(g, dtype, true, q, k, v, o, dout, lse, bias_table, dq, dk, dv, dbias_table,
+                         ws, (size_t)TERRA_SCRATCH_BYTES, stream);
 }
 
 const char* terra_status_string(int status) {
