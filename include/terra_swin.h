@@ -97,9 +97,14 @@ int terra_window_layout(const terra_geom* g, int32_t* offsets, int32_t* counts);
 
 /* Token route, NHWC -> window-major (Sec. IV-D: the route gathers every
  * token into its window-major slot after the window shift).  Bit copy of
- * B*H*W*C elements of `dtype`; x_nhwc and y_win must not overlap. */
+ * B*H*W*C elements of `dtype`; x_nhwc and y_win must not overlap.
+ * d_offsets / d_counts (nullable DEVICE int32 arrays of Mh*Mw+1 and Mh*Mw
+ * entries) receive the per-window first slots and valid-token counts of one
+ * image, as terra_window_layout gives them on the host, written on the same
+ * stream. */
 int terra_window_route(const terra_geom* g, int dtype, const void* x_nhwc,
-                       void* y_win, void* stream);
+                       void* y_win, int32_t* d_offsets, int32_t* d_counts,
+                       void* stream);
 
 /* Inverse token route, window-major -> NHWC: the exact inverse scatter of
  * terra_window_route, and also its adjoint (the backward of the route is the

@@ -86,7 +86,7 @@ def lib():
     L.terra_validate_geometry.argtypes = [G]
     L.terra_window_count.argtypes = [G, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32)]
     L.terra_window_layout.argtypes = [G, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32)]
-    L.terra_window_route.argtypes = [G, i32, vp, vp, vp]
+    L.terra_window_route.argtypes = [G, i32, vp, vp, vp, vp, vp]
     L.terra_window_unroute.argtypes = [G, i32, vp, vp, vp]
     L.terra_winattn_fwd.argtypes = [G, i32, vp, vp, vp, vp, vp, vp, vp]
     L.terra_winattn_fwd_nhwc.argtypes = [G, i32, vp, vp, vp, vp, vp, vp, vp]
@@ -194,16 +194,21 @@ def _sizes(gg):
         (2 * gg.wh - 1) * (2 * gg.ww - 1) * gg.heads
 
 
-def terra_window_route(x_nhwc, g, out=None):
-    """NHWC (B,H,W,C) -> window-major (B,H*W,C), same dtype."""
+def terra_window_route(x_nhwc, g, out=None, offsets=None, counts=None):
+    """NHWC (B,H,W,C) -> window-major (B,H*W,C), same dtype.  offsets /
+    counts: optional int32 device tensors of Mh*Mw+1 / Mh*Mw entries that
+    receive the window layout of one image."""
     import torch
     gg = _geom(g)
     n, _, _ = _sizes(gg)
     if out is None:
         out = torch.empty((gg.B, gg.H * gg.W, gg.C), dtype=x_nhwc.dtype, device=x_nhwc.device)
+    nw = (-(-gg.H // gg.wh)) * (-(-gg.W // gg.ww))
+    d_off = ctypes.c_void_p(0) if offsets is None else _dev(offsets, "offsets", torch.int32, nw + 1)
+    d_cnt = ctypes.c_void_p(0) if counts is None else _dev(counts, "counts", torch.int32, nw)
     _check(lib().terra_window_route(ctypes.byref(gg), _dtype_code(x_nhwc.dtype),
                                     _dev(x_nhwc, "x", None, n), _dev(out, "out", x_nhwc.dtype, n),
-                                    _stream()))
+                                    d_off, d_cnt, _stream()))
     return out
 
 

@@ -14,6 +14,7 @@
 namespace terra {
 hipError_t launch_route(const Geo& g, int row_bytes, const void* src, void* dst, bool forward,
                         hipStream_t stream);
+hipError_t launch_layout(const Geo& g, int32_t* offsets, int32_t* counts, hipStream_t stream);
 hipError_t launch_attn_fwd(const Geo& g, int dt, bool nhwc, const void* q, const void* k,
                            const void* v, const float* table, void* o, float* lse, hipStream_t st);
 hipError_t launch_attn_bwd(const Geo& g, int dt, bool nhwc, const void* q, const void* k,
@@ -97,6 +98,35 @@ terra::Geo make_geo(const terra_geom* g) {
   G.nbins = (2 * g->wh - 1) * G.bstride;
   terra::set_table_stride(G);
   terra::set_col_recips(G);
+  G.cus = terra::kMaxCus;
+  return G;
+}
+
+// Compute units of the current device (asked once per device), clamped to
+// [1, kMaxCus]; the launchers size their persistent grids from it.
+std::mutex g_cus_mu;
+int g_cus[64] = {};
+int device_cus() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) {
+    (void)hipGetLastError();
+    return 256;
+  }
+  std::lock_guard<std::mutex> lock(g_cus_mu);
+  if (g_cus[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 1) {
+      (void)hipGetLastError();
+      n = 256;
+    }
+    g_cus[dev] = n > terra::kMaxCus ? terra::kMaxCus : n;
+  }
+  return g_cus[dev];
+}
+
+terra::Geo launch_geo(const terra_geom* g) {
+  terra::Geo G = make_geo(g);
+  G.cus = device_cus();
   return G;
 }
 
@@ -166,7 +196,7 @@ int terra_window_layout(const terra_geom* g, int32_t* offsets, int32_t* counts) 
 }
 
 static int route_common(const terra_geom* g, int dtype, const void* src, void* dst, bool forward,
-                        void* stream) {
+                        int32_t* d_offsets, int32_t* d_counts, void* stream) {
   int s = check_geom(g);
   if (s) return s;
   if ((s = check_dtype(dtype))) return s;
@@ -179,18 +209,23 @@ static int route_common(const terra_geom* g, int dtype, const void* src, void* d
     return fail(TERRA_ERR_UNSUPPORTED, "window of %d tokens x %lld bytes is too large to route",
                 g->wh * g->ww, (long long)row_bytes);
   terra::Geo G = make_geo(g);
+  if (d_offsets || d_counts) {
+    s = hip_status(terra::launch_layout(G, d_offsets, d_counts, (hipStream_t)stream),
+                   "terra_window_route layout launch");
+    if (s) return s;
+  }
   return hip_status(terra::launch_route(G, (int)row_bytes, src, dst, forward, (hipStream_t)stream),
                     forward ? "terra_window_route launch" : "terra_window_unroute launch");
 }
 
 int terra_window_route(const terra_geom* g, int dtype, const void* x_nhwc, void* y_win,
-                       void* stream) {
-  return route_common(g, dtype, x_nhwc, y_win, true, stream);
+                       int32_t* d_offsets, int32_t* d_counts, void* stream) {
+  return route_common(g, dtype, x_nhwc, y_win, true, d_offsets, d_counts, stream);
 }
 
 int terra_window_unroute(const terra_geom* g, int dtype, const void* y_win, void* x_nhwc,
                          void* stream) {
-  return route_common(g, dtype, y_win, x_nhwc, false, stream);
+  return route_common(g, dtype, y_win, x_nhwc, false, nullptr, nullptr, stream);
 }
 
 }  // extern "C"
@@ -202,7 +237,7 @@ static int attn_fwd_common(const terra_geom* g, int dtype, bool nhwc, const void
   if (s) return s;
   if (!q || !k || !v || !bias_table || !o || !lse)
     return fail(TERRA_ERR_INVALID, "tensor pointer is NULL");
-  terra::Geo G = make_geo(g);
+  terra::Geo G = launch_geo(g);
   return hip_status(terra::launch_attn_fwd(G, dtype, nhwc, q, k, v, bias_table, o, lse,
                                            (hipStream_t)stream),
                     nhwc ? "terra_winattn_fwd_nhwc launch" : "terra_winattn_fwd launch");
@@ -217,8 +252,8 @@ static int attn_bwd_common(const terra_geom* g, int dtype, bool nhwc, const void
   if (s) return s;
   if (!q || !k || !v || !o || !dout || !lse || !bias_table || !dq || !dk || !dv || !dbias_table)
     return fail(TERRA_ERR_INVALID, "tensor pointer is NULL");
-  terra::Geo G = make_geo(g);
-  const size_t need = terra::bwd_workspace(G, dtype);
+  const size_t need = terra::bwd_workspace(make_geo(g), dtype);
+  terra::Geo G = launch_geo(g);
   if (!workspace || workspace_bytes < need)
     return fail(TERRA_ERR_WORKSPACE, "workspace of %zu bytes given, %zu needed",
                 workspace ? workspace_bytes : (size_t)0, need);

@@ -918,7 +918,7 @@ static size_t dkdv_lds(const Geo& g) {
 constexpr int kF32 = 0, kBF16 = 1;
 static int slices_for(const Geo& g, int per_cu) {
   const int items = g.B * g.nwin * num_chunks(g);
-  int n = 256 * per_cu / g.heads;
+  int n = g.cus * per_cu / g.heads;
   if (n > items) n = items;
   return n < 1 ? 1 : n;
 }

@@ -920,14 +920,14 @@ bool win_bwd_ok(const Geo& g, bool bf16_) {
 // Slices of the window range per head; a pure function of the geometry.
 size_t win_bwd_lds(const Geo& g);
 
-// Slices of the window range per head: one round of workgroups over the 256
-// CUs, two resident per CU (two waves per SIMD; the LDS plan fits twice in
+// Slices of the window range per head: one round of workgroups over the
+// device's CUs, two resident per CU (two waves per SIMD; the LDS plan fits twice in
 // 160 KB), so that one workgroup's memory phase overlaps the other's matrix
 // work.  A pure function of the geometry.
 int win_bwd_nslice(const Geo& g) {
   const int total = g.B * g.nwin;
   const int per_cu = win_bwd_lds(g) * 2 <= 160 * 1024 ? 2 : 1;
-  int target = 256 * per_cu / g.heads;
+  int target = g.cus * per_cu / g.heads;
   if (target > total) target = total;
   if (target < 1) target = 1;
   const int per = (total + target - 1) / target;
@@ -967,7 +967,7 @@ size_t win_fwd_pair_lds(const Geo& g) {
 // workgroups, two resident per CU.
 static int win_fwd_pair_nslice(const Geo& g) {
   const int total = g.B * g.nwin;
-  int target = 2 * 256 / (g.heads / 2);
+  int target = 2 * g.cus / (g.heads / 2);
   if (target > total) target = total;
   if (target < 1) target = 1;
   return target;

@@ -90,6 +90,27 @@ __global__ __launch_bounds__(kRouteThreads) void route_kernel(
   }
 }
 
+// Window-major layout of one image on the device: offsets[w] (w <= nwin,
+// offsets[nwin] = H*W) and counts[w] (w < nwin); either may be null.
+__global__ __launch_bounds__(kRouteThreads) void layout_kernel(Geo g, int32_t* offsets,
+                                                               int32_t* counts) {
+  const int w = blockIdx.x * kRouteThreads + threadIdx.x;
+  if (w > g.nwin) return;
+  if (w == g.nwin) {
+    if (offsets) offsets[w] = g.HW;
+    return;
+  }
+  const int i = w / g.Mw, j = w - (w / g.Mw) * g.Mw;
+  if (offsets) offsets[w] = win_offset(g, i, j);
+  if (counts) counts[w] = win_rows(g, i) * win_cols(g, j);
+}
+
+hipError_t launch_layout(const Geo& g, int32_t* offsets, int32_t* counts, hipStream_t stream) {
+  const int grid = (g.nwin + 1 + kRouteThreads - 1) / kRouteThreads;
+  hipLaunchKernelGGL(layout_kernel, dim3(grid), dim3(kRouteThreads), 0, stream, g, offsets, counts);
+  return hipGetLastError();
+}
+
 template <int VEC>
 static hipError_t launch_route_vec(const RouteArgs& A, const void* src, void* dst,
                                    bool forward, hipStream_t stream) {

@@ -37,7 +37,14 @@ struct Geo {
   // 1 / width of full-width windows and of the last column's windows (the
   // float reciprocals fast_div starts from), set on the host.
   float rcols[2];
+  // Compute units the persistent grids are sized for: the device's count at
+  // launch; kMaxCus when sizing workspaces, which are pure functions of the
+  // geometry (every slice count grows with it, so a workspace sized for
+  // kMaxCus covers any device up to that many).
+  int cus;
 };
+
+constexpr int kMaxCus = 512;
 
 __host__ inline void set_table_stride(Geo& g) {
   g.tstride = g.bstride + ((48 - g.bstride % 32) % 32);

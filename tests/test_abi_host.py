@@ -89,11 +89,11 @@ def test_device_calls_reject_bad_arguments_before_launch():
     fake = ctypes.c_void_p(0x1000)
     null = ctypes.c_void_p(0)
     s = ctypes.c_void_p(0)
-    assert L.terra_window_route(ctypes.byref(g), 7, fake, fake, s) == 1       # bad dtype
+    assert L.terra_window_route(ctypes.byref(g), 7, fake, fake, null, null, s) == 1   # bad dtype
     assert L.terra_winattn_fwd(ctypes.byref(g), 3, *([fake] * 6), s) == 1     # bad dtype
     assert L.terra_winattn_bwd_workspace_bytes(ctypes.byref(g), 2) > 0       # fp16
-    assert L.terra_window_route(ctypes.byref(g), 1, null, fake, s) == 1       # NULL
-    assert L.terra_window_route(ctypes.byref(g), 1, fake, fake, s) == 1       # in place
+    assert L.terra_window_route(ctypes.byref(g), 1, null, fake, null, null, s) == 1   # NULL
+    assert L.terra_window_route(ctypes.byref(g), 1, fake, fake, fake, fake, s) == 1   # in place
     assert L.terra_winattn_fwd(ctypes.byref(g), 1, fake, fake, null, fake, fake, fake, s) == 1
     assert L.terra_winattn_fwd(None, 1, fake, fake, fake, fake, fake, fake, s) == 1
     need = L.terra_winattn_bwd_workspace_bytes(ctypes.byref(g), 1)

@@ -95,6 +95,29 @@ def test_route_bit_exact(name):
     assert np.array_equal(back.view(idt).cpu().numpy().view(pat.dtype), pat)
 
 
+@pytest.mark.parametrize("name", ["c3_bf16_85x180_w12", "c4_bf16_128x1080_w8x16", "c5_bf16_256x540_w24"])
+def test_route_writes_the_window_layout_on_the_device(name):
+    # the route's optional device outputs equal the host layout call and the
+    # oracle's window enumeration
+    cfg = ts.CONFIGS[name]
+    g = Geometry(**cfg.geom_kwargs())
+    mh, mw = P.terra_window_count(cfg)
+    x = torch.zeros((cfg.B, cfg.H, cfg.W, cfg.C), dtype=torch.bfloat16, device="cuda")
+    off = torch.full((mh * mw + 1,), -1, dtype=torch.int32, device="cuda")
+    cnt = torch.full((mh * mw,), -1, dtype=torch.int32, device="cuda")
+    P.terra_window_route(x, cfg, offsets=off, counts=cnt)
+    torch.cuda.synchronize()
+    hoff, hcnt = P.terra_window_layout(cfg)
+    assert off.cpu().tolist() == hoff and cnt.cpu().tolist() == hcnt
+    slots = window_slots(g)
+    assert hoff[:-1] == [s for _, s, _ in slots] and hcnt == [n for _, _, n in slots]
+    # counts alone
+    cnt2 = torch.full((mh * mw,), -1, dtype=torch.int32, device="cuda")
+    P.terra_window_route(x, cfg, counts=cnt2)
+    torch.cuda.synchronize()
+    assert cnt2.cpu().tolist() == hcnt
+
+
 def test_route_f32_and_bf16_on_one_geometry():
     # The same geometry routed as 4-byte and as 2-byte elements.
     cfg32 = ts.small_config("r32", "f32", 2, 13, 10, 1, 32, 6, 4, 3, 1, 3)
