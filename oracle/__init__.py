@@ -17,6 +17,9 @@ What it computes (the readings of the paper are listed next to each function):
   fp64 (W-MSA / SW-MSA of the Swin blocks, Sec. IV-A).
 * ``brute``     - the same attention computed over the whole grid in NHWC
   order from a full token-pair mask; it never forms the window-major layout.
+* ``block``     - one pre-norm Swin block around the attention (LayerNorm,
+  QKV projection, attention, output projection, MLP with GELU, two residual
+  branches; Sec. IV-A, IV-C, Table III), forward and backward.
 * ``planner``   - padding of the fixed window assignment (Sec. V-A, Eq. (3)),
   the ragged window ranges of Eq. (4), the SP sub-tile counts of Sec. V-B,
   the DMP height stripes, and every token each rank's route needs, listed
@@ -31,10 +34,10 @@ here.  Each function is instead pinned to mathematics and library routines
 from .geometry import Geometry, window_extents, token_table, window_classes
 from .route import route, unroute
 from .attention import attn_fwd, attn_bwd, attn_fwd_windows, attn_bwd_windows
-from . import brute, planner
+from . import brute, planner, block
 
 __all__ = [
     "Geometry", "window_extents", "token_table", "window_classes",
     "route", "unroute", "attn_fwd", "attn_bwd", "attn_fwd_windows",
-    "attn_bwd_windows", "brute", "planner",
+    "attn_bwd_windows", "brute", "planner", "block",
 ]

@@ -139,3 +139,52 @@ def token_pattern(cfg, width_bytes):
 
 def small_config(name, dtype, B, H, W, heads, head_dim, wh, ww, sh, sw, mask_flags=1):
     return Config(name, dtype, B, H, W, heads, head_dim, wh, ww, sh, sw, mask_flags)
+
+
+# ---------------------------------------------------------------- Swin block
+# Parameter names and shapes of one block for embedding width C (MLP ratio 4).
+BLOCK_PARAMS = [
+    ("ln1_g", lambda C: (C,)), ("ln1_b", lambda C: (C,)),
+    ("w_qkv", lambda C: (3 * C, C)), ("b_qkv", lambda C: (3 * C,)),
+    ("w_proj", lambda C: (C, C)), ("b_proj", lambda C: (C,)),
+    ("ln2_g", lambda C: (C,)), ("ln2_b", lambda C: (C,)),
+    ("w_fc1", lambda C: (4 * C, C)), ("b_fc1", lambda C: (4 * C,)),
+    ("w_fc2", lambda C: (C, 4 * C)), ("b_fc2", lambda C: (C,)),
+]
+
+
+def make_block_inputs(cfg, seed=0):
+    """Input x and upstream gradient dx2 (B x H x W x C, N(0, 1)), the block
+    parameters and the attention bias table, drawn in this order from
+    numpy.random.default_rng(seed): x, dx2, then each parameter in
+    BLOCK_PARAMS order -- LayerNorm gains 1 + 0.1 N(0, 1), LayerNorm shifts
+    and biases 0.02 N(0, 1), weights N(0, 1) / sqrt(fan_in) -- then the table
+    0.02 N(0, 1) of shape (2wh-1, 2ww-1, heads).  x, dx2 and the weights are
+    rounded to the storage type (bf16 / fp16); gains, shifts and biases stay
+    float32."""
+    rng = np.random.default_rng(seed)
+    C = cfg.C
+    shape = (cfg.B, cfg.H, cfg.W, C)
+
+    def store(a):
+        a = a.astype(np.float32)
+        if cfg.dtype == "bf16":
+            return bf16_round(a)
+        if cfg.dtype == "f16":
+            return a.astype(np.float16).astype(np.float32)
+        return a
+
+    out = {"x": store(rng.standard_normal(shape)), "dx2": store(rng.standard_normal(shape))}
+    params = {}
+    for name, shp in BLOCK_PARAMS:
+        dims = shp(C)
+        z = rng.standard_normal(dims)
+        if name.endswith("_g"):
+            params[name] = (1.0 + 0.1 * z).astype(np.float32)
+        elif name.startswith("w_"):
+            params[name] = store(z / np.sqrt(dims[1]))
+        else:
+            params[name] = (0.02 * z).astype(np.float32)
+    out["params"] = params
+    out["table"] = (0.02 * rng.standard_normal((2 * cfg.wh - 1, 2 * cfg.ww - 1, cfg.heads))).astype(np.float32)
+    return out
