@@ -187,6 +187,70 @@ int terra_winattn_bwd_nhwc_noalloc(const terra_geom* g, int dtype, const void* q
                                    void* dv, float* dbias_table, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * One Swin block around the attention (Sec. IV-A Swin blocks, whose linear
+ * layers TP shards in Sec. IV-C; widths as in Table III), pre-norm with two
+ * residual branches, on NHWC tokens of width C = d:
+ *   x1 = x  + Proj(A(LN1(x) W_qkv^T + b_qkv)),  Proj(o) = o W_proj^T + b_proj
+ *   x2 = x1 + GELU(LN2(x1) W_fc1^T + b_fc1) W_fc2^T + b_fc2
+ * LN over the C channels of a token (biased variance, eps 1e-5, gain and
+ * shift); GELU the exact (erf) form; A the shifted-window attention of
+ * terra_winattn_fwd_nhwc with the bias table.  W_qkv is 3C x C (rows
+ * [0,C) -> Q, [C,2C) -> K, [2C,3C) -> V), W_proj C x C, W_fc1 4C x C,
+ * W_fc2 C x 4C, all row-major (out x in) bf16; gains, shifts and biases
+ * float32.  Element type TERRA_BF16 only; C must be a multiple of 128 and
+ * at most 2048, and the geometry must suit the attention.
+ * LayerNorm is applied to the projection inputs while they are staged for
+ * the matrix cores (its output never reaches memory); Q, K and V are
+ * written straight as the NHWC tensors the fused attention reads.
+ * ------------------------------------------------------------------------- */
+
+typedef struct terra_block_params {      /* device pointers                 */
+  const float *ln1_g, *ln1_b;            /* C                               */
+  const void* w_qkv;                     /* bf16 3C x C                     */
+  const float* b_qkv;                    /* 3C                              */
+  const void* w_proj;                    /* bf16 C x C                      */
+  const float* b_proj;                   /* C                               */
+  const float *ln2_g, *ln2_b;            /* C                               */
+  const void* w_fc1;                     /* bf16 4C x C                     */
+  const float* b_fc1;                    /* 4C                              */
+  const void* w_fc2;                     /* bf16 C x 4C                     */
+  const float* b_fc2;                    /* C                               */
+} terra_block_params;
+
+typedef struct terra_block_grads {       /* float32 device outputs, same shapes as the parameters */
+  float *ln1_g, *ln1_b, *w_qkv, *b_qkv, *w_proj, *b_proj, *ln2_g, *ln2_b, *w_fc1, *b_fc1, *w_fc2, *b_fc2;
+} terra_block_grads;
+
+/* Activations the forward writes and the backward reads (device, caller
+ * owned; T = B*H*W tokens): LN statistics (float32 T each), Q, K, V and the
+ * attention output O (bf16 NHWC, T x C), the attention LSE (float32
+ * B x heads x H*W, NHWC token order), x1 (bf16 T x C), the MLP
+ * pre-activation h and its GELU a (bf16 T x 4C). */
+typedef struct terra_block_saved {
+  float *mu1, *rstd1, *mu2, *rstd2;
+  void *q, *k, *v, *o;
+  float* lse;
+  void* x1;
+  void *h, *a;
+} terra_block_saved;
+
+/* Forward: x (bf16 NHWC) -> x2 (bf16 NHWC), filling `saved`. */
+int terra_block_fwd(const terra_geom* g, int dtype, const void* x, const terra_block_params* p,
+                    const float* bias_table, void* x2, const terra_block_saved* saved, void* stream);
+
+/* Device workspace terra_block_bwd needs (0 on invalid input). */
+size_t terra_block_bwd_workspace_bytes(const terra_geom* g, int dtype);
+
+/* Backward from the upstream gradient dx2: dx (bf16 NHWC), every parameter
+ * gradient (float32, summed over all tokens, overwritten) and the bias-table
+ * gradient (overwritten).  x and `saved` as left by terra_block_fwd.
+ * Reductions over tokens run in a fixed order (bit-reproducible). */
+int terra_block_bwd(const terra_geom* g, int dtype, const void* dx2, const void* x,
+                    const terra_block_params* p, const float* bias_table,
+                    const terra_block_saved* saved, void* dx, const terra_block_grads* grads,
+                    float* dbias_table, void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
  * Window assignment across ranks and the per-rank token route.
  *
  * On a multi-GPU run the token grid is held in DMP height stripes (the I/O

@@ -14,11 +14,15 @@ Entry points (same names as the C ABI):
     terra_winattn_bwd_nhwc_noalloc (workspace from a library-held array),
     terra_plan_padded_grid, terra_plan_window_ranges, terra_plan_rank,
     terra_window_route_rank, terra_window_unroute_rank, terra_fragment_pack,
-    terra_fragment_unpack (ragged window assignment and per-rank route)
+    terra_fragment_unpack (ragged window assignment and per-rank route),
+    terra_block_fwd, terra_block_bwd_workspace_bytes, terra_block_bwd (the
+    Swin block around the attention: LayerNorm, projections, MLP)
 """
 
 import ctypes
 import os
+
+import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libterra_swin.so")
@@ -68,6 +72,22 @@ class terra_fragment(ctypes.Structure):
 
 TERRA_MAX_FRAGMENTS = 64
 
+BLOCK_PARAM_NAMES = ("ln1_g", "ln1_b", "w_qkv", "b_qkv", "w_proj", "b_proj", "ln2_g", "ln2_b",
+                     "w_fc1", "b_fc1", "w_fc2", "b_fc2")
+BLOCK_SAVED_NAMES = ("mu1", "rstd1", "mu2", "rstd2", "q", "k", "v", "o", "lse", "x1", "h", "a")
+
+
+class terra_block_params(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in BLOCK_PARAM_NAMES]
+
+
+class terra_block_grads(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in BLOCK_PARAM_NAMES]
+
+
+class terra_block_saved(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in BLOCK_SAVED_NAMES]
+
 _lib = None
 
 
@@ -105,6 +125,13 @@ def lib():
     L.terra_window_unroute_rank.argtypes = [G, i32, i32, i32, vp, vp, vp, vp]
     L.terra_fragment_pack.argtypes = [G, i32, i32, i32, i32, vp, vp, vp]
     L.terra_fragment_unpack.argtypes = [G, i32, i32, i32, i32, vp, vp, vp]
+    L.terra_block_fwd.argtypes = [G, i32, vp, ctypes.POINTER(terra_block_params), vp, vp,
+                                  ctypes.POINTER(terra_block_saved), vp]
+    L.terra_block_bwd_workspace_bytes.argtypes = [G, i32]
+    L.terra_block_bwd_workspace_bytes.restype = sz
+    L.terra_block_bwd.argtypes = [G, i32, vp, vp, ctypes.POINTER(terra_block_params), vp,
+                                  ctypes.POINTER(terra_block_saved), vp, ctypes.POINTER(terra_block_grads),
+                                  vp, vp, sz, vp]
     L.terra_status_string.argtypes = [i32]
     L.terra_status_string.restype = ctypes.c_char_p
     L.terra_last_error.restype = ctypes.c_char_p
@@ -114,7 +141,7 @@ def lib():
                  "terra_winattn_bwd_nhwc_noalloc",
                  "terra_plan_padded_grid", "terra_plan_window_ranges", "terra_plan_rank",
                  "terra_window_route_rank", "terra_window_unroute_rank", "terra_fragment_pack",
-                 "terra_fragment_unpack"):
+                 "terra_fragment_unpack", "terra_block_fwd", "terra_block_bwd"):
         getattr(L, name).restype = i32
     _lib = L
     return L
@@ -398,3 +425,99 @@ def terra_fragment_unpack(frag_buf, src_stripe, g, ranks, dst_rank, src_rank):
     _check(lib().terra_fragment_unpack(ctypes.byref(gg), _dtype_code(dt), ranks, dst_rank, src_rank,
                                        _dev(frag_buf, "frag_buf", dt), _dev(src_stripe, "src_stripe", dt),
                                        _stream()))
+
+
+# ---------------------------------------------------------------- Swin block
+def _block_shapes(gg):
+    T, C = gg.B * gg.H * gg.W, gg.C
+    return {"ln1_g": (C,), "ln1_b": (C,), "w_qkv": (3 * C, C), "b_qkv": (3 * C,), "w_proj": (C, C),
+            "b_proj": (C,), "ln2_g": (C,), "ln2_b": (C,), "w_fc1": (4 * C, C), "b_fc1": (4 * C,),
+            "w_fc2": (C, 4 * C), "b_fc2": (C,)}, T
+
+
+def _params_struct(params, gg):
+    import torch
+    shapes, _ = _block_shapes(gg)
+    st = terra_block_params()
+    for n in BLOCK_PARAM_NAMES:
+        t = params[n]
+        dt = torch.bfloat16 if n.startswith("w_") else torch.float32
+        setattr(st, n, _dev(t, n, dt, int(np.prod(shapes[n]))).value)
+    return st
+
+
+def terra_block_saved_alloc(g, device="cuda"):
+    """Buffers for the activations the block forward saves."""
+    import torch
+    gg = _geom(g)
+    T, C = gg.B * gg.H * gg.W, gg.C
+    nhwc = (gg.B, gg.H, gg.W, C)
+    f32, b16 = torch.float32, torch.bfloat16
+    return {"mu1": torch.empty(T, dtype=f32, device=device), "rstd1": torch.empty(T, dtype=f32, device=device),
+            "mu2": torch.empty(T, dtype=f32, device=device), "rstd2": torch.empty(T, dtype=f32, device=device),
+            "q": torch.empty(nhwc, dtype=b16, device=device), "k": torch.empty(nhwc, dtype=b16, device=device),
+            "v": torch.empty(nhwc, dtype=b16, device=device), "o": torch.empty(nhwc, dtype=b16, device=device),
+            "lse": torch.empty((gg.B, gg.heads, gg.H * gg.W), dtype=f32, device=device),
+            "x1": torch.empty(nhwc, dtype=b16, device=device),
+            "h": torch.empty((gg.B, gg.H, gg.W, 4 * C), dtype=b16, device=device),
+            "a": torch.empty((gg.B, gg.H, gg.W, 4 * C), dtype=b16, device=device)}
+
+
+def _saved_struct(saved, gg):
+    import torch
+    T, C = gg.B * gg.H * gg.W, gg.C
+    sizes = {"mu1": T, "rstd1": T, "mu2": T, "rstd2": T, "q": T * C, "k": T * C, "v": T * C, "o": T * C,
+             "lse": T * gg.heads, "x1": T * C, "h": 4 * T * C, "a": 4 * T * C}
+    st = terra_block_saved()
+    for n in BLOCK_SAVED_NAMES:
+        dt = torch.float32 if n in ("mu1", "rstd1", "mu2", "rstd2", "lse") else torch.bfloat16
+        setattr(st, n, _dev(saved[n], n, dt, sizes[n]).value)
+    return st
+
+
+def terra_block_fwd(x, params, table, g, saved=None, out=None):
+    """One Swin block forward on NHWC bf16 x.  params: dict of device tensors
+    (weights bf16, the rest float32).  Returns (x2, saved)."""
+    import torch
+    gg = _geom(g)
+    T, C = gg.B * gg.H * gg.W, gg.C
+    if saved is None:
+        saved = terra_block_saved_alloc(gg, x.device)
+    if out is None:
+        out = torch.empty_like(x)
+    _check(lib().terra_block_fwd(ctypes.byref(gg), TERRA_BF16, _dev(x, "x", torch.bfloat16, T * C),
+                                 ctypes.byref(_params_struct(params, gg)),
+                                 _dev(table, "table", torch.float32, _sizes(gg)[2]),
+                                 _dev(out, "x2", torch.bfloat16, T * C),
+                                 ctypes.byref(_saved_struct(saved, gg)), _stream()))
+    return out, saved
+
+
+def terra_block_bwd_workspace_bytes(g, dtype="bf16"):
+    return int(lib().terra_block_bwd_workspace_bytes(ctypes.byref(_geom(g)), _dtype_code(dtype)))
+
+
+def terra_block_bwd(dx2, x, params, table, g, saved, out=None, workspace=None):
+    """Backward of the block.  Returns (dx, grads dict, dtable)."""
+    import torch
+    gg = _geom(g)
+    T, C = gg.B * gg.H * gg.W, gg.C
+    shapes, _ = _block_shapes(gg)
+    if out is None:
+        out = (torch.empty_like(x), {n: torch.empty(shapes[n], dtype=torch.float32, device=x.device)
+                                     for n in BLOCK_PARAM_NAMES},
+               torch.empty(table.shape, dtype=torch.float32, device=x.device))
+    dx, grads, dtab = out
+    gst = terra_block_grads()
+    for n in BLOCK_PARAM_NAMES:
+        setattr(gst, n, _dev(grads[n], "d" + n, torch.float32, int(np.prod(shapes[n]))).value)
+    need = terra_block_bwd_workspace_bytes(gg)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
+    _check(lib().terra_block_bwd(ctypes.byref(gg), TERRA_BF16, _dev(dx2, "dx2", torch.bfloat16, T * C),
+                                 _dev(x, "x", torch.bfloat16, T * C), ctypes.byref(_params_struct(params, gg)),
+                                 _dev(table, "table", torch.float32, _sizes(gg)[2]),
+                                 ctypes.byref(_saved_struct(saved, gg)), _dev(dx, "dx", torch.bfloat16, T * C),
+                                 ctypes.byref(gst), _dev(dtab, "dtable", torch.float32, _sizes(gg)[2]),
+                                 _dev(workspace, "workspace"), ctypes.c_size_t(workspace.numel()), _stream()))
+    return dx, grads, dtab

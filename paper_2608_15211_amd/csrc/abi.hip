@@ -4,17 +4,25 @@
 #include <stdarg.h>
 #include <stdint.h>
 #include <stdio.h>
+#include <initializer_list>
 #include <mutex>
 #include <string>
 
 #include "terra_common.h"
 #include "terra_plan.h"
+#include "terra_block.h"
 #include "../../include/terra_swin.h"
 
 namespace terra {
 hipError_t launch_route(const Geo& g, int row_bytes, const void* src, void* dst, bool forward,
                         hipStream_t stream);
 hipError_t launch_layout(const Geo& g, int32_t* offsets, int32_t* counts, hipStream_t stream);
+hipError_t launch_block_fwd(const Geo& g, const void* x, const BlockParams& p, const float* table, void* x2,
+                            const BlockSaved& s, hipStream_t st);
+hipError_t launch_block_bwd(const Geo& g, const void* dx2, const void* x, const BlockParams& p, const float* table,
+                            const BlockSaved& s, void* dx, const BlockGrads& gr, float* dtable, void* ws,
+                            hipStream_t st);
+size_t block_bwd_workspace(const Geo& g);
 hipError_t launch_attn_fwd(const Geo& g, int dt, bool nhwc, const void* q, const void* k,
                            const void* v, const float* table, void* o, float* lse, hipStream_t st);
 hipError_t launch_attn_bwd(const Geo& g, int dt, bool nhwc, const void* q, const void* k,
@@ -296,6 +304,80 @@ int terra_winattn_bwd_nhwc(const terra_geom* g, int dtype, const void* q, const 
                            void* stream) {
   return attn_bwd_common(g, dtype, true, q, k, v, o, dout, lse, bias_table, dq, dk, dv,
                          dbias_table, workspace, workspace_bytes, stream);
+}
+
+}  // extern "C"
+
+namespace {
+int check_block(const terra_geom* g, int dtype) {
+  int s = check_attn(g, dtype);
+  if (s) return s;
+  if (dtype != TERRA_BF16) return fail(TERRA_ERR_UNSUPPORTED, "the Swin block takes TERRA_BF16 only");
+  if (g->C % 128 != 0 || g->C > 2048)
+    return fail(TERRA_ERR_UNSUPPORTED, "the Swin block needs C a multiple of 128 and at most 2048 (C = %d)", g->C);
+  if ((int64_t)g->B * g->H * g->W * 4 * g->C >= kMaxElems)
+    return fail(TERRA_ERR_UNSUPPORTED, "B*H*W*4C must be below 2^31");
+  return ok();
+}
+terra::BlockParams to_params(const terra_block_params* p) {
+  return terra::BlockParams{p->ln1_g, p->ln1_b, p->w_qkv, p->b_qkv, p->w_proj, p->b_proj,
+                            p->ln2_g, p->ln2_b, p->w_fc1, p->b_fc1, p->w_fc2, p->b_fc2};
+}
+terra::BlockSaved to_saved(const terra_block_saved* v) {
+  return terra::BlockSaved{v->mu1, v->rstd1, v->mu2, v->rstd2, v->q, v->k, v->v, v->o, v->lse, v->x1, v->h, v->a};
+}
+terra::BlockGrads to_grads(const terra_block_grads* g) {
+  return terra::BlockGrads{g->ln1_g, g->ln1_b, g->w_qkv, g->b_qkv, g->w_proj, g->b_proj,
+                           g->ln2_g, g->ln2_b, g->w_fc1, g->b_fc1, g->w_fc2, g->b_fc2};
+}
+bool any_null(std::initializer_list<const void*> ps) {
+  for (const void* p : ps)
+    if (!p) return true;
+  return false;
+}
+}  // namespace
+
+extern "C" {
+
+int terra_block_fwd(const terra_geom* g, int dtype, const void* x, const terra_block_params* p,
+                    const float* bias_table, void* x2, const terra_block_saved* sv, void* stream) {
+  int s = check_block(g, dtype);
+  if (s) return s;
+  if (!p || !sv) return fail(TERRA_ERR_INVALID, "parameter or saved-activation struct is NULL");
+  if (any_null({x, bias_table, x2, p->ln1_g, p->ln1_b, p->w_qkv, p->b_qkv, p->w_proj, p->b_proj, p->ln2_g,
+                p->ln2_b, p->w_fc1, p->b_fc1, p->w_fc2, p->b_fc2, sv->mu1, sv->rstd1, sv->mu2, sv->rstd2, sv->q,
+                sv->k, sv->v, sv->o, sv->lse, sv->x1, sv->h, sv->a}))
+    return fail(TERRA_ERR_INVALID, "tensor pointer is NULL");
+  terra::Geo G = launch_geo(g);
+  return hip_status(terra::launch_block_fwd(G, x, to_params(p), bias_table, x2, to_saved(sv), (hipStream_t)stream),
+                    "terra_block_fwd launch");
+}
+
+size_t terra_block_bwd_workspace_bytes(const terra_geom* g, int dtype) {
+  if (check_block(g, dtype)) return 0;
+  return terra::block_bwd_workspace(make_geo(g));
+}
+
+int terra_block_bwd(const terra_geom* g, int dtype, const void* dx2, const void* x, const terra_block_params* p,
+                    const float* bias_table, const terra_block_saved* sv, void* dx, const terra_block_grads* gr,
+                    float* dbias_table, void* workspace, size_t workspace_bytes, void* stream) {
+  int s = check_block(g, dtype);
+  if (s) return s;
+  if (!p || !sv || !gr) return fail(TERRA_ERR_INVALID, "parameter, saved-activation or gradient struct is NULL");
+  if (any_null({dx2, x, bias_table, dx, dbias_table, p->ln1_g, p->ln1_b, p->w_qkv, p->b_qkv, p->w_proj, p->b_proj,
+                p->ln2_g, p->ln2_b, p->w_fc1, p->b_fc1, p->w_fc2, p->b_fc2, sv->mu1, sv->rstd1, sv->mu2,
+                sv->rstd2, sv->q, sv->k, sv->v, sv->o, sv->lse, sv->x1, sv->h, sv->a, gr->ln1_g, gr->ln1_b,
+                gr->w_qkv, gr->b_qkv, gr->w_proj, gr->b_proj, gr->ln2_g, gr->ln2_b, gr->w_fc1, gr->b_fc1,
+                gr->w_fc2, gr->b_fc2}))
+    return fail(TERRA_ERR_INVALID, "tensor pointer is NULL");
+  const size_t need = terra::block_bwd_workspace(make_geo(g));
+  if (!workspace || workspace_bytes < need)
+    return fail(TERRA_ERR_WORKSPACE, "workspace of %zu bytes given, %zu needed", workspace ? workspace_bytes : (size_t)0,
+                need);
+  terra::Geo G = launch_geo(g);
+  return hip_status(terra::launch_block_bwd(G, dx2, x, to_params(p), bias_table, to_saved(sv), dx, to_grads(gr),
+                                            dbias_table, workspace, (hipStream_t)stream),
+                    "terra_block_bwd launch");
 }
 
 int terra_plan_padded_grid(int32_t H, int32_t W, int32_t p, int32_t alpha, int32_t w, int32_t m,

@@ -125,3 +125,29 @@ def test_window_layout_matches_oracle_enumeration(name):
     assert [s for _, s, _ in slots] == off[:-1]
     assert [n for _, _, n in slots] == cnt
     assert off[-1] == cfg.H * cfg.W
+
+
+def test_block_calls_reject_bad_arguments_before_launch():
+    L = P.lib()
+    fake = ctypes.c_void_p(0x1000)
+    s = ctypes.c_void_p(0)
+    ok = P.terra_geom.make(1, 24, 40, 768, 24, 32, 8, 16, 4, 8, 1)
+    bad_c = P.terra_geom.make(1, 24, 40, 96, 3, 32, 8, 16, 4, 8, 1)        # C not a multiple of 128
+    assert L.terra_block_bwd_workspace_bytes(ctypes.byref(bad_c), 1) == 0
+    assert L.terra_block_bwd_workspace_bytes(ctypes.byref(ok), 0) == 0    # fp32: bf16 only
+    assert L.terra_block_bwd_workspace_bytes(ctypes.byref(ok), 1) > 0
+    assert L.terra_block_fwd(ctypes.byref(bad_c), 1, fake, None, fake, fake, None, s) == 2
+    assert L.terra_block_fwd(ctypes.byref(ok), 2, fake, None, fake, fake, None, s) == 2
+    assert L.terra_block_fwd(ctypes.byref(ok), 1, fake, None, fake, fake, None, s) == 1   # NULL structs
+    p = P.terra_block_params()
+    sv = P.terra_block_saved()
+    assert L.terra_block_fwd(ctypes.byref(ok), 1, fake, ctypes.byref(p), fake, fake, ctypes.byref(sv), s) == 1
+    gr = P.terra_block_grads()
+    need = L.terra_block_bwd_workspace_bytes(ctypes.byref(ok), 1)
+    for n in P.BLOCK_PARAM_NAMES:
+        setattr(p, n, 0x1000)
+        setattr(gr, n, 0x1000)
+    for n in P.BLOCK_SAVED_NAMES:
+        setattr(sv, n, 0x1000)
+    assert L.terra_block_bwd(ctypes.byref(ok), 1, fake, fake, ctypes.byref(p), fake, ctypes.byref(sv), fake,
+                             ctypes.byref(gr), fake, fake, ctypes.c_size_t(need - 1), s) == 3
