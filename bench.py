@@ -155,6 +155,72 @@ def cpu_baseline(cfg, seconds_target=8.0, repeats=3):
     }
 
 
+def time_block(cfg, args, dev, flush):
+    """The whole Swin block (LayerNorm, QKV projection, attention, output
+    projection, MLP; forward then backward) on the same grid, timed like the
+    attention step.  Flops: the four linear layers' 24 T C^2 forward and
+    48 T C^2 backward (T tokens) plus the attention's 12 n^2 hd per window
+    and head."""
+    import torch
+    import paper_2608_15211_amd as P
+
+    print("bench: Swin block inputs", file=sys.stderr, flush=True)
+    inp = ts.make_block_inputs(cfg)
+    x = torch.from_numpy(inp["x"]).to(dev).to(torch.bfloat16)
+    dx2 = torch.from_numpy(inp["dx2"]).to(dev).to(torch.bfloat16)
+    params = {n: torch.from_numpy(v).to(dev).to(torch.bfloat16 if n.startswith("w_") else torch.float32)
+              for n, v in inp["params"].items()}
+    table = torch.from_numpy(inp["table"]).to(dev)
+    del inp
+    saved = P.terra_block_saved_alloc(cfg, dev)
+    x2 = torch.empty_like(x)
+    shapes = {n: params[n].shape for n in params}
+    out = (torch.empty_like(x), {n: torch.empty(shapes[n], dtype=torch.float32, device=dev) for n in params},
+           torch.empty_like(table))
+    ws = torch.empty(P.terra_block_bwd_workspace_bytes(cfg), dtype=torch.uint8, device=dev)
+    fws = torch.empty(P.terra_block_fwd_workspace_bytes(cfg), dtype=torch.uint8, device=dev)
+
+    def fwd():
+        P.terra_block_fwd(x, params, table, cfg, saved=saved, out=x2, workspace=fws)
+
+    def bwd():
+        P.terra_block_bwd(dx2, x, params, table, cfg, saved, out=out, workspace=ws)
+
+    for _ in range(max(2, args.warmup // 5)):
+        fwd()
+        bwd()
+    torch.cuda.synchronize()
+    tf, tb = [], []
+    for _ in range(max(5, args.steps // 2)):
+        flush.zero_()
+        e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+        e0.record()
+        fwd()
+        e1.record()
+        bwd()
+        e2.record()
+        tf.append(e0)
+        tb.append((e1, e2))
+    torch.cuda.synchronize()
+    fwd_ms = float(np.median([a.elapsed_time(b) for a, (b, _) in zip(tf, tb)]))
+    bwd_ms = float(np.median([b.elapsed_time(c) for b, c in tb]))
+    T, C = cfg.B * cfg.H * cfg.W, cfg.C
+    alg = algorithmic(cfg)
+    lin_f, lin_b = 24.0 * T * C * C, 48.0 * T * C * C
+    fl_f, fl_b = lin_f + alg["fwd_flops"], lin_b + alg["bwd_flops"]
+    peak = PEAK_BF16_TFLOPS
+    tot = (fl_f + fl_b) / ((fwd_ms + bwd_ms) * 1e-3) / 1e12
+    print("bench: Swin block timed", file=sys.stderr, flush=True)
+    return {"fwd_ms": round(fwd_ms, 4), "bwd_ms": round(bwd_ms, 4),
+            "step_ms": round(fwd_ms + bwd_ms, 4),
+            "tflops": round(tot, 1), "frac_mfma_peak": round(tot / peak, 4),
+            "fwd_tflops": round(fl_f / (fwd_ms * 1e-3) / 1e12, 1),
+            "bwd_tflops": round(fl_b / (bwd_ms * 1e-3) / 1e12, 1),
+            "flops_per_step": fl_f + fl_b,
+            "note": "LayerNorm + QKV + attention + projection + GELU MLP (ratio 4), forward and backward; "
+                    "medians of the timed steps"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -162,6 +228,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--config", default=DEFAULT_CONFIG, choices=list(ts.ALL))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-block", action="store_true", help="skip the Swin-block timing")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the path has no multi-GPU leg in this build "
@@ -320,6 +387,8 @@ def main():
                     "fwd_ms": round(ps_unf["fwd_wm"], 4), "bwd_ms": round(ps_unf["bwd_wm"], 4),
                     "route_ms_per_step": round(ps_unf["route"] + ps_unf["unroute"], 4)},
     }
+    if not args.no_block and cfg.dtype == "bf16" and cfg.C % 128 == 0 and cfg.C <= 2048:
+        line["swin_block"] = time_block(cfg, args, dev, flush)
     if not args.no_cpu_baseline:
         print("bench: timing the oracle on a sample", file=sys.stderr, flush=True)
         cb = cpu_baseline(cfg)

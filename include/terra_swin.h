@@ -199,9 +199,10 @@ int terra_winattn_bwd_nhwc_noalloc(const terra_geom* g, int dtype, const void* q
  * W_fc2 C x 4C, all row-major (out x in) bf16; gains, shifts and biases
  * float32.  Element type TERRA_BF16 only; C must be a multiple of 128 and
  * at most 2048, and the geometry must suit the attention.
- * LayerNorm is applied to the projection inputs while they are staged for
- * the matrix cores (its output never reaches memory); Q, K and V are
- * written straight as the NHWC tensors the fused attention reads.
+ * LayerNorm never writes its output to memory: the forward folds it into
+ * the projection that follows it, the backward applies it to the staged
+ * operand of the weight gradient; Q, K and V are written straight as the
+ * NHWC tensors the fused attention reads.
  * ------------------------------------------------------------------------- */
 
 typedef struct terra_block_params {      /* device pointers                 */
@@ -234,9 +235,20 @@ typedef struct terra_block_saved {
   void *h, *a;
 } terra_block_saved;
 
-/* Forward: x (bf16 NHWC) -> x2 (bf16 NHWC), filling `saved`. */
+/* Device workspace terra_block_fwd needs (0 on invalid input): the QKV and
+ * first MLP weights with the LayerNorm gains folded in, and two per-output
+ * vectors each. */
+size_t terra_block_fwd_workspace_bytes(const terra_geom* g, int dtype);
+
+/* Forward: x (bf16 NHWC) -> x2 (bf16 NHWC), filling `saved`.  Each
+ * LayerNorm is folded into the projection after it: with
+ * Wf[n][k] = bf16(W[n][k] gain_k), s_n = sum_k Wf[n][k] and
+ * c_n = b_n + sum_k W[n][k] shift_k, LN(z) W^T + b = rstd (z Wf^T - mean s) + c,
+ * so the matrix cores run on the raw activations and the normalisation is
+ * applied to the accumulators. */
 int terra_block_fwd(const terra_geom* g, int dtype, const void* x, const terra_block_params* p,
-                    const float* bias_table, void* x2, const terra_block_saved* saved, void* stream);
+                    const float* bias_table, void* x2, const terra_block_saved* saved, void* workspace,
+                    size_t workspace_bytes, void* stream);
 
 /* Device workspace terra_block_bwd needs (0 on invalid input). */
 size_t terra_block_bwd_workspace_bytes(const terra_geom* g, int dtype);

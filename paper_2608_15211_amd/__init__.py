@@ -15,7 +15,8 @@ Entry points (same names as the C ABI):
     terra_plan_padded_grid, terra_plan_window_ranges, terra_plan_rank,
     terra_window_route_rank, terra_window_unroute_rank, terra_fragment_pack,
     terra_fragment_unpack (ragged window assignment and per-rank route),
-    terra_block_fwd, terra_block_bwd_workspace_bytes, terra_block_bwd (the
+    terra_block_fwd_workspace_bytes, terra_block_fwd,
+    terra_block_bwd_workspace_bytes, terra_block_bwd (the
     Swin block around the attention: LayerNorm, projections, MLP)
 """
 
@@ -126,7 +127,9 @@ def lib():
     L.terra_fragment_pack.argtypes = [G, i32, i32, i32, i32, vp, vp, vp]
     L.terra_fragment_unpack.argtypes = [G, i32, i32, i32, i32, vp, vp, vp]
     L.terra_block_fwd.argtypes = [G, i32, vp, ctypes.POINTER(terra_block_params), vp, vp,
-                                  ctypes.POINTER(terra_block_saved), vp]
+                                  ctypes.POINTER(terra_block_saved), vp, sz, vp]
+    L.terra_block_fwd_workspace_bytes.argtypes = [G, i32]
+    L.terra_block_fwd_workspace_bytes.restype = sz
     L.terra_block_bwd_workspace_bytes.argtypes = [G, i32]
     L.terra_block_bwd_workspace_bytes.restype = sz
     L.terra_block_bwd.argtypes = [G, i32, vp, vp, ctypes.POINTER(terra_block_params), vp,
@@ -475,7 +478,11 @@ def _saved_struct(saved, gg):
     return st
 
 
-def terra_block_fwd(x, params, table, g, saved=None, out=None):
+def terra_block_fwd_workspace_bytes(g, dtype="bf16"):
+    return int(lib().terra_block_fwd_workspace_bytes(ctypes.byref(_geom(g)), _dtype_code(dtype)))
+
+
+def terra_block_fwd(x, params, table, g, saved=None, out=None, workspace=None):
     """One Swin block forward on NHWC bf16 x.  params: dict of device tensors
     (weights bf16, the rest float32).  Returns (x2, saved)."""
     import torch
@@ -485,11 +492,15 @@ def terra_block_fwd(x, params, table, g, saved=None, out=None):
         saved = terra_block_saved_alloc(gg, x.device)
     if out is None:
         out = torch.empty_like(x)
+    need = terra_block_fwd_workspace_bytes(gg)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
     _check(lib().terra_block_fwd(ctypes.byref(gg), TERRA_BF16, _dev(x, "x", torch.bfloat16, T * C),
                                  ctypes.byref(_params_struct(params, gg)),
                                  _dev(table, "table", torch.float32, _sizes(gg)[2]),
                                  _dev(out, "x2", torch.bfloat16, T * C),
-                                 ctypes.byref(_saved_struct(saved, gg)), _stream()))
+                                 ctypes.byref(_saved_struct(saved, gg)), _dev(workspace, "workspace"),
+                                 ctypes.c_size_t(workspace.numel()), _stream()))
     return out, saved
 
 

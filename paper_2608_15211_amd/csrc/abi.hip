@@ -18,7 +18,8 @@ hipError_t launch_route(const Geo& g, int row_bytes, const void* src, void* dst,
                         hipStream_t stream);
 hipError_t launch_layout(const Geo& g, int32_t* offsets, int32_t* counts, hipStream_t stream);
 hipError_t launch_block_fwd(const Geo& g, const void* x, const BlockParams& p, const float* table, void* x2,
-                            const BlockSaved& s, hipStream_t st);
+                            const BlockSaved& s, void* ws, hipStream_t st);
+size_t block_fwd_workspace(const Geo& g);
 hipError_t launch_block_bwd(const Geo& g, const void* dx2, const void* x, const BlockParams& p, const float* table,
                             const BlockSaved& s, void* dx, const BlockGrads& gr, float* dtable, void* ws,
                             hipStream_t st);
@@ -315,8 +316,8 @@ int check_block(const terra_geom* g, int dtype) {
   if (dtype != TERRA_BF16) return fail(TERRA_ERR_UNSUPPORTED, "the Swin block takes TERRA_BF16 only");
   if (g->C % 128 != 0 || g->C > 2048)
     return fail(TERRA_ERR_UNSUPPORTED, "the Swin block needs C a multiple of 128 and at most 2048 (C = %d)", g->C);
-  if ((int64_t)g->B * g->H * g->W * 4 * g->C >= kMaxElems)
-    return fail(TERRA_ERR_UNSUPPORTED, "B*H*W*4C must be below 2^31");
+  if ((int64_t)g->B * g->H * g->W * 4 * g->C >= kMaxElems / 2)
+    return fail(TERRA_ERR_UNSUPPORTED, "B*H*W*4C must be below 2^30 (operands under 2 GiB)");
   return ok();
 }
 terra::BlockParams to_params(const terra_block_params* p) {
@@ -339,8 +340,14 @@ bool any_null(std::initializer_list<const void*> ps) {
 
 extern "C" {
 
+size_t terra_block_fwd_workspace_bytes(const terra_geom* g, int dtype) {
+  if (check_block(g, dtype)) return 0;
+  return terra::block_fwd_workspace(make_geo(g));
+}
+
 int terra_block_fwd(const terra_geom* g, int dtype, const void* x, const terra_block_params* p,
-                    const float* bias_table, void* x2, const terra_block_saved* sv, void* stream) {
+                    const float* bias_table, void* x2, const terra_block_saved* sv, void* workspace,
+                    size_t workspace_bytes, void* stream) {
   int s = check_block(g, dtype);
   if (s) return s;
   if (!p || !sv) return fail(TERRA_ERR_INVALID, "parameter or saved-activation struct is NULL");
@@ -348,8 +355,13 @@ int terra_block_fwd(const terra_geom* g, int dtype, const void* x, const terra_b
                 p->ln2_b, p->w_fc1, p->b_fc1, p->w_fc2, p->b_fc2, sv->mu1, sv->rstd1, sv->mu2, sv->rstd2, sv->q,
                 sv->k, sv->v, sv->o, sv->lse, sv->x1, sv->h, sv->a}))
     return fail(TERRA_ERR_INVALID, "tensor pointer is NULL");
+  const size_t need = terra::block_fwd_workspace(make_geo(g));
+  if (!workspace || workspace_bytes < need)
+    return fail(TERRA_ERR_WORKSPACE, "workspace of %zu bytes given, %zu needed", workspace ? workspace_bytes : (size_t)0,
+                need);
   terra::Geo G = launch_geo(g);
-  return hip_status(terra::launch_block_fwd(G, x, to_params(p), bias_table, x2, to_saved(sv), (hipStream_t)stream),
+  return hip_status(terra::launch_block_fwd(G, x, to_params(p), bias_table, x2, to_saved(sv), workspace,
+                                            (hipStream_t)stream),
                     "terra_block_fwd launch");
 }
 

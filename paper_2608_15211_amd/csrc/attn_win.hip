@@ -753,7 +753,6 @@ __global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
     float* __restrict__ partial, Geo g, int nslice, int per_slice, float scale_log2, float scale) {
   constexpr int HD = kBwdHD;
   constexpr int KS = kBwdKS;
-  constexpr int RS = kBwdRS;
   extern __shared__ __align__(16) char smem[];
   bf16* ks = reinterpret_cast<bf16*>(smem);                     // [128][KS] K rows, then dQ
   bf16* vs = ks + kWinMax * KS;                                 // [128][KS] V rows

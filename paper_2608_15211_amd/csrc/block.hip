@@ -26,8 +26,6 @@ constexpr int kGT = 256;          // threads per GEMM workgroup (4 waves, 2 x 2)
 constexpr int kBM = 256;          // workgroup tile rows
 constexpr int kBN = 128;          // workgroup tile columns
 constexpr int kBK = 32;           // contraction depth per stage
-constexpr int kPadR = 8;          // LDS row padding of contraction-contiguous tiles
-constexpr int kPadC = 8;          // LDS row padding of contraction-strided tiles
 
 // A bf16 operand in memory: row-major, split into up to three column blocks
 // of `split` columns each (the Q, K and V tensors of the QKV layer are one
@@ -52,12 +50,13 @@ struct LnArgs {
 };
 
 enum Epi {
-  EPI_BIAS = 0,        // out = bf16(acc + bias)                (column-split output)
+  EPI_LN_QKV = 0,      // LayerNorm folded: out = bf16(rstd (acc - mean s) + c)   (column-split output)
   EPI_BIAS_RES = 1,    // out = bf16(acc + bias + res)
-  EPI_BIAS_GELU = 2,   // out = bf16(acc + bias), out2 = bf16(GELU(acc + bias))
+  EPI_LN_GELU = 2,     // t = rstd (acc - mean s) + c:  out = bf16(t), out2 = bf16(GELU(t))
   EPI_GELU_GRAD = 3,   // out = bf16(acc * GELU'(aux))
   EPI_F32 = 4,         // outf = acc (float32), slice blockIdx.z
   EPI_BF16 = 5,        // out = bf16(acc)
+  EPI_F32_ACC = 6,     // outf += acc (float32)
 };
 
 struct EpiArgs {
@@ -67,61 +66,117 @@ struct EpiArgs {
   const bf16* aux;     // residual or pre-activation, ld = N
   const float* bias;
   float* outf;         // float32 output, ld = N, slice stride M * N
+  const float* mean;   // LayerNorm folded into the epilogue: per-row mean and 1/std,
+  const float* rstd;   // per-column sum of the folded weights (lns) and constant (lnc)
+  const float* lns;
+  const float* lnc;
 };
 
-__device__ inline float gelu_f(float t) { return 0.5f * t * (1.0f + erff(t * 0.70710678118654752f)); }
-__device__ inline float gelu_grad_f(float t) {
-  return 0.5f * (1.0f + erff(t * 0.70710678118654752f)) + t * 0.39894228040143268f * __expf(-0.5f * t * t);
+// Phi(x), the standard normal distribution function, and exp(-x^2 / 2), with
+// erf from Abramowitz and Stegun's rational approximation 7.1.26
+// (|error| <= 1.5e-7, far below bf16 resolution); the Gaussian factor is
+// shared between erf and the GELU derivative.
+__device__ inline void phi_gauss(float x, float& Phi, float& gauss) {
+  const float z = fabsf(x) * 0.70710678118654752f;
+  const float t = 1.0f / (1.0f + 0.3275911f * z);
+  gauss = __expf(-0.5f * x * x);
+  const float poly =
+      t * (0.254829592f + t * (-0.284496736f + t * (1.421413741f + t * (-1.453152027f + t * 1.061405429f))));
+  const float erfz = 1.0f - poly * gauss;
+  Phi = 0.5f * (1.0f + copysignf(erfz, x));
+}
+__device__ inline float gelu_f(float x) {
+  float Phi, g;
+  phi_gauss(x, Phi, g);
+  return x * Phi;
+}
+__device__ inline float gelu_grad_f(float x) {
+  float Phi, g;
+  phi_gauss(x, Phi, g);
+  return Phi + x * 0.39894228040143268f * g;   // Phi(x) + x phi(x)
 }
 
-// Natural-order transposed operand from a tile stored [k][m] (row stride S):
-// lane l receives T[k0 + 8h + x][m0 + l % 32], x = 0..7, h = l / 32.  In
-// each 16-lane group G of the transpose read, lane i gets element i % 4 of
-// the 8 bytes that lane 16G + 4x + i/4 addresses, so lane L addresses row
-// k0 + 8h + (L % 16) / 4 (and 4 rows further for the second read), columns
-// m0 + 16 (G % 2) + 4 (L % 4).
-template <int S>
+// ---------------------------------------------------------------------------
+// LDS tiles.  A stage holds the A tile (kBM output rows x kBK) and the B tile
+// (kBN x kBK), each in its memory layout, unpadded, with the 16-byte chunks
+// of each row permuted by an XOR of the row index so that the matrix-core
+// operand reads hit distinct banks:
+// * KROW tile (memory [R][kBK], 4 chunks a row): chunk c of row r sits at
+//   chunk c ^ ((r >> 2) & 3) - 16 consecutive rows read at one logical chunk
+//   cover all 64 banks;
+// * COLK tile (memory [kBK][R], R / 8 chunks a row): chunk c of row k sits
+//   at chunk c ^ (2 (k & 3)) - the four rows of one transpose read land on
+//   four different 32-byte spans.
+// ---------------------------------------------------------------------------
+template <int R, bool KROW>
+struct Tile {
+  static constexpr int kChunks = R * kBK / 8;   // 16-byte chunks
+  static constexpr int kPer = kChunks / kGT;    // per thread
+  static constexpr int kElems = R * kBK;
+  // element offset of (row, logical chunk) of the memory layout
+  __device__ static int off(int row, int c) {
+    if (KROW) return row * kBK + 8 * (c ^ ((row >> 2) & 3));
+    return row * R + 8 * (c ^ (2 * (row & 3)));
+  }
+  // memory (row, column) of the chunk stored in slot q (slot = chunk position in LDS order)
+  __device__ static void slot_src(int q, int r0, int k0, int& mrow, int& mcol) {
+    if (KROW) {
+      const int row = q >> 2, p = q & 3;
+      mrow = r0 + row;
+      mcol = k0 + 8 * (p ^ ((row >> 2) & 3));
+    } else {
+      const int row = q / (R / 8), p = q - row * (R / 8);
+      mrow = k0 + row;
+      mcol = r0 + 8 * (p ^ (2 * (row & 3)));
+    }
+  }
+};
+
+// Straight operand (KROW tile): lane l receives T[m0 + l % 32][k0 + 8h + x],
+// x = 0..7, h = l / 32, as one 16-byte read.
+template <int R>
+__device__ inline bf16x8 row_operand(const bf16* T, int k0, int m0, int lane) {
+  const int row = m0 + (lane & 31);
+  return *reinterpret_cast<const bf16x8*>(T + Tile<R, true>::off(row, (k0 >> 3) + (lane >> 5)));
+}
+
+// Natural-order transposed operand (COLK tile): lane l receives
+// T[k0 + 8h + x][m0 + l % 32], x = 0..7.  In each 16-lane group G of the
+// transpose read, lane i gets element i % 4 of the 8 bytes that lane
+// 16G + 4x + i/4 addresses, so lane L addresses row k0 + 8h + (L % 16) / 4
+// (4 rows further for the second read), columns m0 + 16 (G % 2) + 4 (L % 4).
+template <int R>
 __device__ inline bf16x8 tr_operand(const bf16* T, int k0, int m0, int lane) {
   const int G = lane >> 4;
-  const bf16* p = T + (k0 + 8 * (G >> 1) + ((lane & 15) >> 2)) * S + m0 + 16 * (G & 1) + 4 * (lane & 3);
-  const v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)p);
-  const v4s hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(p + 4 * S));
+  const int row = k0 + 8 * (G >> 1) + ((lane & 15) >> 2);
+  const int m = m0 + 16 * (G & 1) + 4 * (lane & 3);
+  const int c = m >> 3, e = m & 7;
+  const bf16* p0 = T + Tile<R, false>::off(row, c) + e;
+  const bf16* p1 = T + Tile<R, false>::off(row + 4, c) + e;
+  const v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)p0);
+  const v4s hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)p1);
   typedef short v8s __attribute__((ext_vector_type(8)));
   const v8s o = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
   return __builtin_bit_cast(bf16x8, o);
 }
 
-// Straight operand from a tile stored [m][k] (row stride S): lane l
-// receives T[m0 + l % 32][k0 + 8h + x].
-template <int S>
-__device__ inline bf16x8 row_operand(const bf16* T, int k0, int m0, int lane) {
-  return *reinterpret_cast<const bf16x8*>(T + (m0 + (lane & 31)) * S + k0 + 8 * (lane >> 5));
-}
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+__device__ void raw_buffer_load_lds(i32x4 rsrc, __attribute__((address_space(3))) uint32_t* lds, int size,
+                                    int voffset, int soffset, int offset,
+                                    int aux) __asm("llvm.amdgcn.raw.buffer.load.lds");
 
-// Staging geometry of one operand tile (R rows of the output side x kBK).
-// KROW: the contraction index runs along memory rows (memory [R][kBK]);
-// otherwise down memory columns (memory [kBK][R]).
-template <int R, bool KROW>
-struct Stage {
-  static constexpr int kChunks = R * kBK / 8;                 // 16-byte chunks per stage
-  static constexpr int kPer = kChunks / kGT;                  // per thread
-  static constexpr int kS = KROW ? kBK + kPadR : R + kPadC;   // LDS row stride
-  static constexpr int kElems = KROW ? R * kS : kBK * kS;
-  // memory row / column of chunk c of the tile at (r0 output rows, k0)
-  __device__ static void where(int c, int r0, int k0, int& mrow, int& mcol) {
-    if (KROW) {
-      mrow = r0 + c / (kBK / 8);
-      mcol = k0 + 8 * (c % (kBK / 8));
-    } else {
-      mrow = k0 + c / (R / 8);
-      mcol = r0 + 8 * (c % (R / 8));
-    }
-  }
-  __device__ static int lds_off(int c) {
-    if (KROW) return (c / (kBK / 8)) * kS + 8 * (c % (kBK / 8));
-    return (c / (R / 8)) * kS + 8 * (c % (R / 8));
-  }
-};
+// Buffer descriptor of a whole (single-block) operand: base, size in bytes
+// (below 2^31, so that the offset 2^31 used for rows outside the operand or
+// the contraction slice is past the end and reads zeros).
+__device__ inline i32x4 buffer_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t b = (uint64_t)base;
+  i32x4 r;
+  r[0] = (int)(uint32_t)b;
+  r[1] = (int)(uint32_t)(b >> 32);
+  r[2] = (int)bytes;
+  r[3] = 0x00020000;
+  return r;
+}
 
 template <bool LN>
 __device__ inline uint4 ln_chunk(uint4 raw, const LnArgs& ln, int mrow, int mcol) {
@@ -139,22 +194,71 @@ __device__ inline uint4 ln_chunk(uint4 raw, const LnArgs& ln, int mrow, int mcol
   return __builtin_bit_cast(uint4, v);
 }
 
+// One operand's staging.  DIRECT: 16-byte buffer loads straight into LDS
+// (asynchronous; issued two stages ahead); otherwise loads into registers
+// one stage ahead, the LayerNorm (LN) applied there, then an LDS store -
+// the path for LayerNorm operands and for operands split over several
+// tensors.  KROW: the contraction index runs along memory rows.  VALID:
+// memory rows / columns inside the operand and the contraction slice.
+template <int R, bool KROW, bool DIRECT, bool LN>
+struct Staged {
+  typedef Tile<R, KROW> T;
+  uint4 reg[DIRECT ? 1 : T::kPer];
+  __device__ static bool valid(int mrow, int mcol, int nouter, int kend) {
+    return KROW ? (mrow < nouter && mcol < kend) : (mrow < kend && mcol < nouter);
+  }
+  __device__ void issue_direct(const i32x4& rs, const Mat& X, bf16* tile, int r0, int k0, int nouter, int kend) {
+    const int wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int u = 0; u < T::kPer; ++u) {
+      const int q = u * kGT + threadIdx.x;
+      int mr, mc;
+      T::slot_src(q, r0, k0, mr, mc);
+      const int voff = valid(mr, mc, nouter, kend) ? (int)(((int64_t)mr * X.split + mc) * 2) : (int)0x80000000;
+      bf16* dst = tile + 8 * (u * kGT + wave * 64);      // wave-uniform base of 64 slots
+      raw_buffer_load_lds(rs, (__attribute__((address_space(3))) uint32_t*)(uintptr_t)(uint32_t)(uintptr_t)dst, 16, voff, 0,
+                          0, 0);
+    }
+  }
+  __device__ void load_reg(const Mat& X, const LnArgs& ln, int r0, int k0, int nouter, int kend) {
+#pragma unroll
+    for (int u = 0; u < T::kPer; ++u) {
+      const int q = u * kGT + threadIdx.x;
+      int mr, mc;
+      T::slot_src(q, r0, k0, mr, mc);
+      const bool ok = valid(mr, mc, nouter, kend);
+      reg[u] = ok ? *reinterpret_cast<const uint4*>(X.at(mr, mc)) : make_uint4(0, 0, 0, 0);
+      if (LN && ok) reg[u] = ln_chunk<true>(reg[u], ln, KROW ? mr : mr, mc);
+    }
+  }
+  __device__ void store_reg(bf16* tile) const {
+#pragma unroll
+    for (int u = 0; u < T::kPer; ++u)
+      *reinterpret_cast<uint4*>(tile + 8 * (u * kGT + threadIdx.x)) = reg[u];
+  }
+};
+
+template <int N>
+__device__ inline void wait_vm() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
 // C[M][N] = A[M][K] B[K][N] (+ epilogue).  AKROW: A is memory [M][K]
-// (else [K][M]); BKROW: B is memory [N][K] (else [K][N]).  LNA / LNB:
-// LayerNorm applied to A / B while staging (memory rows = tokens).
-// blockIdx.z: contraction slice [z * kslice, (z+1) * kslice).
-template <bool AKROW, bool BKROW, bool LNA, bool LNB, int EPI>
+// (else [K][M]); BKROW: B is memory [N][K] (else [K][N]).  ADIR / BDIR:
+// operand staged by direct-to-LDS loads (else through registers).  LNA /
+// LNB: LayerNorm applied to A / B while staging (memory rows = tokens).
+// blockIdx.z: contraction slice [z * kslice, (z+1) * kslice).  Three LDS
+// stages: the direct loads of stage kt + 2 and the register loads of stage
+// kt + 1 are in flight while stage kt is on the matrix cores.
+template <bool AKROW, bool BKROW, bool ADIR, bool BDIR, bool LNA, bool LNB, int EPI>
 __global__ __launch_bounds__(kGT, 2) void gemm_kernel(Mat A, Mat B, LnArgs lna, LnArgs lnb, EpiArgs ep,
                                                       int M, int N, int K, int kslice) {
-  typedef Stage<kBM, AKROW> SA;
-  typedef Stage<kBN, BKROW> SB;
+  typedef Staged<kBM, AKROW, ADIR, LNA> OA;
+  typedef Staged<kBN, BKROW, BDIR, LNB> OB;
+  constexpr int kStage = OA::T::kElems + OB::T::kElems;
+  constexpr int kDirectLoads = (ADIR ? OA::T::kPer : 0) + (BDIR ? OB::T::kPer : 0);
   extern __shared__ __align__(16) char smem[];
-  bf16* la[2];
-  bf16* lb[2];
-  la[0] = reinterpret_cast<bf16*>(smem);
-  la[1] = la[0] + SA::kElems;
-  lb[0] = la[1] + SA::kElems;
-  lb[1] = lb[0] + SB::kElems;
+  bf16* lds = reinterpret_cast<bf16*>(smem);
 
   const int nN = N / kBN;
   const int nM = (M + kBM - 1) / kBM;
@@ -168,6 +272,8 @@ __global__ __launch_bounds__(kGT, 2) void gemm_kernel(Mat A, Mat B, LnArgs lna, 
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int wm = (wave >> 1) * 128, wn = (wave & 1) * 64;
+  const i32x4 rsa = buffer_rsrc(A.p[0], ADIR ? (uint32_t)((int64_t)A.rows * A.split * 2) : 0u);
+  const i32x4 rsb = buffer_rsrc(B.p[0], BDIR ? (uint32_t)((int64_t)B.rows * B.split * 2) : 0u);
 
   f32x16 acc[4][2];
 #pragma unroll
@@ -175,60 +281,55 @@ __global__ __launch_bounds__(kGT, 2) void gemm_kernel(Mat A, Mat B, LnArgs lna, 
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
 
-  uint4 ra[SA::kPer], rb[SB::kPer];
-  auto load = [&](int k0) {
-#pragma unroll
-    for (int u = 0; u < SA::kPer; ++u) {
-      int mr, mc;
-      SA::where(threadIdx.x + u * kGT, m0, k0, mr, mc);
-      const bool ok = AKROW ? (mr < M && mc < kend) : (mr < kend && mc < M);
-      ra[u] = ok ? *reinterpret_cast<const uint4*>(A.at(mr, mc)) : make_uint4(0, 0, 0, 0);
-      if (LNA && ok) ra[u] = ln_chunk<true>(ra[u], lna, mr, mc);
-    }
-#pragma unroll
-    for (int u = 0; u < SB::kPer; ++u) {
-      int mr, mc;
-      SB::where(threadIdx.x + u * kGT, n0, k0, mr, mc);
-      const bool ok = BKROW ? (mc < kend) : (mr < kend);
-      rb[u] = ok ? *reinterpret_cast<const uint4*>(B.at(mr, mc)) : make_uint4(0, 0, 0, 0);
-      if (LNB && ok) rb[u] = ln_chunk<true>(rb[u], lnb, mr, mc);
-    }
+  OA oa;
+  OB ob;
+  auto a_tile = [&](int st) { return lds + st * kStage; };
+  auto b_tile = [&](int st) { return lds + st * kStage + OA::T::kElems; };
+  auto issue = [&](int s) {       // direct loads of stage s
+    const int k0 = kbeg + s * kBK;
+    if (ADIR) oa.issue_direct(rsa, A, a_tile(s % 3), m0, k0, M, kend);
+    if (BDIR) ob.issue_direct(rsb, B, b_tile(s % 3), n0, k0, N, kend);
   };
-  auto store = [&](int buf) {
-#pragma unroll
-    for (int u = 0; u < SA::kPer; ++u)
-      *reinterpret_cast<uint4*>(la[buf] + SA::lds_off(threadIdx.x + u * kGT)) = ra[u];
-#pragma unroll
-    for (int u = 0; u < SB::kPer; ++u)
-      *reinterpret_cast<uint4*>(lb[buf] + SB::lds_off(threadIdx.x + u * kGT)) = rb[u];
+  auto load_regs = [&](int s) {   // register loads of stage s
+    const int k0 = kbeg + s * kBK;
+    if (!ADIR) oa.load_reg(A, lna, m0, k0, M, kend);
+    if (!BDIR) ob.load_reg(B, lnb, n0, k0, N, kend);
+  };
+  auto store_regs = [&](int s) {
+    if (!ADIR) oa.store_reg(a_tile(s % 3));
+    if (!BDIR) ob.store_reg(b_tile(s % 3));
   };
 
   const int nk = (kend - kbeg + kBK - 1) / kBK;
   if (nk > 0) {
-    load(kbeg);
-    store(0);
+    load_regs(0);
+    issue(0);
+    if (nk > 1) issue(1);
+    store_regs(0);
   }
-  __syncthreads();
   for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) load(kbeg + (kt + 1) * kBK);
+    if (kt + 1 < nk) wait_vm<kDirectLoads>();
+    else wait_vm<0>();
+    __syncthreads();
+    if (kt + 1 < nk) load_regs(kt + 1);
+    if (kt + 2 < nk) issue(kt + 2);
+    const bf16* ta = a_tile(kt % 3);
+    const bf16* tb = b_tile(kt % 3);
 #pragma unroll
     for (int c = 0; c < kBK / 16; ++c) {
       bf16x8 bo[2];
 #pragma unroll
       for (int j = 0; j < 2; ++j)
-        bo[j] = BKROW ? row_operand<SB::kS>(lb[buf], 16 * c, wn + 32 * j, lane)
-                      : tr_operand<SB::kS>(lb[buf], 16 * c, wn + 32 * j, lane);
+        bo[j] = BKROW ? row_operand<kBN>(tb, 16 * c, wn + 32 * j, lane) : tr_operand<kBN>(tb, 16 * c, wn + 32 * j, lane);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const bf16x8 ao = AKROW ? row_operand<SA::kS>(la[buf], 16 * c, wm + 32 * i, lane)
-                                : tr_operand<SA::kS>(la[buf], 16 * c, wm + 32 * i, lane);
+        const bf16x8 ao =
+            AKROW ? row_operand<kBM>(ta, 16 * c, wm + 32 * i, lane) : tr_operand<kBM>(ta, 16 * c, wm + 32 * i, lane);
 #pragma unroll
         for (int j = 0; j < 2; ++j) mma16(acc[i][j], ao, bo[j]);
       }
     }
-    if (kt + 1 < nk) store(buf ^ 1);
-    __syncthreads();
+    if (kt + 1 < nk) store_regs(kt + 1);
   }
 
   // Epilogue.  acc[i][j] holds rows wm + 32i + 8g + 4h + x (register 4g + x),
@@ -237,7 +338,9 @@ __global__ __launch_bounds__(kGT, 2) void gemm_kernel(Mat A, Mat B, LnArgs lna, 
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     const int n = n0 + wn + 32 * j + col;
-    const float bias = (EPI == EPI_BIAS || EPI == EPI_BIAS_RES || EPI == EPI_BIAS_GELU) ? ep.bias[n] : 0.0f;
+    const float bias = EPI == EPI_BIAS_RES ? ep.bias[n] : 0.0f;
+    const float lns = (EPI == EPI_LN_QKV || EPI == EPI_LN_GELU) ? ep.lns[n] : 0.0f;
+    const float lnc = (EPI == EPI_LN_QKV || EPI == EPI_LN_GELU) ? ep.lnc[n] : 0.0f;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -246,23 +349,64 @@ __global__ __launch_bounds__(kGT, 2) void gemm_kernel(Mat A, Mat B, LnArgs lna, 
         if (m >= M) continue;
         const float v = acc[i][j][r];
         const int64_t o = (int64_t)m * N + n;
-        if (EPI == EPI_BIAS) {
-          const int blk = n / ep.split;
-          ep.out[blk][(int64_t)m * ep.split + (n - blk * ep.split)] = (bf16)(v + bias);
+        if (EPI == EPI_LN_QKV || EPI == EPI_LN_GELU) {
+          const float t = ep.rstd[m] * (v - ep.mean[m] * lns) + lnc;
+          if (EPI == EPI_LN_QKV) {
+            const int blk = n / ep.split;
+            ep.out[blk][(int64_t)m * ep.split + (n - blk * ep.split)] = (bf16)t;
+          } else {
+            ep.out[0][o] = (bf16)t;
+            ep.out2[o] = (bf16)gelu_f(t);
+          }
         } else if (EPI == EPI_BIAS_RES) {
           ep.out[0][o] = (bf16)(v + bias + (float)ep.aux[o]);
-        } else if (EPI == EPI_BIAS_GELU) {
-          const float t = v + bias;
-          ep.out[0][o] = (bf16)t;
-          ep.out2[o] = (bf16)gelu_f(t);
         } else if (EPI == EPI_GELU_GRAD) {
           ep.out[0][o] = (bf16)(v * gelu_grad_f((float)ep.aux[o]));
         } else if (EPI == EPI_F32) {
           ep.outf[(int64_t)blockIdx.z * M * N + o] = v;
+        } else if (EPI == EPI_F32_ACC) {
+          ep.outf[o] += v;
         } else {
           ep.out[0][o] = (bf16)v;
         }
       }
+  }
+}
+
+// LayerNorm folded into the following linear layer: with
+// LN(x)_k = (x_k - mean) rstd gamma_k + beta_k,
+//   LN(x) W^T + b = rstd (x Wf^T - mean s) + c,
+//   Wf[n][k] = bf16(W[n][k] gamma_k),  s_n = sum_k Wf[n][k],
+//   c_n = b_n + sum_k W[n][k] beta_k,
+// so the GEMM runs on the raw activations and the epilogue normalises.  One
+// wave per output row n.
+__global__ __launch_bounds__(256) void ln_fold_kernel(const bf16* __restrict__ W, const float* __restrict__ gamma,
+                                                     const float* __restrict__ beta, const float* __restrict__ bias,
+                                                     bf16* __restrict__ Wf, float* __restrict__ lns,
+                                                     float* __restrict__ lnc, int N, int K) {
+  const int n = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (n >= N) return;
+  float sacc = 0.0f, cacc = 0.0f;
+  for (int k = 8 * lane; k < K; k += 512) {
+    const bf16x8 w = *reinterpret_cast<const bf16x8*>(W + (int64_t)n * K + k);
+    bf16x8 f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      f[i] = (bf16)((float)w[i] * gamma[k + i]);
+      sacc += (float)f[i];
+      cacc += (float)w[i] * beta[k + i];
+    }
+    *reinterpret_cast<bf16x8*>(Wf + (int64_t)n * K + k) = f;
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    sacc += __shfl_xor(sacc, o, 64);
+    cacc += __shfl_xor(cacc, o, 64);
+  }
+  if (lane == 0) {
+    lns[n] = sacc;
+    lnc[n] = cacc + bias[n];
   }
 }
 
@@ -400,6 +544,18 @@ __global__ __launch_bounds__(kRowThreads) void colsum_kernel(Mat X, int ncols, f
   for (int i = 0; i < 8; ++i) part[(int64_t)s * ncols + 8 * c8 + i] = acc[i];
 }
 
+// grp[g][i] = sum of part[s][i] over s in [g * per, (g + 1) * per), in
+// order (n entries per slice).
+__global__ __launch_bounds__(kRowThreads) void group_sum_kernel(const float* __restrict__ part, float* __restrict__ grp,
+                                                                int n, int per) {
+  const int i = blockIdx.x * kRowThreads + threadIdx.x;
+  if (i >= n) return;
+  const int g = blockIdx.y;
+  float acc = 0.0f;
+  for (int sl = g * per; sl < (g + 1) * per; ++sl) acc += part[(int64_t)sl * n + i];
+  grp[(int64_t)g * n + i] = acc;
+}
+
 // out[i] = sum over s < nslice of part[s * stride + i], in slice order.
 __global__ __launch_bounds__(kRowThreads) void slice_sum_kernel(const float* __restrict__ part, float* __restrict__ out,
                                                                 int64_t n, int64_t stride, int nslice) {
@@ -413,34 +569,21 @@ __global__ __launch_bounds__(kRowThreads) void slice_sum_kernel(const float* __r
 // ---------------------------------------------------------------------------
 // Host side.
 // ---------------------------------------------------------------------------
-static size_t gemm_lds(bool akrow, bool bkrow) {
-  const size_t a = akrow ? (size_t)kBM * (kBK + kPadR) : (size_t)kBK * (kBM + kPadC);
-  const size_t b = bkrow ? (size_t)kBN * (kBK + kPadR) : (size_t)kBK * (kBN + kPadC);
-  return 2 * (a + b) * sizeof(bf16);
-}
+constexpr size_t kGemmLds = 3 * (size_t)(kBM + kBN) * kBK * sizeof(bf16);   // three stages
 
-template <bool AKROW, bool BKROW, bool LNA, bool LNB, int EPI>
+template <bool AKROW, bool BKROW, bool ADIR, bool BDIR, bool LNA, bool LNB, int EPI>
 static hipError_t gemm(const Mat& A, const Mat& B, const LnArgs& lna, const LnArgs& lnb, const EpiArgs& ep,
                        int M, int N, int K, int nsplit, hipStream_t st) {
   const int tiles = ((M + kBM - 1) / kBM) * (N / kBN);
   const int kslice = ((K + nsplit - 1) / nsplit + kBK - 1) / kBK * kBK;
-  hipLaunchKernelGGL((gemm_kernel<AKROW, BKROW, LNA, LNB, EPI>), dim3(tiles, 1, nsplit), dim3(kGT),
-                     gemm_lds(AKROW, BKROW), st, A, B, lna, lnb, ep, M, N, K, kslice);
+  hipLaunchKernelGGL((gemm_kernel<AKROW, BKROW, ADIR, BDIR, LNA, LNB, EPI>), dim3(tiles, 1, nsplit), dim3(kGT),
+                     kGemmLds, st, A, B, lna, lnb, ep, M, N, K, kslice);
   return hipGetLastError();
 }
 
 static Mat mat(const void* p, int split, int rows) {
   Mat m;
   m.p[0] = m.p[1] = m.p[2] = (const bf16*)p;
-  m.split = split;
-  m.rows = rows;
-  return m;
-}
-static Mat mat3(const void* p0, const void* p1, const void* p2, int split, int rows) {
-  Mat m;
-  m.p[0] = (const bf16*)p0;
-  m.p[1] = (const bf16*)p1;
-  m.p[2] = (const bf16*)p2;
   m.split = split;
   m.rows = rows;
   return m;
@@ -462,50 +605,88 @@ static hipError_t ln_stats(const void* x, float* mu, float* rs, int T, int C, hi
   return hipGetLastError();
 }
 
+static size_t al(size_t x) { return (x + 255) / 256 * 256; }
+
+// Forward workspace: the folded QKV and fc1 weights and their per-output
+// sums and constants.
+struct FwdWs {
+  size_t wq, wf, sq, cq, sf, cf, total;
+};
+static FwdWs fwd_ws(const Geo& g) {
+  const size_t C = g.C;
+  FwdWs w;
+  size_t off = 0;
+  w.wq = off; off += al(3 * C * C * 2);
+  w.wf = off; off += al(4 * C * C * 2);
+  w.sq = off; off += al(3 * C * 4);
+  w.cq = off; off += al(3 * C * 4);
+  w.sf = off; off += al(4 * C * 4);
+  w.cf = off; off += al(4 * C * 4);
+  w.total = off;
+  return w;
+}
+size_t block_fwd_workspace(const Geo& g) { return fwd_ws(g).total; }
+
+static hipError_t ln_fold(const void* W, const float* gamma, const float* beta, const float* bias, bf16* Wf,
+                          float* lns, float* lnc, int N, int K, hipStream_t st) {
+  hipLaunchKernelGGL(ln_fold_kernel, dim3((N + 3) / 4), dim3(256), 0, st, (const bf16*)W, gamma, beta, bias, Wf, lns,
+                     lnc, N, K);
+  return hipGetLastError();
+}
+
 hipError_t launch_block_fwd(const Geo& g, const void* x, const BlockParams& p, const float* table, void* x2,
-                            const BlockSaved& s, hipStream_t st) {
+                            const BlockSaved& s, void* wsv, hipStream_t st) {
   const int T = g.B * g.H * g.W, C = g.C;
+  const FwdWs w = fwd_ws(g);
+  char* ws = reinterpret_cast<char*>(wsv);
+  bf16* wq = reinterpret_cast<bf16*>(ws + w.wq);
+  bf16* wf = reinterpret_cast<bf16*>(ws + w.wf);
+  float *sq = reinterpret_cast<float*>(ws + w.sq), *cq = reinterpret_cast<float*>(ws + w.cq);
+  float *sf = reinterpret_cast<float*>(ws + w.sf), *cf = reinterpret_cast<float*>(ws + w.cf);
   hipError_t e;
   LnArgs none = {nullptr, nullptr, nullptr, nullptr};
   EpiArgs ep = {};
-  // LN1 statistics, then qkv = LN1(x) W_qkv^T + b_qkv into Q, K, V (NHWC)
-  if ((e = ln_stats(x, s.mu1, s.rstd1, T, C, st)) != hipSuccess) return e;
-  LnArgs ln1 = {s.mu1, s.rstd1, p.ln1_g, p.ln1_b};
+#define TERRA_TRY(x)                    \
+  do {                                  \
+    if ((e = (x)) != hipSuccess) return e; \
+  } while (0)
+  // LN1 statistics; qkv = LN1(x) W_qkv^T + b_qkv with LN1 folded into the
+  // weights and the epilogue, written as Q, K, V (NHWC)
+  TERRA_TRY(ln_stats(x, s.mu1, s.rstd1, T, C, st));
+  TERRA_TRY(ln_fold(p.w_qkv, p.ln1_g, p.ln1_b, p.b_qkv, wq, sq, cq, 3 * C, C, st));
   ep.out[0] = (bf16*)s.q; ep.out[1] = (bf16*)s.k; ep.out[2] = (bf16*)s.v; ep.split = C;
-  ep.bias = p.b_qkv;
-  if ((e = gemm<true, true, true, false, EPI_BIAS>(mat(x, C, T), mat(p.w_qkv, C, 3 * C), ln1, none, ep, T, 3 * C,
-                                                   C, 1, st)) != hipSuccess)
-    return e;
+  ep.mean = s.mu1; ep.rstd = s.rstd1; ep.lns = sq; ep.lnc = cq;
+  TERRA_TRY((gemm<true, true, true, true, false, false, EPI_LN_QKV>(mat(x, C, T), mat(wq, C, 3 * C), none, none, ep,
+                                                                    T, 3 * C, C, 1, st)));
   // windowed attention with the route fused in
-  if ((e = launch_attn_fwd(g, 1, true, s.q, s.k, s.v, table, s.o, s.lse, st)) != hipSuccess) return e;
+  TERRA_TRY(launch_attn_fwd(g, 1, true, s.q, s.k, s.v, table, s.o, s.lse, st));
   // x1 = x + o W_p^T + b_p
   ep = EpiArgs{};
   ep.out[0] = (bf16*)s.x1; ep.split = C; ep.aux = (const bf16*)x; ep.bias = p.b_proj;
-  if ((e = gemm<true, true, false, false, EPI_BIAS_RES>(mat(s.o, C, T), mat(p.w_proj, C, C), none, none, ep, T, C,
-                                                        C, 1, st)) != hipSuccess)
-    return e;
-  // h = LN2(x1) W_1^T + b_1, a = GELU(h)
-  if ((e = ln_stats(s.x1, s.mu2, s.rstd2, T, C, st)) != hipSuccess) return e;
-  LnArgs ln2 = {s.mu2, s.rstd2, p.ln2_g, p.ln2_b};
+  TERRA_TRY((gemm<true, true, true, true, false, false, EPI_BIAS_RES>(mat(s.o, C, T), mat(p.w_proj, C, C), none, none,
+                                                                      ep, T, C, C, 1, st)));
+  // h = LN2(x1) W_1^T + b_1 (LN2 folded), a = GELU(h)
+  TERRA_TRY(ln_stats(s.x1, s.mu2, s.rstd2, T, C, st));
+  TERRA_TRY(ln_fold(p.w_fc1, p.ln2_g, p.ln2_b, p.b_fc1, wf, sf, cf, 4 * C, C, st));
   ep = EpiArgs{};
-  ep.out[0] = (bf16*)s.h; ep.split = 4 * C; ep.out2 = (bf16*)s.a; ep.bias = p.b_fc1;
-  if ((e = gemm<true, true, true, false, EPI_BIAS_GELU>(mat(s.x1, C, T), mat(p.w_fc1, C, 4 * C), ln2, none, ep, T,
-                                                         4 * C, C, 1, st)) != hipSuccess)
-    return e;
+  ep.out[0] = (bf16*)s.h; ep.split = 4 * C; ep.out2 = (bf16*)s.a;
+  ep.mean = s.mu2; ep.rstd = s.rstd2; ep.lns = sf; ep.lnc = cf;
+  TERRA_TRY((gemm<true, true, true, true, false, false, EPI_LN_GELU>(mat(s.x1, C, T), mat(wf, C, 4 * C), none, none,
+                                                                     ep, T, 4 * C, C, 1, st)));
   // x2 = x1 + a W_2^T + b_2
   ep = EpiArgs{};
   ep.out[0] = (bf16*)x2; ep.split = C; ep.aux = (const bf16*)s.x1; ep.bias = p.b_fc2;
-  return gemm<true, true, false, false, EPI_BIAS_RES>(mat(s.a, 4 * C, T), mat(p.w_fc2, 4 * C, C), none, none, ep, T,
-                                                      C, 4 * C, 1, st);
+  TERRA_TRY((gemm<true, true, true, true, false, false, EPI_BIAS_RES>(mat(s.a, 4 * C, T), mat(p.w_fc2, 4 * C, C), none,
+                                                                      none, ep, T, C, 4 * C, 1, st)));
+#undef TERRA_TRY
+  return hipSuccess;
 }
 
 // Backward workspace layout (bytes, 256-aligned pieces).
 struct BwdWs {
   size_t dh, dln, dx1, dO, dq, dk, dv, attn, wpart, cpart, lpart, total;
-  int wsplit, cslices, lnwaves, rows_per_wave, cpart_rows;
+  int wsplit, cslices, lnwaves, rows_per_wave, cpart_rows, lgroups;
 };
-
-static size_t al(size_t x) { return (x + 255) / 256 * 256; }
 
 // A pure function of the geometry: the attention part is sized for kMaxCus
 // whatever device the call runs on.
@@ -519,6 +700,7 @@ static BwdWs block_ws(const Geo& geo) {
   w.cpart_rows = (int)((T + w.cslices - 1) / w.cslices);
   w.lnwaves = 2048;                      // waves of the LayerNorm backward
   w.rows_per_wave = (int)((T + w.lnwaves - 1) / w.lnwaves);
+  w.lgroups = 64;                        // first-level groups of the LayerNorm partials
   size_t off = 0;
   w.dh = off; off += al(T * 4 * C * 2);
   w.dln = off; off += al(T * C * 4);
@@ -530,7 +712,7 @@ static BwdWs block_ws(const Geo& geo) {
   w.attn = off; off += al(bwd_workspace(g, 1));
   w.wpart = off; off += al((size_t)w.wsplit * 4 * C * C * 4);
   w.cpart = off; off += al((size_t)w.cslices * 4 * C * 4);
-  w.lpart = off; off += al((size_t)w.lnwaves * 2 * C * 4);
+  w.lpart = off; off += al((size_t)w.lnwaves * 2 * C * 4 + (size_t)w.lgroups * 2 * C * 4);
   w.total = off;
   return w;
 }
@@ -544,11 +726,19 @@ static hipError_t slice_sum(const float* part, float* out, int64_t n, int nslice
   return hipGetLastError();
 }
 
-// LayerNorm parameter gradients from the per-wave partials [wave][dgamma C | dbeta C].
-static hipError_t ln_param_grads(const float* lpart, float* dgamma, float* dbeta, int C, int nwaves, hipStream_t st) {
-  hipError_t e = slice_sum(lpart, dgamma, C, nwaves, st, 2 * C);
+// LayerNorm parameter gradients from the per-wave partials
+// [wave][dgamma C | dbeta C]: sums over groups of consecutive waves, then
+// over the groups, each in order.
+static hipError_t ln_param_grads(const float* lpart, float* dgamma, float* dbeta, int C, const BwdWs& w,
+                                 hipStream_t st) {
+  float* grp = const_cast<float*>(lpart) + (size_t)w.lnwaves * 2 * C;
+  const int per = w.lnwaves / w.lgroups;
+  hipLaunchKernelGGL(group_sum_kernel, dim3((2 * C + kRowThreads - 1) / kRowThreads, w.lgroups), dim3(kRowThreads),
+                     0, st, lpart, grp, 2 * C, per);
+  hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  return slice_sum(lpart + C, dbeta, C, nwaves, st, 2 * C);
+  if ((e = slice_sum(grp, dgamma, C, w.lgroups, st, 2 * C)) != hipSuccess) return e;
+  return slice_sum(grp + C, dbeta, C, w.lgroups, st, 2 * C);
 }
 
 static hipError_t colsum(const Mat& X, int ncols, float* part, float* out, const BwdWs& w, hipStream_t st) {
@@ -560,7 +750,8 @@ static hipError_t colsum(const Mat& X, int ncols, float* part, float* out, const
 }
 
 // Weight gradient dW[Nl][Kl] = dY^T Z over all tokens (dY: T x Nl, Z: T x Kl),
-// in token slices, reduced in slice order.  LNB: Z = LN(z) applied on the fly.
+// in token slices, reduced in slice order.  LNB: Z = LN(z) applied while
+// staging.
 template <bool LNB>
 static hipError_t wgrad(const Mat& dY, const Mat& Z, const LnArgs& ln, int T, int Nl, int Kl, float* dW,
                         char* ws, const BwdWs& w, hipStream_t st) {
@@ -568,7 +759,7 @@ static hipError_t wgrad(const Mat& dY, const Mat& Z, const LnArgs& ln, int T, in
   EpiArgs ep = {};
   float* part = reinterpret_cast<float*>(ws + w.wpart);
   ep.outf = part;
-  hipError_t e = gemm<false, false, false, LNB, EPI_F32>(dY, Z, none, ln, ep, Nl, Kl, T, w.wsplit, st);
+  hipError_t e = gemm<false, false, true, !LNB, false, LNB, EPI_F32>(dY, Z, none, ln, ep, Nl, Kl, T, w.wsplit, st);
   if (e != hipSuccess) return e;
   return slice_sum(part, dW, (int64_t)Nl * Kl, w.wsplit, st);
 }
@@ -583,58 +774,69 @@ hipError_t launch_block_bwd(const Geo& g, const void* dx2, const void* x, const 
   float* dln = reinterpret_cast<float*>(ws + w.dln);
   bf16* dx1 = reinterpret_cast<bf16*>(ws + w.dx1);
   bf16* dO = reinterpret_cast<bf16*>(ws + w.dO);
-  bf16* dq = reinterpret_cast<bf16*>(ws + w.dq);
-  bf16* dk = reinterpret_cast<bf16*>(ws + w.dk);
-  bf16* dv = reinterpret_cast<bf16*>(ws + w.dv);
+  bf16* dqkv[3] = {reinterpret_cast<bf16*>(ws + w.dq), reinterpret_cast<bf16*>(ws + w.dk),
+                   reinterpret_cast<bf16*>(ws + w.dv)};
   float* cpart = reinterpret_cast<float*>(ws + w.cpart);
   float* lpart = reinterpret_cast<float*>(ws + w.lpart);
   LnArgs none = {nullptr, nullptr, nullptr, nullptr};
   hipError_t e;
   EpiArgs ep = {};
-#define TERRA_TRY(x) \
-  if ((e = (x)) != hipSuccess) return e
+#define TERRA_TRY(x)                    \
+  do {                                  \
+    if ((e = (x)) != hipSuccess) return e; \
+  } while (0)
   // x2 = x1 + a W2^T + b2:  dW2 = dx2^T a, db2 = colsum(dx2), dh = (dx2 W2) * GELU'(h)
-  TERRA_TRY(wgrad<false>(mat(dx2, C, T), mat(s.a, 4 * C, T), none, T, C, 4 * C, gr.w_fc2, ws, w, st));
+  TERRA_TRY((wgrad<false>(mat(dx2, C, T), mat(s.a, 4 * C, T), none, T, C, 4 * C, gr.w_fc2, ws, w, st)));
   TERRA_TRY(colsum(mat(dx2, C, T), C, cpart, gr.b_fc2, w, st));
   ep.out[0] = dh; ep.split = 4 * C; ep.aux = (const bf16*)s.h;
-  TERRA_TRY((gemm<true, false, false, false, EPI_GELU_GRAD>(mat(dx2, C, T), mat(p.w_fc2, 4 * C, C), none, none, ep,
-                                                             T, 4 * C, C, 1, st)));
+  TERRA_TRY((gemm<true, false, true, true, false, false, EPI_GELU_GRAD>(mat(dx2, C, T), mat(p.w_fc2, 4 * C, C), none,
+                                                                       none, ep, T, 4 * C, C, 1, st)));
   // h = LN2(x1) W1^T + b1:  dW1 = dh^T LN2(x1), db1 = colsum(dh), dln2 = dh W1
   LnArgs ln2 = {s.mu2, s.rstd2, p.ln2_g, p.ln2_b};
-  TERRA_TRY(wgrad<true>(mat(dh, 4 * C, T), mat(s.x1, C, T), ln2, T, 4 * C, C, gr.w_fc1, ws, w, st));
+  TERRA_TRY((wgrad<true>(mat(dh, 4 * C, T), mat(s.x1, C, T), ln2, T, 4 * C, C, gr.w_fc1, ws, w, st)));
   TERRA_TRY(colsum(mat(dh, 4 * C, T), 4 * C, cpart, gr.b_fc1, w, st));
   ep = EpiArgs{};
   ep.outf = dln;
-  TERRA_TRY((gemm<true, false, false, false, EPI_F32>(mat(dh, 4 * C, T), mat(p.w_fc1, C, 4 * C), none, none, ep, T,
-                                                       C, 4 * C, 1, st)));
+  TERRA_TRY((gemm<true, false, true, true, false, false, EPI_F32>(mat(dh, 4 * C, T), mat(p.w_fc1, C, 4 * C), none,
+                                                                 none, ep, T, C, 4 * C, 1, st)));
   // dx1 = dx2 + LN2 backward
   hipLaunchKernelGGL(ln_bwd_kernel, dim3(w.lnwaves / 4), dim3(kRowThreads), 0, st, dln, (const bf16*)s.x1, s.mu2,
                      s.rstd2, p.ln2_g, (const bf16*)dx2, dx1, lpart, T, C, w.rows_per_wave);
   TERRA_TRY(hipGetLastError());
-  TERRA_TRY(ln_param_grads(lpart, gr.ln2_g, gr.ln2_b, C, w.lnwaves, st));
+  TERRA_TRY(ln_param_grads(lpart, gr.ln2_g, gr.ln2_b, C, w, st));
   // x1 = x + o Wp^T + bp:  dWp = dx1^T o, dbp = colsum(dx1), dO = dx1 Wp
-  TERRA_TRY(wgrad<false>(mat(dx1, C, T), mat(s.o, C, T), none, T, C, C, gr.w_proj, ws, w, st));
+  TERRA_TRY((wgrad<false>(mat(dx1, C, T), mat(s.o, C, T), none, T, C, C, gr.w_proj, ws, w, st)));
   TERRA_TRY(colsum(mat(dx1, C, T), C, cpart, gr.b_proj, w, st));
   ep = EpiArgs{};
   ep.out[0] = dO; ep.split = C;
-  TERRA_TRY((gemm<true, false, false, false, EPI_BF16>(mat(dx1, C, T), mat(p.w_proj, C, C), none, none, ep, T, C, C,
-                                                        1, st)));
+  TERRA_TRY((gemm<true, false, true, true, false, false, EPI_BF16>(mat(dx1, C, T), mat(p.w_proj, C, C), none, none,
+                                                                  ep, T, C, C, 1, st)));
   // attention backward (route fused in)
-  TERRA_TRY(launch_attn_bwd(g, 1, true, s.q, s.k, s.v, s.o, dO, s.lse, table, dq, dk, dv, dtable, ws + w.attn, st));
-  // qkv = LN1(x) Wqkv^T + bqkv:  dWqkv = dqkv^T LN1(x), dbqkv, dln1 = dqkv Wqkv
+  TERRA_TRY(launch_attn_bwd(g, 1, true, s.q, s.k, s.v, s.o, dO, s.lse, table, dqkv[0], dqkv[1], dqkv[2], dtable,
+                            ws + w.attn, st));
+  // qkv = LN1(x) Wqkv^T + bqkv, one third (Q, K, V) at a time: rows
+  // [iC, (i+1)C) of dWqkv = dY_i^T LN1(x), of dbqkv = colsum(dY_i), and
+  // dln1 = sum_i dY_i Wqkv[iC:(i+1)C]
   LnArgs ln1 = {s.mu1, s.rstd1, p.ln1_g, p.ln1_b};
-  const Mat dqkv = mat3(dq, dk, dv, C, T);
-  TERRA_TRY(wgrad<true>(dqkv, mat(x, C, T), ln1, T, 3 * C, C, gr.w_qkv, ws, w, st));
-  TERRA_TRY(colsum(dqkv, 3 * C, cpart, gr.b_qkv, w, st));
-  ep = EpiArgs{};
-  ep.outf = dln;
-  TERRA_TRY((gemm<true, false, false, false, EPI_F32>(dqkv, mat(p.w_qkv, C, 3 * C), none, none, ep, T, C, 3 * C, 1,
-                                                       st)));
+  for (int i = 0; i < 3; ++i) {
+    const bf16* wi = reinterpret_cast<const bf16*>(p.w_qkv) + (size_t)i * C * C;
+    TERRA_TRY((wgrad<true>(mat(dqkv[i], C, T), mat(x, C, T), ln1, T, C, C, gr.w_qkv + (size_t)i * C * C, ws, w, st)));
+    TERRA_TRY(colsum(mat(dqkv[i], C, T), C, cpart, gr.b_qkv + (size_t)i * C, w, st));
+    ep = EpiArgs{};
+    ep.outf = dln;
+    if (i == 0) {
+      TERRA_TRY((gemm<true, false, true, true, false, false, EPI_F32>(mat(dqkv[i], C, T), mat(wi, C, C), none, none,
+                                                                     ep, T, C, C, 1, st)));
+    } else {
+      TERRA_TRY((gemm<true, false, true, true, false, false, EPI_F32_ACC>(mat(dqkv[i], C, T), mat(wi, C, C), none,
+                                                                         none, ep, T, C, C, 1, st)));
+    }
+  }
   // dx = dx1 + LN1 backward
   hipLaunchKernelGGL(ln_bwd_kernel, dim3(w.lnwaves / 4), dim3(kRowThreads), 0, st, dln, (const bf16*)x, s.mu1,
                      s.rstd1, p.ln1_g, (const bf16*)dx1, (bf16*)dx, lpart, T, C, w.rows_per_wave);
   TERRA_TRY(hipGetLastError());
-  TERRA_TRY(ln_param_grads(lpart, gr.ln1_g, gr.ln1_b, C, w.lnwaves, st));
+  TERRA_TRY(ln_param_grads(lpart, gr.ln1_g, gr.ln1_b, C, w, st));
 #undef TERRA_TRY
   return hipSuccess;
 }

@@ -136,12 +136,15 @@ def test_block_calls_reject_bad_arguments_before_launch():
     assert L.terra_block_bwd_workspace_bytes(ctypes.byref(bad_c), 1) == 0
     assert L.terra_block_bwd_workspace_bytes(ctypes.byref(ok), 0) == 0    # fp32: bf16 only
     assert L.terra_block_bwd_workspace_bytes(ctypes.byref(ok), 1) > 0
-    assert L.terra_block_fwd(ctypes.byref(bad_c), 1, fake, None, fake, fake, None, s) == 2
-    assert L.terra_block_fwd(ctypes.byref(ok), 2, fake, None, fake, fake, None, s) == 2
-    assert L.terra_block_fwd(ctypes.byref(ok), 1, fake, None, fake, fake, None, s) == 1   # NULL structs
+    z = ctypes.c_size_t(0)
+    assert L.terra_block_fwd_workspace_bytes(ctypes.byref(ok), 1) > 0
+    assert L.terra_block_fwd(ctypes.byref(bad_c), 1, fake, None, fake, fake, None, fake, z, s) == 2
+    assert L.terra_block_fwd(ctypes.byref(ok), 2, fake, None, fake, fake, None, fake, z, s) == 2
+    assert L.terra_block_fwd(ctypes.byref(ok), 1, fake, None, fake, fake, None, fake, z, s) == 1   # NULL structs
     p = P.terra_block_params()
     sv = P.terra_block_saved()
-    assert L.terra_block_fwd(ctypes.byref(ok), 1, fake, ctypes.byref(p), fake, fake, ctypes.byref(sv), s) == 1
+    assert L.terra_block_fwd(ctypes.byref(ok), 1, fake, ctypes.byref(p), fake, fake, ctypes.byref(sv), fake, z,
+                             s) == 1
     gr = P.terra_block_grads()
     need = L.terra_block_bwd_workspace_bytes(ctypes.byref(ok), 1)
     for n in P.BLOCK_PARAM_NAMES:
@@ -151,3 +154,6 @@ def test_block_calls_reject_bad_arguments_before_launch():
         setattr(sv, n, 0x1000)
     assert L.terra_block_bwd(ctypes.byref(ok), 1, fake, fake, ctypes.byref(p), fake, ctypes.byref(sv), fake,
                              ctypes.byref(gr), fake, fake, ctypes.c_size_t(need - 1), s) == 3
+    fneed = L.terra_block_fwd_workspace_bytes(ctypes.byref(ok), 1)
+    assert L.terra_block_fwd(ctypes.byref(ok), 1, fake, ctypes.byref(p), fake, fake, ctypes.byref(sv), fake,
+                             ctypes.c_size_t(fneed - 1), s) == 3
