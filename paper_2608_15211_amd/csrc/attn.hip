@@ -155,7 +155,6 @@ __device__ inline void tile_store_rows(const TileRegs<T, HD>& t, T* lds) {
 
 template <typename T, int HD, bool ROWMAJOR, bool TRANS>
 __device__ inline void tile_store(const TileRegs<T, HD>& t, T* lds_rm, T* lds_tr) {
-  constexpr int kTile = tile_of<T, HD>();
   constexpr int kCpr = TileRegs<T, HD>::kCpr;
   constexpr int kElemPerChunk = 16 / sizeof(T);
 #pragma unroll

@@ -13,6 +13,8 @@
 // to an operand while it is staged (from per-token mean and 1/std computed
 // by a small kernel), so normalised activations never reach HBM; bias,
 // residual, GELU and its derivative are applied in the epilogue.
+#include <algorithm>
+
 #include "terra_common.h"
 #include "terra_block.h"
 
@@ -22,32 +24,21 @@ typedef __bf16 bf16;
 typedef short v4s __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4s lds_v4s;
 
-constexpr int kGT = 256;          // threads per GEMM workgroup (4 waves, 2 x 2)
+constexpr int kGT = 512;          // threads per GEMM workgroup (8 waves: 2 rows x 4 columns of 128 x 64)
 constexpr int kBM = 256;          // workgroup tile rows
-constexpr int kBN = 128;          // workgroup tile columns
+constexpr int kBN = 256;          // workgroup tile columns
 constexpr int kBK = 32;           // contraction depth per stage
+constexpr int kEpiS = 68;         // row stride (floats) of a wave's epilogue staging tile
+constexpr int kMaxCusBlock = 256;  // compute units the weight-gradient slices are sized for
 
-// A bf16 operand in memory: row-major, split into up to three column blocks
-// of `split` columns each (the Q, K and V tensors of the QKV layer are one
-// operand of 3C columns held as three C-column tensors).  rows: valid rows.
+// A bf16 operand in memory: row-major, `ld` elements a row, `rows` valid rows.
 struct Mat {
-  const bf16* p[3];
-  int split;
+  const bf16* p;
+  int ld;
   int rows;
-  __device__ const bf16* at(int r, int c) const {
-    const int blk = c / split;
-    return p[blk] + (int64_t)r * split + (c - blk * split);
-  }
+  __device__ const bf16* at(int r, int c) const { return p + (int64_t)r * ld + c; }
 };
 
-// LayerNorm of a staged operand: memory rows are tokens (mean, rstd),
-// memory columns channels (gamma, beta).
-struct LnArgs {
-  const float* mean;
-  const float* rstd;
-  const float* gamma;
-  const float* beta;
-};
 
 enum Epi {
   EPI_LN_QKV = 0,      // LayerNorm folded: out = bf16(rstd (acc - mean s) + c)   (column-split output)
@@ -78,7 +69,7 @@ struct EpiArgs {
 // shared between erf and the GELU derivative.
 __device__ inline void phi_gauss(float x, float& Phi, float& gauss) {
   const float z = fabsf(x) * 0.70710678118654752f;
-  const float t = 1.0f / (1.0f + 0.3275911f * z);
+  const float t = __builtin_amdgcn_rcpf(1.0f + 0.3275911f * z);
   gauss = __expf(-0.5f * x * x);
   const float poly =
       t * (0.254829592f + t * (-0.284496736f + t * (1.421413741f + t * (-1.453152027f + t * 1.061405429f))));
@@ -178,65 +169,28 @@ __device__ inline i32x4 buffer_rsrc(const void* base, uint32_t bytes) {
   return r;
 }
 
-template <bool LN>
-__device__ inline uint4 ln_chunk(uint4 raw, const LnArgs& ln, int mrow, int mcol) {
-  if (!LN) return raw;
-  const float mu = ln.mean[mrow], rs = ln.rstd[mrow];
-  const float4 g0 = *reinterpret_cast<const float4*>(ln.gamma + mcol);
-  const float4 g1 = *reinterpret_cast<const float4*>(ln.gamma + mcol + 4);
-  const float4 b0 = *reinterpret_cast<const float4*>(ln.beta + mcol);
-  const float4 b1 = *reinterpret_cast<const float4*>(ln.beta + mcol + 4);
-  const float g[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
-  const float b[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
-  bf16x8 v = __builtin_bit_cast(bf16x8, raw);
-#pragma unroll
-  for (int i = 0; i < 8; ++i) v[i] = (bf16)(((float)v[i] - mu) * rs * g[i] + b[i]);
-  return __builtin_bit_cast(uint4, v);
-}
-
-// One operand's staging.  DIRECT: 16-byte buffer loads straight into LDS
-// (asynchronous; issued two stages ahead); otherwise loads into registers
-// one stage ahead, the LayerNorm (LN) applied there, then an LDS store -
-// the path for LayerNorm operands and for operands split over several
-// tensors.  KROW: the contraction index runs along memory rows.  VALID:
-// memory rows / columns inside the operand and the contraction slice.
-template <int R, bool KROW, bool DIRECT, bool LN>
-struct Staged {
+// Direct-to-LDS staging of one operand tile: each thread moves kPer 16-byte
+// chunks with buffer loads that write LDS themselves (slot q of the tile is
+// written by thread q % kGT, load q / kGT); chunks outside the operand or
+// the contraction slice read zeros.  KROW: the contraction index runs along
+// memory rows.
+template <int R, bool KROW>
+__device__ inline void stage_direct(const i32x4& rs, const Mat& X, bf16* tile, int r0, int k0, int nouter,
+                                    int kend) {
   typedef Tile<R, KROW> T;
-  uint4 reg[DIRECT ? 1 : T::kPer];
-  __device__ static bool valid(int mrow, int mcol, int nouter, int kend) {
-    return KROW ? (mrow < nouter && mcol < kend) : (mrow < kend && mcol < nouter);
-  }
-  __device__ void issue_direct(const i32x4& rs, const Mat& X, bf16* tile, int r0, int k0, int nouter, int kend) {
-    const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // uniform: the LDS base goes to M0
 #pragma unroll
-    for (int u = 0; u < T::kPer; ++u) {
-      const int q = u * kGT + threadIdx.x;
-      int mr, mc;
-      T::slot_src(q, r0, k0, mr, mc);
-      const int voff = valid(mr, mc, nouter, kend) ? (int)(((int64_t)mr * X.split + mc) * 2) : (int)0x80000000;
-      bf16* dst = tile + 8 * (u * kGT + wave * 64);      // wave-uniform base of 64 slots
-      raw_buffer_load_lds(rs, (__attribute__((address_space(3))) uint32_t*)(uintptr_t)(uint32_t)(uintptr_t)dst, 16, voff, 0,
-                          0, 0);
-    }
+  for (int u = 0; u < T::kPer; ++u) {
+    const int q = u * kGT + threadIdx.x;
+    int mr, mc;
+    T::slot_src(q, r0, k0, mr, mc);
+    const bool ok = KROW ? (mr < nouter && mc < kend) : (mr < kend && mc < nouter);
+    const int voff = ok ? (int)(((int64_t)mr * X.ld + mc) * 2) : (int)0x80000000;
+    bf16* dst = tile + 8 * (u * kGT + wave * 64);      // wave-uniform base of 64 slots
+    raw_buffer_load_lds(rs, (__attribute__((address_space(3))) uint32_t*)(uintptr_t)(uint32_t)(uintptr_t)dst, 16,
+                        voff, 0, 0, 0);
   }
-  __device__ void load_reg(const Mat& X, const LnArgs& ln, int r0, int k0, int nouter, int kend) {
-#pragma unroll
-    for (int u = 0; u < T::kPer; ++u) {
-      const int q = u * kGT + threadIdx.x;
-      int mr, mc;
-      T::slot_src(q, r0, k0, mr, mc);
-      const bool ok = valid(mr, mc, nouter, kend);
-      reg[u] = ok ? *reinterpret_cast<const uint4*>(X.at(mr, mc)) : make_uint4(0, 0, 0, 0);
-      if (LN && ok) reg[u] = ln_chunk<true>(reg[u], ln, KROW ? mr : mr, mc);
-    }
-  }
-  __device__ void store_reg(bf16* tile) const {
-#pragma unroll
-    for (int u = 0; u < T::kPer; ++u)
-      *reinterpret_cast<uint4*>(tile + 8 * (u * kGT + threadIdx.x)) = reg[u];
-  }
-};
+}
 
 template <int N>
 __device__ inline void wait_vm() {
@@ -244,23 +198,20 @@ __device__ inline void wait_vm() {
 }
 
 // C[M][N] = A[M][K] B[K][N] (+ epilogue).  AKROW: A is memory [M][K]
-// (else [K][M]); BKROW: B is memory [N][K] (else [K][N]).  ADIR / BDIR:
-// operand staged by direct-to-LDS loads (else through registers).  LNA /
-// LNB: LayerNorm applied to A / B while staging (memory rows = tokens).
-// blockIdx.z: contraction slice [z * kslice, (z+1) * kslice).  Three LDS
-// stages: the direct loads of stage kt + 2 and the register loads of stage
-// kt + 1 are in flight while stage kt is on the matrix cores.
-template <bool AKROW, bool BKROW, bool ADIR, bool BDIR, bool LNA, bool LNB, int EPI>
-__global__ __launch_bounds__(kGT, 2) void gemm_kernel(Mat A, Mat B, LnArgs lna, LnArgs lnb, EpiArgs ep,
-                                                      int M, int N, int K, int kslice) {
-  typedef Staged<kBM, AKROW, ADIR, LNA> OA;
-  typedef Staged<kBN, BKROW, BDIR, LNB> OB;
-  constexpr int kStage = OA::T::kElems + OB::T::kElems;
-  constexpr int kDirectLoads = (ADIR ? OA::T::kPer : 0) + (BDIR ? OB::T::kPer : 0);
+// (else [K][M]); BKROW: B is memory [N][K] (else [K][N]).  blockIdx.z:
+// contraction slice [z * kslice, (z+1) * kslice).  Three LDS stages: the
+// loads of stage kt + 2 are in flight while stage kt is on the matrix
+// cores.  Eight waves, each a 128 x 64 block of the 256 x 256 tile.
+template <bool AKROW, bool BKROW, int EPI>
+__global__ __launch_bounds__(kGT, 1) void gemm_kernel(Mat A, Mat B, EpiArgs ep, int M, int N, int K, int kslice) {
+  typedef Tile<kBM, AKROW> TA;
+  typedef Tile<kBN, BKROW> TB;
+  constexpr int kStage = TA::kElems + TB::kElems;
+  constexpr int kLoads = TA::kPer + TB::kPer;
   extern __shared__ __align__(16) char smem[];
   bf16* lds = reinterpret_cast<bf16*>(smem);
 
-  const int nN = N / kBN;
+  const int nN = (N + kBN - 1) / kBN;
   const int nM = (M + kBM - 1) / kBM;
   const int tiles = nM * nN;
   int w = blockIdx.x;
@@ -271,9 +222,9 @@ __global__ __launch_bounds__(kGT, 2) void gemm_kernel(Mat A, Mat B, LnArgs lna, 
   const int kend = min(K, kbeg + kslice);
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int wm = (wave >> 1) * 128, wn = (wave & 1) * 64;
-  const i32x4 rsa = buffer_rsrc(A.p[0], ADIR ? (uint32_t)((int64_t)A.rows * A.split * 2) : 0u);
-  const i32x4 rsb = buffer_rsrc(B.p[0], BDIR ? (uint32_t)((int64_t)B.rows * B.split * 2) : 0u);
+  const int wm = (wave >> 2) * 128, wn = (wave & 3) * 64;
+  const i32x4 rsa = buffer_rsrc(A.p, (uint32_t)((int64_t)A.rows * A.ld * 2));
+  const i32x4 rsb = buffer_rsrc(B.p, (uint32_t)((int64_t)B.rows * B.ld * 2));
 
   f32x16 acc[4][2];
 #pragma unroll
@@ -281,37 +232,21 @@ __global__ __launch_bounds__(kGT, 2) void gemm_kernel(Mat A, Mat B, LnArgs lna, 
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
 
-  OA oa;
-  OB ob;
   auto a_tile = [&](int st) { return lds + st * kStage; };
-  auto b_tile = [&](int st) { return lds + st * kStage + OA::T::kElems; };
-  auto issue = [&](int s) {       // direct loads of stage s
+  auto b_tile = [&](int st) { return lds + st * kStage + TA::kElems; };
+  auto issue = [&](int s) {
     const int k0 = kbeg + s * kBK;
-    if (ADIR) oa.issue_direct(rsa, A, a_tile(s % 3), m0, k0, M, kend);
-    if (BDIR) ob.issue_direct(rsb, B, b_tile(s % 3), n0, k0, N, kend);
-  };
-  auto load_regs = [&](int s) {   // register loads of stage s
-    const int k0 = kbeg + s * kBK;
-    if (!ADIR) oa.load_reg(A, lna, m0, k0, M, kend);
-    if (!BDIR) ob.load_reg(B, lnb, n0, k0, N, kend);
-  };
-  auto store_regs = [&](int s) {
-    if (!ADIR) oa.store_reg(a_tile(s % 3));
-    if (!BDIR) ob.store_reg(b_tile(s % 3));
+    stage_direct<kBM, AKROW>(rsa, A, a_tile(s % 3), m0, k0, M, kend);
+    stage_direct<kBN, BKROW>(rsb, B, b_tile(s % 3), n0, k0, N, kend);
   };
 
   const int nk = (kend - kbeg + kBK - 1) / kBK;
-  if (nk > 0) {
-    load_regs(0);
-    issue(0);
-    if (nk > 1) issue(1);
-    store_regs(0);
-  }
+  if (nk > 0) issue(0);
+  if (nk > 1) issue(1);
   for (int kt = 0; kt < nk; ++kt) {
-    if (kt + 1 < nk) wait_vm<kDirectLoads>();
+    if (kt + 1 < nk) wait_vm<kLoads>();
     else wait_vm<0>();
     __syncthreads();
-    if (kt + 1 < nk) load_regs(kt + 1);
     if (kt + 2 < nk) issue(kt + 2);
     const bf16* ta = a_tile(kt % 3);
     const bf16* tb = b_tile(kt % 3);
@@ -329,48 +264,99 @@ __global__ __launch_bounds__(kGT, 2) void gemm_kernel(Mat A, Mat B, LnArgs lna, 
         for (int j = 0; j < 2; ++j) mma16(acc[i][j], ao, bo[j]);
       }
     }
-    if (kt + 1 < nk) store_regs(kt + 1);
   }
+  __syncthreads();   // every wave is done with the stages: their LDS now stages the epilogue
 
-  // Epilogue.  acc[i][j] holds rows wm + 32i + 8g + 4h + x (register 4g + x),
-  // column wn + 32j + lane % 32.
+  // Epilogue, 32 rows of the wave's block at a time: acc[i][j] holds rows
+  // 32i + 8g + 4h + x (register 4g + x), column 32j + lane % 32; they go
+  // through the wave's own LDS tile so that each lane then handles 8
+  // consecutive columns of one row with 16-byte loads and stores.
+  float* et = reinterpret_cast<float*>(smem) + wave * 32 * kEpiS;
   const int h = lane >> 5, col = lane & 31;
+  const int er = lane >> 1, ec = (lane & 1) * 32;     // this lane's row and first column when reading back
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int n = n0 + wn + 32 * j + col;
-    const float bias = EPI == EPI_BIAS_RES ? ep.bias[n] : 0.0f;
-    const float lns = (EPI == EPI_LN_QKV || EPI == EPI_LN_GELU) ? ep.lns[n] : 0.0f;
-    const float lnc = (EPI == EPI_LN_QKV || EPI == EPI_LN_GELU) ? ep.lnc[n] : 0.0f;
+  for (int i = 0; i < 4; ++i) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int j = 0; j < 2; ++j)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int m = m0 + wm + 32 * i + 8 * (r / 4) + 4 * h + (r % 4);
-        if (m >= M) continue;
-        const float v = acc[i][j][r];
-        const int64_t o = (int64_t)m * N + n;
-        if (EPI == EPI_LN_QKV || EPI == EPI_LN_GELU) {
-          const float t = ep.rstd[m] * (v - ep.mean[m] * lns) + lnc;
-          if (EPI == EPI_LN_QKV) {
-            const int blk = n / ep.split;
-            ep.out[blk][(int64_t)m * ep.split + (n - blk * ep.split)] = (bf16)t;
-          } else {
-            ep.out[0][o] = (bf16)t;
-            ep.out2[o] = (bf16)gelu_f(t);
-          }
-        } else if (EPI == EPI_BIAS_RES) {
-          ep.out[0][o] = (bf16)(v + bias + (float)ep.aux[o]);
-        } else if (EPI == EPI_GELU_GRAD) {
-          ep.out[0][o] = (bf16)(v * gelu_grad_f((float)ep.aux[o]));
-        } else if (EPI == EPI_F32) {
-          ep.outf[(int64_t)blockIdx.z * M * N + o] = v;
-        } else if (EPI == EPI_F32_ACC) {
-          ep.outf[o] += v;
-        } else {
-          ep.out[0][o] = (bf16)v;
+      for (int r = 0; r < 16; ++r) et[(8 * (r / 4) + 4 * h + (r % 4)) * kEpiS + 32 * j + col] = acc[i][j][r];
+    __builtin_amdgcn_wave_barrier();
+    const int m = m0 + wm + 32 * i + er;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int n = n0 + wn + ec + 8 * q;
+      const float4 lo = *reinterpret_cast<const float4*>(et + er * kEpiS + ec + 8 * q);
+      const float4 hi = *reinterpret_cast<const float4*>(et + er * kEpiS + ec + 8 * q + 4);
+      float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+      if (m >= M || n >= N) continue;
+      const int64_t o = (int64_t)m * N + n;
+      if (EPI == EPI_LN_QKV || EPI == EPI_LN_GELU) {
+        const float mu = ep.mean[m], rs = ep.rstd[m];
+        bf16x8 t, g;
+#pragma unroll
+        for (int x = 0; x < 8; ++x) {
+          const float y = rs * (v[x] - mu * ep.lns[n + x]) + ep.lnc[n + x];
+          t[x] = (bf16)y;
+          if (EPI == EPI_LN_GELU) g[x] = (bf16)gelu_f(y);
         }
+        if (EPI == EPI_LN_QKV) {
+          const int blk = n / ep.split;
+          *reinterpret_cast<bf16x8*>(ep.out[blk] + (int64_t)m * ep.split + (n - blk * ep.split)) = t;
+        } else {
+          *reinterpret_cast<bf16x8*>(ep.out[0] + o) = t;
+          *reinterpret_cast<bf16x8*>(ep.out2 + o) = g;
+        }
+      } else if (EPI == EPI_BIAS_RES) {
+        const bf16x8 res = *reinterpret_cast<const bf16x8*>(ep.aux + o);
+        bf16x8 t;
+#pragma unroll
+        for (int x = 0; x < 8; ++x) t[x] = (bf16)(v[x] + ep.bias[n + x] + (float)res[x]);
+        *reinterpret_cast<bf16x8*>(ep.out[0] + o) = t;
+      } else if (EPI == EPI_GELU_GRAD) {
+        const bf16x8 hv = *reinterpret_cast<const bf16x8*>(ep.aux + o);
+        bf16x8 t;
+#pragma unroll
+        for (int x = 0; x < 8; ++x) t[x] = (bf16)(v[x] * gelu_grad_f((float)hv[x]));
+        *reinterpret_cast<bf16x8*>(ep.out[0] + o) = t;
+      } else if (EPI == EPI_F32 || EPI == EPI_F32_ACC) {
+        float* dst = ep.outf + (EPI == EPI_F32 ? (int64_t)blockIdx.z * M * N : 0) + o;
+        if (EPI == EPI_F32_ACC) {
+          const float4 a0 = *reinterpret_cast<const float4*>(dst);
+          const float4 a1 = *reinterpret_cast<const float4*>(dst + 4);
+          v[0] += a0.x; v[1] += a0.y; v[2] += a0.z; v[3] += a0.w;
+          v[4] += a1.x; v[5] += a1.y; v[6] += a1.z; v[7] += a1.w;
+        }
+        *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+        *reinterpret_cast<float4*>(dst + 4) = make_float4(v[4], v[5], v[6], v[7]);
+      } else {
+        bf16x8 t;
+#pragma unroll
+        for (int x = 0; x < 8; ++x) t[x] = (bf16)v[x];
+        *reinterpret_cast<bf16x8*>(ep.out[0] + o) = t;
       }
+    }
+    __builtin_amdgcn_wave_barrier();
   }
+}
+
+// LayerNorm applied to a token matrix (the backward's weight gradients take
+// the normalised activations as an operand): out = (z - mean) rstd gamma +
+// beta, rounded to bf16; one thread per 8 channels.
+__global__ __launch_bounds__(256) void ln_apply_kernel(const bf16* __restrict__ z, const float* __restrict__ mean,
+                                                      const float* __restrict__ rstd, const float* __restrict__ gamma,
+                                                      const float* __restrict__ beta, bf16* __restrict__ out, int T,
+                                                      int C) {
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int c8 = C / 8;
+  if (idx >= (int64_t)T * c8) return;
+  const int t = (int)(idx / c8);
+  const int c = 8 * (int)(idx - (int64_t)t * c8);
+  const bf16x8 v = *reinterpret_cast<const bf16x8*>(z + (int64_t)t * C + c);
+  const float mu = mean[t], rs = rstd[t];
+  bf16x8 o;
+#pragma unroll
+  for (int x = 0; x < 8; ++x) o[x] = (bf16)(((float)v[x] - mu) * rs * gamma[c + x] + beta[c + x]);
+  *reinterpret_cast<bf16x8*>(out + (int64_t)t * C + c) = o;
 }
 
 // LayerNorm folded into the following linear layer: with
@@ -525,7 +511,7 @@ __global__ __launch_bounds__(kRowThreads) void ln_bwd_kernel(
   }
 }
 
-// Column sums of a (column-split) bf16 matrix, per slice of rows:
+// Column sums of a bf16 matrix, per slice of rows:
 // part[s][col] = sum over rows [s * rows_per, (s+1) * rows_per) - the bias
 // gradients, reduced afterwards in slice order.  Thread = 8 columns.
 __global__ __launch_bounds__(kRowThreads) void colsum_kernel(Mat X, int ncols, float* __restrict__ part,
@@ -534,14 +520,27 @@ __global__ __launch_bounds__(kRowThreads) void colsum_kernel(Mat X, int ncols, f
   if (8 * c8 >= ncols) return;
   const int s = blockIdx.y;
   const int r0 = s * rows_per, r1 = min(X.rows, r0 + rows_per);
-  float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-  for (int r = r0; r < r1; ++r) {
+  // four independent partial sums (rows r, r+1, r+2, r+3 of each step), so
+  // that four loads are in flight; combined in a fixed order at the end
+  float acc[4][8] = {};
+  int r = r0;
+  for (; r + 4 <= r1; r += 4) {
+    bf16x8 v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) v[u] = *reinterpret_cast<const bf16x8*>(X.at(r + u, 8 * c8));
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int i = 0; i < 8; ++i) acc[u][i] += (float)v[u][i];
+  }
+  for (; r < r1; ++r) {
     const bf16x8 v = *reinterpret_cast<const bf16x8*>(X.at(r, 8 * c8));
 #pragma unroll
-    for (int i = 0; i < 8; ++i) acc[i] += (float)v[i];
+    for (int i = 0; i < 8; ++i) acc[0][i] += (float)v[i];
   }
 #pragma unroll
-  for (int i = 0; i < 8; ++i) part[(int64_t)s * ncols + 8 * c8 + i] = acc[i];
+  for (int i = 0; i < 8; ++i)
+    part[(int64_t)s * ncols + 8 * c8 + i] = (acc[0][i] + acc[1][i]) + (acc[2][i] + acc[3][i]);
 }
 
 // grp[g][i] = sum of part[s][i] over s in [g * per, (g + 1) * per), in
@@ -562,29 +561,38 @@ __global__ __launch_bounds__(kRowThreads) void slice_sum_kernel(const float* __r
   const int64_t i = (int64_t)blockIdx.x * kRowThreads + threadIdx.x;
   if (i >= n) return;
   float acc = 0.0f;
-  for (int s = 0; s < nslice; ++s) acc += part[(int64_t)s * stride + i];
+  int s = 0;
+  for (; s + 8 <= nslice; s += 8) {
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = part[(int64_t)(s + u) * stride + i];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc += v[u];
+  }
+  for (; s < nslice; ++s) acc += part[(int64_t)s * stride + i];
   out[i] = acc;
 }
 
 // ---------------------------------------------------------------------------
 // Host side.
 // ---------------------------------------------------------------------------
-constexpr size_t kGemmLds = 3 * (size_t)(kBM + kBN) * kBK * sizeof(bf16);   // three stages
+constexpr size_t kGemmLds = 3 * (size_t)(kBM + kBN) * kBK * sizeof(bf16);   // three stages (96 KB)
 
-template <bool AKROW, bool BKROW, bool ADIR, bool BDIR, bool LNA, bool LNB, int EPI>
-static hipError_t gemm(const Mat& A, const Mat& B, const LnArgs& lna, const LnArgs& lnb, const EpiArgs& ep,
-                       int M, int N, int K, int nsplit, hipStream_t st) {
-  const int tiles = ((M + kBM - 1) / kBM) * (N / kBN);
+template <bool AKROW, bool BKROW, int EPI>
+static hipError_t gemm(const Mat& A, const Mat& B, const EpiArgs& ep, int M, int N, int K, int nsplit,
+                       hipStream_t st) {
+  const int tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
   const int kslice = ((K + nsplit - 1) / nsplit + kBK - 1) / kBK * kBK;
-  hipLaunchKernelGGL((gemm_kernel<AKROW, BKROW, ADIR, BDIR, LNA, LNB, EPI>), dim3(tiles, 1, nsplit), dim3(kGT),
-                     kGemmLds, st, A, B, lna, lnb, ep, M, N, K, kslice);
+  hipLaunchKernelGGL((gemm_kernel<AKROW, BKROW, EPI>), dim3(tiles, 1, nsplit), dim3(kGT), kGemmLds, st, A, B, ep, M,
+                     N, K, kslice);
   return hipGetLastError();
 }
 
-static Mat mat(const void* p, int split, int rows) {
+
+static Mat mat(const void* p, int ld, int rows) {
   Mat m;
-  m.p[0] = m.p[1] = m.p[2] = (const bf16*)p;
-  m.split = split;
+  m.p = (const bf16*)p;
+  m.ld = ld;
   m.rows = rows;
   return m;
 }
@@ -644,7 +652,6 @@ hipError_t launch_block_fwd(const Geo& g, const void* x, const BlockParams& p, c
   float *sq = reinterpret_cast<float*>(ws + w.sq), *cq = reinterpret_cast<float*>(ws + w.cq);
   float *sf = reinterpret_cast<float*>(ws + w.sf), *cf = reinterpret_cast<float*>(ws + w.cf);
   hipError_t e;
-  LnArgs none = {nullptr, nullptr, nullptr, nullptr};
   EpiArgs ep = {};
 #define TERRA_TRY(x)                    \
   do {                                  \
@@ -656,35 +663,41 @@ hipError_t launch_block_fwd(const Geo& g, const void* x, const BlockParams& p, c
   TERRA_TRY(ln_fold(p.w_qkv, p.ln1_g, p.ln1_b, p.b_qkv, wq, sq, cq, 3 * C, C, st));
   ep.out[0] = (bf16*)s.q; ep.out[1] = (bf16*)s.k; ep.out[2] = (bf16*)s.v; ep.split = C;
   ep.mean = s.mu1; ep.rstd = s.rstd1; ep.lns = sq; ep.lnc = cq;
-  TERRA_TRY((gemm<true, true, true, true, false, false, EPI_LN_QKV>(mat(x, C, T), mat(wq, C, 3 * C), none, none, ep,
+  TERRA_TRY((gemm<true, true, EPI_LN_QKV>(mat(x, C, T), mat(wq, C, 3 * C), ep,
                                                                     T, 3 * C, C, 1, st)));
   // windowed attention with the route fused in
   TERRA_TRY(launch_attn_fwd(g, 1, true, s.q, s.k, s.v, table, s.o, s.lse, st));
   // x1 = x + o W_p^T + b_p
   ep = EpiArgs{};
   ep.out[0] = (bf16*)s.x1; ep.split = C; ep.aux = (const bf16*)x; ep.bias = p.b_proj;
-  TERRA_TRY((gemm<true, true, true, true, false, false, EPI_BIAS_RES>(mat(s.o, C, T), mat(p.w_proj, C, C), none, none,
-                                                                      ep, T, C, C, 1, st)));
+  TERRA_TRY((gemm<true, true, EPI_BIAS_RES>(mat(s.o, C, T), mat(p.w_proj, C, C), ep, T, C, C, 1, st)));
   // h = LN2(x1) W_1^T + b_1 (LN2 folded), a = GELU(h)
   TERRA_TRY(ln_stats(s.x1, s.mu2, s.rstd2, T, C, st));
   TERRA_TRY(ln_fold(p.w_fc1, p.ln2_g, p.ln2_b, p.b_fc1, wf, sf, cf, 4 * C, C, st));
   ep = EpiArgs{};
   ep.out[0] = (bf16*)s.h; ep.split = 4 * C; ep.out2 = (bf16*)s.a;
   ep.mean = s.mu2; ep.rstd = s.rstd2; ep.lns = sf; ep.lnc = cf;
-  TERRA_TRY((gemm<true, true, true, true, false, false, EPI_LN_GELU>(mat(s.x1, C, T), mat(wf, C, 4 * C), none, none,
-                                                                     ep, T, 4 * C, C, 1, st)));
+  TERRA_TRY((gemm<true, true, EPI_LN_GELU>(mat(s.x1, C, T), mat(wf, C, 4 * C), ep, T, 4 * C, C, 1, st)));
   // x2 = x1 + a W_2^T + b_2
   ep = EpiArgs{};
   ep.out[0] = (bf16*)x2; ep.split = C; ep.aux = (const bf16*)s.x1; ep.bias = p.b_fc2;
-  TERRA_TRY((gemm<true, true, true, true, false, false, EPI_BIAS_RES>(mat(s.a, 4 * C, T), mat(p.w_fc2, 4 * C, C), none,
-                                                                      none, ep, T, C, 4 * C, 1, st)));
+  TERRA_TRY((gemm<true, true, EPI_BIAS_RES>(mat(s.a, 4 * C, T), mat(p.w_fc2, 4 * C, C), ep, T, C, 4 * C, 1, st)));
 #undef TERRA_TRY
   return hipSuccess;
 }
 
+// Token slices of a weight gradient dW[Nl][Kl] over T tokens.
+static int wgrad_slices(int T, int Nl, int Kl, int cap) {
+  const int tiles = ((Nl + kBM - 1) / kBM) * ((Kl + kBN - 1) / kBN);
+  int n = (2 * kMaxCusBlock + tiles - 1) / tiles;         // about two workgroups per CU
+  const int per = (T + n - 1) / n;
+  if (per < 4 * kBK) n = (T + 4 * kBK - 1) / (4 * kBK);  // at least four stages a slice
+  return n < 1 ? 1 : (n > cap ? cap : n);
+}
+
 // Backward workspace layout (bytes, 256-aligned pieces).
 struct BwdWs {
-  size_t dh, dln, dx1, dO, dq, dk, dv, attn, wpart, cpart, lpart, total;
+  size_t dh, dln, dx1, dO, dq, dk, dv, ln, attn, wpart, cpart, lpart, total;
   int wsplit, cslices, lnwaves, rows_per_wave, cpart_rows, lgroups;
 };
 
@@ -695,7 +708,7 @@ static BwdWs block_ws(const Geo& geo) {
   g.cus = kMaxCus;
   BwdWs w;
   const size_t T = (size_t)g.B * g.H * g.W, C = g.C;
-  w.wsplit = 16;                         // contraction (token) slices of the weight gradients
+  w.wsplit = 64;                         // most contraction (token) slices of a weight gradient
   w.cslices = 512;                       // row slices of the bias-gradient column sums
   w.cpart_rows = (int)((T + w.cslices - 1) / w.cslices);
   w.lnwaves = 2048;                      // waves of the LayerNorm backward
@@ -709,8 +722,14 @@ static BwdWs block_ws(const Geo& geo) {
   w.dq = off; off += al(T * C * 2);
   w.dk = off; off += al(T * C * 2);
   w.dv = off; off += al(T * C * 2);
+  w.ln = off; off += al(T * C * 2);
   w.attn = off; off += al(bwd_workspace(g, 1));
-  w.wpart = off; off += al((size_t)w.wsplit * 4 * C * C * 4);
+  size_t wmax = 0;                       // largest slices x output of the block's weight gradients
+  for (int i = 0; i < 4; ++i) {
+    const int nl = i == 0 ? (int)C : (i == 1 ? 4 * (int)C : (int)C), kl = i == 0 ? 4 * (int)C : (int)C;
+    wmax = std::max(wmax, (size_t)wgrad_slices((int)T, nl, kl, w.wsplit) * nl * kl);
+  }
+  w.wpart = off; off += al(wmax * 4);
   w.cpart = off; off += al((size_t)w.cslices * 4 * C * 4);
   w.lpart = off; off += al((size_t)w.lnwaves * 2 * C * 4 + (size_t)w.lgroups * 2 * C * 4);
   w.total = off;
@@ -752,16 +771,24 @@ static hipError_t colsum(const Mat& X, int ncols, float* part, float* out, const
 // Weight gradient dW[Nl][Kl] = dY^T Z over all tokens (dY: T x Nl, Z: T x Kl),
 // in token slices, reduced in slice order.  LNB: Z = LN(z) applied while
 // staging.
-template <bool LNB>
-static hipError_t wgrad(const Mat& dY, const Mat& Z, const LnArgs& ln, int T, int Nl, int Kl, float* dW,
-                        char* ws, const BwdWs& w, hipStream_t st) {
-  LnArgs none = {nullptr, nullptr, nullptr, nullptr};
+
+static hipError_t wgrad(const Mat& dY, const Mat& Z, int T, int Nl, int Kl, float* dW, char* ws, const BwdWs& w,
+                        hipStream_t st) {
   EpiArgs ep = {};
   float* part = reinterpret_cast<float*>(ws + w.wpart);
   ep.outf = part;
-  hipError_t e = gemm<false, false, true, !LNB, false, LNB, EPI_F32>(dY, Z, none, ln, ep, Nl, Kl, T, w.wsplit, st);
+  const int ns = wgrad_slices(T, Nl, Kl, w.wsplit);
+  hipError_t e = gemm<false, false, EPI_F32>(dY, Z, ep, Nl, Kl, T, ns, st);
   if (e != hipSuccess) return e;
-  return slice_sum(part, dW, (int64_t)Nl * Kl, w.wsplit, st);
+  return slice_sum(part, dW, (int64_t)Nl * Kl, ns, st);
+}
+
+static hipError_t ln_apply(const void* z, const float* mu, const float* rs, const float* gamma, const float* beta,
+                           bf16* out, int T, int C, hipStream_t st) {
+  const int64_t n = (int64_t)T * (C / 8);
+  hipLaunchKernelGGL(ln_apply_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, (const bf16*)z, mu, rs,
+                     gamma, beta, out, T, C);
+  return hipGetLastError();
 }
 
 hipError_t launch_block_bwd(const Geo& g, const void* dx2, const void* x, const BlockParams& p, const float* table,
@@ -778,7 +805,7 @@ hipError_t launch_block_bwd(const Geo& g, const void* dx2, const void* x, const 
                    reinterpret_cast<bf16*>(ws + w.dv)};
   float* cpart = reinterpret_cast<float*>(ws + w.cpart);
   float* lpart = reinterpret_cast<float*>(ws + w.lpart);
-  LnArgs none = {nullptr, nullptr, nullptr, nullptr};
+  bf16* lnb = reinterpret_cast<bf16*>(ws + w.ln);
   hipError_t e;
   EpiArgs ep = {};
 #define TERRA_TRY(x)                    \
@@ -786,50 +813,47 @@ hipError_t launch_block_bwd(const Geo& g, const void* dx2, const void* x, const 
     if ((e = (x)) != hipSuccess) return e; \
   } while (0)
   // x2 = x1 + a W2^T + b2:  dW2 = dx2^T a, db2 = colsum(dx2), dh = (dx2 W2) * GELU'(h)
-  TERRA_TRY((wgrad<false>(mat(dx2, C, T), mat(s.a, 4 * C, T), none, T, C, 4 * C, gr.w_fc2, ws, w, st)));
+  TERRA_TRY(wgrad(mat(dx2, C, T), mat(s.a, 4 * C, T), T, C, 4 * C, gr.w_fc2, ws, w, st));
   TERRA_TRY(colsum(mat(dx2, C, T), C, cpart, gr.b_fc2, w, st));
   ep.out[0] = dh; ep.split = 4 * C; ep.aux = (const bf16*)s.h;
-  TERRA_TRY((gemm<true, false, true, true, false, false, EPI_GELU_GRAD>(mat(dx2, C, T), mat(p.w_fc2, 4 * C, C), none,
-                                                                       none, ep, T, 4 * C, C, 1, st)));
+  TERRA_TRY((gemm<true, false, EPI_GELU_GRAD>(mat(dx2, C, T), mat(p.w_fc2, 4 * C, C), ep, T, 4 * C, C, 1, st)));
   // h = LN2(x1) W1^T + b1:  dW1 = dh^T LN2(x1), db1 = colsum(dh), dln2 = dh W1
-  LnArgs ln2 = {s.mu2, s.rstd2, p.ln2_g, p.ln2_b};
-  TERRA_TRY((wgrad<true>(mat(dh, 4 * C, T), mat(s.x1, C, T), ln2, T, 4 * C, C, gr.w_fc1, ws, w, st)));
+  TERRA_TRY(ln_apply(s.x1, s.mu2, s.rstd2, p.ln2_g, p.ln2_b, lnb, T, C, st));
+  TERRA_TRY(wgrad(mat(dh, 4 * C, T), mat(lnb, C, T), T, 4 * C, C, gr.w_fc1, ws, w, st));
   TERRA_TRY(colsum(mat(dh, 4 * C, T), 4 * C, cpart, gr.b_fc1, w, st));
   ep = EpiArgs{};
   ep.outf = dln;
-  TERRA_TRY((gemm<true, false, true, true, false, false, EPI_F32>(mat(dh, 4 * C, T), mat(p.w_fc1, C, 4 * C), none,
-                                                                 none, ep, T, C, 4 * C, 1, st)));
+  TERRA_TRY((gemm<true, false, EPI_F32>(mat(dh, 4 * C, T), mat(p.w_fc1, C, 4 * C), ep, T, C, 4 * C, 1, st)));
   // dx1 = dx2 + LN2 backward
   hipLaunchKernelGGL(ln_bwd_kernel, dim3(w.lnwaves / 4), dim3(kRowThreads), 0, st, dln, (const bf16*)s.x1, s.mu2,
                      s.rstd2, p.ln2_g, (const bf16*)dx2, dx1, lpart, T, C, w.rows_per_wave);
   TERRA_TRY(hipGetLastError());
   TERRA_TRY(ln_param_grads(lpart, gr.ln2_g, gr.ln2_b, C, w, st));
   // x1 = x + o Wp^T + bp:  dWp = dx1^T o, dbp = colsum(dx1), dO = dx1 Wp
-  TERRA_TRY((wgrad<false>(mat(dx1, C, T), mat(s.o, C, T), none, T, C, C, gr.w_proj, ws, w, st)));
+  TERRA_TRY(wgrad(mat(dx1, C, T), mat(s.o, C, T), T, C, C, gr.w_proj, ws, w, st));
   TERRA_TRY(colsum(mat(dx1, C, T), C, cpart, gr.b_proj, w, st));
   ep = EpiArgs{};
   ep.out[0] = dO; ep.split = C;
-  TERRA_TRY((gemm<true, false, true, true, false, false, EPI_BF16>(mat(dx1, C, T), mat(p.w_proj, C, C), none, none,
-                                                                  ep, T, C, C, 1, st)));
+  TERRA_TRY((gemm<true, false, EPI_BF16>(mat(dx1, C, T), mat(p.w_proj, C, C), ep, T, C, C, 1, st)));
   // attention backward (route fused in)
   TERRA_TRY(launch_attn_bwd(g, 1, true, s.q, s.k, s.v, s.o, dO, s.lse, table, dqkv[0], dqkv[1], dqkv[2], dtable,
                             ws + w.attn, st));
   // qkv = LN1(x) Wqkv^T + bqkv, one third (Q, K, V) at a time: rows
   // [iC, (i+1)C) of dWqkv = dY_i^T LN1(x), of dbqkv = colsum(dY_i), and
   // dln1 = sum_i dY_i Wqkv[iC:(i+1)C]
-  LnArgs ln1 = {s.mu1, s.rstd1, p.ln1_g, p.ln1_b};
+  TERRA_TRY(ln_apply(x, s.mu1, s.rstd1, p.ln1_g, p.ln1_b, lnb, T, C, st));
+  for (int i = 0; i < 3; ++i) {
+    TERRA_TRY(wgrad(mat(dqkv[i], C, T), mat(lnb, C, T), T, C, C, gr.w_qkv + (size_t)i * C * C, ws, w, st));
+    TERRA_TRY(colsum(mat(dqkv[i], C, T), C, cpart, gr.b_qkv + (size_t)i * C, w, st));
+  }
+  ep = EpiArgs{};
+  ep.outf = dln;
   for (int i = 0; i < 3; ++i) {
     const bf16* wi = reinterpret_cast<const bf16*>(p.w_qkv) + (size_t)i * C * C;
-    TERRA_TRY((wgrad<true>(mat(dqkv[i], C, T), mat(x, C, T), ln1, T, C, C, gr.w_qkv + (size_t)i * C * C, ws, w, st)));
-    TERRA_TRY(colsum(mat(dqkv[i], C, T), C, cpart, gr.b_qkv + (size_t)i * C, w, st));
-    ep = EpiArgs{};
-    ep.outf = dln;
     if (i == 0) {
-      TERRA_TRY((gemm<true, false, true, true, false, false, EPI_F32>(mat(dqkv[i], C, T), mat(wi, C, C), none, none,
-                                                                     ep, T, C, C, 1, st)));
+      TERRA_TRY((gemm<true, false, EPI_F32>(mat(dqkv[i], C, T), mat(wi, C, C), ep, T, C, C, 1, st)));
     } else {
-      TERRA_TRY((gemm<true, false, true, true, false, false, EPI_F32_ACC>(mat(dqkv[i], C, T), mat(wi, C, C), none,
-                                                                         none, ep, T, C, C, 1, st)));
+      TERRA_TRY((gemm<true, false, EPI_F32_ACC>(mat(dqkv[i], C, T), mat(wi, C, C), ep, T, C, C, 1, st)));
     }
   }
   // dx = dx1 + LN1 backward
