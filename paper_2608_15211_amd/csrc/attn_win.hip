@@ -789,14 +789,16 @@ __global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
   // LDS float atomic costs about three clocks per lane).
 #define TERRA_FLUSH_DT(cw)                                                              \
   {                                                                                     \
-    const float rcw = 1.0f / (float)(cw);                                               \
-    const int aq = (int)(((float)qi + 0.5f) * rcw), cq = qi - aq * (cw);                \
+    /* widths are powers of two here (4, 8, 16 or 32): rows and columns by shifts, */   \
+    /* so that nothing of the flush is kept live across the window loop */             \
+    const int lw = __builtin_ctz((unsigned)(cw));                                       \
+    const int aq = qi >> lw, cq = qi & ((cw) - 1);                                      \
     _Pragma("unroll 1") for (int hh = 0; hh < 2; ++hh) {                                \
       if (half == hh) {                                                                 \
         _Pragma("unroll") for (int kb = 0; kb < 4; ++kb)                                \
         _Pragma("unroll") for (int g4 = 0; g4 < 4; ++g4) {                              \
           const int kk = 32 * kb + 8 * g4 + 4 * hh;                                     \
-          const int ak = (int)(((float)kk + 0.5f) * rcw), ck = kk - ak * (cw);          \
+          const int ak = kk >> lw, ck = kk & ((cw) - 1);                                \
           if (aq < g.wh && ak < g.wh) {                                                 \
             const int bin = g.nbins - 1 - ((aq - ak + g.wh - 1) * g.bstride + (cq - ck + g.ww - 1)); \
             mybins[bin] += dta[kb][g4];                                                 \
