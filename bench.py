@@ -192,7 +192,7 @@ def time_block(cfg, args, dev, flush):
     torch.cuda.synchronize()
     tf, tb = [], []
     for _ in range(max(5, args.steps // 2)):
-        flush.zero_()
+        flush()
         e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
         e0.record()
         fwd()
@@ -256,6 +256,11 @@ def main():
     back = {n: torch.empty((cfg.B, cfg.H, cfg.W, cfg.C), dtype=tdt, device=dev)
             for n in ("o", "dq", "dk", "dv")}
     ws = torch.empty(max(1, P.terra_winattn_bwd_workspace_bytes(cfg, tdt)), dtype=torch.uint8, device=dev)
+    # shapes on the general kernels keep O's rounding residual for the
+    # backward's D (no extra sweep over the keys); None elsewhere
+    uses_lo = P.terra_winattn_uses_o_lo(cfg, tdt)
+    o_lo = torch.empty((cfg.B, cfg.H, cfg.W, cfg.C), dtype=tdt, device=dev) if uses_lo else None
+    o_lo_w = torch.empty(shape_w, dtype=tdt, device=dev) if uses_lo else None
 
     fused_phases = ["fwd", "bwd"]
     unfused_phases = ["route", "fwd_wm", "bwd_wm", "unroute"]
@@ -272,26 +277,37 @@ def main():
 
     def step(ev):
         rec(ev, "fwd", lambda: P.terra_winattn_fwd_nhwc(x["q"], x["k"], x["v"], table, cfg,
-                                                         out=back["o"], lse=lse))
+                                                         out=back["o"], lse=lse, o_lo=o_lo))
         rec(ev, "bwd", lambda: P.terra_winattn_bwd_nhwc(x["q"], x["k"], x["v"], back["o"], x["dout"],
                                                          lse, table, cfg, workspace=ws,
                                                          out=(back["dq"], back["dk"], back["dv"],
-                                                              grads[3])))
+                                                              grads[3]), o_lo=o_lo))
 
     def step_unfused(ev):
         for n in ("q", "k", "v"):
             rec(ev, "route", lambda n=n: P.terra_window_route(x[n], cfg, out=w[n]))
-        rec(ev, "fwd_wm", lambda: P.terra_winattn_fwd(w["q"], w["k"], w["v"], table, cfg, out=o, lse=lse))
+        rec(ev, "fwd_wm", lambda: P.terra_winattn_fwd(w["q"], w["k"], w["v"], table, cfg, out=o, lse=lse,
+                                                      o_lo=o_lo_w))
         rec(ev, "route", lambda: P.terra_window_route(x["dout"], cfg, out=w["dout"]))
         rec(ev, "bwd_wm", lambda: P.terra_winattn_bwd(w["q"], w["k"], w["v"], o, w["dout"], lse, table, cfg,
-                                                      out=grads, workspace=ws))
+                                                      out=grads, workspace=ws, o_lo=o_lo_w))
         for n, t in (("o", o), ("dq", grads[0]), ("dk", grads[1]), ("dv", grads[2])):
             rec(ev, "unroute", lambda n=n, t=t: P.terra_window_unroute(t, cfg, out=back[n]))
 
     # Between timed steps (outside the step's events) a 1 GiB buffer is
-    # overwritten so that no step finds the previous one's tensors in the
-    # 256 MB last-level cache (MALL).
-    flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    # overwritten and then a second 1 GiB buffer is read, so that no step
+    # finds the previous one's tensors in the 256 MB last-level cache (MALL).
+    # The read matters: after the write alone the cache is full of dirty
+    # lines, and their write-back lands inside the next step (the 128 x 1080
+    # forward measured 0.268 ms after a write-only flush, 0.217 ms after write + read
+    # or a read alone, 0.218 ms with no flush).
+    flush_w = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    flush_r = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+    flush_sink = torch.empty((), dtype=torch.float32, device=dev)
+
+    def flush():
+        flush_w.zero_()
+        torch.sum(flush_r, dim=0, out=flush_sink)
 
     def timed(fn, phases):
         print("bench: warm-up %d steps" % args.warmup, file=sys.stderr, flush=True)
@@ -302,7 +318,7 @@ def main():
         marks = []
         torch.cuda.synchronize()
         for _ in range(args.steps):
-            flush.zero_()
+            flush()
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record()
             fn(ev)
@@ -360,7 +376,7 @@ def main():
         "warmup": args.warmup,
         "ms_per_step": round(ms_step, 4),
         "ms_per_step_mean": round(ms_step_mean, 4),
-        "step_statistic": "median of the timed steps; 1 GiB cache flush between steps, outside the step",
+        "step_statistic": "median of the timed steps; between steps, outside the step, a 1 GiB write then a 1 GiB read flush the caches",
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,

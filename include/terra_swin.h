@@ -116,29 +116,44 @@ int terra_window_unroute(const terra_geom* g, int dtype, const void* y_win,
  * image, window and head: S = Q K^T / sqrt(head_dim) + bias, masked pairs
  * excluded, P = softmax(S), O = P V, LSE = ln sum exp S (natural log).
  * q, k, v, o: window-major, `dtype`; bias_table: float32 table;
- * lse: float32 B x heads x (H*W).  o and lse are overwritten. */
+ * lse: float32 B x heads x (H*W).  o and lse are overwritten.
+ * o_lo (nullable, same shape and type as o): where
+ * terra_winattn_uses_o_lo(g, dtype) is 1, the forward forms O with P
+ * entering the P V product as two 16-bit parts (so that the float32 O is
+ * exact to about 16 significant bits) and writes O - round(O), rounded to
+ * `dtype`, into o_lo.  Passed on to the backward, it gives
+ * D_q = <dO_q, O_q> without an extra sweep over the keys.  Elsewhere o_lo
+ * is neither written nor read, and with o_lo NULL the forward is unchanged. */
 int terra_winattn_fwd(const terra_geom* g, int dtype, const void* q,
                       const void* k, const void* v, const float* bias_table,
-                      void* o, float* lse, void* stream);
+                      void* o, void* o_lo, float* lse, void* stream);
+
+/* 1 when the forward writes o_lo and the backward reads it for this
+ * geometry and element type (float16 and bfloat16 with windows of more
+ * than 256 tokens, where the key sweep it replaces costs more than the
+ * split product and the extra traffic), 0 when o_lo is ignored, -status on
+ * invalid input. */
+int terra_winattn_uses_o_lo(const terra_geom* g, int dtype);
 
 /* Bytes of device workspace terra_winattn_bwd (and terra_winattn_bwd_nhwc)
  * needs for this geometry (0 on invalid input). */
 size_t terra_winattn_bwd_workspace_bytes(const terra_geom* g, int dtype);
 
 /* Shifted-window attention backward.  Inputs are the forward's inputs, its
- * outputs o and lse, and the upstream gradient dout (window-major).
+ * outputs o, o_lo and lse, and the upstream gradient dout (window-major).
  * Outputs dq, dk, dv (window-major, `dtype`) and dbias_table (float32,
  * table shape, summed over images, windows and allowed pairs) are
- * OVERWRITTEN.  dS = P * (dP - D) where D_q = sum_k P[q,k] dP[q,k] is
- * recomputed inside each window in float32 (it equals <dO_q, O_q> for the
- * unrounded O; `o` is accepted for symmetry with the forward and is not
- * read, because a bf16-rounded O would bias the bias-table gradient).  The
- * bias-table gradient is reduced in a fixed order, so results are
- * bit-reproducible.
+ * OVERWRITTEN.  dS = P * (dP - D), D_q = sum_k P[q,k] dP[q,k] = <dO_q, O_q>
+ * for the exact O, in float32: from o + o_lo when o_lo is not NULL and
+ * terra_winattn_uses_o_lo(g, dtype) is 1, otherwise recomputed inside each
+ * window from P and dP.  The rounded O alone is not used for it: D's
+ * rounding error, alike for every key of a query, would add up over the
+ * windows in the bias-table gradient.  The bias-table gradient is reduced
+ * in a fixed order, so results are bit-reproducible.
  * workspace: device buffer of at least terra_winattn_bwd_workspace_bytes. */
 int terra_winattn_bwd(const terra_geom* g, int dtype, const void* q,
                       const void* k, const void* v, const void* o,
-                      const void* dout, const float* lse,
+                      const void* o_lo, const void* dout, const float* lse,
                       const float* bias_table, void* dq, void* dk, void* dv,
                       float* dbias_table, void* workspace,
                       size_t workspace_bytes, void* stream);
@@ -153,16 +168,16 @@ int terra_winattn_bwd(const terra_geom* g, int dtype, const void* q,
  * bit. */
 int terra_winattn_fwd_nhwc(const terra_geom* g, int dtype, const void* q,
                            const void* k, const void* v,
-                           const float* bias_table, void* o, float* lse,
-                           void* stream);
+                           const float* bias_table, void* o, void* o_lo,
+                           float* lse, void* stream);
 
 /* Fused route + attention backward: terra_winattn_bwd with q, k, v, o,
- * dout, dq, dk, dv as NHWC tensors and lse in NHWC token order, as written
+ * o_lo, dout, dq, dk, dv as NHWC tensors and lse in NHWC token order, as written
  * by terra_winattn_fwd_nhwc.  Needs the workspace of
  * terra_winattn_bwd_workspace_bytes (the same size for both layouts). */
 int terra_winattn_bwd_nhwc(const terra_geom* g, int dtype, const void* q,
                            const void* k, const void* v, const void* o,
-                           const void* dout, const float* lse,
+                           const void* o_lo, const void* dout, const float* lse,
                            const float* bias_table, void* dq, void* dk,
                            void* dv, float* dbias_table, void* workspace,
                            size_t workspace_bytes, void* stream);
@@ -182,7 +197,8 @@ int terra_winattn_bwd_nhwc(const terra_geom* g, int dtype, const void* q,
 #define TERRA_SCRATCH_BYTES (32u << 20)
 int terra_winattn_bwd_nhwc_noalloc(const terra_geom* g, int dtype, const void* q,
                                    const void* k, const void* v, const void* o,
-                                   const void* dout, const float* lse,
+                                   const void* o_lo, const void* dout,
+                                   const float* lse,
                                    const float* bias_table, void* dq, void* dk,
                                    void* dv, float* dbias_table, void* stream);
 

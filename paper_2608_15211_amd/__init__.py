@@ -11,6 +11,8 @@ Entry points (same names as the C ABI):
     terra_window_route, terra_window_unroute, terra_winattn_fwd,
     terra_winattn_bwd_workspace_bytes, terra_winattn_bwd,
     terra_winattn_fwd_nhwc, terra_winattn_bwd_nhwc (route fused in),
+    terra_winattn_uses_o_lo (whether the forward's rounding residual of O
+    serves the backward),
     terra_winattn_bwd_nhwc_noalloc (workspace from a library-held array),
     terra_plan_padded_grid, terra_plan_window_ranges, terra_plan_rank,
     terra_window_route_rank, terra_window_unroute_rank, terra_fragment_pack,
@@ -109,13 +111,15 @@ def lib():
     L.terra_window_layout.argtypes = [G, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_int32)]
     L.terra_window_route.argtypes = [G, i32, vp, vp, vp, vp, vp]
     L.terra_window_unroute.argtypes = [G, i32, vp, vp, vp]
-    L.terra_winattn_fwd.argtypes = [G, i32, vp, vp, vp, vp, vp, vp, vp]
-    L.terra_winattn_fwd_nhwc.argtypes = [G, i32, vp, vp, vp, vp, vp, vp, vp]
+    L.terra_winattn_fwd.argtypes = [G, i32] + [vp] * 8
+    L.terra_winattn_fwd_nhwc.argtypes = [G, i32] + [vp] * 8
+    L.terra_winattn_uses_o_lo.argtypes = [G, i32]
+    L.terra_winattn_uses_o_lo.restype = i32
     L.terra_winattn_bwd_workspace_bytes.argtypes = [G, i32]
     L.terra_winattn_bwd_workspace_bytes.restype = sz
-    L.terra_winattn_bwd.argtypes = [G, i32] + [vp] * 12 + [sz, vp]
-    L.terra_winattn_bwd_nhwc.argtypes = [G, i32] + [vp] * 12 + [sz, vp]
-    L.terra_winattn_bwd_nhwc_noalloc.argtypes = [G, i32] + [vp] * 12
+    L.terra_winattn_bwd.argtypes = [G, i32] + [vp] * 13 + [sz, vp]
+    L.terra_winattn_bwd_nhwc.argtypes = [G, i32] + [vp] * 13 + [sz, vp]
+    L.terra_winattn_bwd_nhwc_noalloc.argtypes = [G, i32] + [vp] * 13
     i64 = ctypes.c_int64
     L.terra_plan_padded_grid.argtypes = [i32] * 7 + [ctypes.POINTER(ctypes.c_int32)] * 2 + \
         [ctypes.POINTER(ctypes.c_double)]
@@ -141,7 +145,7 @@ def lib():
     for name in ("terra_validate_geometry", "terra_window_count", "terra_window_layout",
                  "terra_window_route", "terra_window_unroute", "terra_winattn_fwd",
                  "terra_winattn_bwd", "terra_winattn_fwd_nhwc", "terra_winattn_bwd_nhwc",
-                 "terra_winattn_bwd_nhwc_noalloc",
+                 "terra_winattn_bwd_nhwc_noalloc", "terra_winattn_uses_o_lo",
                  "terra_plan_padded_grid", "terra_plan_window_ranges", "terra_plan_rank",
                  "terra_window_route_rank", "terra_window_unroute_rank", "terra_fragment_pack",
                  "terra_fragment_unpack", "terra_block_fwd", "terra_block_bwd"):
@@ -255,7 +259,12 @@ def terra_window_unroute(y_win, g, out=None):
     return out
 
 
-def _attn_fwd(fn, shape, q, k, v, table, g, out, lse):
+def _opt(t, name, dtype=None, numel=None):
+    """Nullable device pointer: NULL for None, else as _dev."""
+    return ctypes.c_void_p(None) if t is None else _dev(t, name, dtype, numel)
+
+
+def _attn_fwd(fn, shape, q, k, v, table, g, out, lse, o_lo):
     import torch
     gg = _geom(g)
     n, nl, nt = _sizes(gg)
@@ -266,11 +275,11 @@ def _attn_fwd(fn, shape, q, k, v, table, g, out, lse):
         lse = torch.empty((gg.B, gg.heads, gg.H * gg.W), dtype=torch.float32, device=q.device)
     _check(fn(ctypes.byref(gg), _dtype_code(dt), _dev(q, "q", dt, n), _dev(k, "k", dt, n),
               _dev(v, "v", dt, n), _dev(table, "table", torch.float32, nt), _dev(out, "o", dt, n),
-              _dev(lse, "lse", torch.float32, nl), _stream()))
+              _opt(o_lo, "o_lo", dt, n), _dev(lse, "lse", torch.float32, nl), _stream()))
     return out, lse
 
 
-def _attn_bwd(fn, q, k, v, o, dout, lse, table, g, out, workspace):
+def _attn_bwd(fn, q, k, v, o, dout, lse, table, g, out, workspace, o_lo):
     import torch
     gg = _geom(g)
     n, nl, nt = _sizes(gg)
@@ -284,42 +293,54 @@ def _attn_bwd(fn, q, k, v, o, dout, lse, table, g, out, workspace):
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
     _check(fn(ctypes.byref(gg), code, _dev(q, "q", dt, n), _dev(k, "k", dt, n), _dev(v, "v", dt, n),
-              _dev(o, "o", dt, n), _dev(dout, "dout", dt, n), _dev(lse, "lse", torch.float32, nl),
-              _dev(table, "table", torch.float32, nt), _dev(dq, "dq", dt, n), _dev(dk, "dk", dt, n),
-              _dev(dv, "dv", dt, n), _dev(dtab, "dtable", torch.float32, nt),
-              _dev(workspace, "workspace"), ctypes.c_size_t(workspace.numel()), _stream()))
+              _dev(o, "o", dt, n), _opt(o_lo, "o_lo", dt, n), _dev(dout, "dout", dt, n),
+              _dev(lse, "lse", torch.float32, nl), _dev(table, "table", torch.float32, nt),
+              _dev(dq, "dq", dt, n), _dev(dk, "dk", dt, n), _dev(dv, "dv", dt, n),
+              _dev(dtab, "dtable", torch.float32, nt), _dev(workspace, "workspace"),
+              ctypes.c_size_t(workspace.numel()), _stream()))
     return dq, dk, dv, dtab
 
 
-def terra_winattn_fwd(q, k, v, table, g, out=None, lse=None):
+def terra_winattn_fwd(q, k, v, table, g, out=None, lse=None, o_lo=None):
     """Window-major q, k, v (B,H*W,C) and float32 bias table
-    (2wh-1,2ww-1,heads) -> (O (B,H*W,C), LSE float32 (B,heads,H*W))."""
+    (2wh-1,2ww-1,heads) -> (O (B,H*W,C), LSE float32 (B,heads,H*W)).
+    o_lo: optional tensor like O for O's rounding residual (written only
+    where terra_winattn_uses_o_lo is true)."""
     return _attn_fwd(lib().terra_winattn_fwd, lambda gg: (gg.B, gg.H * gg.W, gg.C),
-                     q, k, v, table, g, out, lse)
+                     q, k, v, table, g, out, lse, o_lo)
 
 
-def terra_winattn_fwd_nhwc(q, k, v, table, g, out=None, lse=None):
+def terra_winattn_fwd_nhwc(q, k, v, table, g, out=None, lse=None, o_lo=None):
     """NHWC q, k, v (B,H,W,C), route fused in -> (O (B,H,W,C), LSE float32
-    (B,heads,H*W) in NHWC token order)."""
+    (B,heads,H*W) in NHWC token order); o_lo as for terra_winattn_fwd."""
     return _attn_fwd(lib().terra_winattn_fwd_nhwc, lambda gg: (gg.B, gg.H, gg.W, gg.C),
-                     q, k, v, table, g, out, lse)
+                     q, k, v, table, g, out, lse, o_lo)
 
 
-def terra_winattn_bwd(q, k, v, o, dout, lse, table, g, out=None, workspace=None):
+def terra_winattn_uses_o_lo(g, dtype):
+    """True when the forward writes o_lo and the backward reads it."""
+    r = int(lib().terra_winattn_uses_o_lo(ctypes.byref(_geom(g)), _dtype_code(dtype)))
+    if r < 0:
+        _check(-r)
+    return r == 1
+
+
+def terra_winattn_bwd(q, k, v, o, dout, lse, table, g, out=None, workspace=None, o_lo=None):
     """Window-major tensors.  Returns (dQ, dK, dV, dTable).  `out` may hold
-    preallocated (dq, dk, dv, dtable); `workspace` a uint8 device tensor."""
-    return _attn_bwd(lib().terra_winattn_bwd, q, k, v, o, dout, lse, table, g, out, workspace)
+    preallocated (dq, dk, dv, dtable); `workspace` a uint8 device tensor;
+    `o_lo` the forward's rounding residual of O, if it kept one."""
+    return _attn_bwd(lib().terra_winattn_bwd, q, k, v, o, dout, lse, table, g, out, workspace, o_lo)
 
 
-def terra_winattn_bwd_nhwc(q, k, v, o, dout, lse, table, g, out=None, workspace=None):
+def terra_winattn_bwd_nhwc(q, k, v, o, dout, lse, table, g, out=None, workspace=None, o_lo=None):
     """As terra_winattn_bwd with NHWC tensors and NHWC-ordered LSE."""
-    return _attn_bwd(lib().terra_winattn_bwd_nhwc, q, k, v, o, dout, lse, table, g, out, workspace)
+    return _attn_bwd(lib().terra_winattn_bwd_nhwc, q, k, v, o, dout, lse, table, g, out, workspace, o_lo)
 
 
 TERRA_SCRATCH_BYTES = 32 << 20
 
 
-def terra_winattn_bwd_nhwc_noalloc(q, k, v, o, dout, lse, table, g, out):
+def terra_winattn_bwd_nhwc_noalloc(q, k, v, o, dout, lse, table, g, out, o_lo=None):
     """terra_winattn_bwd_nhwc with no workspace argument: the library's own
     per-GPU scratch array serves.  `out` = preallocated (dq, dk, dv, dtable)."""
     import torch
@@ -329,9 +350,10 @@ def terra_winattn_bwd_nhwc_noalloc(q, k, v, o, dout, lse, table, g, out):
     dq, dk, dv, dtab = out
     _check(lib().terra_winattn_bwd_nhwc_noalloc(
         ctypes.byref(gg), _dtype_code(dt), _dev(q, "q", dt, n), _dev(k, "k", dt, n), _dev(v, "v", dt, n),
-        _dev(o, "o", dt, n), _dev(dout, "dout", dt, n), _dev(lse, "lse", torch.float32, nl),
-        _dev(table, "table", torch.float32, nt), _dev(dq, "dq", dt, n), _dev(dk, "dk", dt, n),
-        _dev(dv, "dv", dt, n), _dev(dtab, "dtable", torch.float32, nt), _stream()))
+        _dev(o, "o", dt, n), _opt(o_lo, "o_lo", dt, n), _dev(dout, "dout", dt, n),
+        _dev(lse, "lse", torch.float32, nl), _dev(table, "table", torch.float32, nt),
+        _dev(dq, "dq", dt, n), _dev(dk, "dk", dt, n), _dev(dv, "dv", dt, n),
+        _dev(dtab, "dtable", torch.float32, nt), _stream()))
     return dq, dk, dv, dtab
 
 
@@ -357,10 +379,6 @@ def terra_plan_rank(g, ranks, rank):
     frags = (terra_fragment * TERRA_MAX_FRAGMENTS)()
     _check(lib().terra_plan_rank(ctypes.byref(_geom(g)), ranks, rank, ctypes.byref(plan), frags))
     return plan.as_dict(), [frags[i].as_dict() for i in range(plan.nfrag)]
-
-
-def _opt(t, name, dtype):
-    return ctypes.c_void_p(0) if t is None else _dev(t, name, dtype)
 
 
 def terra_window_route_rank(stripe, frag_buf, g, ranks, rank, out=None):

@@ -25,11 +25,13 @@ hipError_t launch_block_bwd(const Geo& g, const void* dx2, const void* x, const 
                             hipStream_t st);
 size_t block_bwd_workspace(const Geo& g);
 hipError_t launch_attn_fwd(const Geo& g, int dt, bool nhwc, const void* q, const void* k,
-                           const void* v, const float* table, void* o, float* lse, hipStream_t st);
-hipError_t launch_attn_bwd(const Geo& g, int dt, bool nhwc, const void* q, const void* k,
-                           const void* v, const void* o, const void* dout, const float* lse,
-                           const float* table, void* dq, void* dk, void* dv, float* dtab, void* ws,
+                           const void* v, const float* table, void* o, void* olo, float* lse,
                            hipStream_t st);
+hipError_t launch_attn_bwd(const Geo& g, int dt, bool nhwc, const void* q, const void* k,
+                           const void* v, const void* o, const void* olo, const void* dout,
+                           const float* lse, const float* table, void* dq, void* dk, void* dv,
+                           float* dtab, void* ws, hipStream_t st);
+bool attn_uses_olo(const Geo& g, int dt);
 size_t bwd_workspace(const Geo& g, int dt);
 size_t attn_max_lds(const Geo& g, int dt);
 hipError_t launch_route_rank(const Geo& g, int row_bytes, const RankPlan& plan, const Frag* frags,
@@ -240,20 +242,21 @@ int terra_window_unroute(const terra_geom* g, int dtype, const void* y_win, void
 }  // extern "C"
 
 static int attn_fwd_common(const terra_geom* g, int dtype, bool nhwc, const void* q, const void* k,
-                           const void* v, const float* bias_table, void* o, float* lse,
+                           const void* v, const float* bias_table, void* o, void* o_lo, float* lse,
                            void* stream) {
   int s = check_attn(g, dtype);
   if (s) return s;
   if (!q || !k || !v || !bias_table || !o || !lse)
     return fail(TERRA_ERR_INVALID, "tensor pointer is NULL");
   terra::Geo G = launch_geo(g);
-  return hip_status(terra::launch_attn_fwd(G, dtype, nhwc, q, k, v, bias_table, o, lse,
+  return hip_status(terra::launch_attn_fwd(G, dtype, nhwc, q, k, v, bias_table, o, o_lo, lse,
                                            (hipStream_t)stream),
                     nhwc ? "terra_winattn_fwd_nhwc launch" : "terra_winattn_fwd launch");
 }
 
 static int attn_bwd_common(const terra_geom* g, int dtype, bool nhwc, const void* q, const void* k,
-                           const void* v, const void* o, const void* dout, const float* lse,
+                           const void* v, const void* o, const void* o_lo, const void* dout,
+                           const float* lse,
                            const float* bias_table, void* dq, void* dk, void* dv,
                            float* dbias_table, void* workspace, size_t workspace_bytes,
                            void* stream) {
@@ -266,7 +269,7 @@ static int attn_bwd_common(const terra_geom* g, int dtype, bool nhwc, const void
   if (!workspace || workspace_bytes < need)
     return fail(TERRA_ERR_WORKSPACE, "workspace of %zu bytes given, %zu needed",
                 workspace ? workspace_bytes : (size_t)0, need);
-  return hip_status(terra::launch_attn_bwd(G, dtype, nhwc, q, k, v, o, dout, lse,
+  return hip_status(terra::launch_attn_bwd(G, dtype, nhwc, q, k, v, o, o_lo, dout, lse,
                                            bias_table, dq, dk, dv, dbias_table, workspace,
                                            (hipStream_t)stream),
                     nhwc ? "terra_winattn_bwd_nhwc launch" : "terra_winattn_bwd launch");
@@ -275,14 +278,21 @@ static int attn_bwd_common(const terra_geom* g, int dtype, bool nhwc, const void
 extern "C" {
 
 int terra_winattn_fwd(const terra_geom* g, int dtype, const void* q, const void* k, const void* v,
-                      const float* bias_table, void* o, float* lse, void* stream) {
-  return attn_fwd_common(g, dtype, false, q, k, v, bias_table, o, lse, stream);
+                      const float* bias_table, void* o, void* o_lo, float* lse, void* stream) {
+  return attn_fwd_common(g, dtype, false, q, k, v, bias_table, o, o_lo, lse, stream);
 }
 
 int terra_winattn_fwd_nhwc(const terra_geom* g, int dtype, const void* q, const void* k,
-                           const void* v, const float* bias_table, void* o, float* lse,
-                           void* stream) {
-  return attn_fwd_common(g, dtype, true, q, k, v, bias_table, o, lse, stream);
+                           const void* v, const float* bias_table, void* o, void* o_lo,
+                           float* lse, void* stream) {
+  return attn_fwd_common(g, dtype, true, q, k, v, bias_table, o, o_lo, lse, stream);
+}
+
+int terra_winattn_uses_o_lo(const terra_geom* g, int dtype) {
+  int s = check_attn(g, dtype);
+  if (s) return -s;
+  ok();
+  return terra::attn_uses_olo(make_geo(g), dtype) ? 1 : 0;
 }
 
 size_t terra_winattn_bwd_workspace_bytes(const terra_geom* g, int dtype) {
@@ -291,19 +301,19 @@ size_t terra_winattn_bwd_workspace_bytes(const terra_geom* g, int dtype) {
 }
 
 int terra_winattn_bwd(const terra_geom* g, int dtype, const void* q, const void* k, const void* v,
-                      const void* o, const void* dout, const float* lse, const float* bias_table,
-                      void* dq, void* dk, void* dv, float* dbias_table, void* workspace,
-                      size_t workspace_bytes, void* stream) {
-  return attn_bwd_common(g, dtype, false, q, k, v, o, dout, lse, bias_table, dq, dk, dv,
+                      const void* o, const void* o_lo, const void* dout, const float* lse,
+                      const float* bias_table, void* dq, void* dk, void* dv, float* dbias_table,
+                      void* workspace, size_t workspace_bytes, void* stream) {
+  return attn_bwd_common(g, dtype, false, q, k, v, o, o_lo, dout, lse, bias_table, dq, dk, dv,
                          dbias_table, workspace, workspace_bytes, stream);
 }
 
 int terra_winattn_bwd_nhwc(const terra_geom* g, int dtype, const void* q, const void* k,
-                           const void* v, const void* o, const void* dout, const float* lse,
-                           const float* bias_table, void* dq, void* dk, void* dv,
-                           float* dbias_table, void* workspace, size_t workspace_bytes,
+                           const void* v, const void* o, const void* o_lo, const void* dout,
+                           const float* lse, const float* bias_table, void* dq, void* dk,
+                           void* dv, float* dbias_table, void* workspace, size_t workspace_bytes,
                            void* stream) {
-  return attn_bwd_common(g, dtype, true, q, k, v, o, dout, lse, bias_table, dq, dk, dv,
+  return attn_bwd_common(g, dtype, true, q, k, v, o, o_lo, dout, lse, bias_table, dq, dk, dv,
                          dbias_table, workspace, workspace_bytes, stream);
 }
 
@@ -554,9 +564,10 @@ int scratch_address(void** out) {
 extern "C" {
 
 int terra_winattn_bwd_nhwc_noalloc(const terra_geom* g, int dtype, const void* q, const void* k,
-                                   const void* v, const void* o, const void* dout, const float* lse,
-                                   const float* bias_table, void* dq, void* dk, void* dv,
-                                   float* dbias_table, void* stream) {
+                                   const void* v, const void* o, const void* o_lo,
+                                   const void* dout, const float* lse, const float* bias_table,
+                                   void* dq, void* dk, void* dv, float* dbias_table,
+                                   void* stream) {
   int s = check_attn(g, dtype);
   if (s) return s;
   const size_t need = terra::bwd_workspace(make_geo(g), dtype);
@@ -567,8 +578,8 @@ int terra_winattn_bwd_nhwc_noalloc(const terra_geom* g, int dtype, const void* q
                 need, (size_t)TERRA_SCRATCH_BYTES);
   void* ws = nullptr;
   if ((s = scratch_address(&ws))) return s;
-  return attn_bwd_common(g, dtype, true, q, k, v, o, dout, lse, bias_table, dq, dk, dv, dbias_table,
-                         ws, (size_t)TERRA_SCRATCH_BYTES, stream);
+  return attn_bwd_common(g, dtype, true, q, k, v, o, o_lo, dout, lse, bias_table, dq, dk, dv,
+                         dbias_table, ws, (size_t)TERRA_SCRATCH_BYTES, stream);
 }
 
 const char* terra_status_string(int status) {

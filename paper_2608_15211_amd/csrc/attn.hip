@@ -184,13 +184,15 @@ __device__ inline int token_info(const Geo& g, int i, int j, int cols, int t, in
 // per window, empty chunks of small windows exit at once).  The bias enters
 // the score accumulator before the QK^T product (table times sqrt(hd) in
 // reversed bin order, -inf entries for excluded pairs), so each score costs
-// one multiply-add and one exp2 outside the matrix cores.
+// one multiply-add and one exp2 outside the matrix cores.  With olo (16-bit
+// types, nullable) the PV product also takes P's rounding residual and the
+// epilogue writes O's: the backward's D = <dO, O> then needs no key sweep.
 // ---------------------------------------------------------------------------
-template <typename T, int HD, bool NHWC, bool QUAD>
+template <typename T, int HD, bool NHWC, bool QUAD, bool SPLIT>
 __global__ __launch_bounds__(kThreads) void fwd_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
-    const float* __restrict__ table, T* __restrict__ o, float* __restrict__ lse,
-    Geo g, int nqc, float scale_log2) {
+    const float* __restrict__ table, T* __restrict__ o, T* __restrict__ olo,
+    float* __restrict__ lse, Geo g, int nqc, float scale_log2) {
   constexpr int kTile = tile_of<T, HD>();
   extern __shared__ __align__(16) char smem[];
   T* kt = reinterpret_cast<T*>(smem);                          // [kTile][HD+kPad]
@@ -227,6 +229,7 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(
   const int qlab = qinf >> 24;
   const int qrev = g.nbins - 1 - ((qinf & 0xFFFFFF) + (g.wh - 1) * g.bstride + (g.ww - 1));
   const bool mask = window_has_labels(g, i, j) || (n % kTile) != 0;
+  constexpr bool split = SPLIT && sizeof(T) == 2;
 
   typename Operand<T>::type qop[HD / 16];
 #pragma unroll
@@ -238,6 +241,7 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(
 #pragma unroll
   for (int eb = 0; eb < HD / 32; ++eb) oacc[eb] = f32x16{};
   float m_run = -1e30f, l_run = 0.0f;     // running max (log2 units) and sum
+  constexpr float kPOff = __is_same(T, _Float16) ? 7.0f : 0.0f;
 
   // K, V tiles go HBM -> registers -> LDS, one tile ahead up to head dim 64
   constexpr bool kPrefetch = HD <= 64;
@@ -279,10 +283,14 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(
     // The running maximum moves (and O and the sum are rescaled) only when
     // some query of the wave sees a score more than 2^8 above it: between
     // moves the weights stay below 256, which the fp32 sums and the 16-bit
-    // operands carry as exactly as weights below 1.
+    // operands carry as exactly as weights below 1.  For float16 operands
+    // the weights run 2^kPOff higher (m_run sits kPOff below the maximum;
+    // the sum, and so the LSE, follow), so that weights down to 2^-21 of the
+    // maximum, and the low parts of the split, stay above float16's
+    // subnormal range (6.1e-5), which the operands would lose.
     const float mt = mloc * scale_log2;
-    if (__builtin_amdgcn_ballot_w64(mt > m_run + 8.0f) != 0) {
-      const float mnew = fmaxf(m_run, mt);
+    if (__builtin_amdgcn_ballot_w64(mt > m_run + (kPOff + 8.0f)) != 0) {
+      const float mnew = fmaxf(m_run, mt - kPOff);
       const float alpha = exp2f(m_run - mnew);
       m_run = mnew;
       l_run *= alpha;
@@ -298,15 +306,41 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(
         l_run += p;
       }
     }
+    if constexpr (sizeof(T) == 2) {
+      // 16-bit P operands.  When the caller keeps O_lo, P also enters as
+      // hi + lo (lo = P - hi rounded again), so that the fp32 sum carries
+      // P V to about 16 significant bits rather than the 8 of one rounding.
+      typename Operand<T>::type phi[kTile / 32][2], plo[kTile / 32][2];
 #pragma unroll
-    for (int eb = 0; eb < HD / 32; ++eb) {
-#pragma unroll
-      for (int kb = 0; kb < kTile / 32; ++kb) {
+      for (int kb = 0; kb < kTile / 32; ++kb)
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
-          if constexpr (sizeof(T) == 2) {
-            mma16(oacc[eb], lds_tr_op<T, tr16_stride<HD>()>(vt, kb, c, eb, lane), pack8<T>(s[kb], 8 * c));
-          } else {
+          phi[kb][c] = pack8<T>(s[kb], 8 * c);
+          if constexpr (split) {
+#pragma unroll
+            for (int x = 0; x < 8; ++x)
+              plo[kb][c][x] = from_float<T>(s[kb][8 * c + x] - to_float<T>(phi[kb][c][x]));
+          }
+        }
+#pragma unroll
+      for (int eb = 0; eb < HD / 32; ++eb) {
+#pragma unroll
+        for (int kb = 0; kb < kTile / 32; ++kb) {
+#pragma unroll
+          for (int c = 0; c < 2; ++c) {
+            const auto vop = lds_tr_op<T, tr16_stride<HD>()>(vt, kb, c, eb, lane);
+            mma16(oacc[eb], vop, phi[kb][c]);
+            if constexpr (split) mma16(oacc[eb], vop, plo[kb][c]);
+          }
+        }
+      }
+    } else {
+#pragma unroll
+      for (int eb = 0; eb < HD / 32; ++eb) {
+#pragma unroll
+        for (int kb = 0; kb < kTile / 32; ++kb) {
+#pragma unroll
+          for (int c = 0; c < 2; ++c) {
             const T* row = vt + tr_row<T, HD>(eb * 32 + col) + kb * 32 + 16 * c;
             mma16(oacc[eb], load_op_lds_perm<T>(row, half), pack8<T>(s[kb], 8 * c));
           }
@@ -318,13 +352,32 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(
   if (!qvalid) return;
   const float inv = 1.0f / l_run;
   T* orow = o + wt.tok(g, qi) * g.C + hoff;
+  // O_lo: what rounding O to T left out, itself rounded to T; O + O_lo
+  // carries the fp32 output to about 16 significant bits
+  T* lrow = split ? olo + wt.tok(g, qi) * g.C + hoff : nullptr;
+  const unsigned opq = (unsigned)g.C >> 31;    // 0: C is positive
+  (void)lrow;
+  (void)opq;
 #pragma unroll
   for (int eb = 0; eb < HD / 32; ++eb) {
 #pragma unroll
     for (int grp = 0; grp < 4; ++grp) {
       const int e = eb * 32 + 8 * grp + 4 * half;
 #pragma unroll
-      for (int x = 0; x < 4; ++x) orow[e + x] = from_float<T>(oacc[eb][4 * grp + x] * inv);
+      for (int x = 0; x < 4; ++x) {
+        float val = oacc[eb][4 * grp + x] * inv;
+        // The split needs one float32 value behind both halves: left to
+        // itself the compiler folds the multiply into a float16
+        // mixed-precision multiply on the O_lo side (one rounding of
+        // acc * inv) while the stored O rounds the float32 product again,
+        // and near a tie the two pick different halves.  OR-ing in a zero
+        // the compiler cannot prove (opq) stops that fold.  (An empty asm
+        // register barrier did too, but slowed the whole kernel by half.)
+        if constexpr (split) val = __uint_as_float(__float_as_uint(val) | opq);
+        const T hi = from_float<T>(val);
+        orow[e + x] = hi;
+        if constexpr (split) lrow[e + x] = from_float<T>(val - to_float<T>(hi));
+      }
     }
   }
   if (half == 0) lse[wt.lse_at(g, h, qi)] = (m_run + __log2f(l_run)) * kLn2;
@@ -334,13 +387,18 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(
 // Backward, step 1: D, dQ and the bias-table partials.  One head per
 // workgroup; the workgroup walks items (image, window, query chunk)
 // slice, slice + nslice, ... in a fixed order and accumulates dT in LDS.
-// Per item, a first sweep over the key tiles forms D_q = sum_k P dP in
-// fp32 (equal to <dO_q, O_q> for the unrounded O) and stores it for the
-// dK/dV kernel; the second sweep forms dS, dQ and the bias bins.
+// Per item, D_q = sum_k P dP = <dO_q, O_q> (O unrounded) is formed first
+// and stored for the dK/dV kernel: from the forward's O and its rounding
+// residual O_lo when the caller kept it (olo not null), else by a first
+// sweep over the key tiles in fp32.  The stored 16-bit O alone is not
+// enough: D's rounding error, alike for every key of a query, adds up over
+// the windows in the bias-table gradient.  The (second) sweep forms dS, dQ
+// and the bias bins.
 // ---------------------------------------------------------------------------
 template <typename T, int HD, bool NHWC, bool QUAD, bool RES>
 __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
+    const T* __restrict__ o, const T* __restrict__ olo,
     const T* __restrict__ dout, const float* __restrict__ lse, float* __restrict__ D,
     const float* __restrict__ table, T* __restrict__ dq, float* __restrict__ partial,
     Geo g, int nqc, int nslice, float scale_log2, float scale) {
@@ -397,10 +455,12 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
       dop[c] = qvalid ? load_op_global<T>(dout + wt.tok(g, qi) * g.C + hoff + 16 * c + 8 * half)
                       : zero_op<T>();
     }
-    // sweep 1: D_q.  The K, V tiles go HBM -> registers -> LDS; up to head
-    // dim 64 each tile's loads are issued while the previous tile computes
-    // (after the last tile of sweep 1 come the first tiles of sweep 2); at
-    // head dim 128 the registers this holds would halve the occupancy.
+    // D_q, then the sweep.  The K, V tiles go HBM -> registers -> LDS; up to
+    // head dim 64 each tile's loads are issued while the previous tile
+    // computes (after the last tile of the D sweep, or straight after these
+    // first loads when D comes from O, come the first tiles of the main
+    // sweep); at head dim 128 the registers this holds would halve the
+    // occupancy.
     constexpr bool kPrefetch = HD <= 64;
     TileRegs<T, HD> rk, rv;
     if constexpr (RES) {
@@ -430,7 +490,22 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
       tile_load(rv, v, g, wt, 0, n, hoff);
     }
     float dsum = 0.0f;
-    for (int k0 = 0; k0 < n; k0 += kTile) {
+    if (olo != nullptr) {
+      // D from the forward's output: the two halves of a lane pair hold
+      // alternate 8-element runs of the query's row, like dop
+      if (qvalid) {
+        const T* orow = o + wt.tok(g, qi) * g.C + hoff;
+        const T* lrow = olo + wt.tok(g, qi) * g.C + hoff;
+#pragma unroll
+        for (int c = 0; c < HD / 16; ++c) {
+          const auto ov = load_op_global<T>(orow + 16 * c + 8 * half);
+          const auto lv = load_op_global<T>(lrow + 16 * c + 8 * half);
+#pragma unroll
+          for (int x = 0; x < 8; ++x)
+            dsum += to_float<T>(dop[c][x]) * (to_float<T>(ov[x]) + to_float<T>(lv[x]));
+        }
+      }
+    } else for (int k0 = 0; k0 < n; k0 += kTile) {
       const int tix = RES ? k0 / kTile : 0;
       T* kt = kt0 + tix * kTE;
       T* vr = vr0 + tix * kTE;
@@ -470,7 +545,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
     const float Dq = halves_sum(dsum);
     if (qvalid && half == 0) D[lidx] = Dq;
 
-    // sweep 2: dS, dQ, bias bins
+    // main sweep: dS, dQ, bias bins
     const bool fold = (g.ww % 4 == 0) && (g.W % g.ww) % 4 == 0;   // uniform
     const int cq = qi - fast_div(qi, cols, win_rcols(g, j)) * cols;
     // runs: lanes of one 32-lane half holding consecutive queries of one
@@ -935,17 +1010,25 @@ int bwd_nslice(const Geo& g, int dt) {
 
 template <typename T, int HD, bool NHWC>
 static hipError_t fwd_impl(const Geo& g, const void* q, const void* k, const void* v,
-                           const float* table, void* o, float* lse, hipStream_t st) {
+                           const float* table, void* o, void* olo, float* lse, hipStream_t st) {
   const int nqc = num_chunks(g);
   const int grid = grid8(g.B * g.nwin * g.heads * nqc);
   const float sl2 = kLog2e / sqrtf((float)HD);
   const size_t lds = fwd_lds<T, HD>(g);
-  if (quad_layout(g))
-    hipLaunchKernelGGL((fwd_kernel<T, HD, NHWC, true>), dim3(grid), dim3(kThreads), lds, st,
-                       (const T*)q, (const T*)k, (const T*)v, table, (T*)o, lse, g, nqc, sl2);
-  else
-    hipLaunchKernelGGL((fwd_kernel<T, HD, NHWC, false>), dim3(grid), dim3(kThreads), lds, st,
-                       (const T*)q, (const T*)k, (const T*)v, table, (T*)o, lse, g, nqc, sl2);
+#define TERRA_LAUNCH_FWD(QD, SP)                                                                  \
+  hipLaunchKernelGGL((fwd_kernel<T, HD, NHWC, QD, SP>), dim3(grid), dim3(kThreads), lds, st,       \
+                     (const T*)q, (const T*)k, (const T*)v, table, (T*)o, (T*)olo, lse, g, nqc, sl2)
+  const bool quad = quad_layout(g);
+  if constexpr (sizeof(T) == 2) {
+    if (olo != nullptr) {
+      if (quad) TERRA_LAUNCH_FWD(true, true);
+      else TERRA_LAUNCH_FWD(false, true);
+      return hipGetLastError();
+    }
+  }
+  if (quad) TERRA_LAUNCH_FWD(true, false);
+  else TERRA_LAUNCH_FWD(false, false);
+#undef TERRA_LAUNCH_FWD
   return hipGetLastError();
 }
 
@@ -958,13 +1041,12 @@ size_t bwd_workspace(const Geo& g, int dt) {
 
 template <typename T, int HD, bool NHWC>
 static hipError_t bwd_impl(const Geo& g, const void* q, const void* k, const void* v,
-                           const void* o, const void* dout, const float* lse,
+                           const void* o, const void* olo, const void* dout, const float* lse,
                            const float* table, void* dq, void* dk, void* dv, float* dtab,
                            void* ws, hipStream_t st) {
   const size_t dbytes = (size_t)g.B * g.heads * g.HW * sizeof(float);
   float* D = reinterpret_cast<float*>(ws);
   float* partial = reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + ((dbytes + 255) / 256) * 256);
-  (void)o;  // D is recomputed in-window from P and dP (see the dQ kernel)
   hipError_t e;
   const int nqc = num_chunks(g);
   const float sl2 = kLog2e / sqrtf((float)HD);
@@ -992,8 +1074,8 @@ static hipError_t bwd_impl(const Geo& g, const void* q, const void* k, const voi
   if (nslice > nmax) nslice = nmax;
 #define TERRA_LAUNCH_DQ(QD, RS)                                                                 \
   hipLaunchKernelGGL((bwd_dq_kernel<T, HD, NHWC, QD, RS>), dim3(g.heads * nslice), dim3(kThreads),  \
-                     lds_dq, st, (const T*)q, (const T*)k, (const T*)v, (const T*)dout, lse, D, table, \
-                     (T*)dq, partial, g, nqc, nslice, sl2, scale)
+                     lds_dq, st, (const T*)q, (const T*)k, (const T*)v, (const T*)o, (const T*)olo,  \
+                     (const T*)dout, lse, D, table, (T*)dq, partial, g, nqc, nslice, sl2, scale)
   if constexpr (sizeof(T) == 2 && HD <= 64) {
     if (quad && res) TERRA_LAUNCH_DQ(true, true);
     else if (quad) TERRA_LAUNCH_DQ(true, false);
@@ -1047,56 +1129,74 @@ size_t attn_max_lds(const Geo& g, int dt) {
 
 template <typename T, bool NHWC>
 static hipError_t fwd_generic(const Geo& g, const void* q, const void* k, const void* v,
-                              const float* table, void* o, float* lse, hipStream_t st) {
+                              const float* table, void* o, void* olo, float* lse, hipStream_t st) {
   switch (g.hd) {
-    case 32: return fwd_impl<T, 32, NHWC>(g, q, k, v, table, o, lse, st);
-    case 64: return fwd_impl<T, 64, NHWC>(g, q, k, v, table, o, lse, st);
-    default: return fwd_impl<T, 128, NHWC>(g, q, k, v, table, o, lse, st);
+    case 32: return fwd_impl<T, 32, NHWC>(g, q, k, v, table, o, olo, lse, st);
+    case 64: return fwd_impl<T, 64, NHWC>(g, q, k, v, table, o, olo, lse, st);
+    default: return fwd_impl<T, 128, NHWC>(g, q, k, v, table, o, olo, lse, st);
   }
 }
 
 template <typename T, bool NHWC>
 static hipError_t bwd_generic(const Geo& g, const void* q, const void* k, const void* v,
-                              const void* o, const void* dout, const float* lse, const float* table,
-                              void* dq, void* dk, void* dv, float* dtab, void* ws, hipStream_t st) {
+                              const void* o, const void* olo, const void* dout, const float* lse,
+                              const float* table, void* dq, void* dk, void* dv, float* dtab, void* ws,
+                              hipStream_t st) {
   switch (g.hd) {
-    case 32: return bwd_impl<T, 32, NHWC>(g, q, k, v, o, dout, lse, table, dq, dk, dv, dtab, ws, st);
-    case 64: return bwd_impl<T, 64, NHWC>(g, q, k, v, o, dout, lse, table, dq, dk, dv, dtab, ws, st);
-    default: return bwd_impl<T, 128, NHWC>(g, q, k, v, o, dout, lse, table, dq, dk, dv, dtab, ws, st);
+    case 32: return bwd_impl<T, 32, NHWC>(g, q, k, v, o, olo, dout, lse, table, dq, dk, dv, dtab, ws, st);
+    case 64: return bwd_impl<T, 64, NHWC>(g, q, k, v, o, olo, dout, lse, table, dq, dk, dv, dtab, ws, st);
+    default: return bwd_impl<T, 128, NHWC>(g, q, k, v, o, olo, dout, lse, table, dq, dk, dv, dtab, ws, st);
   }
 }
 
 template <bool NHWC>
 static hipError_t fwd_dispatch(const Geo& g, int dt, const void* q, const void* k, const void* v,
-                               const float* table, void* o, float* lse, hipStream_t st) {
-  if (dt == kF32) return fwd_generic<float, NHWC>(g, q, k, v, table, o, lse, st);
-  if (dt == kBF16) return fwd_generic<__bf16, NHWC>(g, q, k, v, table, o, lse, st);
-  return fwd_generic<_Float16, NHWC>(g, q, k, v, table, o, lse, st);
+                               const float* table, void* o, void* olo, float* lse, hipStream_t st) {
+  if (dt == kF32) return fwd_generic<float, NHWC>(g, q, k, v, table, o, nullptr, lse, st);
+  if (dt == kBF16) return fwd_generic<__bf16, NHWC>(g, q, k, v, table, o, olo, lse, st);
+  return fwd_generic<_Float16, NHWC>(g, q, k, v, table, o, olo, lse, st);
 }
 
 template <bool NHWC>
 static hipError_t bwd_dispatch(const Geo& g, int dt, const void* q, const void* k, const void* v,
-                               const void* o, const void* dout, const float* lse, const float* table,
-                               void* dq, void* dk, void* dv, float* dtab, void* ws, hipStream_t st) {
-  if (dt == kF32) return bwd_generic<float, NHWC>(g, q, k, v, o, dout, lse, table, dq, dk, dv, dtab, ws, st);
-  if (dt == kBF16) return bwd_generic<__bf16, NHWC>(g, q, k, v, o, dout, lse, table, dq, dk, dv, dtab, ws, st);
-  return bwd_generic<_Float16, NHWC>(g, q, k, v, o, dout, lse, table, dq, dk, dv, dtab, ws, st);
+                               const void* o, const void* olo, const void* dout, const float* lse,
+                               const float* table, void* dq, void* dk, void* dv, float* dtab, void* ws,
+                               hipStream_t st) {
+  if (dt == kF32)
+    return bwd_generic<float, NHWC>(g, q, k, v, o, nullptr, dout, lse, table, dq, dk, dv, dtab, ws, st);
+  if (dt == kBF16)
+    return bwd_generic<__bf16, NHWC>(g, q, k, v, o, olo, dout, lse, table, dq, dk, dv, dtab, ws, st);
+  return bwd_generic<_Float16, NHWC>(g, q, k, v, o, olo, dout, lse, table, dq, dk, dv, dtab, ws, st);
+}
+
+// True when the forward writes the rounding residual O_lo and the backward
+// takes D from it: 16-bit types on the generic kernels with windows of more
+// than 256 tokens.  Smaller windows keep the D sweep, which is cheaper there
+// than the split P V product plus the O_lo traffic (measured: 144-token
+// windows, hd 32: forward +0.017 ms, backward -0.011 ms; 64-token windows,
+// hd 128: forward +0.10 ms, backward +0.10 ms; 576-token windows, hd 64:
+// forward +0.26 ms, backward -0.81 ms).
+bool attn_uses_olo(const Geo& g, int dt) {
+  return dt != kF32 && !win_fwd_ok(g, dt == kBF16) && !win_bwd_ok(g, dt == kBF16) && g.wh * g.ww > 256;
 }
 
 // dt: element type code.  nhwc: q, k, v, o (and dout, dq, dk, dv) are
 // B x H x W x C read and written in place (the token route fused into the
 // kernels), LSE in the same token order; otherwise they are window-major.
+// olo (nullable) is written and read only where attn_uses_olo holds.
 hipError_t launch_attn_fwd(const Geo& g, int dt, bool nhwc, const void* q, const void* k,
-                           const void* v, const float* table, void* o, float* lse, hipStream_t st) {
+                           const void* v, const float* table, void* o, void* olo, float* lse,
+                           hipStream_t st) {
   if (win_fwd_ok(g, dt == kBF16)) return launch_win_fwd(g, nhwc, q, k, v, table, o, lse, st);
-  return nhwc ? fwd_dispatch<true>(g, dt, q, k, v, table, o, lse, st)
-              : fwd_dispatch<false>(g, dt, q, k, v, table, o, lse, st);
+  if (!attn_uses_olo(g, dt)) olo = nullptr;
+  return nhwc ? fwd_dispatch<true>(g, dt, q, k, v, table, o, olo, lse, st)
+              : fwd_dispatch<false>(g, dt, q, k, v, table, o, olo, lse, st);
 }
 
 hipError_t launch_attn_bwd(const Geo& g, int dt, bool nhwc, const void* q, const void* k,
-                           const void* v, const void* o, const void* dout, const float* lse,
-                           const float* table, void* dq, void* dk, void* dv, float* dtab, void* ws,
-                           hipStream_t st) {
+                           const void* v, const void* o, const void* olo, const void* dout,
+                           const float* lse, const float* table, void* dq, void* dk, void* dv,
+                           float* dtab, void* ws, hipStream_t st) {
   if (win_bwd_ok(g, dt == kBF16)) {
     const int nslice = win_bwd_nslice(g);
     float* partial = reinterpret_cast<float*>(ws);
@@ -1107,8 +1207,9 @@ hipError_t launch_attn_bwd(const Geo& g, int dt, bool nhwc, const void* q, const
                        st, partial, dtab, g, nslice);
     return hipGetLastError();
   }
-  return nhwc ? bwd_dispatch<true>(g, dt, q, k, v, o, dout, lse, table, dq, dk, dv, dtab, ws, st)
-              : bwd_dispatch<false>(g, dt, q, k, v, o, dout, lse, table, dq, dk, dv, dtab, ws, st);
+  if (!attn_uses_olo(g, dt)) olo = nullptr;
+  return nhwc ? bwd_dispatch<true>(g, dt, q, k, v, o, olo, dout, lse, table, dq, dk, dv, dtab, ws, st)
+              : bwd_dispatch<false>(g, dt, q, k, v, o, olo, dout, lse, table, dq, dk, dv, dtab, ws, st);
 }
 
 }  // namespace terra

@@ -600,10 +600,11 @@ static Mat mat(const void* p, int ld, int rows) {
 constexpr float kLnEps = 1e-5f;
 
 hipError_t launch_attn_fwd(const Geo& g, int dt, bool nhwc, const void* q, const void* k, const void* v,
-                           const float* table, void* o, float* lse, hipStream_t st);
+                           const float* table, void* o, void* olo, float* lse, hipStream_t st);
 hipError_t launch_attn_bwd(const Geo& g, int dt, bool nhwc, const void* q, const void* k, const void* v,
-                           const void* o, const void* dout, const float* lse, const float* table, void* dq,
-                           void* dk, void* dv, float* dtab, void* ws, hipStream_t st);
+                           const void* o, const void* olo, const void* dout, const float* lse,
+                           const float* table, void* dq, void* dk, void* dv, float* dtab, void* ws,
+                           hipStream_t st);
 size_t bwd_workspace(const Geo& g, int dt);
 
 static hipError_t ln_stats(const void* x, float* mu, float* rs, int T, int C, hipStream_t st) {
@@ -666,7 +667,7 @@ hipError_t launch_block_fwd(const Geo& g, const void* x, const BlockParams& p, c
   TERRA_TRY((gemm<true, true, EPI_LN_QKV>(mat(x, C, T), mat(wq, C, 3 * C), ep,
                                                                     T, 3 * C, C, 1, st)));
   // windowed attention with the route fused in
-  TERRA_TRY(launch_attn_fwd(g, 1, true, s.q, s.k, s.v, table, s.o, s.lse, st));
+  TERRA_TRY(launch_attn_fwd(g, 1, true, s.q, s.k, s.v, table, s.o, nullptr, s.lse, st));
   // x1 = x + o W_p^T + b_p
   ep = EpiArgs{};
   ep.out[0] = (bf16*)s.x1; ep.split = C; ep.aux = (const bf16*)x; ep.bias = p.b_proj;
@@ -836,8 +837,8 @@ hipError_t launch_block_bwd(const Geo& g, const void* dx2, const void* x, const 
   ep.out[0] = dO; ep.split = C;
   TERRA_TRY((gemm<true, false, EPI_BF16>(mat(dx1, C, T), mat(p.w_proj, C, C), ep, T, C, C, 1, st)));
   // attention backward (route fused in)
-  TERRA_TRY(launch_attn_bwd(g, 1, true, s.q, s.k, s.v, s.o, dO, s.lse, table, dqkv[0], dqkv[1], dqkv[2], dtable,
-                            ws + w.attn, st));
+  TERRA_TRY(launch_attn_bwd(g, 1, true, s.q, s.k, s.v, s.o, nullptr, dO, s.lse, table, dqkv[0], dqkv[1],
+                            dqkv[2], dtable, ws + w.attn, st));
   // qkv = LN1(x) Wqkv^T + bqkv, one third (Q, K, V) at a time: rows
   // [iC, (i+1)C) of dWqkv = dY_i^T LN1(x), of dbqkv = colsum(dY_i), and
   // dln1 = sum_i dY_i Wqkv[iC:(i+1)C]

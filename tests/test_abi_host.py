@@ -90,29 +90,55 @@ def test_device_calls_reject_bad_arguments_before_launch():
     null = ctypes.c_void_p(0)
     s = ctypes.c_void_p(0)
     assert L.terra_window_route(ctypes.byref(g), 7, fake, fake, null, null, s) == 1   # bad dtype
-    assert L.terra_winattn_fwd(ctypes.byref(g), 3, *([fake] * 6), s) == 1     # bad dtype
+    assert L.terra_winattn_fwd(ctypes.byref(g), 3, *([fake] * 7), s) == 1     # bad dtype
     assert L.terra_winattn_bwd_workspace_bytes(ctypes.byref(g), 2) > 0       # fp16
     assert L.terra_window_route(ctypes.byref(g), 1, null, fake, null, null, s) == 1   # NULL
     assert L.terra_window_route(ctypes.byref(g), 1, fake, fake, fake, fake, s) == 1   # in place
-    assert L.terra_winattn_fwd(ctypes.byref(g), 1, fake, fake, null, fake, fake, fake, s) == 1
-    assert L.terra_winattn_fwd(None, 1, fake, fake, fake, fake, fake, fake, s) == 1
+    assert L.terra_winattn_fwd(ctypes.byref(g), 1, fake, fake, null, fake, fake, fake, fake, s) == 1
+    assert L.terra_winattn_fwd(None, 1, *([fake] * 7), s) == 1
+    # o_lo is optional: a NULL there is not an error (the NULL q below is)
+    assert L.terra_winattn_fwd(ctypes.byref(g), 1, null, fake, fake, fake, fake, null, fake, s) == 1
     need = L.terra_winattn_bwd_workspace_bytes(ctypes.byref(g), 1)
     assert need > 0
-    args = [fake] * 11
+    args = [fake] * 12
     assert L.terra_winattn_bwd(ctypes.byref(g), 1, *args, fake, ctypes.c_size_t(need - 4), s) == 3
     assert L.terra_winattn_bwd(ctypes.byref(g), 1, *args, null, ctypes.c_size_t(need), s) == 3
     # the fused (NHWC) entry points share the checks
-    assert L.terra_winattn_fwd_nhwc(ctypes.byref(g), 1, fake, fake, null, fake, fake, fake, s) == 1
-    assert L.terra_winattn_fwd_nhwc(ctypes.byref(g), 5, *([fake] * 6), s) == 1
+    assert L.terra_winattn_fwd_nhwc(ctypes.byref(g), 1, fake, fake, null, fake, fake, fake, fake, s) == 1
+    assert L.terra_winattn_fwd_nhwc(ctypes.byref(g), 5, *([fake] * 7), s) == 1
     assert L.terra_winattn_bwd_nhwc(ctypes.byref(g), 1, *args, fake, ctypes.c_size_t(need - 4), s) == 3
     assert L.terra_winattn_bwd_nhwc(ctypes.byref(g), 1, null, *args[1:], fake, ctypes.c_size_t(need),
                                     s) == 1
     g2 = P.terra_geom.make(1, 16, 32, 48, 3, 16, 8, 8, 4, 4, 1)
-    assert L.terra_winattn_fwd(ctypes.byref(g2), 1, *([fake] * 6), s) == 2
-    assert L.terra_winattn_fwd_nhwc(ctypes.byref(g2), 1, *([fake] * 6), s) == 2
+    assert L.terra_winattn_fwd(ctypes.byref(g2), 1, *([fake] * 7), s) == 2
+    assert L.terra_winattn_fwd_nhwc(ctypes.byref(g2), 1, *([fake] * 7), s) == 2
     assert L.terra_winattn_bwd_workspace_bytes(ctypes.byref(g2), 1) == 0
     for code in range(5):
         assert L.terra_status_string(code)
+
+
+def test_o_lo_is_used_for_16_bit_windows_above_256_tokens():
+    # 16-bit windows of more than 256 tokens keep O's rounding residual;
+    # smaller windows keep the D sweep (and bf16 windows of at most 128
+    # tokens take the window-resident kernels, which form D in registers);
+    # float32 never keeps it
+    L = P.lib()
+    expect = {"c1_f32_16x32_w8": 0, "c2_bf16_128x256_w8": 0, "c3_bf16_85x180_w12": 0,
+              "c4_bf16_128x1080_w8x16": 0, "c5_bf16_256x540_w24": 1,
+              "p1_f16_256x540_hd128_w8": 0, "p2_f16_256x540_hd128_w32": 1}
+    for name, want in expect.items():
+        cfg = ts.ALL[name]
+        code = {"f32": 0, "bf16": 1, "f16": 2}[cfg.dtype]
+        assert L.terra_winattn_uses_o_lo(ctypes.byref(P._geom(cfg)), code) == want, name
+        assert P.terra_winattn_uses_o_lo(cfg, code) == bool(want)
+    g = P.terra_geom.make(1, 34, 32, 64, 2, 32, 17, 16, 8, 8, 1)     # 272-token windows
+    assert L.terra_winattn_uses_o_lo(ctypes.byref(g), 1) == 1          # bfloat16
+    assert L.terra_winattn_uses_o_lo(ctypes.byref(g), 2) == 1          # float16
+    assert L.terra_winattn_uses_o_lo(ctypes.byref(g), 0) == 0          # float32
+    g = P.terra_geom.make(1, 32, 32, 64, 2, 32, 16, 16, 8, 8, 1)     # 256-token windows
+    assert L.terra_winattn_uses_o_lo(ctypes.byref(g), 2) == 0
+    assert L.terra_winattn_uses_o_lo(ctypes.byref(g), 7) == -1         # bad dtype
+    assert L.terra_winattn_uses_o_lo(None, 1) == -1
 
 
 @pytest.mark.parametrize("name", ts.ORDER)

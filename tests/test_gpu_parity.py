@@ -44,7 +44,7 @@ def _gpu():
 
 
 def _tdtype(cfg):
-    return torch.float32 if cfg.dtype == "f32" else torch.bfloat16
+    return {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[cfg.dtype]
 
 
 def _dev(x, cfg):
@@ -56,7 +56,7 @@ def _host(t):
 
 
 def _bits(t):
-    if t.dtype == torch.bfloat16:
+    if t.dtype in (torch.bfloat16, torch.float16):
         return t.view(torch.int16).cpu().numpy()
     return t.view(torch.int32).cpu().numpy()
 
@@ -132,13 +132,14 @@ def test_route_f32_and_bf16_on_one_geometry():
 
 
 # ------------------------------------------------------------------ attention, small configs
-def _run_gpu(cfg, inp):
+def _run_gpu(cfg, inp, with_lo=False):
     q, k, v, do = (P.terra_window_route(_dev(inp[n], cfg), cfg) for n in ("q", "k", "v", "dout"))
     table = torch.from_numpy(inp["table"]).to("cuda")
-    o, lse = P.terra_winattn_fwd(q, k, v, table, cfg)
-    dq, dk, dv, dt = P.terra_winattn_bwd(q, k, v, o, do, lse, table, cfg)
+    lo = torch.full_like(q, 7.0) if with_lo else None
+    o, lse = P.terra_winattn_fwd(q, k, v, table, cfg, o_lo=lo)
+    dq, dk, dv, dt = P.terra_winattn_bwd(q, k, v, o, do, lse, table, cfg, o_lo=lo)
     torch.cuda.synchronize()
-    return dict(o=o, lse=lse, dq=dq, dk=dk, dv=dv, dt=dt)
+    return dict(o=o, lse=lse, dq=dq, dk=dk, dv=dv, dt=dt, lo=lo)
 
 
 @pytest.mark.parametrize("name", SMALL)
@@ -208,6 +209,49 @@ def test_attention_edge_cases(label, cfg):
     for nm, a, b in (("O", got["o"], o), ("LSE", got["lse"], lse), ("dQ", got["dq"], dq),
                      ("dK", got["dk"], dk), ("dV", got["dv"], dv), ("dT", got["dt"], dt)):
         _assert_close(nm, _host(a), b, cfg)
+
+
+LO_CASES = [
+    # 24 x 24 windows with both wraps masked, two images, ragged both ways
+    ("w24_both_masks", ts.small_config("l1", "bf16", 2, 30, 50, 2, 64, 24, 24, 12, 12, 3)),
+    # 272-token windows (17 x 16), ragged, one query chunk past two full ones
+    ("w17x16_ragged", ts.small_config("l2", "bf16", 1, 40, 37, 2, 64, 17, 16, 8, 8, 1)),
+    # float16, head_dim 32, 24 x 12 windows
+    ("f16_hd32_w24x12", ts.small_config("l3", "f16", 1, 30, 40, 2, 32, 24, 12, 12, 6)),
+    # bfloat16, head_dim 128, 20 x 16 windows
+    ("bf16_hd128_w20x16", ts.small_config("l4", "bf16", 1, 24, 40, 2, 128, 20, 16, 10, 8)),
+    # float16, head_dim 128, 32 x 32 windows (the large model's window)
+    ("f16_hd128_w32", ts.small_config("l5", "f16", 1, 40, 70, 2, 128, 32, 32, 16, 16)),
+]
+
+
+@pytest.mark.parametrize("label,cfg", LO_CASES, ids=[e[0] for e in LO_CASES])
+def test_d_from_the_forwards_rounding_residual(label, cfg):
+    # Shapes on the general kernels can keep O's rounding residual: the
+    # forward then forms O with P split into two 16-bit parts and writes
+    # O_lo, and the backward takes D = <dO, O + O_lo> instead of sweeping the
+    # keys.  O + O_lo must be the exact output to far better than one
+    # rounding (the split leaves about 2^-17 of |O|), O and LSE must meet the
+    # bars, and so must every gradient, the bias-table one included.
+    g = Geometry(**cfg.geom_kwargs())
+    _say("o_lo %s" % label)
+    assert P.terra_winattn_uses_o_lo(cfg, cfg.dtype)
+    inp = ts.make_inputs(cfg, seed=5)
+    got = _run_gpu(cfg, inp, with_lo=True)
+    q, k, v, do = (o_route(inp[n], g) for n in ("q", "k", "v", "dout"))
+    o, lse = attn_fwd(q, k, v, inp["table"], g)
+    dq, dk, dv, dt = attn_bwd(q, k, v, do, inp["table"], g)
+    full = _host(got["o"]) + _host(got["lo"])
+    err, err_hi = np.abs(full - o).max(), np.abs(_host(got["o"]) - o).max()
+    _say("  O + O_lo max abs err %.3g (O alone %.3g)" % (err, err_hi))
+    assert err <= 5e-5 * max(1.0, np.abs(o).max()), "O + O_lo err %.3g (O alone %.3g)" % (err, err_hi)
+    assert err < err_hi / 16, "O + O_lo err %.3g (O alone %.3g)" % (err, err_hi)
+    for nm, a, b in (("O", got["o"], o), ("LSE", got["lse"], lse), ("dQ", got["dq"], dq),
+                     ("dK", got["dk"], dk), ("dV", got["dv"], dv), ("dT", got["dt"], dt)):
+        _assert_close(nm, _host(a), b, cfg)
+    # the same backward without O_lo (the key sweep) agrees to far below the bars
+    base = _run_gpu(cfg, inp)
+    assert np.abs(_host(base["dt"]) - _host(got["dt"])).max() < 1e-3
 
 
 @pytest.mark.parametrize("name", ["c2_bf16_128x256_w8", "c4_small_bf16_24x80_w8x16"])
@@ -339,24 +383,29 @@ def test_c5_attention_sampled_windows():
     # window class: 576, 384, 288 and 192 tokens, the seams, and runs of
     # neighbouring windows that the persistent kernels walk in sequence),
     # plus the whole bias-table gradient from stored oracle values.
+    # Both ways of forming D: the sweep over the keys, and the forward's
+    # O + O_lo (the timed path).
     cfg = ts.CONFIGS["c5_bf16_256x540_w24"]
     g = Geometry(**cfg.geom_kwargs())
     _say("full-size attention %s" % cfg.name)
     inp = ts.make_inputs(cfg)
-    got = _run_gpu(cfg, inp)
+    runs = {"sweep": _run_gpu(cfg, inp), "o_lo": _run_gpu(cfg, inp, with_lo=True)}
     sel = sorted(set(_sample_windows(cfg, g, extra=6)) | {40, 41, 42, 43, 44, 45, 120, 121})
     q, k, v, do = (o_route(inp[n], g) for n in ("q", "k", "v", "dout"))
     fw = attn_fwd_windows(q, k, v, inp["table"], g, sel)
     bw = attn_bwd_windows(q, k, v, do, inp["table"], g, sel)
     slots = {w: (s, n) for w, s, n in window_slots(g)}
-    for w in sel:
-        s, n = slots[w]
-        _assert_close("O[w%d]" % w, _host(got["o"][:, s:s + n]), fw[w][0], cfg)
-        _assert_close("LSE[w%d]" % w, _host(got["lse"][:, :, s:s + n]), fw[w][1], cfg)
-        _assert_close("dQ[w%d]" % w, _host(got["dq"][:, s:s + n]), bw[w][0], cfg)
-        _assert_close("dK[w%d]" % w, _host(got["dk"][:, s:s + n]), bw[w][1], cfg)
-        _assert_close("dV[w%d]" % w, _host(got["dv"][:, s:s + n]), bw[w][2], cfg)
     gold = np.load(os.path.join(GOLDEN, "dtable_%s.npy" % cfg.name))
-    _assert_close("dT", _host(got["dt"]), gold, cfg)
-    sums = _host(got["dt"]).sum(axis=(0, 1))
-    assert np.abs(sums).max() < 1e-2
+    for how, got in runs.items():
+        _say("  D from the %s" % how)
+        for w in sel:
+            s, n = slots[w]
+            _assert_close("O[w%d]" % w, _host(got["o"][:, s:s + n]), fw[w][0], cfg)
+            _assert_close("LSE[w%d]" % w, _host(got["lse"][:, :, s:s + n]), fw[w][1], cfg)
+            _assert_close("dQ[w%d]" % w, _host(got["dq"][:, s:s + n]), bw[w][0], cfg)
+            _assert_close("dK[w%d]" % w, _host(got["dk"][:, s:s + n]), bw[w][1], cfg)
+            _assert_close("dV[w%d]" % w, _host(got["dv"][:, s:s + n]), bw[w][2], cfg)
+        _assert_close("dT", _host(got["dt"]), gold, cfg)
+        _say("  dT max abs err %.3g" % np.abs(_host(got["dt"]) - gold).max())
+        sums = _host(got["dt"]).sum(axis=(0, 1))
+        assert np.abs(sums).max() < 1e-2

@@ -98,9 +98,11 @@ def test_variant_against_oracle(cfg):
     for nm, a, b in (("O", go, o), ("LSE", glse, lse), ("dQ", gq, dq), ("dK", gk, dk), ("dV", gv, dv),
                      ("dT", gt, dt)):
         _assert_close(nm, _host(a), b, cfg)
-    # fused entry points
-    fo, flse = P.terra_winattn_fwd_nhwc(x["q"], x["k"], x["v"], table, cfg)
-    fq, fk, fv, ft = P.terra_winattn_bwd_nhwc(x["q"], x["k"], x["v"], fo, x["dout"], flse, table, cfg)
+    # fused entry points, keeping O's rounding residual where the shape uses it
+    lo = torch.empty_like(x["q"]) if P.terra_winattn_uses_o_lo(cfg, cfg.dtype) else None
+    fo, flse = P.terra_winattn_fwd_nhwc(x["q"], x["k"], x["v"], table, cfg, o_lo=lo)
+    fq, fk, fv, ft = P.terra_winattn_bwd_nhwc(x["q"], x["k"], x["v"], fo, x["dout"], flse, table, cfg,
+                                              o_lo=lo)
     torch.cuda.synchronize()
     for nm, a, b in (("fused O", fo, o_unroute(o, g)), ("fused LSE", flse, _lse_to_nhwc(lse, g)),
                      ("fused dQ", fq, o_unroute(dq, g)), ("fused dK", fk, o_unroute(dk, g)),
@@ -125,8 +127,11 @@ def test_variant_full_size_sampled(name):
     inp = ts.make_inputs(cfg)
     x = {n: _dev(inp[n], cfg) for n in ("q", "k", "v", "dout")}
     table = torch.from_numpy(inp["table"]).to("cuda")
-    fo, flse = P.terra_winattn_fwd_nhwc(x["q"], x["k"], x["v"], table, cfg)
-    fq, fk, fv, ft = P.terra_winattn_bwd_nhwc(x["q"], x["k"], x["v"], fo, x["dout"], flse, table, cfg)
+    # the timed path: O's rounding residual kept where the shape uses it
+    lo = torch.empty_like(x["q"]) if P.terra_winattn_uses_o_lo(cfg, cfg.dtype) else None
+    fo, flse = P.terra_winattn_fwd_nhwc(x["q"], x["k"], x["v"], table, cfg, o_lo=lo)
+    fq, fk, fv, ft = P.terra_winattn_bwd_nhwc(x["q"], x["k"], x["v"], fo, x["dout"], flse, table, cfg,
+                                              o_lo=lo)
     # window-major views of the fused results (the route is a bit copy)
     got = {n: P.terra_window_route(t, cfg) for n, t in (("o", fo), ("dq", fq), ("dk", fk), ("dv", fv))}
     torch.cuda.synchronize()

@@ -36,15 +36,16 @@ def _gpu():
     torch.cuda.synchronize()
 
 
-def _both(cfg):
+def _both(cfg, with_lo=False):
     inp = ts.make_inputs(cfg, seed=7)
     x = {n: torch.from_numpy(inp[n]).to("cuda").to(torch.bfloat16) for n in ("q", "k", "v", "dout")}
     table = torch.from_numpy(inp["table"]).to("cuda")
-    o, lse = P.terra_winattn_fwd_nhwc(x["q"], x["k"], x["v"], table, cfg)
-    ref = P.terra_winattn_bwd_nhwc(x["q"], x["k"], x["v"], o, x["dout"], lse, table, cfg)
+    lo = torch.empty_like(x["q"]) if with_lo else None
+    o, lse = P.terra_winattn_fwd_nhwc(x["q"], x["k"], x["v"], table, cfg, o_lo=lo)
+    ref = P.terra_winattn_bwd_nhwc(x["q"], x["k"], x["v"], o, x["dout"], lse, table, cfg, o_lo=lo)
     out = (torch.full_like(x["q"], 7.0), torch.full_like(x["q"], 7.0), torch.full_like(x["q"], 7.0),
            torch.full_like(table, 7.0))
-    got = P.terra_winattn_bwd_nhwc_noalloc(x["q"], x["k"], x["v"], o, x["dout"], lse, table, cfg, out)
+    got = P.terra_winattn_bwd_nhwc_noalloc(x["q"], x["k"], x["v"], o, x["dout"], lse, table, cfg, out, o_lo=lo)
     torch.cuda.synchronize()
     for name, a, b in zip(("dq", "dk", "dv", "dtable"), got, ref):
         ai = a.view(torch.int16 if a.dtype == torch.bfloat16 else torch.int32)
@@ -59,6 +60,8 @@ def test_noalloc_equals_workspace_backward_twice():
     assert P.terra_winattn_bwd_workspace_bytes(big, "bf16") <= P.TERRA_SCRATCH_BYTES
     _say("noalloc: generic-path geometry")
     _both(big)
+    _say("noalloc: generic-path geometry, D from the forward's O and O_lo")
+    _both(big, with_lo=True)
     _say("noalloc: smaller window-path geometry")
     _both(small)
 
@@ -72,7 +75,7 @@ def test_noalloc_refuses_a_workspace_above_the_array():
     import ctypes
     gg = P.terra_geom.make(**cfg.geom_kwargs())
     vp = lambda x: ctypes.c_void_p(x.data_ptr())  # noqa: E731
-    st = L.terra_winattn_bwd_nhwc_noalloc(ctypes.byref(gg), P.TERRA_BF16, vp(t), vp(t), vp(t), vp(t), vp(t),
-                                          vp(f), vp(f), vp(t), vp(t), vp(t), vp(f), None)
+    st = L.terra_winattn_bwd_nhwc_noalloc(ctypes.byref(gg), P.TERRA_BF16, vp(t), vp(t), vp(t), vp(t), None,
+                                          vp(t), vp(f), vp(f), vp(t), vp(t), vp(t), vp(f), None)
     assert st == 2
     assert b"scratch" in L.terra_last_error()
