@@ -777,9 +777,13 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
 // Backward, step 2: dK and dV.  Grid: B * nwin * heads * nkc (key chunks of
 // 128; a wave owns 32 keys and walks the window's queries in LDS tiles).
 // 16-bit types ask for two resident workgroups per CU: at head_dim 128 the
-// compiler otherwise takes 280 registers (one wave per SIMD); capped at 256
-// it spills 13 words and runs 10 % faster.  Three per CU (168 registers)
-// spill inside the loop at head_dim 64 and run 25 % slower.
+// compiler otherwise takes 280 registers (one wave per SIMD).  Capped at 256
+// (two waves per SIMD) it keeps the matrix loop free of spills and spills 5
+// (window-major) or 8 (NHWC) words of staging addresses, reloaded once per
+// 64-query tile; the loop's lean form below took that down from 17 and 21
+// words (backward -2 % at 1024-token windows, -6 % at 64-token ones).
+// Three workgroups per CU (168 registers) spill inside the loop at
+// head_dim 64 and run 25 % slower.
 // ---------------------------------------------------------------------------
 template <typename T, int HD, bool NHWC, bool QUAD>
 __global__ __launch_bounds__(kThreads, sizeof(T) == 2 ? 2 : 1) void bwd_dkdv_kernel(
@@ -823,6 +827,7 @@ __global__ __launch_bounds__(kThreads, sizeof(T) == 2 ? 2 : 1) void bwd_dkdv_ker
   const int kinf = token_info(g, i, j, cols, kvalid ? ki : 0, n);
   const int klab = kvalid ? (kinf >> 24) : 0xFE;
   const int kfwd = (g.wh - 1) * g.bstride + (g.ww - 1) - (kinf & 0xFFFFFF);
+  const float inv_sl2 = 1.0f / scale_log2;
 
   typename Operand<T>::type kop[HD / 16], vop[HD / 16];
 #pragma unroll
@@ -865,10 +870,17 @@ __global__ __launch_bounds__(kThreads, sizeof(T) == 2 ? 2 : 1) void bwd_dkdv_ker
       tile_load(rd, dout, g, wt, t0 + kTile, n, hoff);
     }
     if (!wactive) continue;
-#pragma unroll
+    // head_dim 128: one 32-query block at a time (unrolled, the two blocks'
+    // operands overlap and the 256 registers spill)
+#pragma unroll(HD == 128 ? 1 : kTile / 32)
     for (int qb = 0; qb < kTile / 32; ++qb) {
       // registers 4g..4g+3 hold queries 32qb + 8g + 4*half + 0..3: their
-      // log-sum-exp and D are four consecutive LDS words
+      // log-sum-exp and D are four consecutive LDS words.
+      // At head_dim 128 the score accumulator starts at bias - LSE (in
+      // score units), as the dP one starts at -D, so that no per-query value
+      // stays in registers across the products, and dS replaces dP in place
+      // (-20 % spill there; at head_dim 64 the plain form is 1.5 % faster).
+      constexpr bool kLean = HD == 128;
       f32x16 s = mask ? bias_init_t<QUAD, true>(qinfo, tab, qb, half, kfwd, klab, g.nbins)
                       : bias_init_t<QUAD, false>(qinfo, tab, qb, half, kfwd, klab, g.nbins);
       f32x16 dp, lq;
@@ -879,7 +891,8 @@ __global__ __launch_bounds__(kThreads, sizeof(T) == 2 ? 2 : 1) void bwd_dkdv_ker
 #pragma unroll
         for (int x = 0; x < 4; ++x) {
           dp[4 * g4 + x] = d4[x];      // dP - D straight from the product
-          lq[4 * g4 + x] = l4[x];
+          if constexpr (kLean) s[4 * g4 + x] -= l4[x] * inv_sl2;
+          else lq[4 * g4 + x] = l4[x];
         }
       }
 #pragma unroll
@@ -887,13 +900,16 @@ __global__ __launch_bounds__(kThreads, sizeof(T) == 2 ? 2 : 1) void bwd_dkdv_ker
         mma16(s, load_op_lds<T>(qr + (qb * 32 + col) * (HD + kPad) + 16 * c + 8 * half), kop[c]);
         mma16(dp, load_op_lds<T>(dr + (qb * 32 + col) * (HD + kPad) + 16 * c + 8 * half), vop[c]);
       }
-      f32x16 ds;
+      f32x16 dsr;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float p = __builtin_amdgcn_exp2f(s[r] * scale_log2 - lq[r]);
-        ds[r] = p * dp[r];
+        const float p = kLean ? __builtin_amdgcn_exp2f(s[r] * scale_log2)
+                              : __builtin_amdgcn_exp2f(s[r] * scale_log2 - lq[r]);
+        if constexpr (kLean) dp[r] *= p;          // dS
+        else dsr[r] = p * dp[r];
         s[r] = p;
       }
+      const f32x16& ds = kLean ? dp : dsr;
 #pragma unroll
       for (int eb = 0; eb < HD / 32; ++eb) {
 #pragma unroll
