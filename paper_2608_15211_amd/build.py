@@ -14,7 +14,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libterra_swin.so")
-SOURCES = ["route.hip", "attn.hip", "attn_win.hip", "plan.hip", "block.hip", "abi.hip"]
+SOURCES = ["route.hip", "attn.hip", "attn_win.hip", "dtab.hip", "plan.hip", "block.hip", "abi.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -41,6 +41,9 @@ hipError_t launch_win_fwd(const Geo& g, bool nhwc, const void* q, const void* k,
 hipError_t launch_win_bwd(const Geo& g, bool nhwc, const void* q, const void* k, const void* v,
                           const void* dout, const float* lse, const float* table, void* dq,
                           void* dk, void* dv, float* partial, int nslice, hipStream_t st);
+// Fixed-order sum of the per-slice bias-gradient partials (dtab.hip).
+hipError_t launch_dtab_reduce(const Geo& g, const float* partial, float* dtab, int nslice,
+                              hipStream_t st);
 
 constexpr int kThreads = 256;   // 4 waves
 constexpr int kWaveQ = 32;      // queries (or keys) per wave
@@ -945,25 +948,6 @@ __global__ __launch_bounds__(kThreads, sizeof(T) == 2 ? 2 : 1) void bwd_dkdv_ker
 }
 
 // ---------------------------------------------------------------------------
-// Backward, step 3: dT[bin][h] = sum over slices of the partials, in slice
-// order (deterministic).  Consecutive threads take consecutive bins of one
-// head, so each slice's loads are contiguous, and the loop is unrolled so
-// that loads issue ahead of the additions, which stay in slice order.
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kThreads) void dtab_reduce_kernel(
-    const float* __restrict__ partial, float* __restrict__ dtab, Geo g, int nslice) {
-  const int idx = blockIdx.x * kThreads + threadIdx.x;
-  if (idx >= g.nbins * g.heads) return;
-  const int h = idx / g.nbins;
-  const int bin = idx - h * g.nbins;
-  const float* p = partial + (int64_t)h * nslice * g.nbins + bin;
-  float acc = 0.0f;
-#pragma unroll 8
-  for (int s = 0; s < nslice; ++s) acc += p[(int64_t)s * g.nbins];
-  dtab[bin * g.heads + h] = acc;
-}
-
-// ---------------------------------------------------------------------------
 // Host-side launchers (called by the C ABI after validation).
 // ---------------------------------------------------------------------------
 static inline int num_chunks(const Geo& g) { return (g.wh * g.ww + kChunk - 1) / kChunk; }
@@ -1116,10 +1100,7 @@ static hipError_t bwd_impl(const Geo& g, const void* q, const void* k, const voi
                        (T*)dk, (T*)dv, g, nqc, sl2, scale);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int nred = g.nbins * g.heads;
-  hipLaunchKernelGGL(dtab_reduce_kernel, dim3((nred + kThreads - 1) / kThreads), dim3(kThreads), 0,
-                     st, partial, dtab, g, nslice);
-  return hipGetLastError();
+  return launch_dtab_reduce(g, partial, dtab, nslice, st);
 }
 
 // Element type codes of the C ABI: 0 float, 1 bfloat16, 2 float16.
@@ -1218,10 +1199,7 @@ hipError_t launch_attn_bwd(const Geo& g, int dt, bool nhwc, const void* q, const
     float* partial = reinterpret_cast<float*>(ws);
     hipError_t e = launch_win_bwd(g, nhwc, q, k, v, dout, lse, table, dq, dk, dv, partial, nslice, st);
     if (e != hipSuccess) return e;
-    const int nred = g.nbins * g.heads;
-    hipLaunchKernelGGL(dtab_reduce_kernel, dim3((nred + kThreads - 1) / kThreads), dim3(kThreads), 0,
-                       st, partial, dtab, g, nslice);
-    return hipGetLastError();
+    return launch_dtab_reduce(g, partial, dtab, nslice, st);
   }
   if (!attn_uses_olo(g, dt)) olo = nullptr;
   return nhwc ? bwd_dispatch<true>(g, dt, q, k, v, o, olo, dout, lse, table, dq, dk, dv, dtab, ws, st)
