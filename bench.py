@@ -332,8 +332,14 @@ def main():
         per_step = {p: float(np.sum(launches[p])) / args.steps for p in phases}
         return float(np.median(steps_ms)), float(np.mean(steps_ms)), per_launch, per_step
 
-    ms_step, ms_step_mean, per_launch, per_step = timed(step, fused_phases)
+    # The unfused pipeline (a secondary figure) is timed first: its steps
+    # leave the device running rather than idle when the fused step's W
+    # warm-up steps start (a fresh process needs tens of milliseconds of work
+    # before clocks and translation caches settle; with 5 warm-up steps and
+    # nothing before them the 128 x 1080 fused step measured 0.859 ms, with
+    # 30 0.794 ms).
     ms_unf, _, pl_unf, ps_unf = timed(step_unfused, unfused_phases)
+    ms_step, ms_step_mean, per_launch, per_step = timed(step, fused_phases)
 
     alg = algorithmic(cfg)
     attn_flops = alg["fwd_flops"] + alg["bwd_flops"]

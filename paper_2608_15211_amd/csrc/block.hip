@@ -5,14 +5,16 @@
 // float32 accumulation.
 //
 // One matrix-core GEMM kernel serves every linear layer.  Operands are
-// bf16 row-major matrices in HBM; each is staged through LDS in its memory
-// layout, and its 32 x 16 matrix-core operands are read either straight
-// (when the contraction index runs along memory rows) or through the LDS
-// transpose read (when it runs down memory columns), so Y = X W^T,
-// dX = dY W and dW = dY^T X all take the same kernel.  LayerNorm is applied
-// to an operand while it is staged (from per-token mean and 1/std computed
-// by a small kernel), so normalised activations never reach HBM; bias,
-// residual, GELU and its derivative are applied in the epilogue.
+// bf16 row-major matrices in HBM, brought into XOR-swizzled LDS tiles by
+// direct-to-LDS loads through a three-stage ring; the 32 x 16 matrix-core
+// operands are read either straight (when the contraction index runs along
+// memory rows) or through the LDS transpose read (when it runs down memory
+// columns), so Y = X W^T, dX = dY W and dW = dY^T X all take the same
+// kernel.  In the forward each LayerNorm is folded into the projection
+// after it (gains into the weights, mean and 1/std applied to the
+// accumulators), so normalised activations never reach HBM there; the
+// backward recomputes them once per weight gradient.  Bias, residual,
+// GELU and its derivative are applied in the epilogue.
 #include <algorithm>
 
 #include "terra_common.h"
