@@ -231,8 +231,9 @@ def main():
     ap.add_argument("--no-block", action="store_true", help="skip the Swin-block timing")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: the path has no multi-GPU leg in this build "
-              "(see DESIGN.md for how it would shard); run with --gpus 1", file=sys.stderr)
+        print("bench.py measures one GPU only: the attention path has no multi-GPU leg "
+              "(it would shard by windows and heads, exchanging only boundary rows); run with --gpus 1",
+              file=sys.stderr)
         sys.exit(2)
 
     import torch

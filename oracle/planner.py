@@ -20,7 +20,7 @@ Definitions followed
   windows.
 * Sec. IV-B: the I/O topology cuts the grid into contiguous height stripes,
   one per DMP rank.  Reading used for grids whose height is not a multiple
-  of the rank count (this build does not pad): rank r holds rows
+  of the rank count (no grid is padded here): rank r holds rows
   [floor(r H / P), floor((r + 1) H / P)), the same floor rule as Eq. (4).
 * Sec. IV-D: a token's global coordinate (u, v) fixes both its DMP source
   rank (the stripe holding row u) and, through the window shift, the window
