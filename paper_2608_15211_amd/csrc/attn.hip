@@ -627,30 +627,78 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
         }
       }
       if (!wactive) continue;
+      // Head dim 64: the S and dP products of every key block of the tile
+      // first, then per block dS and dQ += dS K, so that one block's exp
+      // runs while the next block's products are on the matrix cores; each
+      // block's K and V operands are read from LDS before its bias (dQ
+      // kernel -3 % at 576-token windows).  Otherwise one block at a time:
+      // at head dim 128 the held operands and accumulators would spill, and
+      // at head dim 32 they would cost the third resident wave per SIMD.
+      constexpr bool kHold = HD == 64;
       f32x16 dsb[kTile / 32];
+      if constexpr (kHold) {
+        f32x16 sb[kTile / 32];
 #pragma unroll
-      for (int kb = 0; kb < kTile / 32; ++kb) {
-        f32x16 s = mask ? bias_init<QUAD, true>(kinfo, tab, kb, half, qrev, qlab, g.nbins)
+        for (int kb = 0; kb < kTile / 32; ++kb) {
+          typename Operand<T>::type kop_[HD / 16], vop_[HD / 16];
+#pragma unroll
+          for (int c = 0; c < HD / 16; ++c) {
+            kop_[c] = load_op_lds<T>(kt + (kb * 32 + col) * (HD + kPad) + 16 * c + 8 * half);
+            vop_[c] = load_op_lds<T>(vr + (kb * 32 + col) * (HD + kPad) + 16 * c + 8 * half);
+          }
+          __builtin_amdgcn_sched_barrier(0);
+          sb[kb] = mask ? bias_init<QUAD, true>(kinfo, tab, kb, half, qrev, qlab, g.nbins)
                         : bias_init<QUAD, false>(kinfo, tab, kb, half, qrev, qlab, g.nbins);
-        f32x16 dp;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) dp[r] = -Dq;      // dP - D straight from the product
+          for (int r = 0; r < 16; ++r) dsb[kb][r] = -Dq;      // dP - D straight from the product
 #pragma unroll
-        for (int c = 0; c < HD / 16; ++c) {
-          mma16(s, load_op_lds<T>(kt + (kb * 32 + col) * (HD + kPad) + 16 * c + 8 * half), qop[c]);
-          mma16(dp, load_op_lds<T>(vr + (kb * 32 + col) * (HD + kPad) + 16 * c + 8 * half), dop[c]);
+          for (int c = 0; c < HD / 16; ++c) {
+            mma16(sb[kb], kop_[c], qop[c]);
+            mma16(dsb[kb], vop_[c], dop[c]);
+          }
         }
 #pragma unroll
-        for (int r = 0; r < 16; ++r) dsb[kb][r] = __builtin_amdgcn_exp2f(s[r] * scale_log2 - lse2) * dp[r];
+        for (int kb = 0; kb < kTile / 32; ++kb) {
 #pragma unroll
-        for (int eb = 0; eb < HD / 32; ++eb) {
+          for (int r = 0; r < 16; ++r) dsb[kb][r] *= __builtin_amdgcn_exp2f(sb[kb][r] * scale_log2 - lse2);
 #pragma unroll
-          for (int c = 0; c < 2; ++c) {
-            if constexpr (sizeof(T) == 2) {
-              mma16(dqacc[eb], lds_tr_op<T, HD + kPad>(kt, kb, c, eb, lane), pack8<T>(dsb[kb], 8 * c));
-            } else {
-              const T* row = ktt + tr_row<T, HD>(eb * 32 + col) + kb * 32 + 16 * c;
-              mma16(dqacc[eb], load_op_lds_perm<T>(row, half), pack8<T>(dsb[kb], 8 * c));
+          for (int eb = 0; eb < HD / 32; ++eb) {
+#pragma unroll
+            for (int c = 0; c < 2; ++c) {
+              if constexpr (sizeof(T) == 2) {
+                mma16(dqacc[eb], lds_tr_op<T, HD + kPad>(kt, kb, c, eb, lane), pack8<T>(dsb[kb], 8 * c));
+              } else {
+                const T* row = ktt + tr_row<T, HD>(eb * 32 + col) + kb * 32 + 16 * c;
+                mma16(dqacc[eb], load_op_lds_perm<T>(row, half), pack8<T>(dsb[kb], 8 * c));
+              }
+            }
+          }
+        }
+      } else {
+#pragma unroll
+        for (int kb = 0; kb < kTile / 32; ++kb) {
+          f32x16 s = mask ? bias_init<QUAD, true>(kinfo, tab, kb, half, qrev, qlab, g.nbins)
+                          : bias_init<QUAD, false>(kinfo, tab, kb, half, qrev, qlab, g.nbins);
+          f32x16 dp;
+#pragma unroll
+          for (int r = 0; r < 16; ++r) dp[r] = -Dq;      // dP - D straight from the product
+#pragma unroll
+          for (int c = 0; c < HD / 16; ++c) {
+            mma16(s, load_op_lds<T>(kt + (kb * 32 + col) * (HD + kPad) + 16 * c + 8 * half), qop[c]);
+            mma16(dp, load_op_lds<T>(vr + (kb * 32 + col) * (HD + kPad) + 16 * c + 8 * half), dop[c]);
+          }
+#pragma unroll
+          for (int r = 0; r < 16; ++r) dsb[kb][r] = __builtin_amdgcn_exp2f(s[r] * scale_log2 - lse2) * dp[r];
+#pragma unroll
+          for (int eb = 0; eb < HD / 32; ++eb) {
+#pragma unroll
+            for (int c = 0; c < 2; ++c) {
+              if constexpr (sizeof(T) == 2) {
+                mma16(dqacc[eb], lds_tr_op<T, HD + kPad>(kt, kb, c, eb, lane), pack8<T>(dsb[kb], 8 * c));
+              } else {
+                const T* row = ktt + tr_row<T, HD>(eb * 32 + col) + kb * 32 + 16 * c;
+                mma16(dqacc[eb], load_op_lds_perm<T>(row, half), pack8<T>(dsb[kb], 8 * c));
+              }
             }
           }
         }
@@ -963,6 +1011,18 @@ __global__ __launch_bounds__(kThreads, sizeof(T) == 2 ? 2 : 1) void bwd_dkdv_ker
       // stays in registers across the products, and dS replaces dP in place
       // (-20 % spill there; at head_dim 64 the plain form is 1.5 % faster).
       constexpr bool kLean = HD == 128;
+      // up to head dim 64, the block's Q and dO operands are read from LDS
+      // before its bias (-1 % at 576-token windows)
+      constexpr bool kHold = HD <= 64;
+      typename Operand<T>::type qo_[kHold ? HD / 16 : 1], do_[kHold ? HD / 16 : 1];
+      if constexpr (kHold) {
+#pragma unroll
+        for (int c = 0; c < HD / 16; ++c) {
+          qo_[c] = load_op_lds<T>(qr + (qb * 32 + col) * (HD + kPad) + 16 * c + 8 * half);
+          do_[c] = load_op_lds<T>(dr + (qb * 32 + col) * (HD + kPad) + 16 * c + 8 * half);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
       f32x16 s = mask ? bias_init_t<QUAD, true>(qinfo, tab, qb, half, kfwd, klab, g.nbins)
                       : bias_init_t<QUAD, false>(qinfo, tab, qb, half, kfwd, klab, g.nbins);
       f32x16 dp, lq;
@@ -979,8 +1039,13 @@ __global__ __launch_bounds__(kThreads, sizeof(T) == 2 ? 2 : 1) void bwd_dkdv_ker
       }
 #pragma unroll
       for (int c = 0; c < HD / 16; ++c) {
-        mma16(s, load_op_lds<T>(qr + (qb * 32 + col) * (HD + kPad) + 16 * c + 8 * half), kop[c]);
-        mma16(dp, load_op_lds<T>(dr + (qb * 32 + col) * (HD + kPad) + 16 * c + 8 * half), vop[c]);
+        if constexpr (kHold) {
+          mma16(s, qo_[c], kop[c]);
+          mma16(dp, do_[c], vop[c]);
+        } else {
+          mma16(s, load_op_lds<T>(qr + (qb * 32 + col) * (HD + kPad) + 16 * c + 8 * half), kop[c]);
+          mma16(dp, load_op_lds<T>(dr + (qb * 32 + col) * (HD + kPad) + 16 * c + 8 * half), vop[c]);
+        }
       }
       f32x16 dsr;
 #pragma unroll
