@@ -294,12 +294,14 @@ __global__ __launch_bounds__(kWinThreads) void fwd_win_kernel(
 
 // ---------------------------------------------------------------------------
 // Forward for head_dim 32 and an even head count: one workgroup of 8 waves
-// per (head pair, run of consecutive windows), two resident per CU (one's
-// loads overlap the other's matrix work; loading one window ahead measured
-// slower).  Global memory is touched only in row-contiguous 128-byte
-// segments (8 lanes per token row): Q, K and V are staged through LDS (V
-// transposed by the staging stores) and O goes back through LDS.  Wave w handles head
-// 2*hp + (w >> 2) and queries [32*(w&3), 32*(w&3)+32).
+// per (head pair, run of consecutive windows), two resident per CU.  Each
+// window's rows are loaded into registers while the previous window
+// computes (126 registers, still four waves per SIMD; -4 % against loading
+// at the top of each window).  Global memory is touched only in
+// row-contiguous 128-byte segments (8 lanes per token row): Q, K and V are
+// staged through LDS (V row-major, read transposed by the LDS transpose
+// read) and O goes back through LDS.  Wave w handles head 2*hp + (w >> 2)
+// and queries [32*(w&3), 32*(w&3)+32).
 // ---------------------------------------------------------------------------
 constexpr int kPairThreads = 512;
 
@@ -384,7 +386,7 @@ __global__ __launch_bounds__(kPairThreads, 4) void fwd_win_pair_kernel(
     const WinTokens<NHWC> wt(g, b, wi, wj);
     const bool qvalid = qi < n;
 
-    pair_load_rows<NHWC>(rows, g, wl, cbase, q, k, v);
+    if (wl == wbeg) pair_load_rows<NHWC>(rows, g, wl, cbase, q, k, v);
     __syncthreads();   // the previous window is done with LDS
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
@@ -397,6 +399,7 @@ __global__ __launch_bounds__(kPairThreads, 4) void fwd_win_pair_kernel(
     }
     if (threadIdx.x < kWinMax) kinfo[threadIdx.x] = win_token_info(g, wi, wj, cols, threadIdx.x, n);
     __syncthreads();
+    if (wl + 1 < wend) pair_load_rows<NHWC>(rows, g, wl + 1, cbase, q, k, v);   // next window
 
     // Softmax over the two halves of the window's keys in turn (running
     // max and sum; a half with no allowed key for a query leaves it as it
