@@ -223,7 +223,7 @@ __global__ __launch_bounds__(kWinThreads) void fwd_win_kernel(
         store4_bf16(vts + (32 * eb + col) * (kWinMax + 8) + 32 * wave + 8 * g4 + 4 * half, t, g4, 1.0f);
     }
   }
-  __syncthreads();
+  lds_barrier();
   if (wave >= nkb) return;
 
   const int qi = 32 * wave + col;
@@ -387,7 +387,7 @@ __global__ __launch_bounds__(kPairThreads, 4) void fwd_win_pair_kernel(
     const bool qvalid = qi < n;
 
     if (wl == wbeg) pair_load_rows<NHWC>(rows, g, wl, cbase, q, k, v);
-    __syncthreads();   // the previous window is done with LDS
+    lds_barrier();   // the previous window is done with LDS
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
       const int idx = threadIdx.x + u * kPairThreads;
@@ -398,7 +398,7 @@ __global__ __launch_bounds__(kPairThreads, 4) void fwd_win_pair_kernel(
       *reinterpret_cast<uint4*>(vrs + t * VH + row * HD + e0) = rows.v[u];
     }
     if (threadIdx.x < kWinMax) kinfo[threadIdx.x] = win_token_info(g, wi, wj, cols, threadIdx.x, n);
-    __syncthreads();
+    lds_barrier();
     if (wl + 1 < wend) pair_load_rows<NHWC>(rows, g, wl + 1, cbase, q, k, v);   // next window
 
     // Softmax over the two halves of the window's keys in turn (running
@@ -464,7 +464,7 @@ __global__ __launch_bounds__(kPairThreads, 4) void fwd_win_pair_kernel(
       }
       l = halves_sum(l);
     }
-    __syncthreads();   // every wave has read its Q rows; qs now takes O
+    lds_barrier();   // every wave has read its Q rows; qs now takes O
     if (active) {
       const float inv = 1.0f / l;
 #pragma unroll
@@ -472,7 +472,7 @@ __global__ __launch_bounds__(kPairThreads, 4) void fwd_win_pair_kernel(
         store4_bf16(qs + (hs * kWinMax + qi) * KS + 8 * g4 + 4 * half, oacc, g4, inv);
       if (qvalid && half == 0) lse[wt.lse_at(g, h, qi)] = (m + __log2f(l)) * kLn2;
     }
-    __syncthreads();
+    lds_barrier();
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
       const int idx = threadIdx.x + u * kPairThreads;
@@ -686,13 +686,13 @@ __device__ __forceinline__ void bwd_rotation(BwdWave& st, f32x4 (&dta)[4], f32x4
 #pragma unroll
   for (int r = 0; r < 16; ++r) ds2[r] = p2[r] * (ds2[r] - st.D);
   bwd_step_tail<W, 0>(st, p0, ds0, dta[W], dtb[W], dqacc);
-  __syncthreads();
+  lds_barrier();
   bwd_step_tail<(W + 1) & 3, 1>(st, p1, ds1, dta[(W + 1) & 3], dtb[(W + 1) & 3], dqacc);
-  __syncthreads();
+  lds_barrier();
   bwd_step_tail<(W + 2) & 3, 2>(st, p2, ds2, dta[(W + 2) & 3], dtb[(W + 2) & 3], dqacc);
-  __syncthreads();
+  lds_barrier();
   bwd_step<(W + 3) & 3, 3, QUAD, MASK>(st, dta[(W + 3) & 3], dtb[(W + 3) & 3], dqacc);
-  __syncthreads();
+  lds_barrier();
 }
 
 template <bool QUAD, bool MASK>
@@ -831,7 +831,7 @@ __global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
     }
 
     bwd_load_rows<NHWC>(rows, g, wl, h, qi, q, k, v, dout, lse);
-    __syncthreads();   // the previous window is done with LDS
+    lds_barrier();   // the previous window is done with LDS
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
       const int idx = threadIdx.x + u * kWinThreads;
@@ -844,7 +844,7 @@ __global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
     if (threadIdx.x < kWinMax) kinfo[threadIdx.x] = win_token_info(g, wi, wj, cols, threadIdx.x, n);
     BwdWave st;
     st.lse2 = rows.lse2;
-    __syncthreads();
+    lds_barrier();
 
     st.ks = ks;
     st.vs = vs;
@@ -876,7 +876,7 @@ __global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
     // then row-contiguous stores of dQ, dV and dK
 #pragma unroll
     for (int g4 = 0; g4 < 4; ++g4) store4_bf16(ks + qi * KS + 8 * g4 + 4 * half, dqacc, g4, scale);
-    __syncthreads();
+    lds_barrier();
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
       const int idx = threadIdx.x + u * kWinThreads;
@@ -897,7 +897,7 @@ __global__ __launch_bounds__(kWinThreads, 2) void bwd_win_kernel(
   }
   if (acc_cols > 0) TERRA_FLUSH_DT(acc_cols);
 #undef TERRA_FLUSH_DT
-  __syncthreads();
+  lds_barrier();
   for (int y = threadIdx.x; y < g.nbins; y += kWinThreads) {
     const int ry = g.nbins - 1 - y;
     partial[((int64_t)h * nslice + slice) * g.nbins + y] =

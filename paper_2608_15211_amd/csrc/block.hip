@@ -153,24 +153,6 @@ __device__ inline bf16x8 tr_operand(const bf16* T, int k0, int m0, int lane) {
   return __builtin_bit_cast(bf16x8, o);
 }
 
-typedef int i32x4 __attribute__((ext_vector_type(4)));
-__device__ void raw_buffer_load_lds(i32x4 rsrc, __attribute__((address_space(3))) uint32_t* lds, int size,
-                                    int voffset, int soffset, int offset,
-                                    int aux) __asm("llvm.amdgcn.raw.buffer.load.lds");
-
-// Buffer descriptor of a whole (single-block) operand: base, size in bytes
-// (below 2^31, so that the offset 2^31 used for rows outside the operand or
-// the contraction slice is past the end and reads zeros).
-__device__ inline i32x4 buffer_rsrc(const void* base, uint32_t bytes) {
-  const uint64_t b = (uint64_t)base;
-  i32x4 r;
-  r[0] = (int)(uint32_t)b;
-  r[1] = (int)(uint32_t)(b >> 32);
-  r[2] = (int)bytes;
-  r[3] = 0x00020000;
-  return r;
-}
-
 // Direct-to-LDS staging of one operand tile: each thread moves kPer 16-byte
 // chunks with buffer loads that write LDS themselves (slot q of the tile is
 // written by thread q % kGT, load q / kGT); chunks outside the operand or
@@ -194,10 +176,6 @@ __device__ inline void stage_direct(const i32x4& rs, const Mat& X, bf16* tile, i
   }
 }
 
-template <int N>
-__device__ inline void wait_vm() {
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
 
 // C[M][N] = A[M][K] B[K][N] (+ epilogue).  AKROW: A is memory [M][K]
 // (else [K][M]); BKROW: B is memory [N][K] (else [K][N]).  blockIdx.z:
@@ -248,7 +226,7 @@ __global__ __launch_bounds__(kGT, 1) void gemm_kernel(Mat A, Mat B, EpiArgs ep, 
   for (int kt = 0; kt < nk; ++kt) {
     if (kt + 1 < nk) wait_vm<kLoads>();
     else wait_vm<0>();
-    __syncthreads();
+    lds_barrier();     // stage kt is in LDS; stage kt + 1 may still be loading
     if (kt + 2 < nk) issue(kt + 2);
     const bf16* ta = a_tile(kt % 3);
     const bf16* tb = b_tile(kt % 3);

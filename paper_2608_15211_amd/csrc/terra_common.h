@@ -285,4 +285,49 @@ __device__ inline typename Operand<T>::type pack8(const f32x16& acc, int r0) {
   return o;
 }
 
+// ---------------------------------------------------------------------------
+// Direct-to-LDS loads.  A buffer load with the LDS bit moves 16 bytes per
+// lane from global memory straight into LDS: lane l of the instruction
+// writes bytes [16 l, 16 l + 16) past its wave-uniform LDS base (held in
+// M0), without passing through registers.  The compiler does not see that
+// LDS write, so a wave waits for the load count (wait_vm) and the
+// workgroup then synchronises before any wave reads those bytes.
+// ---------------------------------------------------------------------------
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+__device__ void raw_buffer_load_lds(i32x4 rsrc, __attribute__((address_space(3))) uint32_t* lds, int size,
+                                    int voffset, int soffset, int offset,
+                                    int aux) __asm("llvm.amdgcn.raw.buffer.load.lds");
+
+// Buffer descriptor of a whole operand: base, size in bytes (below 2^31, so
+// that the offset 2^31 used for rows outside the operand is past the end and
+// reads zeros).
+__device__ inline i32x4 buffer_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t b = (uint64_t)base;
+  i32x4 r;
+  r[0] = (int)(uint32_t)b;
+  r[1] = (int)(uint32_t)(b >> 32);
+  r[2] = (int)bytes;
+  r[3] = 0x00020000;
+  return r;
+}
+
+// Wait until at most N of this wave's vector-memory operations are
+// outstanding (they complete in issue order).
+template <int N>
+__device__ inline void wait_vm() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Workgroup barrier for LDS hand-offs only: the wave's own LDS operations
+// complete, then the barrier.  Unlike __syncthreads() it carries no memory
+// fence, whose release half would make every wave wait for all of its
+// outstanding global loads, the direct-to-LDS ones still meant to be in
+// flight included.  Direct-to-LDS data a wave is about to hand over must be
+// waited for with wait_vm first.
+__device__ inline void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 }  // namespace terra
