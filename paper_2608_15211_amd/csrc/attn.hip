@@ -288,18 +288,18 @@ __global__ __launch_bounds__(kThreads) void fwd_kernel(
     tile_load(rv, v, g, wt, 0, n, hoff);
   }
   tok_fill(tt, g, wt, n);
-  if (!kPrefetch && NHWC) __syncthreads();   // the first tile comes from the table too
+  if (!kPrefetch && NHWC) lds_barrier();   // the first tile comes from the table too
   for (int k0 = 0; k0 < n; k0 += kTile) {
     if (!kPrefetch) {
       tile_load_tt(rk, k, g, wt, tt, k0, n, hoff);
       tile_load_tt(rv, v, g, wt, tt, k0, n, hoff);
     }
-    __syncthreads();
+    lds_barrier();
     tile_store<T, HD, true, false>(rk, kt, nullptr);
     if (sizeof(T) == 2) tile_store_rows<T, HD, tr16_stride<HD>()>(rv, vt);
     else tile_store<T, HD, false, true>(rv, nullptr, vt);
     if (threadIdx.x < kTile) kinfo[threadIdx.x] = token_info(g, i, j, cols, k0 + threadIdx.x, n);
-    __syncthreads();
+    lds_barrier();
     if (kPrefetch && k0 + kTile < n) {
       tile_load_tt(rk, k, g, wt, tt, k0 + kTile, n, hoff);
       tile_load_tt(rv, v, g, wt, tt, k0 + kTile, n, hoff);
@@ -512,7 +512,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
       // them without staging or barriers
       tile_load(rk, k, g, wt, 0, n, hoff);
       tile_load(rv, v, g, wt, 0, n, hoff);
-      __syncthreads();                  // the previous item is done with the tiles
+      lds_barrier();                  // the previous item is done with the tiles
       for (int t0 = 0; t0 < n; t0 += kTile) {
         TileRegs<T, HD> nk = rk, nv = rv;
         if (t0 + kTile < n) {
@@ -527,14 +527,14 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
         rk = nk;
         rv = nv;
       }
-      __syncthreads();
+      lds_barrier();
     } else if (kPrefetch) {
       tile_load(rk, k, g, wt, 0, n, hoff);
       tile_load(rv, v, g, wt, 0, n, hoff);
     }
     if constexpr (!RES) {
       tok_fill(tt, g, wt, n);
-      if (!kPrefetch && NHWC) __syncthreads();   // the first tile comes from the table too
+      if (!kPrefetch && NHWC) lds_barrier();   // the first tile comes from the table too
     }
     float dsum = 0.0f;
     if (olo != nullptr) {
@@ -562,11 +562,11 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
           tile_load_tt(rk, k, g, wt, tt, k0, n, hoff);
           tile_load_tt(rv, v, g, wt, tt, k0, n, hoff);
         }
-        __syncthreads();
+        lds_barrier();
         tile_store<T, HD, true, false>(rk, kt, nullptr);
         tile_store<T, HD, true, false>(rv, vr, nullptr);
         if (threadIdx.x < kTile) kinfo[threadIdx.x] = token_info(g, i, j, cols, k0 + threadIdx.x, n);
-        __syncthreads();
+        lds_barrier();
         if (kPrefetch) {
           const int nk0 = k0 + kTile < n ? k0 + kTile : 0;
           tile_load_tt(rk, k, g, wt, tt, nk0, n, hoff);
@@ -616,11 +616,11 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
           tile_load_tt(rk, k, g, wt, tt, k0, n, hoff);
           tile_load_tt(rv, v, g, wt, tt, k0, n, hoff);
         }
-        __syncthreads();
+        lds_barrier();
         tile_store<T, HD, true, sizeof(T) == 4>(rk, kt, ktt);
         tile_store<T, HD, true, false>(rv, vr, nullptr);
         if (threadIdx.x < kTile) kinfo[threadIdx.x] = token_info(g, i, j, cols, k0 + threadIdx.x, n);
-        __syncthreads();
+        lds_barrier();
         if (kPrefetch && k0 + kTile < n) {
           tile_load_tt(rk, k, g, wt, tt, k0 + kTile, n, hoff);
           tile_load_tt(rv, v, g, wt, tt, k0 + kTile, n, hoff);
@@ -862,7 +862,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
         }
     }
   }
-  __syncthreads();
+  lds_barrier();
   float* out = partial + ((int64_t)h * nslice + slice) * g.nbins;
   for (int x = threadIdx.x; x < g.nbins; x += kThreads)
     out[x] = ((dtab[x] + dtab[g.nbins + x]) + dtab[2 * g.nbins + x]) + dtab[3 * g.nbins + x];
@@ -952,7 +952,7 @@ __global__ __launch_bounds__(kThreads, sizeof(T) == 2 ? 2 : 1) void bwd_dkdv_ker
   constexpr bool kTab = !kPrefetch;
   if constexpr (kTab) {
     tok_fill(tt, g, wt, n);
-    if (NHWC) __syncthreads();   // the first tile comes from the table too
+    if (NHWC) lds_barrier();   // the first tile comes from the table too
   }
   // Per-query words of a tile (threads below kTile): label/bias word,
   // log-sum-exp in log2 units (+inf for padding queries: P = 0) and -D (the
@@ -974,7 +974,7 @@ __global__ __launch_bounds__(kThreads, sizeof(T) == 2 ? 2 : 1) void bwd_dkdv_ker
       tile_load_tt(rq, q, g, wt, tt, t0, n, hoff);
       tile_load_tt(rd, dout, g, wt, tt, t0, n, hoff);
     }
-    __syncthreads();
+    lds_barrier();
     tile_store<T, HD, true, sizeof(T) == 4>(rq, qr, qtt);
     tile_store<T, HD, true, sizeof(T) == 4>(rd, dr, dtt);
     if (threadIdx.x < kTile) {
@@ -990,7 +990,7 @@ __global__ __launch_bounds__(kThreads, sizeof(T) == 2 ? 2 : 1) void bwd_dkdv_ker
         qd[threadIdx.x] = t < n ? -D[li] : 0.0f;
       }
     }
-    __syncthreads();
+    lds_barrier();
     if (t0 + kTile < n) {
       if constexpr (kTab) {
         words(t0 + kTile);
