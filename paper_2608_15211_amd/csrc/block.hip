@@ -98,8 +98,11 @@ __device__ inline float gelu_grad_f(float x) {
 //   chunk c ^ ((r >> 2) & 3) - 16 consecutive rows read at one logical chunk
 //   cover all 64 banks;
 // * COLK tile (memory [kBK][R], R / 8 chunks a row): chunk c of row k sits
-//   at chunk c ^ (2 (k & 3)) - the four rows of one transpose read land on
-//   four different 32-byte spans.
+//   at chunk c ^ (4 (k & 3)) - each half-wave of a transpose read takes 64
+//   bytes from each of four rows, and these land on four different 64-byte
+//   spans of the 256 bytes the LDS banks cover (measured: no bank conflicts;
+//   with c ^ (2 (k & 3)) 0.8-2 conflict cycles per LDS instruction, though
+//   no slower).
 // ---------------------------------------------------------------------------
 template <int R, bool KROW>
 struct Tile {
@@ -109,7 +112,7 @@ struct Tile {
   // element offset of (row, logical chunk) of the memory layout
   __device__ static int off(int row, int c) {
     if (KROW) return row * kBK + 8 * (c ^ ((row >> 2) & 3));
-    return row * R + 8 * (c ^ (2 * (row & 3)));
+    return row * R + 8 * (c ^ (4 * (row & 3)));
   }
   // memory (row, column) of the chunk stored in slot q (slot = chunk position in LDS order)
   __device__ static void slot_src(int q, int r0, int k0, int& mrow, int& mcol) {
@@ -120,7 +123,7 @@ struct Tile {
     } else {
       const int row = q / (R / 8), p = q - row * (R / 8);
       mrow = k0 + row;
-      mcol = r0 + 8 * (p ^ (2 * (row & 3)));
+      mcol = r0 + 8 * (p ^ (4 * (row & 3)));
     }
   }
 };
