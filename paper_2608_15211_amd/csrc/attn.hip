@@ -215,6 +215,28 @@ __device__ inline int token_info(const Geo& g, int i, int j, int cols, int t, in
   return (a * g.bstride + c) | (lab << 24);
 }
 
+// bias_init with each key's bias offset also held as a byte offset, knb[k]
+// = 4 x (offset of key k): one group of four keys then costs one address add
+// from tabq, the lane's row of the reversed table in bytes.  Labels still
+// come from kinfo, and an excluded pair reads its bin (always inside the
+// table) and is replaced by -inf.
+template <bool QUAD, bool MASK>
+__device__ inline f32x16 bias_init_nb(const int* kinfo, const int* knb, const char* tabq, int kb,
+                                      int half, int qlab) {
+  f32x16 c;
+#pragma unroll
+  for (int g4 = 0; g4 < 4; ++g4) {
+    const int kk = 32 * kb + 8 * g4 + 4 * half;
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+      const int kx = QUAD ? kk : kk + x;
+      c[4 * g4 + x] = reinterpret_cast<const float*>(tabq + knb[kx])[QUAD ? x : 0];
+      if (MASK && (kinfo[kx] >> 24) != qlab) c[4 * g4 + x] = -INFINITY;
+    }
+  }
+  return c;
+}
+
 // ---------------------------------------------------------------------------
 // Forward.  Grid: B * nwin * heads * nqc workgroups (nqc query chunks of 128
 // per window, empty chunks of small windows exit at once).  The bias enters
@@ -449,8 +471,9 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
   T* kt0 = reinterpret_cast<T*>(smem);                // K  nt x [kTile][HD+kPad]
   T* vr0 = kt0 + nt * kTE;                            // V  nt x [kTile][HD+kPad]
   T* ktt = vr0 + nt * kTE;                            // K^T (transposed tile, fp32)
-  int* kinfo0 = reinterpret_cast<int*>(ktt + ttile_size<T, HD>());   // nt x [kTile]
-  float* tab = reinterpret_cast<float*>(kinfo0 + nt * kTile);   // [nbins+4], reversed
+  // nt x {[kTile] label/offset words, [kTile] 4 x offset}
+  int* kinfo0 = reinterpret_cast<int*>(ktt + ttile_size<T, HD>());
+  float* tab = reinterpret_cast<float*>(kinfo0 + 2 * nt * kTile);   // [nbins+4], reversed
   float* dtab = tab + g.nbins + 4;                    // [4][nbins], one per wave
   // [wh*ww] token offsets of the current item.  One buffer serves: the last
   // read of an item (the prefetch of its last tile) comes before the
@@ -485,6 +508,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
     const int qlab = qinf >> 24;
     const int qoff = (qinf & 0xFFFFFF) + (g.wh - 1) * g.bstride + (g.ww - 1);
     const int qrev = g.nbins - 1 - qoff;
+    const char* tabq = reinterpret_cast<const char*>(tab + qrev);
     const int64_t lidx = wt.lse_at(g, h, qvalid ? qi : 0);
     // +inf for padding queries: their P is exactly 0
     const float lse2 = qvalid ? lse[lidx] * kLog2e : INFINITY;
@@ -522,8 +546,11 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
         const int tix = t0 / kTile;
         tile_store<T, HD, true, false>(rk, kt0 + tix * kTE, nullptr);
         tile_store<T, HD, true, false>(rv, vr0 + tix * kTE, nullptr);
-        if (threadIdx.x < kTile)
-          kinfo0[tix * kTile + threadIdx.x] = token_info(g, i, j, cols, t0 + threadIdx.x, n);
+        if (threadIdx.x < kTile) {
+          const int inf = token_info(g, i, j, cols, t0 + threadIdx.x, n);
+          kinfo0[tix * 2 * kTile + threadIdx.x] = inf;
+          kinfo0[tix * 2 * kTile + kTile + threadIdx.x] = 4 * (inf & 0xFFFFFF);
+        }
         rk = nk;
         rv = nv;
       }
@@ -556,7 +583,8 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
       const int tix = RES ? k0 / kTile : 0;
       T* kt = kt0 + tix * kTE;
       T* vr = vr0 + tix * kTE;
-      int* kinfo = kinfo0 + tix * kTile;
+      int* kinfo = kinfo0 + tix * 2 * kTile;
+      int* knb = kinfo + kTile;
       if constexpr (!RES) {
         if (!kPrefetch) {
           tile_load_tt(rk, k, g, wt, tt, k0, n, hoff);
@@ -565,7 +593,11 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
         lds_barrier();
         tile_store<T, HD, true, false>(rk, kt, nullptr);
         tile_store<T, HD, true, false>(rv, vr, nullptr);
-        if (threadIdx.x < kTile) kinfo[threadIdx.x] = token_info(g, i, j, cols, k0 + threadIdx.x, n);
+        if (threadIdx.x < kTile) {
+          const int inf = token_info(g, i, j, cols, k0 + threadIdx.x, n);
+          kinfo[threadIdx.x] = inf;
+          knb[threadIdx.x] = 4 * (inf & 0xFFFFFF);
+        }
         lds_barrier();
         if (kPrefetch) {
           const int nk0 = k0 + kTile < n ? k0 + kTile : 0;
@@ -576,8 +608,8 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
       if (!wactive) continue;
 #pragma unroll
       for (int kb = 0; kb < kTile / 32; ++kb) {
-        f32x16 s = mask ? bias_init<QUAD, true>(kinfo, tab, kb, half, qrev, qlab, g.nbins)
-                        : bias_init<QUAD, false>(kinfo, tab, kb, half, qrev, qlab, g.nbins);
+        f32x16 s = mask ? bias_init_nb<QUAD, true>(kinfo, knb, tabq, kb, half, qlab)
+                        : bias_init_nb<QUAD, false>(kinfo, knb, tabq, kb, half, qlab);
         f32x16 dp = f32x16{};
 #pragma unroll
         for (int c = 0; c < HD / 16; ++c) {
@@ -610,7 +642,8 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
       const int tix = RES ? k0 / kTile : 0;
       T* kt = kt0 + tix * kTE;
       T* vr = vr0 + tix * kTE;
-      int* kinfo = kinfo0 + tix * kTile;
+      int* kinfo = kinfo0 + tix * 2 * kTile;
+      int* knb = kinfo + kTile;
       if constexpr (!RES) {
         if (!kPrefetch) {
           tile_load_tt(rk, k, g, wt, tt, k0, n, hoff);
@@ -619,7 +652,11 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
         lds_barrier();
         tile_store<T, HD, true, sizeof(T) == 4>(rk, kt, ktt);
         tile_store<T, HD, true, false>(rv, vr, nullptr);
-        if (threadIdx.x < kTile) kinfo[threadIdx.x] = token_info(g, i, j, cols, k0 + threadIdx.x, n);
+        if (threadIdx.x < kTile) {
+          const int inf = token_info(g, i, j, cols, k0 + threadIdx.x, n);
+          kinfo[threadIdx.x] = inf;
+          knb[threadIdx.x] = 4 * (inf & 0xFFFFFF);
+        }
         lds_barrier();
         if (kPrefetch && k0 + kTile < n) {
           tile_load_tt(rk, k, g, wt, tt, k0 + kTile, n, hoff);
@@ -647,8 +684,8 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
             vop_[c] = load_op_lds<T>(vr + (kb * 32 + col) * (HD + kPad) + 16 * c + 8 * half);
           }
           __builtin_amdgcn_sched_barrier(0);
-          sb[kb] = mask ? bias_init<QUAD, true>(kinfo, tab, kb, half, qrev, qlab, g.nbins)
-                        : bias_init<QUAD, false>(kinfo, tab, kb, half, qrev, qlab, g.nbins);
+          sb[kb] = mask ? bias_init_nb<QUAD, true>(kinfo, knb, tabq, kb, half, qlab)
+                        : bias_init_nb<QUAD, false>(kinfo, knb, tabq, kb, half, qlab);
 #pragma unroll
           for (int r = 0; r < 16; ++r) dsb[kb][r] = -Dq;      // dP - D straight from the product
 #pragma unroll
@@ -677,8 +714,8 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
       } else {
 #pragma unroll
         for (int kb = 0; kb < kTile / 32; ++kb) {
-          f32x16 s = mask ? bias_init<QUAD, true>(kinfo, tab, kb, half, qrev, qlab, g.nbins)
-                          : bias_init<QUAD, false>(kinfo, tab, kb, half, qrev, qlab, g.nbins);
+          f32x16 s = mask ? bias_init_nb<QUAD, true>(kinfo, knb, tabq, kb, half, qlab)
+                          : bias_init_nb<QUAD, false>(kinfo, knb, tabq, kb, half, qlab);
           f32x16 dp;
 #pragma unroll
           for (int r = 0; r < 16; ++r) dp[r] = -Dq;      // dP - D straight from the product
@@ -719,6 +756,9 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
       // three lanes (bin of (q', k+3)), and the few that would leave a run
       // shorter than three lanes are added on their own.
       float* mybins = dtab + wave * g.nbins;
+      // bin of (this lane's query, key kk): qbins - knb[kk] in bytes
+      char* qbins = reinterpret_cast<char*>(mybins + qoff);
+      auto bin = [&](int kk) -> float& { return *reinterpret_cast<float*>(qbins - knb[kk]); };
       if (fold) {
         float fa[kTile / 32][4], fb[kTile / 32][4];
 #pragma unroll
@@ -739,8 +779,8 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
         // group g4 (fa at (q, k), fb at (q, k+3)).
         auto upd = [&](int kb, int g4, float va, float vb) {
           const int kk = kb * 32 + 8 * g4 + 4 * half;
-          if (va != 0.0f) mybins[qoff - (kinfo[kk] & 0xFFFFFF)] += va;
-          if (vb != 0.0f) mybins[qoff - (kinfo[kk + 3] & 0xFFFFFF)] += vb;
+          if (va != 0.0f) bin(kk) += va;
+          if (vb != 0.0f) bin(kk + 3) += vb;
         };
         if constexpr (kTile == 64) {
           // Both halves update with one instruction when their keys are at
@@ -757,37 +797,39 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
             // the key words are read before the first update.  Word index of
             // this lane's group: 36 half + 8t in the first round, 32 - 36 half
             // + 8t in the second, 32 (half 0) or 28 (half 1) left over.
-            int w1[4][2], w2[3][2], wl[2];
+            float* w1[4][2];
+            float* w2[3][2];
+            float* wl[2];
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
               const int kk = 36 * half + 8 * t;
-              w1[t][0] = qoff - (kinfo[kk] & 0xFFFFFF);
-              w1[t][1] = qoff - (kinfo[kk + 3] & 0xFFFFFF);
+              w1[t][0] = &bin(kk);
+              w1[t][1] = &bin(kk + 3);
             }
 #pragma unroll
             for (int t = 1; t < 4; ++t) {
               const int kk = 32 - 36 * half + 8 * t;
-              w2[t - 1][0] = qoff - (kinfo[kk] & 0xFFFFFF);
-              w2[t - 1][1] = qoff - (kinfo[kk + 3] & 0xFFFFFF);
+              w2[t - 1][0] = &bin(kk);
+              w2[t - 1][1] = &bin(kk + 3);
             }
             {
               const int kk = half ? 28 : 32;
-              wl[0] = qoff - (kinfo[kk] & 0xFFFFFF);
-              wl[1] = qoff - (kinfo[kk + 3] & 0xFFFFFF);
+              wl[0] = &bin(kk);
+              wl[1] = &bin(kk + 3);
             }
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
-              mybins[w1[t][0]] += half ? fa[1][t] : fa[0][t];
-              mybins[w1[t][1]] += half ? fb[1][t] : fb[0][t];
+              *w1[t][0] += half ? fa[1][t] : fa[0][t];
+              *w1[t][1] += half ? fb[1][t] : fb[0][t];
             }
 #pragma unroll
             for (int t = 1; t < 4; ++t) {
-              mybins[w2[t - 1][0]] += half ? fa[0][t - 1] : fa[1][t];
-              mybins[w2[t - 1][1]] += half ? fb[0][t - 1] : fb[1][t];
+              *w2[t - 1][0] += half ? fa[0][t - 1] : fa[1][t];
+              *w2[t - 1][1] += half ? fb[0][t - 1] : fb[1][t];
             }
-            if (half == 0) { mybins[wl[0]] += fa[1][0]; mybins[wl[1]] += fb[1][0]; }
+            if (half == 0) { *wl[0] += fa[1][0]; *wl[1] += fb[1][0]; }
             __builtin_amdgcn_wave_barrier();
-            if (half == 1) { mybins[wl[0]] += fa[0][3]; mybins[wl[1]] += fb[0][3]; }
+            if (half == 1) { *wl[0] += fa[0][3]; *wl[1] += fb[0][3]; }
             __builtin_amdgcn_wave_barrier();
           } else {
 #pragma unroll
@@ -828,7 +870,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
 #pragma unroll
                   for (int x = 1; x < 3; ++x)
                     if (run < x && rest < 3 - x && dsb[kb][4 * g4 + x] != 0.0f)
-                      mybins[qoff - (kinfo[kk + x] & 0xFFFFFF)] += dsb[kb][4 * g4 + x];
+                      bin(kk + x) += dsb[kb][4 * g4 + x];
                 }
             }
             __builtin_amdgcn_wave_barrier();
@@ -842,8 +884,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
             for (int kb = 0; kb < kTile / 32; ++kb)
 #pragma unroll
               for (int r = 0; r < 16; ++r) {
-                const int inf = kinfo[kb * 32 + acc_row(r, half)];
-                if (dsb[kb][r] != 0.0f) mybins[qoff - (inf & 0xFFFFFF)] += dsb[kb][r];
+                if (dsb[kb][r] != 0.0f) bin(kb * 32 + acc_row(r, half)) += dsb[kb][r];
               }
           }
           __builtin_amdgcn_wave_barrier();
@@ -1117,7 +1158,7 @@ template <typename T, int HD>
 static size_t dq_lds(const Geo& g) {
   constexpr int kTile = tile_of<T, HD>();
   const int nt = dq_tiles<T, HD>(g);
-  return sizeof(T) * (2 * nt * kTile * (HD + kPad) + ttile_size<T, HD>()) + 4 * nt * kTile +
+  return sizeof(T) * (2 * nt * kTile * (HD + kPad) + ttile_size<T, HD>()) + 8 * nt * kTile +
          4 * (g.nbins + 4) + 16 * g.nbins + 4 * g.wh * g.ww;
 }
 template <typename T, int HD>
