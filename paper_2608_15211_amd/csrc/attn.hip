@@ -237,6 +237,26 @@ __device__ inline f32x16 bias_init_nb(const int* kinfo, const int* knb, const ch
   return c;
 }
 
+// The key-major form (lane = key, registers = queries of query block QB):
+// qnb[t] = 4 x (offset of query t), tabk the lane's row of the forward-order
+// table in bytes.
+template <bool QUAD, bool MASK>
+__device__ inline f32x16 bias_init_t_nb(const int* qinfo, const int* qnb, const char* tabk, int qb,
+                                        int half, int klab) {
+  f32x16 c;
+#pragma unroll
+  for (int g4 = 0; g4 < 4; ++g4) {
+    const int qq = 32 * qb + 8 * g4 + 4 * half;
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+      const int qx = QUAD ? qq : qq + x;
+      c[4 * g4 + x] = reinterpret_cast<const float*>(tabk + qnb[qx])[QUAD ? x : 0];
+      if (MASK && (qinfo[qx] >> 24) != klab) c[4 * g4 + x] = -INFINITY;
+    }
+  }
+  return c;
+}
+
 // ---------------------------------------------------------------------------
 // Forward.  Grid: B * nwin * heads * nqc workgroups (nqc query chunks of 128
 // per window, empty chunks of small windows exit at once).  The bias enters
@@ -934,7 +954,8 @@ __global__ __launch_bounds__(kThreads, sizeof(T) == 2 ? 2 : 1) void bwd_dkdv_ker
   T* qtt = dr + kTile * (HD + kPad);                  // Q^T (transposed tile, fp32)
   T* dtt = qtt + ttile_size<T, HD>();                // dO^T (fp32)
   int* qinfo = reinterpret_cast<int*>(dtt + ttile_size<T, HD>());
-  float* ql = reinterpret_cast<float*>(qinfo + kTile);   // lse2 per query
+  int* qnb = qinfo + kTile;                               // 4 x bias offset per query
+  float* ql = reinterpret_cast<float*>(qnb + kTile);     // lse2 per query
   float* qd = ql + kTile;                                 // -D per query
   float* tab = qd + kTile;                                // [nbins+4], forward order
   uint32_t* tt = reinterpret_cast<uint32_t*>(tab + g.nbins + 4);   // [wh*ww] token offsets
@@ -964,6 +985,7 @@ __global__ __launch_bounds__(kThreads, sizeof(T) == 2 ? 2 : 1) void bwd_dkdv_ker
   const int kinf = token_info(g, i, j, cols, kvalid ? ki : 0, n);
   const int klab = kvalid ? (kinf >> 24) : 0xFE;
   const int kfwd = (g.wh - 1) * g.bstride + (g.ww - 1) - (kinf & 0xFFFFFF);
+  const char* tabk = reinterpret_cast<const char*>(tab + kfwd);
   const float inv_sl2 = 1.0f / scale_log2;
 
   typename Operand<T>::type kop[HD / 16], vop[HD / 16];
@@ -1021,11 +1043,14 @@ __global__ __launch_bounds__(kThreads, sizeof(T) == 2 ? 2 : 1) void bwd_dkdv_ker
     if (threadIdx.x < kTile) {
       if constexpr (kTab) {
         qinfo[threadIdx.x] = winf;
+        qnb[threadIdx.x] = 4 * (winf & 0xFFFFFF);
         ql[threadIdx.x] = wl;
         qd[threadIdx.x] = wd;
       } else {
         const int t = t0 + threadIdx.x;
-        qinfo[threadIdx.x] = token_info(g, i, j, cols, t, n);
+        const int inf = token_info(g, i, j, cols, t, n);
+        qinfo[threadIdx.x] = inf;
+        qnb[threadIdx.x] = 4 * (inf & 0xFFFFFF);
         const int64_t li = t < n ? wt.lse_at(g, h, t) : 0;
         ql[threadIdx.x] = t < n ? lse[li] * kLog2e : INFINITY;
         qd[threadIdx.x] = t < n ? -D[li] : 0.0f;
@@ -1064,8 +1089,14 @@ __global__ __launch_bounds__(kThreads, sizeof(T) == 2 ? 2 : 1) void bwd_dkdv_ker
         }
         __builtin_amdgcn_sched_barrier(0);
       }
-      f32x16 s = mask ? bias_init_t<QUAD, true>(qinfo, tab, qb, half, kfwd, klab, g.nbins)
-                      : bias_init_t<QUAD, false>(qinfo, tab, qb, half, kfwd, klab, g.nbins);
+      // (the byte-offset form costs head dim 128 extra spill)
+      f32x16 s;
+      if constexpr (HD <= 64)
+        s = mask ? bias_init_t_nb<QUAD, true>(qinfo, qnb, tabk, qb, half, klab)
+                 : bias_init_t_nb<QUAD, false>(qinfo, qnb, tabk, qb, half, klab);
+      else
+        s = mask ? bias_init_t<QUAD, true>(qinfo, tab, qb, half, kfwd, klab, g.nbins)
+                 : bias_init_t<QUAD, false>(qinfo, tab, qb, half, kfwd, klab, g.nbins);
       f32x16 dp, lq;
 #pragma unroll
       for (int g4 = 0; g4 < 4; ++g4) {
@@ -1164,7 +1195,7 @@ static size_t dq_lds(const Geo& g) {
 template <typename T, int HD>
 static size_t dkdv_lds(const Geo& g) {
   constexpr int kTile = tile_of<T, HD>();
-  return sizeof(T) * (2 * kTile * (HD + kPad) + 2 * ttile_size<T, HD>()) + 12 * kTile + 4 * (g.nbins + 4) +
+  return sizeof(T) * (2 * kTile * (HD + kPad) + 2 * ttile_size<T, HD>()) + 16 * kTile + 4 * (g.nbins + 4) +
          (HD > 64 ? 4 * g.wh * g.ww : 0);    // token table (head dim 128 only)
 }
 
