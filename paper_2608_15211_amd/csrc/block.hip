@@ -38,6 +38,10 @@ struct Mat {
   const bf16* p;
   int ld;
   int rows;
+  // Three-part operand (read only by SEG kernels): three [rows][segw]
+  // matrices side by side, part i at element offset i * segstride from p.
+  int segw;
+  int64_t segstride;
   __device__ const bf16* at(int r, int c) const { return p + (int64_t)r * ld + c; }
 };
 
@@ -163,7 +167,7 @@ __device__ inline bf16x8 tr_operand(const bf16* T, int k0, int m0, int lane) {
 // memory rows.
 template <int R, bool KROW>
 __device__ inline void stage_direct(const i32x4& rs, const Mat& X, bf16* tile, int r0, int k0, int nouter,
-                                    int kend) {
+                                    int kend, int64_t base = 0) {
   typedef Tile<R, KROW> T;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // uniform: the LDS base goes to M0
 #pragma unroll
@@ -172,7 +176,7 @@ __device__ inline void stage_direct(const i32x4& rs, const Mat& X, bf16* tile, i
     int mr, mc;
     T::slot_src(q, r0, k0, mr, mc);
     const bool ok = KROW ? (mr < nouter && mc < kend) : (mr < kend && mc < nouter);
-    const int voff = ok ? (int)(((int64_t)mr * X.ld + mc) * 2) : (int)0x80000000;
+    const int voff = ok ? (int)((base + (int64_t)mr * X.ld + mc) * 2) : (int)0x80000000;
     bf16* dst = tile + 8 * (u * kGT + wave * 64);      // wave-uniform base of 64 slots
     raw_buffer_load_lds(rs, (__attribute__((address_space(3))) uint32_t*)(uintptr_t)(uint32_t)(uintptr_t)dst, 16,
                         voff, 0, 0, 0);
@@ -185,7 +189,10 @@ __device__ inline void stage_direct(const i32x4& rs, const Mat& X, bf16* tile, i
 // contraction slice [z * kslice, (z+1) * kslice).  Three LDS stages: the
 // loads of stage kt + 2 are in flight while stage kt is on the matrix
 // cores.  Eight waves, each a 128 x 64 block of the 256 x 256 tile.
-template <bool AKROW, bool BKROW, int EPI>
+// SEG: A is a three-part operand split along K (AKROW; A.segw a multiple of
+// kBK) or along M (else; A.segw a multiple of kBM), so that every stage
+// (AKROW) or every workgroup tile (else) reads one part.
+template <bool AKROW, bool BKROW, int EPI, bool SEG = false>
 __global__ __launch_bounds__(kGT, 1) void gemm_kernel(Mat A, Mat B, EpiArgs ep, int M, int N, int K, int kslice) {
   typedef Tile<kBM, AKROW> TA;
   typedef Tile<kBN, BKROW> TB;
@@ -206,7 +213,7 @@ __global__ __launch_bounds__(kGT, 1) void gemm_kernel(Mat A, Mat B, EpiArgs ep, 
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int wm = (wave >> 2) * 128, wn = (wave & 3) * 64;
-  const i32x4 rsa = buffer_rsrc(A.p, (uint32_t)((int64_t)A.rows * A.ld * 2));
+  const i32x4 rsa = buffer_rsrc(A.p, (uint32_t)(((int64_t)A.rows * A.ld + (SEG ? 2 * A.segstride : 0)) * 2));
   const i32x4 rsb = buffer_rsrc(B.p, (uint32_t)((int64_t)B.rows * B.ld * 2));
 
   f32x16 acc[4][2];
@@ -219,7 +226,17 @@ __global__ __launch_bounds__(kGT, 1) void gemm_kernel(Mat A, Mat B, EpiArgs ep, 
   auto b_tile = [&](int st) { return lds + st * kStage + TA::kElems; };
   auto issue = [&](int s) {
     const int k0 = kbeg + s * kBK;
-    stage_direct<kBM, AKROW>(rsa, A, a_tile(s % 3), m0, k0, M, kend);
+    if constexpr (SEG && AKROW) {
+      const int seg = k0 / A.segw;
+      stage_direct<kBM, true>(rsa, A, a_tile(s % 3), m0, k0 - seg * A.segw, M, min(kend - seg * A.segw, A.segw),
+                              seg * A.segstride);
+    } else if constexpr (SEG) {
+      const int seg = m0 / A.segw;
+      stage_direct<kBM, false>(rsa, A, a_tile(s % 3), m0 - seg * A.segw, k0, min(M - seg * A.segw, A.segw), kend,
+                               seg * A.segstride);
+    } else {
+      stage_direct<kBM, AKROW>(rsa, A, a_tile(s % 3), m0, k0, M, kend);
+    }
     stage_direct<kBN, BKROW>(rsb, B, b_tile(s % 3), n0, k0, N, kend);
   };
 
@@ -561,13 +578,13 @@ __global__ __launch_bounds__(kRowThreads) void slice_sum_kernel(const float* __r
 // ---------------------------------------------------------------------------
 constexpr size_t kGemmLds = 3 * (size_t)(kBM + kBN) * kBK * sizeof(bf16);   // three stages (96 KB)
 
-template <bool AKROW, bool BKROW, int EPI>
+template <bool AKROW, bool BKROW, int EPI, bool SEG = false>
 static hipError_t gemm(const Mat& A, const Mat& B, const EpiArgs& ep, int M, int N, int K, int nsplit,
                        hipStream_t st) {
   const int tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
   const int kslice = ((K + nsplit - 1) / nsplit + kBK - 1) / kBK * kBK;
-  hipLaunchKernelGGL((gemm_kernel<AKROW, BKROW, EPI>), dim3(tiles, 1, nsplit), dim3(kGT), kGemmLds, st, A, B, ep, M,
-                     N, K, kslice);
+  hipLaunchKernelGGL((gemm_kernel<AKROW, BKROW, EPI, SEG>), dim3(tiles, 1, nsplit), dim3(kGT), kGemmLds, st, A, B, ep,
+                     M, N, K, kslice);
   return hipGetLastError();
 }
 
@@ -577,6 +594,8 @@ static Mat mat(const void* p, int ld, int rows) {
   m.p = (const bf16*)p;
   m.ld = ld;
   m.rows = rows;
+  m.segw = 0;
+  m.segstride = 0;
   return m;
 }
 
@@ -710,7 +729,8 @@ static BwdWs block_ws(const Geo& geo) {
   w.attn = off; off += al(bwd_workspace(g, 1));
   size_t wmax = 0;                       // largest slices x output of the block's weight gradients
   for (int i = 0; i < 4; ++i) {
-    const int nl = i == 0 ? (int)C : (i == 1 ? 4 * (int)C : (int)C), kl = i == 0 ? 4 * (int)C : (int)C;
+    const int nl = i == 0 ? (int)C : (i == 1 ? 4 * (int)C : (i == 2 ? 3 * (int)C : (int)C));
+    const int kl = i == 0 ? 4 * (int)C : (int)C;
     wmax = std::max(wmax, (size_t)wgrad_slices((int)T, nl, kl, w.wsplit) * nl * kl);
   }
   w.wpart = off; off += al(wmax * 4);
@@ -765,6 +785,25 @@ static hipError_t wgrad(const Mat& dY, const Mat& Z, int T, int Nl, int Kl, floa
   hipError_t e = gemm<false, false, EPI_F32>(dY, Z, ep, Nl, Kl, T, ns, st);
   if (e != hipSuccess) return e;
   return slice_sum(part, dW, (int64_t)Nl * Kl, ns, st);
+}
+
+// The three-part operand's buffer resource covers 2 segstride + T C
+// elements; its byte offsets must stay below 2^31.
+static bool seg_fits(int T, int C, int64_t segstride) {
+  return (2 * segstride + (int64_t)T * C) * 2 < ((int64_t)1 << 31);
+}
+
+// dWqkv[3C][C] = [dQ dK dV]^T Z over all tokens in one product (dy3: the
+// three-part T x 3C operand), in token slices reduced in slice order.
+static hipError_t wgrad3(const Mat& dy3, const Mat& Z, int T, int C, float* dW, char* ws, const BwdWs& w,
+                         hipStream_t st) {
+  EpiArgs ep = {};
+  float* part = reinterpret_cast<float*>(ws + w.wpart);
+  ep.outf = part;
+  const int ns = wgrad_slices(T, 3 * C, C, w.wsplit);
+  hipError_t e = gemm<false, false, EPI_F32, true>(dy3, Z, ep, 3 * C, C, T, ns, st);
+  if (e != hipSuccess) return e;
+  return slice_sum(part, dW, (int64_t)3 * C * C, ns, st);
 }
 
 static hipError_t ln_apply(const void* z, const float* mu, const float* rs, const float* gamma, const float* beta,
@@ -826,18 +865,33 @@ hipError_t launch_block_bwd(const Geo& g, const void* dx2, const void* x, const 
   // [iC, (i+1)C) of dWqkv = dY_i^T LN1(x), of dbqkv = colsum(dY_i), and
   // dln1 = sum_i dY_i Wqkv[iC:(i+1)C]
   TERRA_TRY(ln_apply(x, s.mu1, s.rstd1, p.ln1_g, p.ln1_b, lnb, T, C, st));
+  // dQ, dK, dV sit at equal strides in the workspace: one T x 3C operand of
+  // three parts, so that dWqkv is one product over all tokens and dln one
+  // product over 3C (instead of three, two of them adding float32 results)
+  Mat dy3 = mat(dqkv[0], C, T);
+  dy3.segw = C;
+  dy3.segstride = (int64_t)(w.dk - w.dq) / 2;
+  const bool seg_w = C % kBM == 0 && seg_fits(T, C, dy3.segstride);
+  const bool seg_d = C % kBK == 0 && seg_fits(T, C, dy3.segstride);
+  if (seg_w) {
+    TERRA_TRY(wgrad3(dy3, mat(lnb, C, T), T, C, gr.w_qkv, ws, w, st));
+  }
   for (int i = 0; i < 3; ++i) {
-    TERRA_TRY(wgrad(mat(dqkv[i], C, T), mat(lnb, C, T), T, C, C, gr.w_qkv + (size_t)i * C * C, ws, w, st));
+    if (!seg_w) TERRA_TRY(wgrad(mat(dqkv[i], C, T), mat(lnb, C, T), T, C, C, gr.w_qkv + (size_t)i * C * C, ws, w, st));
     TERRA_TRY(colsum(mat(dqkv[i], C, T), C, cpart, gr.b_qkv + (size_t)i * C, w, st));
   }
   ep = EpiArgs{};
   ep.outf = dln;
-  for (int i = 0; i < 3; ++i) {
-    const bf16* wi = reinterpret_cast<const bf16*>(p.w_qkv) + (size_t)i * C * C;
-    if (i == 0) {
-      TERRA_TRY((gemm<true, false, EPI_F32>(mat(dqkv[i], C, T), mat(wi, C, C), ep, T, C, C, 1, st)));
-    } else {
-      TERRA_TRY((gemm<true, false, EPI_F32_ACC>(mat(dqkv[i], C, T), mat(wi, C, C), ep, T, C, C, 1, st)));
+  if (seg_d) {
+    TERRA_TRY((gemm<true, false, EPI_F32, true>(dy3, mat(p.w_qkv, C, 3 * C), ep, T, C, 3 * C, 1, st)));
+  } else {
+    for (int i = 0; i < 3; ++i) {
+      const bf16* wi = reinterpret_cast<const bf16*>(p.w_qkv) + (size_t)i * C * C;
+      if (i == 0) {
+        TERRA_TRY((gemm<true, false, EPI_F32>(mat(dqkv[i], C, T), mat(wi, C, C), ep, T, C, C, 1, st)));
+      } else {
+        TERRA_TRY((gemm<true, false, EPI_F32_ACC>(mat(dqkv[i], C, T), mat(wi, C, C), ep, T, C, C, 1, st)));
+      }
     }
   }
   // dx = dx1 + LN1 backward
