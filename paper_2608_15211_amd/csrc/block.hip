@@ -573,6 +573,26 @@ __global__ __launch_bounds__(kRowThreads) void slice_sum_kernel(const float* __r
   out[i] = acc;
 }
 
+// out[c][r] = in[r][c] for a rows x cols bf16 matrix: the backward's copies
+// of the weights in [N][K] order, so that its data-gradient products read
+// their B operand with straight rather than transposed LDS reads (a few MB,
+// once per backward).
+__global__ __launch_bounds__(256) void transpose_kernel(const bf16* __restrict__ in, bf16* __restrict__ out,
+                                                        int rows, int cols) {
+  __shared__ bf16 t[32][33];
+  const int c0 = blockIdx.x * 32, r0 = blockIdx.y * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  for (int y = ty; y < 32; y += 8) {
+    const int r = r0 + y, c = c0 + tx;
+    if (r < rows && c < cols) t[y][tx] = in[(int64_t)r * cols + c];
+  }
+  __syncthreads();
+  for (int y = ty; y < 32; y += 8) {
+    const int c = c0 + y, r = r0 + tx;
+    if (c < cols && r < rows) out[(int64_t)c * rows + r] = t[tx][y];
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Host side.
 // ---------------------------------------------------------------------------
@@ -700,7 +720,7 @@ static int wgrad_slices(int T, int Nl, int Kl, int cap) {
 
 // Backward workspace layout (bytes, 256-aligned pieces).
 struct BwdWs {
-  size_t dh, dln, dx1, dO, dq, dk, dv, ln, attn, wpart, cpart, lpart, total;
+  size_t dh, dln, dx1, dO, dq, dk, dv, ln, wt, attn, wpart, cpart, lpart, total;
   int wsplit, cslices, lnwaves, rows_per_wave, cpart_rows, lgroups;
 };
 
@@ -726,6 +746,7 @@ static BwdWs block_ws(const Geo& geo) {
   w.dk = off; off += al(T * C * 2);
   w.dv = off; off += al(T * C * 2);
   w.ln = off; off += al(T * C * 2);
+  w.wt = off; off += al(12 * C * C * 2);  // transposed W_fc2, W_fc1, W_proj, W_qkv
   w.attn = off; off += al(bwd_workspace(g, 1));
   size_t wmax = 0;                       // largest slices x output of the block's weight gradients
   for (int i = 0; i < 4; ++i) {
@@ -806,6 +827,12 @@ static hipError_t wgrad3(const Mat& dy3, const Mat& Z, int T, int C, float* dW, 
   return slice_sum(part, dW, (int64_t)3 * C * C, ns, st);
 }
 
+static hipError_t transpose(const void* in, bf16* out, int rows, int cols, hipStream_t st) {
+  hipLaunchKernelGGL(transpose_kernel, dim3((cols + 31) / 32, (rows + 31) / 32), dim3(256), 0, st, (const bf16*)in,
+                     out, rows, cols);
+  return hipGetLastError();
+}
+
 static hipError_t ln_apply(const void* z, const float* mu, const float* rs, const float* gamma, const float* beta,
                            bf16* out, int T, int C, hipStream_t st) {
   const int64_t n = (int64_t)T * (C / 8);
@@ -835,18 +862,27 @@ hipError_t launch_block_bwd(const Geo& g, const void* dx2, const void* x, const 
   do {                                  \
     if ((e = (x)) != hipSuccess) return e; \
   } while (0)
+  // the weights in [N][K] order for the data-gradient products
+  bf16* wt_fc2 = reinterpret_cast<bf16*>(ws + w.wt);        // [4C][C]
+  bf16* wt_fc1 = wt_fc2 + (size_t)4 * C * C;                // [C][4C]
+  bf16* wt_proj = wt_fc1 + (size_t)4 * C * C;               // [C][C]
+  bf16* wt_qkv = wt_proj + (size_t)C * C;                   // [C][3C]
+  TERRA_TRY(transpose(p.w_fc2, wt_fc2, C, 4 * C, st));
+  TERRA_TRY(transpose(p.w_fc1, wt_fc1, 4 * C, C, st));
+  TERRA_TRY(transpose(p.w_proj, wt_proj, C, C, st));
+  TERRA_TRY(transpose(p.w_qkv, wt_qkv, 3 * C, C, st));
   // x2 = x1 + a W2^T + b2:  dW2 = dx2^T a, db2 = colsum(dx2), dh = (dx2 W2) * GELU'(h)
   TERRA_TRY(wgrad(mat(dx2, C, T), mat(s.a, 4 * C, T), T, C, 4 * C, gr.w_fc2, ws, w, st));
   TERRA_TRY(colsum(mat(dx2, C, T), C, cpart, gr.b_fc2, w, st));
   ep.out[0] = dh; ep.split = 4 * C; ep.aux = (const bf16*)s.h;
-  TERRA_TRY((gemm<true, false, EPI_GELU_GRAD>(mat(dx2, C, T), mat(p.w_fc2, 4 * C, C), ep, T, 4 * C, C, 1, st)));
+  TERRA_TRY((gemm<true, true, EPI_GELU_GRAD>(mat(dx2, C, T), mat(wt_fc2, C, 4 * C), ep, T, 4 * C, C, 1, st)));
   // h = LN2(x1) W1^T + b1:  dW1 = dh^T LN2(x1), db1 = colsum(dh), dln2 = dh W1
   TERRA_TRY(ln_apply(s.x1, s.mu2, s.rstd2, p.ln2_g, p.ln2_b, lnb, T, C, st));
   TERRA_TRY(wgrad(mat(dh, 4 * C, T), mat(lnb, C, T), T, 4 * C, C, gr.w_fc1, ws, w, st));
   TERRA_TRY(colsum(mat(dh, 4 * C, T), 4 * C, cpart, gr.b_fc1, w, st));
   ep = EpiArgs{};
   ep.outf = dln;
-  TERRA_TRY((gemm<true, false, EPI_F32>(mat(dh, 4 * C, T), mat(p.w_fc1, C, 4 * C), ep, T, C, 4 * C, 1, st)));
+  TERRA_TRY((gemm<true, true, EPI_F32>(mat(dh, 4 * C, T), mat(wt_fc1, 4 * C, C), ep, T, C, 4 * C, 1, st)));
   // dx1 = dx2 + LN2 backward
   hipLaunchKernelGGL(ln_bwd_kernel, dim3(w.lnwaves / 4), dim3(kRowThreads), 0, st, dln, (const bf16*)s.x1, s.mu2,
                      s.rstd2, p.ln2_g, (const bf16*)dx2, dx1, lpart, T, C, w.rows_per_wave);
@@ -857,7 +893,7 @@ hipError_t launch_block_bwd(const Geo& g, const void* dx2, const void* x, const 
   TERRA_TRY(colsum(mat(dx1, C, T), C, cpart, gr.b_proj, w, st));
   ep = EpiArgs{};
   ep.out[0] = dO; ep.split = C;
-  TERRA_TRY((gemm<true, false, EPI_BF16>(mat(dx1, C, T), mat(p.w_proj, C, C), ep, T, C, C, 1, st)));
+  TERRA_TRY((gemm<true, true, EPI_BF16>(mat(dx1, C, T), mat(wt_proj, C, C), ep, T, C, C, 1, st)));
   // attention backward (route fused in)
   TERRA_TRY(launch_attn_bwd(g, 1, true, s.q, s.k, s.v, s.o, nullptr, dO, s.lse, table, dqkv[0], dqkv[1],
                             dqkv[2], dtable, ws + w.attn, st));
@@ -883,7 +919,7 @@ hipError_t launch_block_bwd(const Geo& g, const void* dx2, const void* x, const 
   ep = EpiArgs{};
   ep.outf = dln;
   if (seg_d) {
-    TERRA_TRY((gemm<true, false, EPI_F32, true>(dy3, mat(p.w_qkv, C, 3 * C), ep, T, C, 3 * C, 1, st)));
+    TERRA_TRY((gemm<true, true, EPI_F32, true>(dy3, mat(wt_qkv, 3 * C, C), ep, T, C, 3 * C, 1, st)));
   } else {
     for (int i = 0; i < 3; ++i) {
       const bf16* wi = reinterpret_cast<const bf16*>(p.w_qkv) + (size_t)i * C * C;
