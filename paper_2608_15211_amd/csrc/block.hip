@@ -712,7 +712,9 @@ hipError_t launch_block_fwd(const Geo& g, const void* x, const BlockParams& p, c
 // Token slices of a weight gradient dW[Nl][Kl] over T tokens.
 static int wgrad_slices(int T, int Nl, int Kl, int cap) {
   const int tiles = ((Nl + kBM - 1) / kBM) * ((Kl + kBN - 1) / kBN);
-  int n = (2 * kMaxCusBlock + tiles - 1) / tiles;         // about two workgroups per CU
+  // two whole rounds of one workgroup per CU (a third, nearly empty round
+  // would leave most CUs idle for a whole slice)
+  int n = (2 * kMaxCusBlock) / tiles;
   const int per = (T + n - 1) / n;
   if (per < 4 * kBK) n = (T + 4 * kBK - 1) / (4 * kBK);  // at least four stages a slice
   return n < 1 ? 1 : (n > cap ? cap : n);
