@@ -520,6 +520,15 @@ __global__ __launch_bounds__(kRowThreads) void colsum_kernel(Mat X, int ncols, f
   if (8 * c8 >= ncols) return;
   const int s = blockIdx.y;
   const int r0 = s * rows_per, r1 = min(X.rows, r0 + rows_per);
+  // a three-part X (segw > 0): column c of part c / segw
+  const bf16* xb = X.p;
+  int col = 8 * c8;
+  if (X.segw > 0) {
+    const int sg = col / X.segw;
+    xb += sg * X.segstride;
+    col -= sg * X.segw;
+  }
+  auto at = [&](int r) { return reinterpret_cast<const bf16x8*>(xb + (int64_t)r * X.ld + col); };
   // four independent partial sums (rows r, r+1, r+2, r+3 of each step), so
   // that four loads are in flight; combined in a fixed order at the end
   float acc[4][8] = {};
@@ -527,14 +536,14 @@ __global__ __launch_bounds__(kRowThreads) void colsum_kernel(Mat X, int ncols, f
   for (; r + 4 <= r1; r += 4) {
     bf16x8 v[4];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) v[u] = *reinterpret_cast<const bf16x8*>(X.at(r + u, 8 * c8));
+    for (int u = 0; u < 4; ++u) v[u] = *at(r + u);
 #pragma unroll
     for (int u = 0; u < 4; ++u)
 #pragma unroll
       for (int i = 0; i < 8; ++i) acc[u][i] += (float)v[u][i];
   }
   for (; r < r1; ++r) {
-    const bf16x8 v = *reinterpret_cast<const bf16x8*>(X.at(r, 8 * c8));
+    const bf16x8 v = *at(r);
 #pragma unroll
     for (int i = 0; i < 8; ++i) acc[0][i] += (float)v[i];
   }
@@ -555,22 +564,30 @@ __global__ __launch_bounds__(kRowThreads) void group_sum_kernel(const float* __r
   grp[(int64_t)g * n + i] = acc;
 }
 
-// out[i] = sum over s < nslice of part[s * stride + i], in slice order.
-__global__ __launch_bounds__(kRowThreads) void slice_sum_kernel(const float* __restrict__ part, float* __restrict__ out,
-                                                                int64_t n, int64_t stride, int nslice) {
-  const int64_t i = (int64_t)blockIdx.x * kRowThreads + threadIdx.x;
-  if (i >= n) return;
+// out[i] = sum over s < nslice of part[s * stride + i].  A workgroup takes
+// 64 consecutive i; its four waves sum the slices s = 4j + wave in order,
+// and the four sums are added in wave order (a fixed order for every i), so
+// that a long slice list is four short dependent chains.
+__global__ __launch_bounds__(256) void slice_sum_kernel(const float* __restrict__ part, float* __restrict__ out,
+                                                        int64_t n, int64_t stride, int nslice) {
+  __shared__ float red[4][64];
+  const int c = threadIdx.x & 63, q = threadIdx.x >> 6;
+  const int64_t i = (int64_t)blockIdx.x * 64 + c;
   float acc = 0.0f;
-  int s = 0;
-  for (; s + 8 <= nslice; s += 8) {
-    float v[8];
+  if (i < n) {
+    int s = q;
+    for (; s + 28 < nslice; s += 32) {
+      float v[8];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) v[u] = part[(int64_t)(s + u) * stride + i];
+      for (int u = 0; u < 8; ++u) v[u] = part[(int64_t)(s + 4 * u) * stride + i];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) acc += v[u];
+      for (int u = 0; u < 8; ++u) acc += v[u];
+    }
+    for (; s < nslice; s += 4) acc += part[(int64_t)s * stride + i];
   }
-  for (; s < nslice; ++s) acc += part[(int64_t)s * stride + i];
-  out[i] = acc;
+  red[q][c] = acc;
+  __syncthreads();
+  if (q == 0 && i < n) out[i] = ((red[0][c] + red[1][c]) + red[2][c]) + red[3][c];
 }
 
 // out[c][r] = in[r][c] for a rows x cols bf16 matrix: the backward's copies
@@ -767,8 +784,8 @@ size_t block_bwd_workspace(const Geo& g) { return block_ws(g).total; }
 
 static hipError_t slice_sum(const float* part, float* out, int64_t n, int nslice, hipStream_t st,
                             int64_t stride = -1) {
-  hipLaunchKernelGGL(slice_sum_kernel, dim3((unsigned)((n + kRowThreads - 1) / kRowThreads)), dim3(kRowThreads), 0,
-                     st, part, out, n, stride < 0 ? n : stride, nslice);
+  hipLaunchKernelGGL(slice_sum_kernel, dim3((unsigned)((n + 63) / 64)), dim3(256), 0, st, part, out, n,
+                     stride < 0 ? n : stride, nslice);
   return hipGetLastError();
 }
 
@@ -914,10 +931,11 @@ hipError_t launch_block_bwd(const Geo& g, const void* dx2, const void* x, const 
   if (seg_w) {
     TERRA_TRY(wgrad3(dy3, mat(lnb, C, T), T, C, gr.w_qkv, ws, w, st));
   }
-  for (int i = 0; i < 3; ++i) {
-    if (!seg_w) TERRA_TRY(wgrad(mat(dqkv[i], C, T), mat(lnb, C, T), T, C, C, gr.w_qkv + (size_t)i * C * C, ws, w, st));
-    TERRA_TRY(colsum(mat(dqkv[i], C, T), C, cpart, gr.b_qkv + (size_t)i * C, w, st));
+  if (!seg_w) {
+    for (int i = 0; i < 3; ++i)
+      TERRA_TRY(wgrad(mat(dqkv[i], C, T), mat(lnb, C, T), T, C, C, gr.w_qkv + (size_t)i * C * C, ws, w, st));
   }
+  TERRA_TRY(colsum(dy3, 3 * C, cpart, gr.b_qkv, w, st));
   ep = EpiArgs{};
   ep.outf = dln;
   if (seg_d) {
