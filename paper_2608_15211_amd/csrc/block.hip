@@ -28,7 +28,7 @@ typedef __attribute__((address_space(3))) v4s lds_v4s;
 
 constexpr int kGT = 512;          // threads per GEMM workgroup (8 waves: 2 rows x 4 columns of 128 x 64)
 constexpr int kBM = 256;          // workgroup tile rows
-constexpr int kBN = 256;          // workgroup tile columns
+constexpr int kBN = 256;          // workgroup tile columns (128 in the four-wave form)
 constexpr int kBK = 32;           // contraction depth per stage
 constexpr int kEpiS = 68;         // row stride (floats) of a wave's epilogue staging tile
 constexpr int kMaxCusBlock = 256;  // compute units the weight-gradient slices are sized for
@@ -108,10 +108,10 @@ __device__ inline float gelu_grad_f(float x) {
 //   with c ^ (2 (k & 3)) 0.8-2 conflict cycles per LDS instruction, though
 //   no slower).
 // ---------------------------------------------------------------------------
-template <int R, bool KROW>
+template <int R, bool KROW, int NT = kGT>
 struct Tile {
   static constexpr int kChunks = R * kBK / 8;   // 16-byte chunks
-  static constexpr int kPer = kChunks / kGT;    // per thread
+  static constexpr int kPer = kChunks / NT;     // per thread (NT threads)
   static constexpr int kElems = R * kBK;
   // element offset of (row, logical chunk) of the memory layout
   __device__ static int off(int row, int c) {
@@ -165,19 +165,19 @@ __device__ inline bf16x8 tr_operand(const bf16* T, int k0, int m0, int lane) {
 // written by thread q % kGT, load q / kGT); chunks outside the operand or
 // the contraction slice read zeros.  KROW: the contraction index runs along
 // memory rows.
-template <int R, bool KROW>
+template <int R, bool KROW, int NT = kGT>
 __device__ inline void stage_direct(const i32x4& rs, const Mat& X, bf16* tile, int r0, int k0, int nouter,
                                     int kend, int64_t base = 0) {
-  typedef Tile<R, KROW> T;
+  typedef Tile<R, KROW, NT> T;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // uniform: the LDS base goes to M0
 #pragma unroll
   for (int u = 0; u < T::kPer; ++u) {
-    const int q = u * kGT + threadIdx.x;
+    const int q = u * NT + threadIdx.x;
     int mr, mc;
     T::slot_src(q, r0, k0, mr, mc);
     const bool ok = KROW ? (mr < nouter && mc < kend) : (mr < kend && mc < nouter);
     const int voff = ok ? (int)((base + (int64_t)mr * X.ld + mc) * 2) : (int)0x80000000;
-    bf16* dst = tile + 8 * (u * kGT + wave * 64);      // wave-uniform base of 64 slots
+    bf16* dst = tile + 8 * (u * NT + wave * 64);       // wave-uniform base of 64 slots
     raw_buffer_load_lds(rs, (__attribute__((address_space(3))) uint32_t*)(uintptr_t)(uint32_t)(uintptr_t)dst, 16,
                         voff, 0, 0, 0);
   }
@@ -192,27 +192,34 @@ __device__ inline void stage_direct(const i32x4& rs, const Mat& X, bf16* tile, i
 // SEG: A is a three-part operand split along K (AKROW; A.segw a multiple of
 // kBK) or along M (else; A.segw a multiple of kBM), so that every stage
 // (AKROW) or every workgroup tile (else) reads one part.
-template <bool AKROW, bool BKROW, int EPI, bool SEG = false>
-__global__ __launch_bounds__(kGT, 1) void gemm_kernel(Mat A, Mat B, EpiArgs ep, int M, int N, int K, int kslice) {
-  typedef Tile<kBM, AKROW> TA;
-  typedef Tile<kBN, BKROW> TB;
+// NW = 4: four waves and a 256 x 128 tile (72 KB of stages), so that two
+// workgroups share a CU and one's prologue and epilogue (its operand
+// latency, output traffic and, for some epilogues, input traffic) overlap
+// the other's matrix work; for short contractions, where that per-tile time
+// is a large part of the whole.
+template <bool AKROW, bool BKROW, int EPI, bool SEG = false, int NW = 8>
+__global__ __launch_bounds__(NW * 64, 8 / NW) void gemm_kernel(Mat A, Mat B, EpiArgs ep, int M, int N, int K,
+                                                                int kslice) {
+  constexpr int NT = NW * 64, BN = NW * 32;
+  typedef Tile<kBM, AKROW, NT> TA;
+  typedef Tile<BN, BKROW, NT> TB;
   constexpr int kStage = TA::kElems + TB::kElems;
   constexpr int kLoads = TA::kPer + TB::kPer;
   extern __shared__ __align__(16) char smem[];
   bf16* lds = reinterpret_cast<bf16*>(smem);
 
-  const int nN = (N + kBN - 1) / kBN;
+  const int nN = (N + BN - 1) / BN;
   const int nM = (M + kBM - 1) / kBM;
   const int tiles = nM * nN;
   int w = blockIdx.x;
   if (tiles % 8 == 0) w = (blockIdx.x % 8) * (tiles / 8) + blockIdx.x / 8;   // same-XCD neighbours
   const int tm = w / nN, tn = w - (w / nN) * nN;
-  const int m0 = tm * kBM, n0 = tn * kBN;
+  const int m0 = tm * kBM, n0 = tn * BN;
   const int kbeg = blockIdx.z * kslice;
   const int kend = min(K, kbeg + kslice);
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int wm = (wave >> 2) * 128, wn = (wave & 3) * 64;
+  const int wm = (wave / (NW / 2)) * 128, wn = (wave % (NW / 2)) * 64;
   const i32x4 rsa = buffer_rsrc(A.p, (uint32_t)(((int64_t)A.rows * A.ld + (SEG ? 2 * A.segstride : 0)) * 2));
   const i32x4 rsb = buffer_rsrc(B.p, (uint32_t)((int64_t)B.rows * B.ld * 2));
 
@@ -228,16 +235,16 @@ __global__ __launch_bounds__(kGT, 1) void gemm_kernel(Mat A, Mat B, EpiArgs ep, 
     const int k0 = kbeg + s * kBK;
     if constexpr (SEG && AKROW) {
       const int seg = k0 / A.segw;
-      stage_direct<kBM, true>(rsa, A, a_tile(s % 3), m0, k0 - seg * A.segw, M, min(kend - seg * A.segw, A.segw),
-                              seg * A.segstride);
+      stage_direct<kBM, true, NT>(rsa, A, a_tile(s % 3), m0, k0 - seg * A.segw, M,
+                                  min(kend - seg * A.segw, A.segw), seg * A.segstride);
     } else if constexpr (SEG) {
       const int seg = m0 / A.segw;
-      stage_direct<kBM, false>(rsa, A, a_tile(s % 3), m0 - seg * A.segw, k0, min(M - seg * A.segw, A.segw), kend,
-                               seg * A.segstride);
+      stage_direct<kBM, false, NT>(rsa, A, a_tile(s % 3), m0 - seg * A.segw, k0, min(M - seg * A.segw, A.segw),
+                                   kend, seg * A.segstride);
     } else {
-      stage_direct<kBM, AKROW>(rsa, A, a_tile(s % 3), m0, k0, M, kend);
+      stage_direct<kBM, AKROW, NT>(rsa, A, a_tile(s % 3), m0, k0, M, kend);
     }
-    stage_direct<kBN, BKROW>(rsb, B, b_tile(s % 3), n0, k0, N, kend);
+    stage_direct<BN, BKROW, NT>(rsb, B, b_tile(s % 3), n0, k0, N, kend);
   };
 
   const int nk = (kend - kbeg + kBK - 1) / kBK;
@@ -255,7 +262,7 @@ __global__ __launch_bounds__(kGT, 1) void gemm_kernel(Mat A, Mat B, EpiArgs ep, 
       bf16x8 bo[2];
 #pragma unroll
       for (int j = 0; j < 2; ++j)
-        bo[j] = BKROW ? row_operand<kBN>(tb, 16 * c, wn + 32 * j, lane) : tr_operand<kBN>(tb, 16 * c, wn + 32 * j, lane);
+        bo[j] = BKROW ? row_operand<BN>(tb, 16 * c, wn + 32 * j, lane) : tr_operand<BN>(tb, 16 * c, wn + 32 * j, lane);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const bf16x8 ao =
@@ -613,15 +620,16 @@ __global__ __launch_bounds__(256) void transpose_kernel(const bf16* __restrict__
 // ---------------------------------------------------------------------------
 // Host side.
 // ---------------------------------------------------------------------------
-constexpr size_t kGemmLds = 3 * (size_t)(kBM + kBN) * kBK * sizeof(bf16);   // three stages (96 KB)
-
-template <bool AKROW, bool BKROW, int EPI, bool SEG = false>
+template <bool AKROW, bool BKROW, int EPI, bool SEG = false, int NW = 8>
 static hipError_t gemm(const Mat& A, const Mat& B, const EpiArgs& ep, int M, int N, int K, int nsplit,
                        hipStream_t st) {
-  const int tiles = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
+  constexpr int BN = NW * 32;
+  // three stages: 96 KB (eight waves), 72 KB (four)
+  constexpr size_t lds = 3 * (size_t)(kBM + BN) * kBK * sizeof(bf16);
+  const int tiles = ((M + kBM - 1) / kBM) * ((N + BN - 1) / BN);
   const int kslice = ((K + nsplit - 1) / nsplit + kBK - 1) / kBK * kBK;
-  hipLaunchKernelGGL((gemm_kernel<AKROW, BKROW, EPI, SEG>), dim3(tiles, 1, nsplit), dim3(kGT), kGemmLds, st, A, B, ep,
-                     M, N, K, kslice);
+  hipLaunchKernelGGL((gemm_kernel<AKROW, BKROW, EPI, SEG, NW>), dim3(tiles, 1, nsplit), dim3(NW * 64), lds, st, A, B,
+                     ep, M, N, K, kslice);
   return hipGetLastError();
 }
 
@@ -703,14 +711,14 @@ hipError_t launch_block_fwd(const Geo& g, const void* x, const BlockParams& p, c
   TERRA_TRY(ln_fold(p.w_qkv, p.ln1_g, p.ln1_b, p.b_qkv, wq, sq, cq, 3 * C, C, st));
   ep.out[0] = (bf16*)s.q; ep.out[1] = (bf16*)s.k; ep.out[2] = (bf16*)s.v; ep.split = C;
   ep.mean = s.mu1; ep.rstd = s.rstd1; ep.lns = sq; ep.lnc = cq;
-  TERRA_TRY((gemm<true, true, EPI_LN_QKV>(mat(x, C, T), mat(wq, C, 3 * C), ep,
+  TERRA_TRY((gemm<true, true, EPI_LN_QKV, false, 4>(mat(x, C, T), mat(wq, C, 3 * C), ep,
                                                                     T, 3 * C, C, 1, st)));
   // windowed attention with the route fused in
   TERRA_TRY(launch_attn_fwd(g, 1, true, s.q, s.k, s.v, table, s.o, nullptr, s.lse, st));
   // x1 = x + o W_p^T + b_p
   ep = EpiArgs{};
   ep.out[0] = (bf16*)s.x1; ep.split = C; ep.aux = (const bf16*)x; ep.bias = p.b_proj;
-  TERRA_TRY((gemm<true, true, EPI_BIAS_RES>(mat(s.o, C, T), mat(p.w_proj, C, C), ep, T, C, C, 1, st)));
+  TERRA_TRY((gemm<true, true, EPI_BIAS_RES, false, 4>(mat(s.o, C, T), mat(p.w_proj, C, C), ep, T, C, C, 1, st)));
   // h = LN2(x1) W_1^T + b_1 (LN2 folded), a = GELU(h)
   TERRA_TRY(ln_stats(s.x1, s.mu2, s.rstd2, T, C, st));
   TERRA_TRY(ln_fold(p.w_fc1, p.ln2_g, p.ln2_b, p.b_fc1, wf, sf, cf, 4 * C, C, st));
@@ -894,7 +902,7 @@ hipError_t launch_block_bwd(const Geo& g, const void* dx2, const void* x, const 
   TERRA_TRY(wgrad(mat(dx2, C, T), mat(s.a, 4 * C, T), T, C, 4 * C, gr.w_fc2, ws, w, st));
   TERRA_TRY(colsum(mat(dx2, C, T), C, cpart, gr.b_fc2, w, st));
   ep.out[0] = dh; ep.split = 4 * C; ep.aux = (const bf16*)s.h;
-  TERRA_TRY((gemm<true, true, EPI_GELU_GRAD>(mat(dx2, C, T), mat(wt_fc2, C, 4 * C), ep, T, 4 * C, C, 1, st)));
+  TERRA_TRY((gemm<true, true, EPI_GELU_GRAD, false, 4>(mat(dx2, C, T), mat(wt_fc2, C, 4 * C), ep, T, 4 * C, C, 1, st)));
   // h = LN2(x1) W1^T + b1:  dW1 = dh^T LN2(x1), db1 = colsum(dh), dln2 = dh W1
   TERRA_TRY(ln_apply(s.x1, s.mu2, s.rstd2, p.ln2_g, p.ln2_b, lnb, T, C, st));
   TERRA_TRY(wgrad(mat(dh, 4 * C, T), mat(lnb, C, T), T, 4 * C, C, gr.w_fc1, ws, w, st));
@@ -912,7 +920,7 @@ hipError_t launch_block_bwd(const Geo& g, const void* dx2, const void* x, const 
   TERRA_TRY(colsum(mat(dx1, C, T), C, cpart, gr.b_proj, w, st));
   ep = EpiArgs{};
   ep.out[0] = dO; ep.split = C;
-  TERRA_TRY((gemm<true, true, EPI_BF16>(mat(dx1, C, T), mat(wt_proj, C, C), ep, T, C, C, 1, st)));
+  TERRA_TRY((gemm<true, true, EPI_BF16, false, 4>(mat(dx1, C, T), mat(wt_proj, C, C), ep, T, C, C, 1, st)));
   // attention backward (route fused in)
   TERRA_TRY(launch_attn_bwd(g, 1, true, s.q, s.k, s.v, s.o, nullptr, dO, s.lse, table, dqkv[0], dqkv[1],
                             dqkv[2], dtable, ws + w.attn, st));
