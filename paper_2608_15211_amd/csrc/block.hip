@@ -571,11 +571,30 @@ __global__ __launch_bounds__(kRowThreads) void group_sum_kernel(const float* __r
   grp[(int64_t)g * n + i] = acc;
 }
 
-// out[i] = sum over s < nslice of part[s * stride + i].  A workgroup takes
-// 64 consecutive i; its four waves sum the slices s = 4j + wave in order,
-// and the four sums are added in wave order (a fixed order for every i), so
-// that a long slice list is four short dependent chains.
-__global__ __launch_bounds__(256) void slice_sum_kernel(const float* __restrict__ part, float* __restrict__ out,
+// out[i] = sum over s < nslice of part[s * stride + i], in slice order (few
+// slices, many outputs: the weight gradients).
+__global__ __launch_bounds__(kRowThreads) void slice_sum_kernel(const float* __restrict__ part, float* __restrict__ out,
+                                                                int64_t n, int64_t stride, int nslice) {
+  const int64_t i = (int64_t)blockIdx.x * kRowThreads + threadIdx.x;
+  if (i >= n) return;
+  float acc = 0.0f;
+  int s = 0;
+  for (; s + 8 <= nslice; s += 8) {
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = part[(int64_t)(s + u) * stride + i];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc += v[u];
+  }
+  for (; s < nslice; ++s) acc += part[(int64_t)s * stride + i];
+  out[i] = acc;
+}
+
+// The same for many slices and few outputs (the column sums' 512 row
+// slices): a workgroup takes 64 consecutive i; its four waves sum the slices
+// s = 4j + wave in order, and the four sums are added in wave order (a fixed
+// order for every i), so that the slice list is four short dependent chains.
+__global__ __launch_bounds__(256) void slice_sum4_kernel(const float* __restrict__ part, float* __restrict__ out,
                                                         int64_t n, int64_t stride, int nslice) {
   __shared__ float red[4][64];
   const int c = threadIdx.x & 63, q = threadIdx.x >> 6;
@@ -792,8 +811,13 @@ size_t block_bwd_workspace(const Geo& g) { return block_ws(g).total; }
 
 static hipError_t slice_sum(const float* part, float* out, int64_t n, int nslice, hipStream_t st,
                             int64_t stride = -1) {
-  hipLaunchKernelGGL(slice_sum_kernel, dim3((unsigned)((n + 63) / 64)), dim3(256), 0, st, part, out, n,
-                     stride < 0 ? n : stride, nslice);
+  if (nslice >= 64) {
+    hipLaunchKernelGGL(slice_sum4_kernel, dim3((unsigned)((n + 63) / 64)), dim3(256), 0, st, part, out, n,
+                       stride < 0 ? n : stride, nslice);
+  } else {
+    hipLaunchKernelGGL(slice_sum_kernel, dim3((unsigned)((n + kRowThreads - 1) / kRowThreads)), dim3(kRowThreads), 0,
+                       st, part, out, n, stride < 0 ? n : stride, nslice);
+  }
   return hipGetLastError();
 }
 
