@@ -453,8 +453,9 @@ __global__ __launch_bounds__(kRowThreads) void ln_stats_kernel(const bf16* __res
 // ---------------------------------------------------------------------------
 constexpr int kLnMaxChunks = 4;   // C <= 4 * 512 = 2048
 
+template <typename DY>
 __global__ __launch_bounds__(kRowThreads) void ln_bwd_kernel(
-    const float* __restrict__ dy, const bf16* __restrict__ z, const float* __restrict__ mean,
+    const DY* __restrict__ dy, const bf16* __restrict__ z, const float* __restrict__ mean,
     const float* __restrict__ rstd, const float* __restrict__ gamma, const bf16* __restrict__ dres,
     bf16* __restrict__ dz, float* __restrict__ part, int T, int C, int rows_per_wave) {
   const int gw = blockIdx.x * (kRowThreads / 64) + (threadIdx.x >> 6);
@@ -476,9 +477,16 @@ __global__ __launch_bounds__(kRowThreads) void ln_bwd_kernel(
       const int ch = 8 * (lane + 64 * c);
       if (ch < C) {
         const bf16x8 zv = *reinterpret_cast<const bf16x8*>(z + (int64_t)row * C + ch);
-        const float4 d0 = *reinterpret_cast<const float4*>(dy + (int64_t)row * C + ch);
-        const float4 d1 = *reinterpret_cast<const float4*>(dy + (int64_t)row * C + ch + 4);
-        const float d[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
+        float d[8];
+        if constexpr (sizeof(DY) == 4) {
+          const float4 d0 = *reinterpret_cast<const float4*>(dy + (int64_t)row * C + ch);
+          const float4 d1 = *reinterpret_cast<const float4*>(dy + (int64_t)row * C + ch + 4);
+          d[0] = d0.x; d[1] = d0.y; d[2] = d0.z; d[3] = d0.w; d[4] = d1.x; d[5] = d1.y; d[6] = d1.z; d[7] = d1.w;
+        } else {
+          const bf16x8 dv = *reinterpret_cast<const bf16x8*>(dy + (int64_t)row * C + ch);
+#pragma unroll
+          for (int i = 0; i < 8; ++i) d[i] = (float)dv[i];
+        }
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
           zh[c][i] = ((float)zv[i] - mu) * rs;
@@ -900,6 +908,7 @@ hipError_t launch_block_bwd(const Geo& g, const void* dx2, const void* x, const 
   char* ws = reinterpret_cast<char*>(wsv);
   bf16* dh = reinterpret_cast<bf16*>(ws + w.dh);
   float* dln = reinterpret_cast<float*>(ws + w.dln);
+  bf16* dlnb = reinterpret_cast<bf16*>(ws + w.dln);     // the same buffer holding bf16
   bf16* dx1 = reinterpret_cast<bf16*>(ws + w.dx1);
   bf16* dO = reinterpret_cast<bf16*>(ws + w.dO);
   bf16* dqkv[3] = {reinterpret_cast<bf16*>(ws + w.dq), reinterpret_cast<bf16*>(ws + w.dk),
@@ -931,12 +940,13 @@ hipError_t launch_block_bwd(const Geo& g, const void* dx2, const void* x, const 
   TERRA_TRY(ln_apply(s.x1, s.mu2, s.rstd2, p.ln2_g, p.ln2_b, lnb, T, C, st));
   TERRA_TRY(wgrad(mat(dh, 4 * C, T), mat(lnb, C, T), T, 4 * C, C, gr.w_fc1, ws, w, st));
   TERRA_TRY(colsum(mat(dh, 4 * C, T), 4 * C, cpart, gr.b_fc1, w, st));
+  // dln2 in bf16, like the other gradients the products hand on
   ep = EpiArgs{};
-  ep.outf = dln;
-  TERRA_TRY((gemm<true, true, EPI_F32>(mat(dh, 4 * C, T), mat(wt_fc1, 4 * C, C), ep, T, C, 4 * C, 1, st)));
+  ep.out[0] = dlnb; ep.split = C;
+  TERRA_TRY((gemm<true, true, EPI_BF16>(mat(dh, 4 * C, T), mat(wt_fc1, 4 * C, C), ep, T, C, 4 * C, 1, st)));
   // dx1 = dx2 + LN2 backward
-  hipLaunchKernelGGL(ln_bwd_kernel, dim3(w.lnwaves / 4), dim3(kRowThreads), 0, st, dln, (const bf16*)s.x1, s.mu2,
-                     s.rstd2, p.ln2_g, (const bf16*)dx2, dx1, lpart, T, C, w.rows_per_wave);
+  hipLaunchKernelGGL(ln_bwd_kernel<bf16>, dim3(w.lnwaves / 4), dim3(kRowThreads), 0, st, dlnb, (const bf16*)s.x1,
+                     s.mu2, s.rstd2, p.ln2_g, (const bf16*)dx2, dx1, lpart, T, C, w.rows_per_wave);
   TERRA_TRY(hipGetLastError());
   TERRA_TRY(ln_param_grads(lpart, gr.ln2_g, gr.ln2_b, C, w, st));
   // x1 = x + o Wp^T + bp:  dWp = dx1^T o, dbp = colsum(dx1), dO = dx1 Wp
@@ -969,10 +979,11 @@ hipError_t launch_block_bwd(const Geo& g, const void* dx2, const void* x, const 
   }
   TERRA_TRY(colsum(dy3, 3 * C, cpart, gr.b_qkv, w, st));
   ep = EpiArgs{};
-  ep.outf = dln;
   if (seg_d) {
-    TERRA_TRY((gemm<true, true, EPI_F32, true>(dy3, mat(wt_qkv, 3 * C, C), ep, T, C, 3 * C, 1, st)));
+    ep.out[0] = dlnb; ep.split = C;
+    TERRA_TRY((gemm<true, true, EPI_BF16, true>(dy3, mat(wt_qkv, 3 * C, C), ep, T, C, 3 * C, 1, st)));
   } else {
+    ep.outf = dln;
     for (int i = 0; i < 3; ++i) {
       const bf16* wi = reinterpret_cast<const bf16*>(p.w_qkv) + (size_t)i * C * C;
       if (i == 0) {
@@ -983,8 +994,13 @@ hipError_t launch_block_bwd(const Geo& g, const void* dx2, const void* x, const 
     }
   }
   // dx = dx1 + LN1 backward
-  hipLaunchKernelGGL(ln_bwd_kernel, dim3(w.lnwaves / 4), dim3(kRowThreads), 0, st, dln, (const bf16*)x, s.mu1,
-                     s.rstd1, p.ln1_g, (const bf16*)dx1, (bf16*)dx, lpart, T, C, w.rows_per_wave);
+  if (seg_d) {
+    hipLaunchKernelGGL(ln_bwd_kernel<bf16>, dim3(w.lnwaves / 4), dim3(kRowThreads), 0, st, dlnb, (const bf16*)x,
+                       s.mu1, s.rstd1, p.ln1_g, (const bf16*)dx1, (bf16*)dx, lpart, T, C, w.rows_per_wave);
+  } else {
+    hipLaunchKernelGGL(ln_bwd_kernel<float>, dim3(w.lnwaves / 4), dim3(kRowThreads), 0, st, dln, (const bf16*)x,
+                       s.mu1, s.rstd1, p.ln1_g, (const bf16*)dx1, (bf16*)dx, lpart, T, C, w.rows_per_wave);
+  }
   TERRA_TRY(hipGetLastError());
   TERRA_TRY(ln_param_grads(lpart, gr.ln1_g, gr.ln1_b, C, w, st));
 #undef TERRA_TRY
