@@ -453,16 +453,17 @@ __global__ __launch_bounds__(kRowThreads) void ln_stats_kernel(const bf16* __res
 // ---------------------------------------------------------------------------
 constexpr int kLnMaxChunks = 4;   // C <= 4 * 512 = 2048
 
-template <typename DY>
+// NCH = ceil(C / 512) chunk slots a lane (registers for C, not for 2048)
+template <typename DY, int NCH>
 __global__ __launch_bounds__(kRowThreads) void ln_bwd_kernel(
     const DY* __restrict__ dy, const bf16* __restrict__ z, const float* __restrict__ mean,
     const float* __restrict__ rstd, const float* __restrict__ gamma, const bf16* __restrict__ dres,
     bf16* __restrict__ dz, float* __restrict__ part, int T, int C, int rows_per_wave) {
   const int gw = blockIdx.x * (kRowThreads / 64) + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
-  float dg[kLnMaxChunks][8], db[kLnMaxChunks][8];
+  float dg[NCH][8], db[NCH][8];
 #pragma unroll
-  for (int c = 0; c < kLnMaxChunks; ++c)
+  for (int c = 0; c < NCH; ++c)
 #pragma unroll
     for (int i = 0; i < 8; ++i) dg[c][i] = db[c][i] = 0.0f;
   const int r0 = gw * rows_per_wave;
@@ -470,10 +471,10 @@ __global__ __launch_bounds__(kRowThreads) void ln_bwd_kernel(
   const float invC = 1.0f / (float)C;
   for (int row = r0; row < r1; ++row) {
     const float mu = mean[row], rs = rstd[row];
-    float zh[kLnMaxChunks][8], gg[kLnMaxChunks][8];
+    float zh[NCH][8], gg[NCH][8];
     float s1 = 0.0f, s2 = 0.0f;
 #pragma unroll
-    for (int c = 0; c < kLnMaxChunks; ++c) {
+    for (int c = 0; c < NCH; ++c) {
       const int ch = 8 * (lane + 64 * c);
       if (ch < C) {
         const bf16x8 zv = *reinterpret_cast<const bf16x8*>(z + (int64_t)row * C + ch);
@@ -501,7 +502,7 @@ __global__ __launch_bounds__(kRowThreads) void ln_bwd_kernel(
     s1 = wave_sum(s1) * invC;
     s2 = wave_sum(s2) * invC;
 #pragma unroll
-    for (int c = 0; c < kLnMaxChunks; ++c) {
+    for (int c = 0; c < NCH; ++c) {
       const int ch = 8 * (lane + 64 * c);
       if (ch < C) {
         const bf16x8 rv = *reinterpret_cast<const bf16x8*>(dres + (int64_t)row * C + ch);
@@ -514,7 +515,7 @@ __global__ __launch_bounds__(kRowThreads) void ln_bwd_kernel(
   }
   float* pg = part + (int64_t)gw * 2 * C;
 #pragma unroll
-  for (int c = 0; c < kLnMaxChunks; ++c) {
+  for (int c = 0; c < NCH; ++c) {
     const int ch = 8 * (lane + 64 * c);
     if (ch < C) {
 #pragma unroll
@@ -788,9 +789,9 @@ static BwdWs block_ws(const Geo& geo) {
   w.wsplit = 64;                         // most contraction (token) slices of a weight gradient
   w.cslices = 512;                       // row slices of the bias-gradient column sums
   w.cpart_rows = (int)((T + w.cslices - 1) / w.cslices);
-  w.lnwaves = 2048;                      // waves of the LayerNorm backward
+  w.lnwaves = 4096;                      // waves of the LayerNorm backward
   w.rows_per_wave = (int)((T + w.lnwaves - 1) / w.lnwaves);
-  w.lgroups = 64;                        // first-level groups of the LayerNorm partials
+  w.lgroups = 128;                       // first-level groups of the LayerNorm partials (32 waves each)
   size_t off = 0;
   w.dh = off; off += al(T * 4 * C * 2);
   w.dln = off; off += al(T * C * 4);
@@ -886,6 +887,28 @@ static hipError_t wgrad3(const Mat& dy3, const Mat& Z, int T, int C, float* dW, 
   return slice_sum(part, dW, (int64_t)3 * C * C, ns, st);
 }
 
+// dz = LayerNorm backward of dy (float32 or bf16) + dres, and the per-wave
+// gain/shift partials, with the chunk count C needs.
+template <typename DY>
+static hipError_t ln_bwd(const DY* dy, const void* z, const float* mean, const float* rstd, const float* gamma,
+                         const void* dres, void* dz, float* part, int T, int C, const BwdWs& w, hipStream_t st) {
+  const dim3 grid(w.lnwaves / 4), block(kRowThreads);
+  const bf16* zb = (const bf16*)z;
+  const bf16* rb = (const bf16*)dres;
+  bf16* ob = (bf16*)dz;
+  switch ((C + 511) / 512) {
+    case 1: hipLaunchKernelGGL((ln_bwd_kernel<DY, 1>), grid, block, 0, st, dy, zb, mean, rstd, gamma, rb, ob, part, T,
+                               C, w.rows_per_wave); break;
+    case 2: hipLaunchKernelGGL((ln_bwd_kernel<DY, 2>), grid, block, 0, st, dy, zb, mean, rstd, gamma, rb, ob, part, T,
+                               C, w.rows_per_wave); break;
+    case 3: hipLaunchKernelGGL((ln_bwd_kernel<DY, 3>), grid, block, 0, st, dy, zb, mean, rstd, gamma, rb, ob, part, T,
+                               C, w.rows_per_wave); break;
+    default: hipLaunchKernelGGL((ln_bwd_kernel<DY, 4>), grid, block, 0, st, dy, zb, mean, rstd, gamma, rb, ob, part,
+                                T, C, w.rows_per_wave); break;
+  }
+  return hipGetLastError();
+}
+
 static hipError_t transpose(const void* in, bf16* out, int rows, int cols, hipStream_t st) {
   hipLaunchKernelGGL(transpose_kernel, dim3((cols + 31) / 32, (rows + 31) / 32), dim3(256), 0, st, (const bf16*)in,
                      out, rows, cols);
@@ -945,9 +968,7 @@ hipError_t launch_block_bwd(const Geo& g, const void* dx2, const void* x, const 
   ep.out[0] = dlnb; ep.split = C;
   TERRA_TRY((gemm<true, true, EPI_BF16>(mat(dh, 4 * C, T), mat(wt_fc1, 4 * C, C), ep, T, C, 4 * C, 1, st)));
   // dx1 = dx2 + LN2 backward
-  hipLaunchKernelGGL(ln_bwd_kernel<bf16>, dim3(w.lnwaves / 4), dim3(kRowThreads), 0, st, dlnb, (const bf16*)s.x1,
-                     s.mu2, s.rstd2, p.ln2_g, (const bf16*)dx2, dx1, lpart, T, C, w.rows_per_wave);
-  TERRA_TRY(hipGetLastError());
+  TERRA_TRY(ln_bwd(dlnb, s.x1, s.mu2, s.rstd2, p.ln2_g, dx2, dx1, lpart, T, C, w, st));
   TERRA_TRY(ln_param_grads(lpart, gr.ln2_g, gr.ln2_b, C, w, st));
   // x1 = x + o Wp^T + bp:  dWp = dx1^T o, dbp = colsum(dx1), dO = dx1 Wp
   TERRA_TRY(wgrad(mat(dx1, C, T), mat(s.o, C, T), T, C, C, gr.w_proj, ws, w, st));
@@ -995,13 +1016,10 @@ hipError_t launch_block_bwd(const Geo& g, const void* dx2, const void* x, const 
   }
   // dx = dx1 + LN1 backward
   if (seg_d) {
-    hipLaunchKernelGGL(ln_bwd_kernel<bf16>, dim3(w.lnwaves / 4), dim3(kRowThreads), 0, st, dlnb, (const bf16*)x,
-                       s.mu1, s.rstd1, p.ln1_g, (const bf16*)dx1, (bf16*)dx, lpart, T, C, w.rows_per_wave);
+    TERRA_TRY(ln_bwd(dlnb, x, s.mu1, s.rstd1, p.ln1_g, dx1, dx, lpart, T, C, w, st));
   } else {
-    hipLaunchKernelGGL(ln_bwd_kernel<float>, dim3(w.lnwaves / 4), dim3(kRowThreads), 0, st, dln, (const bf16*)x,
-                       s.mu1, s.rstd1, p.ln1_g, (const bf16*)dx1, (bf16*)dx, lpart, T, C, w.rows_per_wave);
+    TERRA_TRY(ln_bwd(dln, x, s.mu1, s.rstd1, p.ln1_g, dx1, dx, lpart, T, C, w, st));
   }
-  TERRA_TRY(hipGetLastError());
   TERRA_TRY(ln_param_grads(lpart, gr.ln1_g, gr.ln1_b, C, w, st));
 #undef TERRA_TRY
   return hipSuccess;
