@@ -415,28 +415,35 @@ __device__ inline float wave_sum(float x) {
   return x;
 }
 
+// Mean and 1/std of each row, one wave a row: the row is read once into
+// registers (C <= 2048: four 8-element chunks a lane) and the variance is
+// taken about the mean from there.
 __global__ __launch_bounds__(kRowThreads) void ln_stats_kernel(const bf16* __restrict__ x, float* __restrict__ mean,
                                                                float* __restrict__ rstd, int T, int C, float eps) {
   const int row = blockIdx.x * (kRowThreads / 64) + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (row >= T) return;
   const bf16* p = x + (int64_t)row * C;
-  float s = 0.0f;
-  for (int c = 8 * lane; c < C; c += 512) {
-    const bf16x8 v = *reinterpret_cast<const bf16x8*>(p + c);
+  bf16x8 v[4];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) s += (float)v[i];
-  }
+  for (int c = 0; c < 4; ++c)
+    if (8 * lane + 512 * c < C) v[c] = *reinterpret_cast<const bf16x8*>(p + 8 * lane + 512 * c);
+  float s = 0.0f;
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+    if (8 * lane + 512 * c < C)
+#pragma unroll
+      for (int i = 0; i < 8; ++i) s += (float)v[c][i];
   const float mu = wave_sum(s) / (float)C;
   float q = 0.0f;
-  for (int c = 8 * lane; c < C; c += 512) {
-    const bf16x8 v = *reinterpret_cast<const bf16x8*>(p + c);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const float d = (float)v[i] - mu;
-      q += d * d;
-    }
-  }
+  for (int c = 0; c < 4; ++c)
+    if (8 * lane + 512 * c < C)
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float d = (float)v[c][i] - mu;
+        q += d * d;
+      }
   const float var = wave_sum(q) / (float)C;
   if (lane == 0) {
     mean[row] = mu;
