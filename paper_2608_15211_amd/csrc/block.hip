@@ -67,6 +67,9 @@ struct EpiArgs {
   const float* rstd;   // per-column sum of the folded weights (lns) and constant (lnc)
   const float* lns;
   const float* lnc;
+  // EPI_GELU_GRAD: column sums of the bf16 output over each wave's 128 rows,
+  // partial row 2 (tile row) + (wave row), ld = N (nullable)
+  float* colpart;
 };
 
 // Phi(x), the standard normal distribution function, and exp(-x^2 / 2), with
@@ -281,6 +284,8 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void gemm_kernel(Mat A, Mat B, Epi
   float* et = reinterpret_cast<float*>(smem) + wave * 32 * kEpiS;
   const int h = lane >> 5, col = lane & 31;
   const int er = lane >> 1, ec = (lane & 1) * 32;     // this lane's row and first column when reading back
+  constexpr bool kCol = EPI == EPI_GELU_GRAD;
+  float cs[kCol ? 4 : 1][8] = {};                      // this lane's column sums over its four rows
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
 #pragma unroll
@@ -325,6 +330,10 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void gemm_kernel(Mat A, Mat B, Epi
 #pragma unroll
         for (int x = 0; x < 8; ++x) t[x] = (bf16)(v[x] * gelu_grad_f((float)hv[x]));
         *reinterpret_cast<bf16x8*>(ep.out[0] + o) = t;
+        if constexpr (kCol) {
+#pragma unroll
+          for (int x = 0; x < 8; ++x) cs[q][x] += (float)t[x];
+        }
       } else if (EPI == EPI_F32 || EPI == EPI_F32_ACC) {
         float* dst = ep.outf + (EPI == EPI_F32 ? (int64_t)blockIdx.z * M * N : 0) + o;
         if (EPI == EPI_F32_ACC) {
@@ -343,6 +352,22 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void gemm_kernel(Mat A, Mat B, Epi
       }
     }
     __builtin_amdgcn_wave_barrier();
+  }
+  if constexpr (kCol) {
+    // the wave's 32 lanes of each parity hold four-row sums of the same 32
+    // columns: through the wave's staging tile, lane c then adds column c
+    // over the 32 lanes' rows in order
+    if (ep.colpart != nullptr) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int x = 0; x < 8; ++x) et[er * kEpiS + ec + 8 * q + x] = cs[q][x];
+      __builtin_amdgcn_wave_barrier();
+      float sum = 0.0f;
+      for (int r = 0; r < 32; ++r) sum += et[r * kEpiS + lane];
+      const int n = n0 + wn + lane;
+      if (n < N) ep.colpart[(int64_t)(2 * tm + wm / 128) * N + n] = sum;
+    }
   }
 }
 
@@ -817,7 +842,8 @@ static BwdWs block_ws(const Geo& geo) {
     wmax = std::max(wmax, (size_t)wgrad_slices((int)T, nl, kl, w.wsplit) * nl * kl);
   }
   w.wpart = off; off += al(wmax * 4);
-  w.cpart = off; off += al((size_t)w.cslices * 4 * C * 4);
+  // column-sum partials: the colsum slices, or the dh product's 2 ceil(T/256) rows
+  w.cpart = off; off += al((size_t)std::max((size_t)w.cslices, 2 * ((T + kBM - 1) / kBM)) * 4 * C * 4);
   w.lpart = off; off += al((size_t)w.lnwaves * 2 * C * 4 + (size_t)w.lgroups * 2 * C * 4);
   w.total = off;
   return w;
@@ -964,12 +990,14 @@ hipError_t launch_block_bwd(const Geo& g, const void* dx2, const void* x, const 
   // x2 = x1 + a W2^T + b2:  dW2 = dx2^T a, db2 = colsum(dx2), dh = (dx2 W2) * GELU'(h)
   TERRA_TRY(wgrad(mat(dx2, C, T), mat(s.a, 4 * C, T), T, C, 4 * C, gr.w_fc2, ws, w, st));
   TERRA_TRY(colsum(mat(dx2, C, T), C, cpart, gr.b_fc2, w, st));
-  ep.out[0] = dh; ep.split = 4 * C; ep.aux = (const bf16*)s.h;
+  // db1 = colsum(dh) from the same epilogue: per-wave partial rows, then a
+  // fixed-order sum of the 2 ceil(T / 256) partials
+  ep.out[0] = dh; ep.split = 4 * C; ep.aux = (const bf16*)s.h; ep.colpart = cpart;
   TERRA_TRY((gemm<true, true, EPI_GELU_GRAD, false, 4>(mat(dx2, C, T), mat(wt_fc2, C, 4 * C), ep, T, 4 * C, C, 1, st)));
+  TERRA_TRY(slice_sum(cpart, gr.b_fc1, 4 * C, 2 * ((T + kBM - 1) / kBM), st));
   // h = LN2(x1) W1^T + b1:  dW1 = dh^T LN2(x1), db1 = colsum(dh), dln2 = dh W1
   TERRA_TRY(ln_apply(s.x1, s.mu2, s.rstd2, p.ln2_g, p.ln2_b, lnb, T, C, st));
   TERRA_TRY(wgrad(mat(dh, 4 * C, T), mat(lnb, C, T), T, 4 * C, C, gr.w_fc1, ws, w, st));
-  TERRA_TRY(colsum(mat(dh, 4 * C, T), 4 * C, cpart, gr.b_fc1, w, st));
   // dln2 in bf16, like the other gradients the products hand on
   ep = EpiArgs{};
   ep.out[0] = dlnb; ep.split = C;
