@@ -286,6 +286,26 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void gemm_kernel(Mat A, Mat B, Epi
   const int er = lane >> 1, ec = (lane & 1) * 32;     // this lane's row and first column when reading back
   constexpr bool kCol = EPI == EPI_GELU_GRAD;
   float cs[kCol ? 4 : 1][8] = {};                      // this lane's column sums over its four rows
+  // per-column epilogue constants of this lane's 32 columns, loaded once
+  // for the four row blocks (LayerNorm fold: s and c; bias)
+  constexpr bool kLn = EPI == EPI_LN_QKV || EPI == EPI_LN_GELU;
+  constexpr int kPc = kLn ? 2 : (EPI == EPI_BIAS_RES ? 1 : 0);
+  float pc[kPc > 0 ? kPc : 1][4][8];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int n = n0 + wn + ec + 8 * q;     // N is a multiple of 8
+#pragma unroll
+    for (int a = 0; a < kPc; ++a) {
+      const float* src = kLn ? (a == 0 ? ep.lns : ep.lnc) : ep.bias;
+      float4 lo = make_float4(0.f, 0.f, 0.f, 0.f), hi = lo;
+      if (n < N) {
+        lo = *reinterpret_cast<const float4*>(src + n);
+        hi = *reinterpret_cast<const float4*>(src + n + 4);
+      }
+      pc[a][q][0] = lo.x; pc[a][q][1] = lo.y; pc[a][q][2] = lo.z; pc[a][q][3] = lo.w;
+      pc[a][q][4] = hi.x; pc[a][q][5] = hi.y; pc[a][q][6] = hi.z; pc[a][q][7] = hi.w;
+    }
+  }
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
 #pragma unroll
@@ -307,7 +327,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void gemm_kernel(Mat A, Mat B, Epi
         bf16x8 t, g;
 #pragma unroll
         for (int x = 0; x < 8; ++x) {
-          const float y = rs * (v[x] - mu * ep.lns[n + x]) + ep.lnc[n + x];
+          const float y = rs * (v[x] - mu * pc[0][q][x]) + pc[1][q][x];
           t[x] = (bf16)y;
           if (EPI == EPI_LN_GELU) g[x] = (bf16)gelu_f(y);
         }
@@ -322,7 +342,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void gemm_kernel(Mat A, Mat B, Epi
         const bf16x8 res = *reinterpret_cast<const bf16x8*>(ep.aux + o);
         bf16x8 t;
 #pragma unroll
-        for (int x = 0; x < 8; ++x) t[x] = (bf16)(v[x] + ep.bias[n + x] + (float)res[x]);
+        for (int x = 0; x < 8; ++x) t[x] = (bf16)(v[x] + pc[0][q][x] + (float)res[x]);
         *reinterpret_cast<bf16x8*>(ep.out[0] + o) = t;
       } else if (EPI == EPI_GELU_GRAD) {
         const bf16x8 hv = *reinterpret_cast<const bf16x8*>(ep.aux + o);
