@@ -724,6 +724,32 @@ static Mat mat(const void* p, int ld, int rows) {
   return m;
 }
 
+// A product whose 256 x 256 tiles do not fill whole rounds of one
+// workgroup per CU (N = C: 3 column tiles by ceil(T / 256) row tiles, 6.3
+// rounds on the 128x1080 grid): the rows of the whole rounds go to the
+// eight-wave form, the rest to the four-wave form, whose 256 x 128 tiles
+// spread the last partial round over twice as many workgroups.  A is
+// K-major and the epilogue writes (and, for the residual, reads) rows of
+// N, offset by the first part's rows.
+template <bool BKROW, int EPI, bool SEG = false>
+static hipError_t gemm_rounds(const Mat& A, const Mat& B, const EpiArgs& ep, int M, int N, int K, hipStream_t st) {
+  static_assert(EPI == EPI_BF16 || EPI == EPI_BIAS_RES, "row offsets are set for these epilogues");
+  const int ntn = (N + kBN - 1) / kBN, nM = (M + kBM - 1) / kBM;
+  const int r1 = ((nM * ntn) / kMaxCusBlock) * kMaxCusBlock / ntn;   // row tiles in whole rounds
+  if (r1 == 0 || r1 >= nM) return gemm<true, BKROW, EPI, SEG>(A, B, ep, M, N, K, 1, st);
+  const int m1 = r1 * kBM;
+  hipError_t e = gemm<true, BKROW, EPI, SEG>(A, B, ep, m1, N, K, 1, st);
+  if (e != hipSuccess) return e;
+  Mat a2 = A;
+  a2.p = A.p + (int64_t)m1 * A.ld;
+  a2.rows = A.rows - m1;
+  EpiArgs e2 = ep;
+  e2.out[0] = ep.out[0] + (int64_t)m1 * N;
+  if (EPI == EPI_BIAS_RES) e2.aux = ep.aux + (int64_t)m1 * N;
+  return gemm<true, BKROW, EPI, SEG, 4>(a2, B, e2, M - m1, N, K, 1, st);
+}
+
+
 constexpr float kLnEps = 1e-5f;
 
 hipError_t launch_attn_fwd(const Geo& g, int dt, bool nhwc, const void* q, const void* k, const void* v,
@@ -809,7 +835,7 @@ hipError_t launch_block_fwd(const Geo& g, const void* x, const BlockParams& p, c
   // x2 = x1 + a W_2^T + b_2
   ep = EpiArgs{};
   ep.out[0] = (bf16*)x2; ep.split = C; ep.aux = (const bf16*)s.x1; ep.bias = p.b_fc2;
-  TERRA_TRY((gemm<true, true, EPI_BIAS_RES>(mat(s.a, 4 * C, T), mat(p.w_fc2, 4 * C, C), ep, T, C, 4 * C, 1, st)));
+  TERRA_TRY((gemm_rounds<true, EPI_BIAS_RES>(mat(s.a, 4 * C, T), mat(p.w_fc2, 4 * C, C), ep, T, C, 4 * C, st)));
 #undef TERRA_TRY
   return hipSuccess;
 }
@@ -1021,7 +1047,7 @@ hipError_t launch_block_bwd(const Geo& g, const void* dx2, const void* x, const 
   // dln2 in bf16, like the other gradients the products hand on
   ep = EpiArgs{};
   ep.out[0] = dlnb; ep.split = C;
-  TERRA_TRY((gemm<true, true, EPI_BF16>(mat(dh, 4 * C, T), mat(wt_fc1, 4 * C, C), ep, T, C, 4 * C, 1, st)));
+  TERRA_TRY((gemm_rounds<true, EPI_BF16>(mat(dh, 4 * C, T), mat(wt_fc1, 4 * C, C), ep, T, C, 4 * C, st)));
   // dx1 = dx2 + LN2 backward
   TERRA_TRY(ln_bwd(dlnb, s.x1, s.mu2, s.rstd2, p.ln2_g, dx2, dx1, lpart, T, C, w, st));
   TERRA_TRY(ln_param_grads(lpart, gr.ln2_g, gr.ln2_b, C, w, st));
@@ -1057,7 +1083,7 @@ hipError_t launch_block_bwd(const Geo& g, const void* dx2, const void* x, const 
   ep = EpiArgs{};
   if (seg_d) {
     ep.out[0] = dlnb; ep.split = C;
-    TERRA_TRY((gemm<true, true, EPI_BF16, true>(dy3, mat(wt_qkv, 3 * C, C), ep, T, C, 3 * C, 1, st)));
+    TERRA_TRY((gemm_rounds<true, EPI_BF16, true>(dy3, mat(wt_qkv, 3 * C, C), ep, T, C, 3 * C, st)));
   } else {
     ep.outf = dln;
     for (int i = 0; i < 3; ++i) {
