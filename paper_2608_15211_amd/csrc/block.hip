@@ -735,7 +735,8 @@ template <bool BKROW, int EPI, bool SEG = false>
 static hipError_t gemm_rounds(const Mat& A, const Mat& B, const EpiArgs& ep, int M, int N, int K, hipStream_t st) {
   static_assert(EPI == EPI_BF16 || EPI == EPI_BIAS_RES, "row offsets are set for these epilogues");
   const int ntn = (N + kBN - 1) / kBN, nM = (M + kBM - 1) / kBM;
-  const int r1 = ((nM * ntn) / kMaxCusBlock) * kMaxCusBlock / ntn;   // row tiles in whole rounds
+  int r1 = ((nM * ntn) / kMaxCusBlock) * kMaxCusBlock / ntn;   // row tiles in whole rounds
+  while (r1 > 0 && (r1 * ntn) % 8 != 0) --r1;   // a tile count the XCD-grouped order takes
   if (r1 == 0 || r1 >= nM) return gemm<true, BKROW, EPI, SEG>(A, B, ep, M, N, K, 1, st);
   const int m1 = r1 * kBM;
   hipError_t e = gemm<true, BKROW, EPI, SEG>(A, B, ep, m1, N, K, 1, st);
